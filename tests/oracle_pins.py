@@ -1,0 +1,384 @@
+"""Pins of the CPU oracle against facts fixed outside the oracle.
+
+Each ``pin_*`` takes an oracle handle (``oracle.Oracle``) and raises
+AssertionError when the oracle disagrees with a closed form, a dense
+brute-force model (``brute.py``), an invariant of unitary evolution, or a
+derivative computed another way. ``test_oracle_pins.py`` runs them against the
+real oracle; ``test_oracle_mutants.py`` runs them against deliberately broken
+copies of the oracle to show each plausible mistake fails at least one pin.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+import brute
+import workloads as W
+
+TOL = 1e-12
+
+
+def _g(kind, q0, q1=-1, src=W.SRC_NONE, index=0):
+    return [kind, q0, q1, src, index]
+
+
+def _arr(gs):
+    return np.asarray(gs, dtype=np.int32).reshape(-1, 5)
+
+
+def _close(a, b, tol=TOL, what=""):
+    a = np.asarray(a, dtype=np.complex128)
+    b = np.asarray(b, dtype=np.complex128)
+    err = float(np.max(np.abs(a - b))) if a.size else 0.0
+    assert err <= tol, f"{what}: max abs err {err:.3e} > {tol:.1e}"
+
+
+THETAS = np.array([-2.9, -1.3, -0.4, 0.0, 0.35, 1.1, 2.2, 3.0])
+
+
+# --------------------------------------------------------------------------
+# one-qubit closed forms (Bloch-sphere rotations)
+
+def pin_rotations_on_zero(orc):
+    """RX(t)|0> and RY(t)|0> give <Z> = cos t, d<Z>/dt = -sin t; RZ leaves |0> alone."""
+    for kind in (W.RX, W.RY, W.RZ):
+        gates = _arr([_g(kind, 0, -1, W.SRC_WEIGHT, 0)])
+        for t in THETAS:
+            r = orc.run(1, gates, np.zeros((1, 0)), [t], grad_out=[[1.0]])
+            want = 1.0 if kind == W.RZ else math.cos(t)
+            dwant = 0.0 if kind == W.RZ else -math.sin(t)
+            _close(r["expz"][0, 0], want, what=f"{W.KIND_NAMES[kind]} <Z>")
+            _close(r["grad_weights"][0], dwant, what=f"{W.KIND_NAMES[kind]} grad")
+
+
+def pin_rotation_axes(orc):
+    """H, RZ(phi), then RX(t) or RY(t): Bloch vector (cos phi, sin phi, 0) rotated.
+
+    About x: <Z> = sin(phi) sin(t). About y: <Z> = -cos(phi) sin(t). These fix
+    the axis and sense of each rotation and the relative phase RZ applies.
+    """
+    for phi in (-1.0, 0.3, 2.0):
+        for t in THETAS:
+            for kind, want in ((W.RX, math.sin(phi) * math.sin(t)),
+                               (W.RY, -math.cos(phi) * math.sin(t))):
+                gates = _arr([_g(W.H, 0), _g(W.RZ, 0, -1, W.SRC_INPUT, 0),
+                              _g(kind, 0, -1, W.SRC_WEIGHT, 0)])
+                r = orc.run(1, gates, [[phi]], [t], grad_out=[[1.0]])
+                _close(r["expz"][0, 0], want, what=f"axis {W.KIND_NAMES[kind]}")
+                if kind == W.RX:
+                    dphi, dt = math.cos(phi) * math.sin(t), math.sin(phi) * math.cos(t)
+                else:
+                    dphi, dt = math.sin(phi) * math.sin(t), -math.cos(phi) * math.cos(t)
+                _close(r["grad_inputs"][0, 0], dphi, what="d/dphi")
+                _close(r["grad_weights"][0], dt, what="d/dt")
+
+
+def pin_h_rz_h(orc):
+    """H RZ(t) H |0> is RX(t)|0> up to a phase: <Z> = cos t."""
+    gates = _arr([_g(W.H, 0), _g(W.RZ, 0, -1, W.SRC_WEIGHT, 0), _g(W.H, 0)])
+    for t in THETAS:
+        r = orc.run(1, gates, np.zeros((1, 0)), [t], grad_out=[[1.0]])
+        _close(r["expz"][0, 0], math.cos(t), what="H RZ H")
+        _close(r["grad_weights"][0], -math.sin(t), what="H RZ H grad")
+
+
+def pin_hybrid_node(orc):
+    """The paper's hybrid network node (appendix on hybrid quantum-classical
+    networks): one qubit, H then RY(input).
+
+    <Z> = -sin t, so P(1) = (1 + sin t) / 2. The node's backward takes the
+    difference of P(1) at t +- pi/2 without a 1/2 factor, which is cos t; the
+    exact derivative d<Z>/dt is -cos t.
+    """
+    gates = _arr([_g(W.H, 0), _g(W.RY, 0, -1, W.SRC_INPUT, 0)])
+    for t in THETAS:
+        r = orc.run(1, gates, [[t]], [], grad_out=[[1.0]])
+        _close(r["expz"][0, 0], -math.sin(t), what="hybrid node <Z>")
+        _close(r["grad_inputs"][0, 0], -math.cos(t), what="hybrid node grad")
+        p1 = [(1.0 - orc.run(1, gates, [[t + s]], [])["expz"][0, 0]) / 2.0
+              for s in (math.pi / 2, -math.pi / 2)]
+        _close(p1[0] - p1[1], math.cos(t), what="hybrid node shifted difference")
+
+
+def pin_shared_parameter(orc):
+    """The paper's compatibility example: H on every qubit, then RY(t) on every
+    qubit with ONE shared parameter. <Z_i> = -sin t for all i and
+    d/dt sum_i <Z_i> = -n cos t (every occurrence of the parameter adds up)."""
+    for n in (1, 3, 5):
+        gates = _arr([_g(W.H, q) for q in range(n)] +
+                     [_g(W.RY, q, -1, W.SRC_WEIGHT, 0) for q in range(n)])
+        for t in THETAS[::2]:
+            r = orc.run(n, gates, np.zeros((1, 0)), [t], grad_out=np.ones((1, n)))
+            _close(r["expz"][0], np.full(n, -math.sin(t)), what="shared <Z>")
+            _close(r["grad_weights"][0], -n * math.cos(t), what="shared grad")
+
+
+# --------------------------------------------------------------------------
+# two-qubit gates: truth tables and entanglement
+
+def _basis_prep(bits):
+    """RY(pi) on each set bit: maps |0> to |1> (a real rotation, no phase issue)."""
+    return [_g(W.RY, q, -1, W.SRC_INPUT, 0) for q, b in enumerate(bits) if b]
+
+
+def pin_cnot_truth_table(orc):
+    """CNOT(c, t) on every basis state of 3 qubits flips bit t iff bit c is 1."""
+    n = 3
+    for c in range(n):
+        for t in range(n):
+            if c == t:
+                continue
+            for v in range(1 << n):
+                bits = [(v >> q) & 1 for q in range(n)]
+                gates = _arr(_basis_prep(bits) + [_g(W.CNOT, c, t)])
+                r = orc.run(n, gates, [[math.pi]], [])
+                out = list(bits)
+                out[t] ^= bits[c]
+                _close(r["expz"][0], [1 - 2 * b for b in out], tol=1e-12,
+                       what=f"CNOT({c},{t}) on {bits}")
+
+
+def pin_cnot_chain_parity(orc):
+    """A linear CNOT chain (0,1), (1,2), ... writes prefix parities into each bit."""
+    n = 4
+    for v in range(1 << n):
+        bits = [(v >> q) & 1 for q in range(n)]
+        gates = _arr(_basis_prep(bits) + [_g(W.CNOT, q, q + 1) for q in range(n - 1)])
+        r = orc.run(n, gates, [[math.pi]], [])
+        pref = np.cumsum(bits) % 2
+        _close(r["expz"][0], 1 - 2 * pref, what=f"chain on {bits}")
+
+
+def pin_cz_kickback(orc):
+    """H(t) CZ(c, t) H(t) acts as CNOT(c, t) (truth table); CZ is symmetric."""
+    n = 2
+    for c, t in ((0, 1), (1, 0)):
+        for v in range(4):
+            bits = [(v >> q) & 1 for q in range(n)]
+            for a, b in ((c, t), (t, c)):
+                gates = _arr(_basis_prep(bits) + [_g(W.H, t), _g(W.CZ, a, b), _g(W.H, t)])
+                r = orc.run(n, gates, [[math.pi]], [])
+                out = list(bits)
+                out[t] ^= bits[c]
+                _close(r["expz"][0], [1 - 2 * x for x in out], what=f"CZ kickback {bits}")
+
+
+def pin_bell(orc):
+    """H(0) CNOT(0,1): (|00> + |11>)/sqrt2, so <Z0> = <Z1> = 0 and <Z0 Z1> = 1.
+    RY(t) on 0 then CNOT(0,1): <Z0> = <Z1> = cos t. RY(t) on the target only:
+    <Z0> = 1, <Z1> = cos t."""
+    r = orc.run(2, _arr([_g(W.H, 0), _g(W.CNOT, 0, 1)]), np.zeros((1, 0)), [], want_state=True)
+    _close(r["expz"][0], [0.0, 0.0], what="Bell <Z>")
+    psi = r["state"][0]
+    zz = np.sum(np.abs(psi) ** 2 * np.array([1, -1, -1, 1]))
+    _close(zz, 1.0, what="Bell <ZZ>")
+    _close(psi, np.array([1, 0, 0, 1]) / math.sqrt(2), what="Bell state")
+    for t in THETAS:
+        r = orc.run(2, _arr([_g(W.RY, 0, -1, W.SRC_WEIGHT, 0), _g(W.CNOT, 0, 1)]),
+                    np.zeros((1, 0)), [t])
+        _close(r["expz"][0], [math.cos(t)] * 2, what="RY then CNOT")
+        r = orc.run(2, _arr([_g(W.RY, 1, -1, W.SRC_WEIGHT, 0), _g(W.CNOT, 0, 1)]),
+                    np.zeros((1, 0)), [t])
+        _close(r["expz"][0], [1.0, math.cos(t)], what="target-only RY then CNOT")
+
+
+# --------------------------------------------------------------------------
+# brute force and invariants
+
+def _random_case(n, G, seed, B=2, F=3, P=4):
+    gates = W.random_circuit(n, G, F, P, seed)
+    x, w, g = W.random_inputs(B, F, P, n, seed + 1)
+    return gates, x, w, g
+
+
+def pin_brute_force(orc):
+    """Random circuits on 1..4 qubits over every gate kind: states, <Z_i> and VJP
+    gradients equal the dense Kronecker-product model within 1e-12."""
+    for n in (1, 2, 3, 4):
+        for seed in range(3):
+            gates, x, w, g = _random_case(n, 14, 1000 * n + seed)
+            r = orc.run(n, gates, x, w, grad_out=g, want_state=True)
+            b = brute.run(n, gates, x, w, grad_out=g)
+            _close(r["state"], b["state"], what=f"brute state n={n}")
+            _close(r["expz"], b["expz"], what=f"brute expz n={n}")
+            _close(r["grad_inputs"], b["grad_inputs"], what=f"brute grad_x n={n}")
+            _close(r["grad_weights"], b["grad_weights"], what=f"brute grad_w n={n}")
+
+
+def pin_unitarity(orc):
+    """Norm is preserved, un-applying every gate returns psi to |0...0>, and
+    lambda[0] at the end of the sweep equals sum_i g_i <Z_i> (because
+    <e0| U^dag O U |e0> = <O>)."""
+    for n in (3, 6):
+        gates, x, w, g = _random_case(n, 40, 77 + n, B=3)
+        r = orc.run(n, gates, x, w, grad_out=g, want_state=True, want_back=True)
+        _close(np.sum(np.abs(r["state"]) ** 2, axis=1), np.ones(3), what="norm")
+        e0 = np.zeros((3, 1 << n))
+        e0[:, 0] = 1
+        _close(r["back_psi"], e0, what="inverse sweep")
+        _close(r["back_lam0"], np.sum(g * r["expz"], axis=1), what="lambda_0[0]")
+
+
+def pin_param_shift(orc):
+    """Adjoint VJP equals the two-term parameter-shift rule (exact for
+    exp(-i t P / 2)), on random circuits and on the 4-qubit workload."""
+    for n, seed in ((3, 5), (5, 6)):
+        gates, x, w, g = _random_case(n, 30, seed)
+        r = orc.run(n, gates, x, w, grad_out=g)
+        gi, gw = orc.param_shift(n, gates, x, w, g)
+        _close(r["grad_inputs"], gi, tol=1e-12, what="shift grad_x")
+        _close(r["grad_weights"], gw, tol=1e-12, what="shift grad_w")
+    wl = W.get("4q")
+    x, w, g = wl.inputs()
+    r = orc.run(wl.n, wl.gates(), x, w, grad_out=g)
+    gi, gw = orc.param_shift(wl.n, wl.gates(), x, w, g)
+    _close(r["grad_inputs"], gi, what="4q shift grad_x")
+    _close(r["grad_weights"], gw, what="4q shift grad_w")
+
+
+def pin_finite_difference(orc):
+    """Central differences (h = 1e-5) of sum_i g_i <Z_i> match the VJP to ~1e-9."""
+    n = 4
+    gates, x, w, g = _random_case(n, 24, 31, B=2)
+    r = orc.run(n, gates, x, w, grad_out=g)
+    h = 1e-5
+
+    def f(xx, ww):
+        return float(np.sum(g * orc.run(n, gates, xx, ww)["expz"]))
+
+    for p in range(w.size):
+        wp, wm = w.astype(np.float64), w.astype(np.float64)
+        wp[p] += h
+        wm[p] -= h
+        _close((f(x, wp) - f(x, wm)) / (2 * h), r["grad_weights"][p], tol=1e-8, what="fd w")
+    for b in range(x.shape[0]):
+        for k in range(x.shape[1]):
+            xp, xm = x.astype(np.float64), x.astype(np.float64)
+            xp[b, k] += h
+            xm[b, k] -= h
+            # only sample b depends on x[b]; the other rows cancel
+            _close((f(xp, w) - f(xm, w)) / (2 * h), r["grad_inputs"][b, k], tol=1e-8, what="fd x")
+
+
+def pin_vjp_structure(orc):
+    """VJP is linear in grad_out; weight gradients add over the batch; one-hot
+    grad_out gives one Jacobian row."""
+    n = 4
+    gates, x, w, g = _random_case(n, 30, 41, B=3)
+    g2 = np.roll(g, 1, axis=1) * 0.7
+    r1 = orc.run(n, gates, x, w, grad_out=g)
+    r2 = orc.run(n, gates, x, w, grad_out=g2)
+    r12 = orc.run(n, gates, x, w, grad_out=2.0 * g - 3.0 * g2)
+    _close(r12["grad_weights"], 2 * r1["grad_weights"] - 3 * r2["grad_weights"], what="linear w")
+    _close(r12["grad_inputs"], 2 * r1["grad_inputs"] - 3 * r2["grad_inputs"], what="linear x")
+    acc = np.zeros_like(r1["grad_weights"])
+    for b in range(3):
+        rb = orc.run(n, gates, x[b:b + 1], w, grad_out=g[b:b + 1])
+        acc += rb["grad_weights"]
+        _close(rb["grad_inputs"][0], r1["grad_inputs"][b], what="per-sample x")
+        _close(rb["expz"][0], r1["expz"][b], what="per-sample expz")
+    _close(acc, r1["grad_weights"], what="batch additivity")
+    # Jacobian row q from a one-hot grad_out vs the brute-force derivative
+    for q in range(n):
+        oh = np.zeros((1, n))
+        oh[0, q] = 1.0
+        ro = orc.run(n, gates, x[:1], w, grad_out=oh)
+        bo = brute.run(n, gates, x[:1], w, grad_out=oh)
+        _close(ro["grad_weights"], bo["grad_weights"], what="jacobian row")
+
+
+# --------------------------------------------------------------------------
+# product states at larger n: SO(3) closed form per qubit
+
+def _so3(kind, t):
+    c, s = math.cos(t), math.sin(t)
+    if kind == W.RX:
+        return np.array([[1, 0, 0], [0, c, -s], [0, s, c]])
+    if kind == W.RY:
+        return np.array([[c, 0, s], [0, 1, 0], [-s, 0, c]])
+    if kind == W.RZ:
+        return np.array([[c, -s, 0], [s, c, 0], [0, 0, 1]])
+    if kind == W.H:  # x <-> z, y -> -y
+        return np.array([[0, 0, 1], [0, -1, 0], [1, 0, 0]], dtype=float)
+    raise ValueError(kind)
+
+
+def _so3_gen(kind):
+    return {W.RX: np.array([[0, 0, 0], [0, 0, -1], [0, 1, 0]]),
+            W.RY: np.array([[0, 0, 1], [0, 0, 0], [-1, 0, 0]]),
+            W.RZ: np.array([[0, -1, 0], [1, 0, 0], [0, 0, 0]])}[kind]
+
+
+def product_state_reference(n, gates, x_b, w, g_b):
+    """Closed form for circuits with no two-qubit gates: each qubit's Bloch
+    vector starts at (0,0,1) and is rotated by SO(3) matrices; <Z_q> is its z
+    component, and d<Z_q>/dt inserts the rotation generator at that gate."""
+    F, P = len(x_b), len(w)
+    expz = np.zeros(n)
+    gx = np.zeros(F)
+    gw = np.zeros(P)
+    for q in range(n):
+        seq = [(int(gg[0]), (x_b[gg[4]] if gg[3] == W.SRC_INPUT else w[gg[4]] if gg[3] == W.SRC_WEIGHT else 0.0),
+                int(gg[3]), int(gg[4])) for gg in gates if int(gg[1]) == q]
+        mats = [_so3(k, t) for k, t, _, _ in seq]
+        v = np.array([0.0, 0.0, 1.0])
+        for m in mats:
+            v = m @ v
+        expz[q] = v[2]
+        for i, (k, t, src, idx) in enumerate(seq):
+            if k == W.H:
+                continue
+            u = np.array([0.0, 0.0, 1.0])
+            for j, m in enumerate(mats):
+                u = (_so3_gen(k) @ m if j == i else m) @ u
+            if src == W.SRC_WEIGHT:
+                gw[idx] += g_b[q] * u[2]
+            else:
+                gx[idx] += g_b[q] * u[2]
+    return expz, gx, gw
+
+
+def pin_product_states(orc):
+    """Workload-shaped circuits with the entanglers removed (n = 8 and 11)
+    against the per-qubit SO(3) closed form."""
+    for name, n in (("24q", 8), ("16q", 11), ("10q", 9)):
+        wl = W.scaled(W.get(name), n=n, batch=2, layers=3, entangler=None, dtype="c128")
+        x, w, g = wl.inputs()
+        gates = wl.gates()
+        r = orc.run(n, gates, x, w, grad_out=g)
+        for b in range(2):
+            e, gx, gw = product_state_reference(n, gates, x[b], w, g[b])
+            _close(r["expz"][b], e, tol=1e-12, what=f"{name} product expz")
+            _close(r["grad_inputs"][b], gx, tol=1e-12, what=f"{name} product grad_x")
+        gw_all = sum(product_state_reference(n, gates, x[b], w, g[b])[2] for b in range(2))
+        _close(r["grad_weights"], gw_all, tol=1e-12, what=f"{name} product grad_w")
+
+
+def pin_cyclic_shift(orc):
+    """The ring-CZ workload family is symmetric under relabelling q -> q+1 mod n:
+    shifting features, per-qubit weights and grad_out shifts every output."""
+    n = 6
+    wl = W.scaled(W.get("16q"), n=n, batch=2, layers=2, dtype="c128")
+    x, w, g = wl.inputs()
+    gates = wl.gates()
+    R = len(wl.rotations)
+    r = orc.run(n, gates, x, w, grad_out=g)
+    xs = np.roll(x, 1, axis=1)
+    gs = np.roll(g, 1, axis=1)
+    ws = np.roll(w.reshape(wl.layers, n, R), 1, axis=1).reshape(-1)
+    rs = orc.run(n, gates, xs, ws, grad_out=gs)
+    _close(rs["expz"], np.roll(r["expz"], 1, axis=1), tol=1e-12, what="shift expz")
+    _close(rs["grad_inputs"], np.roll(r["grad_inputs"], 1, axis=1), tol=1e-12, what="shift gx")
+    _close(rs["grad_weights"],
+           np.roll(r["grad_weights"].reshape(wl.layers, n, R), 1, axis=1).reshape(-1),
+           tol=1e-12, what="shift gw")
+
+
+ALL_PINS = [
+    pin_rotations_on_zero, pin_rotation_axes, pin_h_rz_h, pin_hybrid_node,
+    pin_shared_parameter, pin_cnot_truth_table, pin_cnot_chain_parity, pin_cz_kickback,
+    pin_bell, pin_brute_force, pin_unitarity, pin_param_shift, pin_finite_difference,
+    pin_vjp_structure, pin_product_states, pin_cyclic_shift,
+]

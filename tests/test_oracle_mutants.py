@@ -1,0 +1,74 @@
+"""Plant plausible mistakes in copies of the oracle (CPU only) and check that the
+pin battery catches every one of them: evidence that the pins constrain each
+part of the oracle (gate matrices, orientation, expectation, adjoint sweep,
+gradient accumulation, parameter shift)."""
+
+import os
+import shutil
+
+import pytest
+
+import oracle
+import oracle_pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
+
+# (name, original text, replacement)
+MUTANTS = [
+    ("ry_sign", "m[1] = -s; m[2] = s;", "m[1] = s; m[2] = -s;"),
+    ("full_angle", "double c = cos(0.5 * theta), s = sin(0.5 * theta);",
+     "double c = cos(theta), s = sin(theta);"),
+    ("rx_sign", "m[1] = -I * s; m[2] = -I * s;", "m[1] = I * s; m[2] = I * s;"),
+    ("rz_phases_swapped", "m[0] = c - I * s; m[1] = 0; m[2] = 0; m[3] = c + I * s;",
+     "m[0] = c + I * s; m[1] = 0; m[2] = 0; m[3] = c - I * s;"),
+    ("h_sign", "m[2] = r; m[3] = -r;", "m[2] = -r; m[3] = r;"),
+    ("cnot_orientation", "const int64_t cb = (int64_t)1 << c, tb = (int64_t)1 << t;",
+     "const int64_t cb = (int64_t)1 << t, tb = (int64_t)1 << c;"),
+    ("cz_any_bit", "if ((j & ab) == ab) psi[j] = -psi[j];", "if (j & ab) psi[j] = -psi[j];"),
+    ("transposed_operand", "psi[j] = m[0] * a + m[1] * b;\n        psi[j | bit] = m[2] * a + m[3] * b;",
+     "psi[j] = m[0] * a + m[2] * b;\n        psi[j | bit] = m[1] * a + m[3] * b;"),
+    ("expect_sign", "return (j & c->bit) ? -p : p;", "return (j & c->bit) ? p : -p;"),
+    ("expect_wrong_qubit", "term_ctx c = { psi, NULL, (int64_t)1 << q, 0 };",
+     "term_ctx c = { psi, NULL, (int64_t)1 << (q ^ 1), 0 };"),
+    ("no_dagger", "if (dagger) { adjoint2(m, a);", "if (0) { adjoint2(m, a);"),
+    ("dagger_without_transpose", "a[0] = conj(m[0]); a[1] = conj(m[2]);\n    a[2] = conj(m[1]);",
+     "a[0] = conj(m[0]); a[1] = conj(m[1]);\n    a[2] = conj(m[2]);"),
+    ("re_instead_of_im", "return cimag(conj(c->lam[j]) * pj);", "return creal(conj(c->lam[j]) * pj);"),
+    ("y_generator_sign", "case G_RY: pj = (j & b) ? I * c->psi[j ^ b] : -I * c->psi[j ^ b]; break;",
+     "case G_RY: pj = (j & b) ? -I * c->psi[j ^ b] : I * c->psi[j ^ b]; break;"),
+    ("x_generator_as_z", "case G_RX: pj = c->psi[j ^ b]; break;", "case G_RX: pj = c->psi[j]; break;"),
+    ("seed_sign", "d += ((j >> q) & 1) ? -g_b[q] : g_b[q];", "d += ((j >> q) & 1) ? g_b[q] : -g_b[q];"),
+    ("shared_param_overwrite", "if (gk->src == SRC_WEIGHT) { if (grad_w) grad_w[gk->index] += v; }",
+     "if (gk->src == SRC_WEIGHT) { if (grad_w) grad_w[gk->index] = v; }"),
+    # psi one gate behind lambda in the inner product (un-applying both first
+    # would be equivalent: a rotation commutes with its own generator)
+    ("psi_lambda_misaligned",
+     "double v = im_inner(lam, psi, dim, gk->q0, gk->kind);",
+     "apply_gate(psi, dim, gk, th, 1);\n"
+     "                double v = im_inner(lam, psi, dim, gk->q0, gk->kind);\n"
+     "                apply_gate(psi, dim, gk, th, 0);"),
+    ("shift_without_half", "double d = 0.5 * (fp - fm);", "double d = (fp - fm);"),
+    ("lambda_not_unapplied", "            apply_gate(lam, dim, gk, th, 1);\n", "\n"),
+]
+
+
+@pytest.fixture(scope="module")
+def mutant_dir(tmp_path_factory):
+    return tmp_path_factory.mktemp("oracle_mutants")
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(mutant_dir, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    path = mutant_dir / f"{name}.c"
+    path.write_text(src.replace(old, new))
+    lib = oracle.compile_source(str(path), str(mutant_dir / f"lib{name}.so"))
+    orc = oracle.Oracle(lib)
+    caught = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin(orc)
+        except AssertionError:
+            caught.append(pin.__name__)
+    assert caught, f"mutant {name} passed every pin"
