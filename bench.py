@@ -1,0 +1,145 @@
+"""Benchmark: one fused forward + adjoint call of the batched quantum layer.
+
+A step is one ``ql_forward_backward`` call over one batch of synthetic inputs
+already resident in HBM: angle binding, every forward tile pass, the fused
+<Z>/seed/first-backward pass, every backward pass and the reductions. The
+metric is amplitude-gate updates per second, U = 3 * G * B * 2^n per step (the
+forward applies G gates to psi, the adjoint sweep un-applies G gates on psi and
+on lambda), plus the dominant kernel's achieved HBM bandwidth against the
+MI355X peak.
+
+Prints one JSON line. ``--gpus`` above 1 is not supported (one GPU holds the
+whole state; the batch/state sharding design is documented separately).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+METRIC = "amplitude-gate updates/s (batched fwd+adjoint grad); % of HBM peak BW"
+HBM_PEAK_GBS = 8000.0
+
+
+def cpu_baseline(wl, n_gates: int):
+    """The CPU oracle (complex128, all host threads) on a bounded sample of the
+    same workload: the first `n_gates` gates of the circuit at full size, one
+    sample, forward + adjoint."""
+    import oracle
+    x, w, g = wl.inputs()
+    gates = wl.gates()[:n_gates]
+    oracle.build()
+    t0 = time.perf_counter()
+    oracle.run(wl.n, gates, x[:1], w, grad_out=g[:1])
+    dt = time.perf_counter() - t0
+    upd = 3.0 * n_gates * (1 << wl.n)
+    return {"value": upd / dt, "unit": "amplitude-gate updates/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"first {n_gates} of {wl.n_gates} gates of {wl.name}, batch row 0 of "
+                      f"{wl.batch}, n={wl.n}, complex128, forward + adjoint; {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="30q", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--cpu-gates", type=int, default=8,
+                    help="gates in the CPU-oracle sample (0 disables it)")
+    ap.add_argument("--no-timing", action="store_true",
+                    help="time only the whole step (no per-kernel events)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: --gpus {args.gpus} is not supported; this build runs on one GPU "
+              "(every workload fits one MI355X).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2301_03251_amd as Q
+
+    wl = W.get(args.workload)
+    x, w, g = wl.inputs()
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    runner = Q.Runner(circ, wl.dtype)
+    real = torch.float32 if wl.dtype == "c64" else torch.float64
+    dev = torch.device("cuda")
+    xt = torch.from_numpy(x).to(dev, real)
+    wt = torch.from_numpy(w).to(dev, real)
+    gt = torch.from_numpy(g).to(dev, real)
+    outs = (torch.empty((wl.batch, wl.n), dtype=real, device=dev),
+            torch.empty((wl.batch, wl.n_inputs), dtype=real, device=dev),
+            torch.empty(wl.n_weights, dtype=real, device=dev))
+    runner.workspace(wl.batch, Q.MODE_FWD_BWD)
+
+    for _ in range(args.warmup):
+        runner.forward_backward(xt, wt, gt, outs=outs)
+    torch.cuda.synchronize()
+
+    timing = not args.no_timing
+    circ.timing(timing)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        runner.forward_backward(xt, wt, gt, outs=outs)
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / args.steps
+    kms, kcnt = circ.timing_read() if timing else ([0.0] * 4, [0] * 4)
+    circ.timing(False)
+
+    info = circ.plan_info(wl.dtype)
+    U = wl.updates()
+    line = {
+        "metric": METRIC,
+        "value": U / (ms_step / 1e3),
+        "unit": "amplitude-gate updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "n_qubits": wl.n, "batch": wl.batch,
+                   "gates": wl.n_gates, "weights": wl.n_weights,
+                   "updates_per_step": U, "tile_passes": info["n_passes"],
+                   "tile_qubits": info["tile_qubits"]},
+    }
+    if timing and kcnt[0] > 0:
+        tile_ms = kms[0] / args.steps
+        state_bytes = circ.state_bytes(wl.dtype, wl.batch)
+        achieved = state_bytes / (tile_ms / 1e3) / 1e9
+        line["roofline"] = {"bound": "hbm", "kernel": "k_tile", "achieved": achieved,
+                            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                            "traffic": None,
+                            "launches_per_step": kcnt[0] / args.steps,
+                            "kernel_ms_per_step": tile_ms,
+                            "algorithmic_bytes_per_step": state_bytes}
+        line["kernel_ms_per_step"] = {"k_tile": kms[0] / args.steps, "k_whole": kms[1] / args.steps,
+                                      "k_bind": kms[2] / args.steps, "k_reduce": kms[3] / args.steps}
+    elif timing and kcnt[1] > 0:
+        line["roofline"] = {"bound": "alu", "kernel": "k_whole", "achieved": None, "peak": None,
+                            "unit": None, "frac": None, "traffic": None,
+                            "kernel_ms_per_step": kms[1] / args.steps}
+    if args.cpu_gates > 0:
+        line["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_gates, wl.n_gates))
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

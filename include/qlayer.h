@@ -1,0 +1,177 @@
+/*
+ * qlayer.h -- C ABI of the batched quantum-layer library (HIP, gfx950).
+ *
+ * The library simulates a batch of parameterised quantum circuits on one
+ * GPU and returns what the paper's quantum node hands to the rest of a hybrid
+ * network (Sec. "Quantum Node"): the measured outputs in the forward pass and,
+ * for back-propagation (Sec. "Optimization", hybrid optimisation), the
+ * gradient of the loss with respect to the circuit parameters. The quantum
+ * node's backward returns the gradient multiplied by the upstream gradient
+ * (appendix, hybrid quantum-classical network, class Hybrid), i.e. a
+ * vector-Jacobian product. The angles of the rotation gates are bound either
+ * to input features (angle encoding, Sec. "Quantum Data") or to trainable
+ * weights shared by every sample of the batch.
+ *
+ * Conventions
+ *   - qubit q is bit q of the amplitude index; the initial state is |0...0>;
+ *   - H = [[1,1],[1,-1]]/sqrt(2); RX(t), RY(t), RZ(t) = exp(-i t P / 2) for
+ *     P = X, Y, Z; CNOT(q0 = control, q1 = target); CZ(q0, q1);
+ *   - expz[b][i] is the exact expectation <Z_i> of sample b (the limit of
+ *     infinitely many measurement shots), no renormalisation;
+ *   - grad_inputs[b][f]  = sum_i grad_out[b][i] d expz[b][i] / d inputs[b][f]
+ *     grad_weights[p]    = sum_b sum_i grad_out[b][i] d expz[b][i] / d weights[p]
+ *     (every occurrence of an input or weight in the gate list adds up);
+ *   - gradients are computed by adjoint differentiation (one reverse sweep
+ *     that un-applies the gates and accumulates Im<lambda|P|psi> per rotation).
+ *
+ * Precision: QL_C64 states are complex64 (fp32 real/imag), angles, grad_out
+ * and all outputs are fp32; QL_C128 uses complex128 and fp64 throughout.
+ * Every reduction (over amplitudes, workgroups and the batch) accumulates in
+ * fp64 in a fixed order, so results are bit-reproducible run to run.
+ *
+ * Memory: all array arguments of ql_forward / ql_forward_backward are DEVICE
+ * pointers on the current HIP device, row-major and contiguous, owned by the
+ * caller. The caller also provides the device workspace (size from
+ * ql_workspace_bytes). The library never allocates device memory in these
+ * calls; it only writes the workspace and the outputs. Outputs are
+ * overwritten (not accumulated). Buffers must not alias each other or the
+ * workspace.
+ *
+ * Errors: every function returns QL_OK (0) or a negative QL_E* code and sets a
+ * thread-local message readable with ql_last_error(). All argument checks
+ * happen before anything is launched. Calls are asynchronous on the given
+ * stream; results are valid once the stream has been synchronised. A circuit
+ * handle is immutable after creation and may be used from several threads and
+ * streams at once, each with its own workspace.
+ */
+#ifndef QLAYER_H
+#define QLAYER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Gate kinds. */
+enum { QL_H = 0, QL_RX = 1, QL_RY = 2, QL_RZ = 3, QL_CNOT = 4, QL_CZ = 5 };
+
+/* Where a rotation angle comes from: H/CNOT/CZ use QL_SRC_NONE; RX/RY/RZ use
+ * QL_SRC_INPUT (feature `index` of each sample) or QL_SRC_WEIGHT (trainable
+ * weight `index`). */
+enum { QL_SRC_NONE = 0, QL_SRC_INPUT = 1, QL_SRC_WEIGHT = 2 };
+
+/* One gate. One-qubit gates use q0 and set q1 = -1. */
+typedef struct {
+    int32_t kind, q0, q1, src, index;
+} ql_gate;
+
+typedef enum { QL_C64 = 0, QL_C128 = 1 } ql_dtype;
+
+enum { QL_MODE_FWD = 0, QL_MODE_FWD_BWD = 1 };
+
+enum {
+    QL_OK = 0,
+    QL_EINVAL = -1,       /* invalid argument (gate, index, pointer, size) */
+    QL_ENOMEM = -2,       /* workspace too small, size overflow, host allocation failed */
+    QL_EUNSUPPORTED = -3, /* too many qubits for this dtype or option out of range */
+    QL_EHIP = -4          /* HIP runtime error (message from hipGetErrorString) */
+};
+
+/* Largest qubit count per dtype. */
+#define QL_MAX_QUBITS_C64 32
+#define QL_MAX_QUBITS_C128 31
+
+/* Optional planning knobs; zero means "library default". They change how the
+ * work is split into kernel passes, never the results beyond fp rounding. */
+typedef struct {
+    int32_t log_regs;           /* amplitudes per thread = 2^log_regs (2..5) */
+    int32_t log_threads;        /* threads per workgroup = 2^log_threads (6..8) */
+    int32_t low_qubits;         /* qubits 0..low_qubits-1 are in every tile (1..8) */
+    int32_t max_gates_per_pass; /* cap on gates per tile pass (>= 1) */
+    int32_t force_tiled;        /* 1: never use the whole-state-in-LDS kernel */
+    int32_t wg_per_sample;      /* workgroups per sample in a tile pass */
+} ql_options;
+
+typedef struct ql_circuit ql_circuit; /* opaque */
+
+/* Validate the gate list and build the pass plans for both dtypes.
+ * n_qubits in [1, 32]; gates[n_gates] as above; n_inputs features per sample
+ * and n_weights trainable weights index the angle sources. The gate list is
+ * copied. Returns QL_EINVAL for a bad qubit, q0 == q1, a wrong source for the
+ * kind, an index out of range or a NULL pointer. */
+int ql_circuit_create(int32_t n_qubits, const ql_gate* gates, int32_t n_gates,
+                      int32_t n_inputs, int32_t n_weights, ql_circuit** out);
+
+/* Same with planning options (NULL = defaults). */
+int ql_circuit_create_ex(int32_t n_qubits, const ql_gate* gates, int32_t n_gates,
+                         int32_t n_inputs, int32_t n_weights, const ql_options* opts,
+                         ql_circuit** out);
+
+void ql_circuit_destroy(ql_circuit* c);
+
+/* Bytes of device workspace a call with this dtype, batch and mode needs. */
+int ql_workspace_bytes(const ql_circuit* c, ql_dtype dtype, int64_t batch, int mode,
+                       size_t* out);
+
+/* Forward: inputs[batch][n_inputs], weights[n_weights] -> expz[batch][n_qubits].
+ * inputs may be NULL when n_inputs == 0, weights when n_weights == 0. */
+int ql_forward(const ql_circuit* c, ql_dtype dtype, int64_t batch,
+               const void* inputs, const void* weights, void* expz,
+               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Forward + adjoint VJP. grad_out[batch][n_qubits] is the upstream gradient;
+ * grad_inputs[batch][n_inputs] and grad_weights[n_weights] may each be NULL
+ * (not computed). expz is written as in ql_forward. */
+int ql_forward_backward(const ql_circuit* c, ql_dtype dtype, int64_t batch,
+                        const void* inputs, const void* weights, const void* grad_out,
+                        void* expz, void* grad_inputs, void* grad_weights,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* ql_last_error(void);
+
+/* ---- introspection (host only, no GPU needed) ---------------------------- */
+
+typedef struct {
+    int32_t kernel;        /* 0 = whole state in LDS (one workgroup per sample), 1 = tile passes */
+    int32_t n_passes;      /* forward tile passes (1 for the whole-state kernel) */
+    int32_t tile_qubits;   /* qubits per tile (log2 amplitudes per workgroup tile) */
+    int32_t log_regs;      /* amplitudes per thread = 2^log_regs */
+    int32_t log_threads;   /* threads per workgroup = 2^log_threads */
+    int32_t low_qubits;    /* contiguous low qubits in every tile */
+    int32_t n_transposes;  /* LDS layout changes summed over the forward passes */
+    int32_t n_param_gates; /* rotation gates (gradient slots) */
+} ql_plan_info;
+
+int ql_plan_info_get(const ql_circuit* c, ql_dtype dtype, ql_plan_info* out);
+
+/* Forward schedule: pass_of_gate[n_gates] receives the pass that applies each
+ * gate, order[n_gates] the gate indices in execution order (pass by pass). */
+int ql_plan_schedule(const ql_circuit* c, ql_dtype dtype, int32_t* pass_of_gate,
+                     int32_t* order);
+
+/* Algorithmic HBM bytes of the state passes of one call (reads + writes of
+ * psi and lambda by the tile kernel; 0 for the whole-state kernel). */
+int ql_plan_state_bytes(const ql_circuit* c, ql_dtype dtype, int64_t batch, int mode,
+                        double* out);
+
+/* ---- timing (for benchmarks) --------------------------------------------- */
+
+/* When enabled on a handle, every kernel launch of a call is bracketed by HIP
+ * events on the call's stream; ql_timing_read synchronises on the last event
+ * and returns the summed milliseconds per kernel class:
+ * ms[0] tile passes, ms[1] whole-state kernel, ms[2] angle binding,
+ * ms[3] reductions; launches[0..3] the launch counts. Reading resets them.
+ * Not thread-safe: one timed call in flight per handle. */
+int ql_timing_enable(ql_circuit* c, int enable);
+int ql_timing_read(ql_circuit* c, double ms[4], int32_t launches[4]);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QLAYER_H */

@@ -1,0 +1,9 @@
+"""Batched quantum-layer simulation on MI355X (gfx950): forward <Z_i> and adjoint
+VJP gradients of parameterised circuits, in hand-written HIP kernels behind a
+C ABI (``include/qlayer.h``). See ``qlayer.py`` for the Python binding."""
+
+from .qlayer import (C64, C128, MODE_FWD, MODE_FWD_BWD, Circuit, QLError, Runner,  # noqa: F401
+                     load, quantum_layer_function)
+
+__all__ = ["C64", "C128", "MODE_FWD", "MODE_FWD_BWD", "Circuit", "QLError", "Runner", "load",
+           "quantum_layer_function"]

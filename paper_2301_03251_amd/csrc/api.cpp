@@ -1,0 +1,533 @@
+// api.cpp -- the C ABI (qlayer.h): validation, workspace layout, launch order.
+//
+// One call = angle binding, then either one whole-state launch (small n) or
+// the forward tile passes, a fused pass (last forward pass + <Z> partials +
+// lambda seed + first backward pass), the remaining backward passes in reverse
+// order, and the final reductions -- all on the caller's stream, no host
+// synchronisation, no device allocation.
+#include "qlayer.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "launch.hpp"
+#include "plan.hpp"
+
+using namespace qlayer;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Device tables of one dtype's plan, packed into one blob that each call
+// copies into the head of the workspace.
+struct Tables {
+    std::vector<uint8_t> blob;
+    size_t off_pass = 0, off_phase = 0, off_ops = 0, off_gslot = 0, off_slots = 0;
+    size_t off_xptr = 0, off_xslot = 0, off_wptr = 0, off_wslot = 0, off_gates = 0;
+    std::vector<DevPass> passes;
+};
+
+template <typename T>
+size_t put(std::vector<uint8_t>& blob, const std::vector<T>& v) {
+    size_t off = align256(blob.size());
+    blob.resize(off + std::max<size_t>(sizeof(T) * v.size(), 16), 0);
+    if (!v.empty()) std::memcpy(blob.data() + off, v.data(), sizeof(T) * v.size());
+    return off;
+}
+
+void build_tables(const Circuit& c, int dt, Tables& T) {
+    const Plan& pl = c.plan[dt];
+    std::vector<DevPass> passes;
+    std::vector<DevOp> ops;
+    std::vector<int32_t> gsl;
+    if (!pl.whole_state) {
+        for (const PassPlan& pp : pl.passes) {
+            DevPass d{};
+            d.k = pl.k;
+            d.log_t = pl.log_t;
+            uint64_t in_tile = 0;
+            for (int j = 0; j < pl.k; j++) {
+                d.tile_qubit[j] = pp.qubits[j];
+                in_tile |= 1ull << pp.qubits[j];
+            }
+            for (int q = 0; q < c.n; q++)
+                if (!(in_tile >> q & 1)) d.fixed_qubit[d.n_fixed++] = q;
+            d.fwd_begin = (int)ops.size();
+            ops.insert(ops.end(), pp.fwd_ops.begin(), pp.fwd_ops.end());
+            d.fwd_end = (int)ops.size();
+            d.bwd_begin = (int)ops.size();
+            ops.insert(ops.end(), pp.bwd_ops.begin(), pp.bwd_ops.end());
+            d.bwd_end = (int)ops.size();
+            d.load_phase = pp.first_phase;
+            d.bwd_phase = pp.last_phase;
+            d.gslot_base = (int)gsl.size();
+            gsl.insert(gsl.end(), pp.gslots.begin(), pp.gslots.end());
+            d.n_gslots = (int)pp.gslots.size();
+            d.n_exchanges = pp.n_transposes;
+            passes.push_back(d);
+        }
+    }
+    std::vector<SlotSrc> slots;
+    for (int gi : c.slot_gate) slots.push_back({c.gates[gi].src, c.gates[gi].index});
+    std::vector<int32_t> xptr(c.n_inputs + 1, 0), wptr(c.n_weights + 1, 0), xs, ws;
+    for (int f = 0; f < c.n_inputs; f++) {
+        for (int s = 0; s < (int)slots.size(); s++)
+            if (slots[s].src == S_INPUT && slots[s].index == f) xs.push_back(s);
+        xptr[f + 1] = (int)xs.size();
+    }
+    for (int p = 0; p < c.n_weights; p++) {
+        for (int s = 0; s < (int)slots.size(); s++)
+            if (slots[s].src == S_WEIGHT && slots[s].index == p) ws.push_back(s);
+        wptr[p + 1] = (int)ws.size();
+    }
+    std::vector<DevGate> gates;
+    for (const Gate& g : c.gates) gates.push_back({g.kind, g.q0, g.q1, g.slot});
+
+    T.blob.clear();
+    T.off_pass = put(T.blob, passes);
+    T.off_phase = put(T.blob, pl.phases);
+    T.off_ops = put(T.blob, ops);
+    T.off_gslot = put(T.blob, gsl);
+    T.off_slots = put(T.blob, slots);
+    T.off_xptr = put(T.blob, xptr);
+    T.off_xslot = put(T.blob, xs);
+    T.off_wptr = put(T.blob, wptr);
+    T.off_wslot = put(T.blob, ws);
+    T.off_gates = put(T.blob, gates);
+    T.blob.resize(align256(T.blob.size()), 0);
+    T.passes = passes;
+}
+
+struct Layout {
+    size_t tables = 0, coef = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
+    int n_wg = 1;
+};
+
+bool mul_ok(size_t a, size_t b, size_t& out) {
+    if (a != 0 && b > SIZE_MAX / a) return false;
+    out = a * b;
+    return true;
+}
+
+}  // namespace
+
+struct ql_circuit {
+    Circuit c;
+    Tables t[2];
+    // timing
+    int timing = 0;
+    struct Ev {
+        hipEvent_t a, b;
+        int cls;
+    };
+    std::vector<Ev> ev;
+    size_t ev_used = 0;
+};
+
+namespace {
+
+int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L) {
+    const Circuit& c = h->c;
+    const Plan& pl = c.plan[dt];
+    const size_t amp = dt == 0 ? 8 : 16;
+    if (B < 1) return fail(QL_EINVAL, "batch must be >= 1");
+    if (B > (int64_t)1 << 30) return fail(QL_EINVAL, "batch too large");
+    const int maxq = dt == 0 ? QL_MAX_QUBITS_C64 : QL_MAX_QUBITS_C128;
+    if (c.n > maxq) return fail(QL_EUNSUPPORTED, "too many qubits for this dtype");
+    L = Layout{};
+    if (pl.whole_state) {
+        L.n_wg = 1;
+    } else {
+        const int64_t tiles = (int64_t)1 << (c.n - pl.k);
+        int64_t nwg = c.opts.wg_per_sample ? c.opts.wg_per_sample : (2048 + B - 1) / B;
+        nwg = std::max<int64_t>(1, std::min<int64_t>(nwg, tiles));
+        if (nwg * B > (int64_t)INT32_MAX) return fail(QL_ENOMEM, "grid too large");
+        L.n_wg = (int)nwg;
+    }
+    const bool bwd = mode == QL_MODE_FWD_BWD;
+    size_t off = 0, sz = 0;
+    L.tables = off;
+    off = align256(off + h->t[dt].blob.size());
+    L.coef = off;
+    if (!mul_ok((size_t)B * (size_t)std::max(1, (int)c.slot_gate.size()), amp, sz)) return fail(QL_ENOMEM, "size overflow");
+    off = align256(off + sz);
+    L.zpart = off;
+    if (!mul_ok((size_t)B * (size_t)L.n_wg, (size_t)c.n * 8, sz)) return fail(QL_ENOMEM, "size overflow");
+    off = align256(off + sz);
+    if (bwd) {
+        L.gpart = off;
+        if (!mul_ok((size_t)B * (size_t)L.n_wg, (size_t)std::max(1, (int)c.slot_gate.size()) * 8, sz))
+            return fail(QL_ENOMEM, "size overflow");
+        off = align256(off + sz);
+    }
+    if (!pl.whole_state && pl.passes.size() > 1) {
+        size_t st;
+        if (!mul_ok((size_t)B, ((size_t)1 << c.n) * amp, st)) return fail(QL_ENOMEM, "size overflow");
+        L.psi = off;
+        off = align256(off + st);
+        if (bwd) {
+            L.lam = off;
+            off = align256(off + st);
+        }
+    }
+    L.total = off;
+    return QL_OK;
+}
+
+std::mutex g_dev_mu;
+std::set<int> g_dev_ready;
+size_t g_lds_limit = 65536;
+
+int ensure_device() {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(QL_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    if (g_dev_ready.count(dev)) return QL_OK;
+    int optin = 0;
+    if (hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) != hipSuccess || optin <= 0)
+        optin = 65536;
+    e = configure_kernels((size_t)optin);
+    if (e != hipSuccess) return fail(QL_EHIP, std::string("hipFuncSetAttribute: ") + hipGetErrorString(e));
+    g_lds_limit = (size_t)optin;
+    g_dev_ready.insert(dev);
+    return QL_OK;
+}
+
+struct Timer {
+    ql_circuit* h;
+    hipStream_t s;
+    int cls = 0;
+    void start(int c) {
+        cls = c;
+        if (!h->timing) return;
+        if (h->ev_used == h->ev.size()) {
+            ql_circuit::Ev e{};
+            if (hipEventCreate(&e.a) != hipSuccess || hipEventCreate(&e.b) != hipSuccess) return;
+            h->ev.push_back(e);
+        }
+        h->ev[h->ev_used].cls = c;
+        (void)hipEventRecord(h->ev[h->ev_used].a, s);
+    }
+    void stop() {
+        if (!h->timing || h->ev_used >= h->ev.size()) return;
+        (void)hipEventRecord(h->ev[h->ev_used].b, s);
+        h->ev_used++;
+    }
+};
+
+int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* inputs,
+        const void* weights, const void* grad_out, void* expz, void* grad_inputs,
+        void* grad_weights, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (!hc) return fail(QL_EINVAL, "circuit is NULL");
+    ql_circuit* h = const_cast<ql_circuit*>(hc);  // only the timing state is touched
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    const int dt = (int)dtype;
+    const Circuit& c = h->c;
+    const Plan& pl = c.plan[dt];
+    const Tables& T = h->t[dt];
+    const bool bwd = mode == QL_MODE_FWD_BWD;
+    Layout L;
+    int rc = compute_layout(h, dt, B, mode, L);
+    if (rc) return rc;
+    if (!expz) return fail(QL_EINVAL, "expz is NULL");
+    if (c.n_inputs > 0 && !inputs) return fail(QL_EINVAL, "inputs is NULL");
+    if (c.n_weights > 0 && !weights) return fail(QL_EINVAL, "weights is NULL");
+    if (bwd && !grad_out) return fail(QL_EINVAL, "grad_out is NULL");
+    if (!ws) return fail(QL_EINVAL, "workspace is NULL");
+    if (ws_bytes < L.total)
+        return fail(QL_ENOMEM, "workspace too small: need " + std::to_string(L.total) + " bytes, got " +
+                                   std::to_string(ws_bytes));
+    rc = ensure_device();
+    if (rc) return rc;
+
+    const size_t amp = dt == 0 ? 8 : 16;
+    uint8_t* W = (uint8_t*)ws;
+    const int n_slots = (int)c.slot_gate.size();
+    hipError_t e = hipMemcpyAsync(W + L.tables, T.blob.data(), T.blob.size(), hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return fail(QL_EHIP, std::string("table upload: ") + hipGetErrorString(e));
+    Timer tm{h, stream};
+
+    BindArgs ba{};
+    ba.inputs = inputs;
+    ba.weights = weights;
+    ba.slots = (const SlotSrc*)(W + L.tables + T.off_slots);
+    ba.coef = W + L.coef;
+    ba.B = B;
+    ba.n_slots = n_slots;
+    ba.F = c.n_inputs;
+    tm.start(2);
+    e = launch_bind(dt, ba, stream);
+    tm.stop();
+    if (e != hipSuccess) return fail(QL_EHIP, std::string("k_bind: ") + hipGetErrorString(e));
+
+    double* zpart = (double*)(W + L.zpart);
+    double* gpart = bwd ? (double*)(W + L.gpart) : nullptr;
+    if (pl.whole_state) {
+        WholeArgs wa{};
+        wa.gates = (const DevGate*)(W + L.tables + T.off_gates);
+        wa.n_gates = (int)c.gates.size();
+        wa.n = c.n;
+        wa.n_slots = n_slots;
+        wa.bwd = bwd ? 1 : 0;
+        wa.B = B;
+        wa.coef = W + L.coef;
+        wa.grad_out = grad_out;
+        wa.zpart = zpart;
+        wa.gpart = gpart;
+        const int dim = 1 << c.n;
+        const int threads = std::max(64, std::min(256, dim / 4));
+        const size_t lds = 2 * (size_t)dim * amp + (size_t)c.n * (threads / 64) * 8 + 64;
+        if (lds > g_lds_limit) return fail(QL_EUNSUPPORTED, "state does not fit in LDS");
+        tm.start(1);
+        e = launch_whole(dt, wa, threads, lds, stream);
+        tm.stop();
+        if (e != hipSuccess) return fail(QL_EHIP, std::string("k_whole: ") + hipGetErrorString(e));
+    } else {
+        const int m = (int)pl.passes.size();
+        const int threads = 1 << pl.log_t;
+        const int NW = threads / 64;
+        auto launch_pass = [&](int p, int flags) -> int {
+            const DevPass& d = T.passes[p];
+            TileArgs ta{};
+            ta.psi = L.psi ? (void*)(W + L.psi) : nullptr;
+            ta.lam = L.lam ? (void*)(W + L.lam) : nullptr;
+            ta.pass = (const DevPass*)(W + L.tables + T.off_pass) + p;
+            ta.phases = (const DevPhase*)(W + L.tables + T.off_phase);
+            ta.ops = (const DevOp*)(W + L.tables + T.off_ops);
+            ta.gslots = (const int32_t*)(W + L.tables + T.off_gslot) + d.gslot_base;
+            ta.coef = W + L.coef;
+            ta.grad_out = grad_out;
+            ta.zpart = zpart;
+            ta.gpart = gpart;
+            ta.B = B;
+            ta.tiles = (int64_t)1 << (c.n - pl.k);
+            ta.n = c.n;
+            ta.n_slots = n_slots;
+            ta.n_wg = L.n_wg;
+            ta.flags = flags;
+            ta.n_gslots = (flags & PF_BWD) ? d.n_gslots : 0;
+            ta.lds_tile_bytes = d.n_exchanges > 0 ? (int)(((size_t)1 << pl.k) * amp) : 0;
+            const size_t lds = (size_t)ta.lds_tile_bytes + (size_t)(c.n + ta.n_gslots) * NW * 8;
+            if (lds > g_lds_limit) return fail(QL_EUNSUPPORTED, "tile pass needs more LDS than available");
+            tm.start(0);
+            hipError_t le = launch_tile(dt, pl.log_r, (flags & PF_BWD) != 0, ta, threads, lds, stream);
+            tm.stop();
+            if (le != hipSuccess) return fail(QL_EHIP, std::string("k_tile: ") + hipGetErrorString(le));
+            return QL_OK;
+        };
+        for (int p = 0; p + 1 < m; p++) {
+            rc = launch_pass(p, (p == 0 ? PF_INIT : 0) | PF_FWD | PF_STORE_PSI);
+            if (rc) return rc;
+        }
+        int last = (m == 1 ? PF_INIT : 0) | PF_FWD | PF_ZPART;
+        if (bwd) last |= PF_SEED | PF_BWD | (m > 1 ? (PF_STORE_PSI | PF_STORE_LAM) : 0);
+        rc = launch_pass(m - 1, last);
+        if (rc) return rc;
+        if (bwd)
+            for (int p = m - 2; p >= 0; p--) {
+                rc = launch_pass(p, PF_LOAD_LAM | PF_BWD | (p > 0 ? (PF_STORE_PSI | PF_STORE_LAM) : 0));
+                if (rc) return rc;
+            }
+    }
+
+    ReduceArgs ra{};
+    ra.zpart = zpart;
+    ra.gpart = gpart;
+    ra.expz = expz;
+    ra.grad_inputs = grad_inputs;
+    ra.grad_weights = grad_weights;
+    ra.x_ptr = (const int32_t*)(W + L.tables + T.off_xptr);
+    ra.x_slot = (const int32_t*)(W + L.tables + T.off_xslot);
+    ra.w_ptr = (const int32_t*)(W + L.tables + T.off_wptr);
+    ra.w_slot = (const int32_t*)(W + L.tables + T.off_wslot);
+    ra.B = B;
+    ra.n = c.n;
+    ra.n_wg = L.n_wg;
+    ra.F = c.n_inputs;
+    ra.P = c.n_weights;
+    ra.n_slots = n_slots;
+    ra.grads = bwd ? 1 : 0;
+    tm.start(3);
+    e = launch_reduce(dt, ra, stream);
+    tm.stop();
+    if (e != hipSuccess) return fail(QL_EHIP, std::string("k_reduce: ") + hipGetErrorString(e));
+    return QL_OK;
+}
+
+Options to_options(const ql_options* o) {
+    Options r;
+    if (o) {
+        r.log_regs = o->log_regs;
+        r.log_threads = o->log_threads;
+        r.low_qubits = o->low_qubits;
+        r.max_gates_per_pass = o->max_gates_per_pass;
+        r.force_tiled = o->force_tiled;
+        r.wg_per_sample = o->wg_per_sample;
+    }
+    return r;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ql_circuit_create_ex(int32_t n_qubits, const ql_gate* gates, int32_t n_gates, int32_t n_inputs,
+                         int32_t n_weights, const ql_options* opts, ql_circuit** out) {
+    if (!out) return fail(QL_EINVAL, "out is NULL");
+    *out = nullptr;
+    static_assert(sizeof(ql_gate) == 5 * sizeof(int32_t), "ql_gate layout");
+    ql_circuit* h = new (std::nothrow) ql_circuit();
+    if (!h) return fail(QL_ENOMEM, "host allocation failed");
+    std::string err;
+    try {
+        err = build_circuit(n_qubits, (const int32_t*)gates, n_gates, n_inputs, n_weights,
+                            to_options(opts), h->c);
+        if (err.empty())
+            for (int dt = 0; dt < 2; dt++) build_tables(h->c, dt, h->t[dt]);
+    } catch (const std::bad_alloc&) {
+        delete h;
+        return fail(QL_ENOMEM, "host allocation failed");
+    }
+    if (!err.empty()) {
+        delete h;
+        return fail(err.compare(0, 7, "option:") == 0 ? QL_EUNSUPPORTED : QL_EINVAL, err);
+    }
+    *out = h;
+    g_err.clear();
+    return QL_OK;
+}
+
+int ql_circuit_create(int32_t n_qubits, const ql_gate* gates, int32_t n_gates, int32_t n_inputs,
+                      int32_t n_weights, ql_circuit** out) {
+    return ql_circuit_create_ex(n_qubits, gates, n_gates, n_inputs, n_weights, nullptr, out);
+}
+
+void ql_circuit_destroy(ql_circuit* h) {
+    if (!h) return;
+    for (auto& e : h->ev) {
+        (void)hipEventDestroy(e.a);
+        (void)hipEventDestroy(e.b);
+    }
+    delete h;
+}
+
+int ql_workspace_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, int mode, size_t* out) {
+    if (!h || !out) return fail(QL_EINVAL, "NULL argument");
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    if (mode != QL_MODE_FWD && mode != QL_MODE_FWD_BWD) return fail(QL_EINVAL, "unknown mode");
+    Layout L;
+    int rc = compute_layout(h, (int)dtype, batch, mode, L);
+    if (rc) return rc;
+    *out = L.total;
+    return QL_OK;
+}
+
+int ql_forward(const ql_circuit* h, ql_dtype dtype, int64_t batch, const void* inputs,
+               const void* weights, void* expz, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int rc = run(h, dtype, batch, QL_MODE_FWD, inputs, weights, nullptr, expz, nullptr, nullptr, ws,
+                 ws_bytes, stream);
+    if (rc == QL_OK) g_err.clear();
+    return rc;
+}
+
+int ql_forward_backward(const ql_circuit* h, ql_dtype dtype, int64_t batch, const void* inputs,
+                        const void* weights, const void* grad_out, void* expz, void* grad_inputs,
+                        void* grad_weights, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int rc = run(h, dtype, batch, QL_MODE_FWD_BWD, inputs, weights, grad_out, expz, grad_inputs,
+                 grad_weights, ws, ws_bytes, stream);
+    if (rc == QL_OK) g_err.clear();
+    return rc;
+}
+
+const char* ql_last_error(void) { return g_err.c_str(); }
+
+int ql_plan_info_get(const ql_circuit* h, ql_dtype dtype, ql_plan_info* out) {
+    if (!h || !out) return fail(QL_EINVAL, "NULL argument");
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    const Plan& pl = h->c.plan[(int)dtype];
+    ql_plan_info r{};
+    r.kernel = pl.whole_state ? 0 : 1;
+    r.n_passes = (int)pl.passes.size();
+    r.tile_qubits = pl.k;
+    r.log_regs = pl.log_r;
+    r.log_threads = pl.log_t;
+    r.low_qubits = pl.low;
+    for (const auto& pp : pl.passes) r.n_transposes += pp.n_transposes;
+    r.n_param_gates = (int)h->c.slot_gate.size();
+    *out = r;
+    return QL_OK;
+}
+
+int ql_plan_schedule(const ql_circuit* h, ql_dtype dtype, int32_t* pass_of_gate, int32_t* order) {
+    if (!h || !pass_of_gate || !order) return fail(QL_EINVAL, "NULL argument");
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    const Plan& pl = h->c.plan[(int)dtype];
+    const int G = (int)h->c.gates.size();
+    for (int i = 0; i < G; i++) pass_of_gate[i] = -1;
+    int k = 0;
+    for (int p = 0; p < (int)pl.passes.size(); p++)
+        for (int gi : pl.passes[p].gates) {
+            if (k < G) order[k] = gi;
+            k++;
+            pass_of_gate[gi] = p;
+        }
+    return k == G ? QL_OK : fail(QL_EINVAL, "schedule size mismatch");
+}
+
+int ql_plan_state_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, int mode, double* out) {
+    if (!h || !out) return fail(QL_EINVAL, "NULL argument");
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    const Plan& pl = h->c.plan[(int)dtype];
+    const double S = (double)batch * (double)((size_t)1 << h->c.n) * (dtype == QL_C64 ? 8.0 : 16.0);
+    const int m = (int)pl.passes.size();
+    double units = 0;
+    if (!pl.whole_state && m > 1) units = mode == QL_MODE_FWD_BWD ? 6.0 * m - 6.0 : 2.0 * m - 2.0;
+    *out = units * S;
+    return QL_OK;
+}
+
+int ql_timing_enable(ql_circuit* h, int enable) {
+    if (!h) return fail(QL_EINVAL, "NULL argument");
+    h->timing = enable ? 1 : 0;
+    h->ev_used = 0;
+    return QL_OK;
+}
+
+int ql_timing_read(ql_circuit* h, double ms[4], int32_t launches[4]) {
+    if (!h || !ms || !launches) return fail(QL_EINVAL, "NULL argument");
+    for (int i = 0; i < 4; i++) {
+        ms[i] = 0;
+        launches[i] = 0;
+    }
+    if (h->ev_used > 0) {
+        hipError_t e = hipEventSynchronize(h->ev[h->ev_used - 1].b);
+        if (e != hipSuccess) return fail(QL_EHIP, std::string("hipEventSynchronize: ") + hipGetErrorString(e));
+    }
+    for (size_t i = 0; i < h->ev_used; i++) {
+        float t = 0;
+        if (hipEventElapsedTime(&t, h->ev[i].a, h->ev[i].b) == hipSuccess) {
+            ms[h->ev[i].cls] += t;
+            launches[h->ev[i].cls]++;
+        }
+    }
+    h->ev_used = 0;
+    return QL_OK;
+}
+
+}  // extern "C"

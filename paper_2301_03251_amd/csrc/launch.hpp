@@ -1,0 +1,85 @@
+// launch.hpp -- host-side launchers of the HIP kernels (kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+#include "plan.hpp"
+
+namespace qlayer {
+
+// Rotation slot -> (src, index); one row per slot.
+struct SlotSrc {
+    int32_t src, index;
+};
+
+// Whole-state (one workgroup per sample, state in LDS) gate entry.
+struct DevGate {
+    int32_t kind, q0, q1, slot;
+};
+
+struct BindArgs {
+    const void* inputs;   // [B][F] Real
+    const void* weights;  // [P] Real
+    const SlotSrc* slots; // [n_slots]
+    void* coef;           // [B][n_slots] complex (cos, sin) of theta/2
+    int64_t B;
+    int32_t n_slots, F;
+};
+
+struct WholeArgs {
+    const DevGate* gates;
+    int32_t n_gates, n, n_slots;
+    int32_t bwd;          // 1: run the adjoint sweep
+    int64_t B;
+    const void* coef;     // [B][n_slots]
+    const void* grad_out; // [B][n] Real
+    double* zpart;        // [B][n]           (one workgroup per sample)
+    double* gpart;        // [n_slots][B]
+};
+
+struct TileArgs {
+    void* psi;                 // [B][2^n] complex
+    void* lam;                 // [B][2^n] complex
+    const DevPass* pass;
+    const DevPhase* phases;
+    const DevOp* ops;
+    const int32_t* gslots;     // pass-local gradient index -> rotation slot
+    const void* coef;          // [B][n_slots]
+    const void* grad_out;      // [B][n] Real
+    double* zpart;             // [B][n_wg][n]
+    double* gpart;             // [n_slots][B][n_wg]
+    int64_t B;
+    int64_t tiles;             // tiles per sample = 2^(n-k)
+    int32_t n, n_slots, n_wg, flags;
+    int32_t n_gslots;          // gradient accumulators of this pass
+    int32_t lds_tile_bytes;    // 0 when the pass needs no LDS exchange
+};
+
+struct ReduceArgs {
+    const double* zpart;   // [B][n_wg][n]
+    const double* gpart;   // [n_slots][B][n_wg]
+    void* expz;            // [B][n] Real
+    void* grad_inputs;     // [B][F] Real or null
+    void* grad_weights;    // [P] Real or null
+    const int32_t* x_ptr;  // [F+1] CSR: rotation slots bound to input f
+    const int32_t* x_slot;
+    const int32_t* w_ptr;  // [P+1] CSR: rotation slots bound to weight p
+    const int32_t* w_slot;
+    int64_t B;
+    int32_t n, n_wg, F, P, n_slots;
+    int32_t grads;         // 1: reduce gradients too
+};
+
+// dtype: 0 = complex64 / fp32, 1 = complex128 / fp64. Return hipError_t.
+hipError_t launch_bind(int dtype, const BindArgs& a, hipStream_t s);
+hipError_t launch_whole(int dtype, const WholeArgs& a, int threads, size_t lds, hipStream_t s);
+hipError_t launch_tile(int dtype, int log_r, bool bwd, const TileArgs& a, int threads, size_t lds,
+                       hipStream_t s);
+hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s);
+
+// Raise the dynamic-LDS limit of every kernel on the current device.
+hipError_t configure_kernels(size_t max_lds);
+
+}  // namespace qlayer

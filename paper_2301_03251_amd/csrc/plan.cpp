@@ -1,0 +1,346 @@
+// plan.cpp -- circuit validation and the tile-pass planner (host C++, no HIP).
+#include "plan.hpp"
+
+#include <algorithm>
+#include <cstdio>
+
+namespace qlayer {
+
+namespace {
+
+std::string fmt(const char* f, long a = 0, long b = 0, long c = 0) {
+    char buf[256];
+    std::snprintf(buf, sizeof buf, f, a, b, c);
+    return buf;
+}
+
+bool is_rotation(int kind) { return kind == K_RX || kind == K_RY || kind == K_RZ; }
+
+// Tile qubit a gate must hold in the tile (-1: none; diagonal gates and CNOT
+// controls can be fixed bits of the tile).
+int needed_tile_qubit(const Gate& g) {
+    switch (g.kind) {
+        case K_H: case K_RX: case K_RY: return g.q0;
+        case K_CNOT: return g.q1;
+        default: return -1;
+    }
+}
+
+int n_qubits_of(const Gate& g) { return (g.kind == K_CNOT || g.kind == K_CZ) ? 2 : 1; }
+
+// Greedy scan of the not-yet-scheduled gates for a candidate tile qubit set.
+// `tile` (a bitmask over qubits) may grow up to `cap` qubits when `grow`.
+// Returns the executed gate indices in order. A skipped gate blocks its
+// qubits, so every executed gate only commutes past skipped gates acting on
+// other qubits.
+std::vector<int> scan(const std::vector<Gate>& gates, const std::vector<char>& done,
+                      uint64_t& tile, int cap, bool grow, int max_gates) {
+    std::vector<int> exec;
+    uint64_t blocked = 0;
+    int count = __builtin_popcountll(tile);
+    for (int i = 0; i < (int)gates.size(); i++) {
+        if (done[i]) continue;
+        const Gate& g = gates[i];
+        uint64_t qs = (1ull << g.q0) | (n_qubits_of(g) == 2 ? (1ull << g.q1) : 0);
+        if (qs & blocked) { blocked |= qs; continue; }
+        if (max_gates > 0 && (int)exec.size() >= max_gates) { blocked |= qs; continue; }
+        int need = needed_tile_qubit(g);
+        bool ok = need < 0 || (tile >> need & 1);
+        if (!ok && grow && count < cap) {
+            tile |= 1ull << need;
+            count++;
+            ok = true;
+        }
+        if (ok) exec.push_back(i);
+        else blocked |= qs;
+    }
+    return exec;
+}
+
+DevPhase make_phase(const std::vector<int>& tq, const std::vector<int>& reg_bits, int k) {
+    DevPhase p{};
+    uint32_t regmask = 0;
+    for (int m = 0; m < (int)reg_bits.size(); m++) {
+        p.reg_bit[m] = reg_bits[m];
+        regmask |= 1u << reg_bits[m];
+    }
+    p.thr_mask = ((k >= 32) ? 0xffffffffu : ((1u << k) - 1)) & ~regmask;
+    int R = 1 << reg_bits.size();
+    for (int i = 0; i < R; i++) {
+        uint32_t off = 0, goff = 0;
+        for (int m = 0; m < (int)reg_bits.size(); m++)
+            if (i >> m & 1) {
+                off |= 1u << reg_bits[m];
+                goff |= 1u << tq[reg_bits[m]];
+            }
+        p.reg_off[i] = off;
+        p.greg_off[i] = goff;
+    }
+    return p;
+}
+
+// Schedule the gates of one pass onto register phases.
+void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_r, int low,
+                   std::vector<DevPhase>& phases) {
+    const int r = log_r;
+    std::vector<int> bit_of(64, -1);  // qubit -> tile bit
+    for (int j = 0; j < k; j++) bit_of[pp.qubits[j]] = j;
+
+    std::vector<int> pending = pp.gates;
+    auto need_bit = [&](const Gate& g) -> int {
+        int q = needed_tile_qubit(g);
+        return q < 0 ? -1 : bit_of[q];
+    };
+    // choose up to r register bits by a virtual ordered scan; `forbid` masks
+    // tile bits that may not be chosen.
+    auto choose = [&](uint32_t forbid, const std::vector<int>& keep) {
+        std::vector<int> chosen;
+        uint64_t blocked = 0;
+        for (int gi : pending) {
+            const Gate& g = gates[gi];
+            uint64_t qs = (1ull << g.q0) | (n_qubits_of(g) == 2 ? (1ull << g.q1) : 0);
+            if (qs & blocked) { blocked |= qs; continue; }
+            int b = need_bit(g);
+            if (b < 0 || std::find(chosen.begin(), chosen.end(), b) != chosen.end()) continue;
+            if ((int)chosen.size() < r && !(forbid >> b & 1)) chosen.push_back(b);
+            else blocked |= qs;
+        }
+        // fill: previous register bits first, then the lowest allowed bits
+        for (int b : keep)
+            if ((int)chosen.size() < r && !(forbid >> b & 1) &&
+                std::find(chosen.begin(), chosen.end(), b) == chosen.end())
+                chosen.push_back(b);
+        for (int b = k - 1; b >= 0 && (int)chosen.size() < r; b--)
+            if (!(forbid >> b & 1) && std::find(chosen.begin(), chosen.end(), b) == chosen.end())
+                chosen.push_back(b);
+        for (int b = k - 1; b >= 0 && (int)chosen.size() < r; b--)
+            if (std::find(chosen.begin(), chosen.end(), b) == chosen.end()) chosen.push_back(b);
+        std::sort(chosen.begin(), chosen.end());
+        return chosen;
+    };
+    const uint32_t low_mask = (low >= 32) ? 0xffffffffu : ((1u << low) - 1);
+
+    std::vector<int> regs = choose(low_mask, {});
+    int cur_phase = (int)phases.size();
+    phases.push_back(make_phase(pp.qubits, regs, k));
+    pp.first_phase = cur_phase;
+
+    // gradient accumulators: one per rotation in this pass
+    std::vector<int> gslot_of(gates.size(), -1);
+    int n_gs = 0;
+
+    auto loc = [&](int q, uint8_t& type, uint8_t& pos) {
+        int j = bit_of[q];
+        if (j < 0) { type = LOC_FIX; pos = (uint8_t)q; return; }
+        auto it = std::find(regs.begin(), regs.end(), j);
+        if (it != regs.end()) { type = LOC_REG; pos = (uint8_t)(it - regs.begin()); }
+        else { type = LOC_THR; pos = (uint8_t)j; }
+    };
+    struct Rec { DevOp op; int prev_phase; };
+    std::vector<Rec> recs;
+
+    while (!pending.empty()) {
+        uint64_t blocked = 0;
+        std::vector<int> rest;
+        for (int gi : pending) {
+            const Gate& g = gates[gi];
+            uint64_t qs = (1ull << g.q0) | (n_qubits_of(g) == 2 ? (1ull << g.q1) : 0);
+            int b = need_bit(g);
+            bool ok = !(qs & blocked) &&
+                      (b < 0 || std::find(regs.begin(), regs.end(), b) != regs.end());
+            if (!ok) { blocked |= qs; rest.push_back(gi); continue; }
+            DevOp op{};
+            op.slot = g.slot;
+            op.gslot = -1;
+            op.kind = (uint8_t)g.kind;
+            if (is_rotation(g.kind)) {
+                gslot_of[gi] = n_gs++;
+                op.gslot = gslot_of[gi];
+                pp.gslots.push_back(g.slot);
+            }
+            switch (g.kind) {
+                case K_H: case K_RX: case K_RY:
+                    op.code = OP_G1;
+                    loc(g.q0, op.a_type, op.a_pos);
+                    break;
+                case K_RZ:
+                    loc(g.q0, op.a_type, op.a_pos);
+                    op.code = op.a_type == LOC_REG ? OP_G1 : OP_RZ_U;
+                    break;
+                case K_CNOT:
+                    op.code = OP_CNOT;
+                    loc(g.q1, op.a_type, op.a_pos);
+                    loc(g.q0, op.b_type, op.b_pos);
+                    break;
+                case K_CZ:
+                    op.code = OP_CZ;
+                    loc(g.q0, op.a_type, op.a_pos);
+                    loc(g.q1, op.b_type, op.b_pos);
+                    break;
+            }
+            recs.push_back({op, -1});
+        }
+        pending.swap(rest);
+        if (pending.empty()) break;
+        regs = choose(0, regs);
+        int np = (int)phases.size();
+        phases.push_back(make_phase(pp.qubits, regs, k));
+        DevOp t{};
+        t.code = OP_TRANSPOSE;
+        t.arg = (uint16_t)np;
+        t.slot = -1;
+        t.gslot = -1;
+        recs.push_back({t, cur_phase});
+        cur_phase = np;
+        pp.n_transposes++;
+    }
+    // end in a layout whose register bits avoid the low (contiguous) tile
+    // bits, so the store and the next load are coalesced
+    bool low_in_regs = false;
+    for (int b : regs) low_in_regs |= (b < low);
+    if (low_in_regs) {
+        std::vector<int> keep;
+        for (int b : regs) if (b >= low) keep.push_back(b);
+        pending.clear();
+        regs = choose(low_mask, keep);
+        int np = (int)phases.size();
+        phases.push_back(make_phase(pp.qubits, regs, k));
+        DevOp t{};
+        t.code = OP_TRANSPOSE;
+        t.arg = (uint16_t)np;
+        t.slot = -1;
+        t.gslot = -1;
+        recs.push_back({t, cur_phase});
+        cur_phase = np;
+        pp.n_transposes++;
+    }
+    pp.last_phase = cur_phase;
+    for (auto& rc : recs) pp.fwd_ops.push_back(rc.op);
+    for (int i = (int)recs.size() - 1; i >= 0; i--) {
+        DevOp op = recs[i].op;
+        if (op.code == OP_TRANSPOSE) op.arg = (uint16_t)recs[i].prev_phase;
+        pp.bwd_ops.push_back(op);
+    }
+}
+
+}  // namespace
+
+int whole_state_max_qubits(int dtype) { return dtype == 0 ? 12 : 11; }
+
+std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, int n_weights,
+                          const Options& opts, Circuit& out) {
+    if (n < 1 || n > 32) return fmt("n_qubits=%ld out of range [1, 32]", n);
+    if (n_gates < 0) return "n_gates < 0";
+    if (n_gates > 0 && !g5) return "gates is NULL";
+    if (n_inputs < 0 || n_weights < 0) return "negative n_inputs or n_weights";
+    if (n_gates > (1 << 24)) return "too many gates";
+    out = Circuit{};
+    out.n = n;
+    out.n_inputs = n_inputs;
+    out.n_weights = n_weights;
+    out.opts = opts;
+    for (int i = 0; i < n_gates; i++) {
+        Gate g{g5[5 * i], g5[5 * i + 1], g5[5 * i + 2], g5[5 * i + 3], g5[5 * i + 4], -1};
+        if (g.kind < K_H || g.kind > K_CZ) return fmt("gate %ld: unknown kind %ld", i, g.kind);
+        if (g.q0 < 0 || g.q0 >= n) return fmt("gate %ld: qubit %ld out of range", i, g.q0);
+        if (g.kind == K_CNOT || g.kind == K_CZ) {
+            if (g.q1 < 0 || g.q1 >= n) return fmt("gate %ld: qubit %ld out of range", i, g.q1);
+            if (g.q1 == g.q0) return fmt("gate %ld: q0 == q1 == %ld", i, g.q0);
+        } else if (g.q1 != -1) {
+            return fmt("gate %ld: one-qubit gate needs q1 = -1 (got %ld)", i, g.q1);
+        }
+        if (is_rotation(g.kind)) {
+            if (g.src == S_INPUT) {
+                if (g.index < 0 || g.index >= n_inputs)
+                    return fmt("gate %ld: input index %ld out of range [0, %ld)", i, g.index, n_inputs);
+            } else if (g.src == S_WEIGHT) {
+                if (g.index < 0 || g.index >= n_weights)
+                    return fmt("gate %ld: weight index %ld out of range [0, %ld)", i, g.index, n_weights);
+            } else {
+                return fmt("gate %ld: rotation needs src INPUT or WEIGHT (got %ld)", i, g.src);
+            }
+            g.slot = (int)out.slot_gate.size();
+            out.slot_gate.push_back(i);
+        } else if (g.src != S_NONE) {
+            return fmt("gate %ld: H/CNOT/CZ take no angle source (got %ld)", i, g.src);
+        }
+        out.gates.push_back(g);
+    }
+    const Options& o = opts;
+    if (o.log_regs && (o.log_regs < 2 || o.log_regs > MAX_LOG_R)) return "option: log_regs out of range [2, 5]";
+    if (o.log_threads && (o.log_threads < 6 || o.log_threads > 8)) return "option: log_threads out of range [6, 8]";
+    if (o.low_qubits && (o.low_qubits < 1 || o.low_qubits > 8)) return "option: low_qubits out of range [1, 8]";
+    if (o.max_gates_per_pass < 0) return "option: max_gates_per_pass < 0";
+    if (o.wg_per_sample < 0) return "option: wg_per_sample < 0";
+    for (int dt = 0; dt < 2; dt++) {
+        std::string e = build_plan(out, dt, out.plan[dt]);
+        if (!e.empty()) return e;
+    }
+    return "";
+}
+
+std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
+    pl = Plan{};
+    pl.n = c.n;
+    pl.n_slots = (int)c.slot_gate.size();
+    const Options& o = c.opts;
+    if (c.n < 8 || (!o.force_tiled && c.n <= whole_state_max_qubits(dtype))) {
+        pl.whole_state = true;
+        PassPlan pp;
+        for (int i = 0; i < (int)c.gates.size(); i++) pp.gates.push_back(i);
+        for (int q = 0; q < c.n; q++) pp.qubits.push_back(q);
+        pl.passes.push_back(pp);
+        pl.k = c.n;
+        return "";
+    }
+    int log_r = o.log_regs ? o.log_regs : (dtype == 0 ? 5 : 4);
+    int log_t = o.log_threads ? o.log_threads : 8;
+    while (log_r + log_t > c.n && log_t > 6) log_t--;
+    while (log_r + log_t > c.n && log_r > 2) log_r--;
+    if (log_r + log_t > c.n) return "circuit too small for the tile kernel";
+    const int k = log_r + log_t;
+    int low = o.low_qubits ? o.low_qubits : (dtype == 0 ? 4 : 3);
+    if (low > k - 1) low = k - 1;
+    if (c.n == k) low = k;
+    pl.k = k;
+    pl.log_r = log_r;
+    pl.log_t = log_t;
+    pl.low = low;
+
+    const int G = (int)c.gates.size();
+    std::vector<char> done(G, 0);
+    int remaining = G;
+    const uint64_t low_tile = (low >= 64) ? ~0ull : ((1ull << low) - 1);
+    while (remaining > 0 || pl.passes.empty()) {
+        // candidates: first-need greedy growth, and contiguous windows of the
+        // high qubits; keep the one that executes the most gates
+        std::vector<int> best;
+        uint64_t best_tile = 0;
+        {
+            uint64_t t = low_tile;
+            best = scan(c.gates, done, t, k, true, o.max_gates_per_pass);
+            best_tile = t;
+        }
+        const int h = k - low;
+        for (int s = low; s + h <= c.n; s++) {
+            uint64_t t = low_tile | (((1ull << h) - 1) << s);
+            std::vector<int> e = scan(c.gates, done, t, k, false, o.max_gates_per_pass);
+            if (e.size() > best.size()) { best = e; best_tile = t; }
+        }
+        if (best.empty() && remaining > 0) return "planner made no progress";
+        // fill the tile up to k qubits with the lowest unused qubits
+        for (int q = 0; q < c.n && __builtin_popcountll(best_tile) < k; q++) best_tile |= 1ull << q;
+        PassPlan pp;
+        for (int q = 0; q < c.n; q++) if (best_tile >> q & 1) pp.qubits.push_back(q);
+        pp.gates = best;
+        for (int gi : best) done[gi] = 1;
+        remaining -= (int)best.size();
+        schedule_pass(c.gates, pp, k, log_r, low, pl.phases);
+        pl.passes.push_back(std::move(pp));
+        if (G == 0) break;
+    }
+    if (pl.phases.size() > 65535) return "plan too large (phases)";
+    return "";
+}
+
+}  // namespace qlayer

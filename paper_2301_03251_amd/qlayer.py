@@ -1,0 +1,260 @@
+"""ctypes binding of ``libqlayer.so`` (C ABI in ``include/qlayer.h``).
+
+Argument marshalling only: every step of the forward pass, the adjoint sweep
+and the reductions runs in the library's HIP kernels. PyTorch supplies device
+memory and the current stream. There is no CPU fallback: if the library is
+missing the import of the entry points raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libqlayer.so")
+
+C64, C128 = 0, 1
+MODE_FWD, MODE_FWD_BWD = 0, 1
+DTYPES = {"c64": C64, "c128": C128}
+ERRORS = {-1: "QL_EINVAL", -2: "QL_ENOMEM", -3: "QL_EUNSUPPORTED", -4: "QL_EHIP"}
+
+
+class QLError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class _Options(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("log_regs", "log_threads", "low_qubits",
+                                              "max_gates_per_pass", "force_tiled",
+                                              "wg_per_sample")]
+
+
+class _PlanInfo(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "n_passes", "tile_qubits", "log_regs",
+                                              "log_threads", "low_qubits", "n_transposes",
+                                              "n_param_gates")]
+
+
+_lib = None
+EXPORTS = ("ql_circuit_create", "ql_circuit_create_ex", "ql_circuit_destroy",
+           "ql_workspace_bytes", "ql_forward", "ql_forward_backward", "ql_last_error",
+           "ql_plan_info_get", "ql_plan_schedule", "ql_plan_state_bytes",
+           "ql_timing_enable", "ql_timing_read")
+
+
+def load():
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python paper_2301_03251_amd/build.py` (no CPU fallback exists)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.ql_circuit_create.argtypes = [I32, P, I32, I32, I32, ctypes.POINTER(P)]
+    lib.ql_circuit_create_ex.argtypes = [I32, P, I32, I32, I32, ctypes.POINTER(_Options),
+                                         ctypes.POINTER(P)]
+    lib.ql_circuit_destroy.argtypes = [P]
+    lib.ql_circuit_destroy.restype = None
+    lib.ql_workspace_bytes.argtypes = [P, ctypes.c_int, I64, ctypes.c_int, ctypes.POINTER(SZ)]
+    lib.ql_forward.argtypes = [P, ctypes.c_int, I64, P, P, P, P, SZ, P]
+    lib.ql_forward_backward.argtypes = [P, ctypes.c_int, I64, P, P, P, P, P, P, P, SZ, P]
+    lib.ql_last_error.argtypes = []
+    lib.ql_last_error.restype = ctypes.c_char_p
+    lib.ql_plan_info_get.argtypes = [P, ctypes.c_int, ctypes.POINTER(_PlanInfo)]
+    lib.ql_plan_schedule.argtypes = [P, ctypes.c_int, P, P]
+    lib.ql_plan_state_bytes.argtypes = [P, ctypes.c_int, I64, ctypes.c_int,
+                                        ctypes.POINTER(ctypes.c_double)]
+    lib.ql_timing_enable.argtypes = [P, ctypes.c_int]
+    lib.ql_timing_read.argtypes = [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]
+    for name in ("ql_circuit_create", "ql_circuit_create_ex", "ql_workspace_bytes", "ql_forward",
+                 "ql_forward_backward", "ql_plan_info_get", "ql_plan_schedule",
+                 "ql_plan_state_bytes", "ql_timing_enable", "ql_timing_read"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(rc):
+    if rc != 0:
+        raise QLError(rc, load().ql_last_error().decode())
+
+
+def _dt(dtype):
+    return DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+
+
+class Circuit:
+    """A validated gate list with its pass plans (``ql_circuit_create_ex``)."""
+
+    def __init__(self, n_qubits, gates, n_inputs, n_weights, **options):
+        lib = load()
+        g = np.ascontiguousarray(np.asarray(gates, dtype=np.int32).reshape(-1, 5))
+        self.n = int(n_qubits)
+        self.gates = g
+        self.n_inputs, self.n_weights = int(n_inputs), int(n_weights)
+        opts = _Options(**{k: int(v) for k, v in options.items()})
+        h = ctypes.c_void_p()
+        _check(lib.ql_circuit_create_ex(self.n, g.ctypes.data_as(ctypes.c_void_p), g.shape[0],
+                                        self.n_inputs, self.n_weights, ctypes.byref(opts),
+                                        ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().ql_circuit_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def handle(self):
+        return self._h
+
+    def workspace_bytes(self, dtype, batch, mode=MODE_FWD_BWD) -> int:
+        out = ctypes.c_size_t()
+        _check(load().ql_workspace_bytes(self._h, _dt(dtype), int(batch), int(mode), ctypes.byref(out)))
+        return out.value
+
+    def plan_info(self, dtype) -> dict:
+        info = _PlanInfo()
+        _check(load().ql_plan_info_get(self._h, _dt(dtype), ctypes.byref(info)))
+        return {f: getattr(info, f) for f, _ in _PlanInfo._fields_}
+
+    def schedule(self, dtype):
+        G = self.gates.shape[0]
+        pog = np.zeros(max(G, 1), dtype=np.int32)
+        order = np.zeros(max(G, 1), dtype=np.int32)
+        _check(load().ql_plan_schedule(self._h, _dt(dtype), pog.ctypes.data_as(ctypes.c_void_p),
+                                       order.ctypes.data_as(ctypes.c_void_p)))
+        return pog[:G], order[:G]
+
+    def state_bytes(self, dtype, batch, mode=MODE_FWD_BWD) -> float:
+        out = ctypes.c_double()
+        _check(load().ql_plan_state_bytes(self._h, _dt(dtype), int(batch), int(mode), ctypes.byref(out)))
+        return out.value
+
+    def timing(self, enable: bool):
+        _check(load().ql_timing_enable(self._h, 1 if enable else 0))
+
+    def timing_read(self):
+        ms = (ctypes.c_double * 4)()
+        cnt = (ctypes.c_int32 * 4)()
+        _check(load().ql_timing_read(self._h, ms, cnt))
+        return list(ms), list(cnt)
+
+    # raw entry points: device pointers as ints, stream as int (hipStream_t)
+    def forward_raw(self, dtype, batch, inputs, weights, expz, ws, ws_bytes, stream):
+        _check(load().ql_forward(self._h, _dt(dtype), int(batch), inputs, weights, expz, ws,
+                                 int(ws_bytes), stream))
+
+    def forward_backward_raw(self, dtype, batch, inputs, weights, grad_out, expz, grad_inputs,
+                             grad_weights, ws, ws_bytes, stream):
+        _check(load().ql_forward_backward(self._h, _dt(dtype), int(batch), inputs, weights,
+                                          grad_out, expz, grad_inputs, grad_weights, ws,
+                                          int(ws_bytes), stream))
+
+
+# ---------------------------------------------------------------------------
+# torch plumbing (device memory and streams only)
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+class Runner:
+    """Holds a circuit, a dtype and a reusable device workspace."""
+
+    def __init__(self, circuit: Circuit, dtype="c64", device="cuda"):
+        torch = _torch()
+        self.c = circuit
+        self.dtype = dtype
+        self.real = torch.float32 if _dt(dtype) == C64 else torch.float64
+        self.device = torch.device(device)
+        self._ws = None
+
+    def workspace(self, batch, mode):
+        torch = _torch()
+        need = self.c.workspace_bytes(self.dtype, batch, mode)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        return self._ws
+
+    def _args(self, inputs, weights, B):
+        torch = _torch()
+        x = inputs if inputs is not None else torch.empty((B, 0), dtype=self.real, device=self.device)
+        w = weights if weights is not None else torch.empty(0, dtype=self.real, device=self.device)
+        for t in (x, w):
+            if t.dtype != self.real or t.device.type != "cuda" or not t.is_contiguous():
+                raise ValueError("inputs/weights must be contiguous CUDA tensors of the layer's real dtype")
+        return x, w
+
+    def forward(self, inputs, weights, out=None):
+        torch = _torch()
+        B = int(inputs.shape[0])
+        x, w = self._args(inputs, weights, B)
+        expz = out if out is not None else torch.empty((B, self.c.n), dtype=self.real, device=self.device)
+        ws = self.workspace(B, MODE_FWD)
+        self.c.forward_raw(self.dtype, B, _ptr(x) if self.c.n_inputs else None,
+                           _ptr(w) if self.c.n_weights else None, _ptr(expz), _ptr(ws), ws.numel(),
+                           ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
+        return expz
+
+    def forward_backward(self, inputs, weights, grad_out, want_inputs=True, want_weights=True,
+                         outs=None):
+        torch = _torch()
+        B = int(inputs.shape[0])
+        x, w = self._args(inputs, weights, B)
+        if grad_out.dtype != self.real or not grad_out.is_contiguous():
+            raise ValueError("grad_out must be a contiguous tensor of the layer's real dtype")
+        if outs is None:
+            expz = torch.empty((B, self.c.n), dtype=self.real, device=self.device)
+            gx = torch.empty((B, self.c.n_inputs), dtype=self.real, device=self.device) if want_inputs else None
+            gw = torch.empty(self.c.n_weights, dtype=self.real, device=self.device) if want_weights else None
+        else:
+            expz, gx, gw = outs
+        ws = self.workspace(B, MODE_FWD_BWD)
+        self.c.forward_backward_raw(
+            self.dtype, B, _ptr(x) if self.c.n_inputs else None, _ptr(w) if self.c.n_weights else None,
+            _ptr(grad_out), _ptr(expz), _ptr(gx) if (gx is not None and self.c.n_inputs) else None,
+            _ptr(gw) if (gw is not None and self.c.n_weights) else None, _ptr(ws), ws.numel(),
+            ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
+        return expz, gx, gw
+
+
+def quantum_layer_function():
+    """``torch.autograd.Function`` whose forward returns <Z_i> and whose
+    backward runs one fused forward + adjoint call for the VJP."""
+    torch = _torch()
+
+    class QuantumLayerFn(torch.autograd.Function):
+        @staticmethod
+        def forward(ctx, runner, inputs, weights):
+            ctx.runner = runner
+            ctx.save_for_backward(inputs, weights)
+            return runner.forward(inputs.contiguous(), weights.contiguous())
+
+        @staticmethod
+        def backward(ctx, grad_expz):
+            inputs, weights = ctx.saved_tensors
+            _, gx, gw = ctx.runner.forward_backward(
+                inputs.contiguous(), weights.contiguous(), grad_expz.contiguous(),
+                want_inputs=ctx.needs_input_grad[1], want_weights=ctx.needs_input_grad[2])
+            return None, gx, gw
+
+    return QuantumLayerFn

@@ -1,0 +1,172 @@
+"""Host-side checks of the C ABI (no GPU): exports, validation, planner invariants,
+workspace arithmetic. Nothing here launches a kernel."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qlayer.h")
+
+Q = pytest.importorskip("paper_2301_03251_amd")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return Q.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    decl = re.findall(r"\b(ql_[a-z_0-9]+)\s*\(", open(HEADER).read())
+    names = sorted(set(decl))
+    assert len(names) >= 12
+    for name in names:
+        assert hasattr(lib, name), f"{name} declared in qlayer.h but not exported"
+
+
+def test_product_package_never_uses_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2301_03251_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".hpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text, f"{f} mentions the oracle"
+
+
+def _err(fn):
+    with pytest.raises(Q.QLError) as e:
+        fn()
+    return e.value.code
+
+
+G1 = [[W.RY, 0, -1, W.SRC_WEIGHT, 0]]
+
+
+@pytest.mark.parametrize("gates,n,F,P,code", [
+    ([[W.RY, 3, -1, W.SRC_WEIGHT, 0]], 3, 0, 1, -1),     # qubit out of range
+    ([[W.CNOT, 1, 1, 0, 0]], 3, 0, 0, -1),               # q0 == q1
+    ([[W.CZ, 0, 5, 0, 0]], 3, 0, 0, -1),                 # q1 out of range
+    ([[W.H, 0, -1, W.SRC_WEIGHT, 0]], 3, 0, 1, -1),      # H with a source
+    ([[W.RX, 0, -1, W.SRC_NONE, 0]], 3, 0, 1, -1),       # rotation without source
+    ([[W.RZ, 0, -1, W.SRC_INPUT, 2]], 3, 2, 0, -1),      # input index out of range
+    ([[W.RZ, 0, -1, W.SRC_WEIGHT, -1]], 3, 0, 1, -1),    # negative weight index
+    ([[9, 0, -1, 0, 0]], 3, 0, 0, -1),                   # unknown kind
+    ([[W.RY, 0, 1, W.SRC_WEIGHT, 0]], 3, 0, 1, -1),      # one-qubit gate with q1
+    (G1, 0, 0, 1, -1),                                   # n = 0
+    (G1, 33, 0, 1, -1),                                  # n = 33
+])
+def test_create_rejects(lib, gates, n, F, P, code):
+    assert _err(lambda: Q.Circuit(n, np.array(gates, np.int32), F, P)) == code
+
+
+@pytest.mark.parametrize("opts", [dict(log_regs=1), dict(log_regs=6), dict(log_threads=5),
+                                  dict(log_threads=9), dict(low_qubits=9), dict(wg_per_sample=-1)])
+def test_create_rejects_options(lib, opts):
+    assert _err(lambda: Q.Circuit(14, np.array(G1, np.int32), 0, 1, **opts)) == -3
+
+
+def test_create_null_pointers(lib):
+    h = ctypes.c_void_p()
+    assert lib.ql_circuit_create(3, None, 2, 0, 0, ctypes.byref(h)) == -1
+    assert lib.ql_circuit_create(3, None, 0, 0, 0, None) == -1
+    assert lib.ql_last_error()
+
+
+def test_call_validation_before_launch(lib):
+    """Errors that are caught before anything touches a GPU."""
+    c = Q.Circuit(14, np.array(G1, np.int32), 0, 1)
+    need = c.workspace_bytes("c64", 2)
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    # NULL workspace, workspace too small, NULL expz, NULL weights, bad batch, bad dtype
+    assert _err(lambda: c.forward_backward_raw("c64", 2, None, fake, fake, fake, None, None,
+                                               None, need, None)) == -1
+    assert _err(lambda: c.forward_backward_raw("c64", 2, None, fake, fake, fake, None, None,
+                                               fake, need - 1, None)) == -2
+    assert _err(lambda: c.forward_backward_raw("c64", 2, None, fake, fake, None, None, None,
+                                               fake, need, None)) == -1
+    assert _err(lambda: c.forward_raw("c64", 2, None, None, fake, fake, need, None)) == -1
+    assert _err(lambda: c.forward_backward_raw("c64", 2, None, fake, None, fake, None, None,
+                                               fake, need, None)) == -1
+    assert _err(lambda: c.forward_raw("c64", 0, None, fake, fake, fake, need, None)) == -1
+    assert _err(lambda: c.forward_raw(7, 2, None, fake, fake, fake, need, None)) == -1
+    assert _err(lambda: c.workspace_bytes("c64", 1 << 31)) == -1
+
+
+def test_workspace_arithmetic(lib):
+    wl = W.get("30q")
+    c = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    S = (1 << 30) * 8
+    fb = c.workspace_bytes("c64", 1)
+    fw = c.workspace_bytes("c64", 1, Q.MODE_FWD)
+    assert 2 * S <= fb < 2 * S + (64 << 20)      # psi + lambda + small tables/partials
+    assert S <= fw < S + (64 << 20)              # psi only
+    assert c.workspace_bytes("c128", 1) >= 4 * S
+    m = c.plan_info("c64")["n_passes"]
+    assert c.state_bytes("c64", 1) == (6 * m - 6) * S
+    assert c.state_bytes("c64", 1, Q.MODE_FWD) == (2 * m - 2) * S
+    small = Q.Circuit(4, W.get("4q").gates(), 4, 16)
+    assert small.state_bytes("c128", 8) == 0.0   # whole state in LDS: no HBM state traffic
+
+
+def _check_schedule(c, gates, dtype):
+    pog, order = c.schedule(dtype)
+    G = gates.shape[0]
+    assert sorted(order.tolist()) == list(range(G)), "every gate scheduled exactly once"
+    assert np.all(pog >= 0)
+    pos = np.empty(G, dtype=np.int64)
+    pos[order] = np.arange(G)
+    # passes are contiguous in the execution order
+    assert np.all(np.diff(pog[order]) >= 0)
+    # gates that share a qubit keep their relative order
+    last = {}
+    for i, g in enumerate(gates):
+        qs = [int(g[1])] + ([int(g[2])] if g[0] in (W.CNOT, W.CZ) else [])
+        for q in qs:
+            if q in last:
+                assert pos[last[q]] < pos[i], f"gate {i} overtakes gate {last[q]} on qubit {q}"
+            last[q] = i
+
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_workload_plans(lib, name):
+    wl = W.get(name)
+    c = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    for dt in ("c64", "c128"):
+        _check_schedule(c, wl.gates(), dt)
+        info = c.plan_info(dt)
+        assert info["n_param_gates"] == sum(1 for g in wl.gates() if g[0] in W.ROTATIONS)
+        if wl.n <= (12 if dt == "c64" else 11):
+            assert info["kernel"] == 0 and info["n_passes"] == 1
+        else:
+            assert info["kernel"] == 1 and info["tile_qubits"] == info["log_regs"] + info["log_threads"]
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("opts", [dict(force_tiled=1), dict(force_tiled=1, max_gates_per_pass=1),
+                                  dict(log_regs=2, log_threads=6, low_qubits=1),
+                                  dict(log_regs=3, log_threads=7, max_gates_per_pass=5)])
+def test_random_plans(lib, seed, opts):
+    n = 10 + seed % 5
+    gates = W.random_circuit(n, 150, 4, 6, seed=seed)
+    c = Q.Circuit(n, gates, 4, 6, **opts)
+    for dt in ("c64", "c128"):
+        _check_schedule(c, gates, dt)
+        info = c.plan_info(dt)
+        if opts.get("max_gates_per_pass") == 1:
+            assert info["n_passes"] == gates.shape[0]
+
+
+def test_pass_counts_are_small(lib):
+    """Fusion budget of the light-cone planner on the large workloads: far fewer
+    passes than layers x qubits."""
+    for name, limit in (("16q", 8), ("24q", 20), ("30q", 16)):
+        wl = W.get(name)
+        c = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+        assert c.plan_info("c64")["n_passes"] <= limit, name

@@ -1,0 +1,316 @@
+"""HIP path vs the CPU oracle, through the C ABI (needs an MI355X).
+
+Tolerances: 1e-5 absolute for complex64 and 1e-12 absolute for complex128, on
+<Z_i>, input gradients and weight gradients. The oracle always runs in
+complex128 on the exact (float32-rounded for complex64) values the GPU gets.
+"""
+
+from __future__ import annotations
+
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import oracle_pins
+import workloads as W
+
+torch = pytest.importorskip("torch")
+import paper_2301_03251_amd as Q  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"c64": 1e-5, "c128": 1e-12}
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    Q.load()
+
+
+def _real(dtype):
+    return torch.float32 if dtype == "c64" else torch.float64
+
+
+def _dev(a, dtype):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=_real(dtype))
+
+
+def gpu_fb(circ, dtype, x, w, g, runner=None):
+    r = runner or Q.Runner(circ, dtype)
+    e, gx, gw = r.forward_backward(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype))
+    torch.cuda.synchronize()
+    return {"expz": e.cpu().double().numpy(), "grad_inputs": gx.cpu().double().numpy(),
+            "grad_weights": gw.cpu().double().numpy()}
+
+
+def check(got, want, tol, what, keys=("expz", "grad_inputs", "grad_weights")):
+    for k in keys:
+        a, b = np.asarray(got[k], dtype=np.float64), np.asarray(want[k], dtype=np.float64)
+        assert a.shape == b.shape, f"{what} {k}: shape {a.shape} vs {b.shape}"
+        err = float(np.max(np.abs(a - b))) if a.size else 0.0
+        assert err <= tol, f"{what} {k}: max abs err {err:.3e} > {tol:.0e}"
+
+
+# ---------------------------------------------------------------------------
+# the five workloads
+
+@pytest.mark.parametrize("name", ["4q", "10q"])
+def test_workload_full(name):
+    wl = W.get(name)
+    x, w, g = wl.inputs()
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    got = gpu_fb(circ, wl.dtype, x, w, g)
+    want = oracle.run(wl.n, wl.gates(), x, w, grad_out=g)
+    check(got, want, TOL[wl.dtype], name)
+
+
+@pytest.mark.parametrize("name", ["10q", "16q"])
+def test_workload_in_c128(name):
+    """The same circuits in complex128: separates logic errors from fp32 rounding."""
+    wl = W.scaled(W.get(name), dtype="c128")
+    x, w, g = wl.inputs()
+    rows = [0, 1, wl.batch - 1] if wl.batch > 64 else list(range(wl.batch))
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    got = gpu_fb(circ, "c128", x, w, g)
+    want = oracle.run(wl.n, wl.gates(), x[rows], w, grad_out=g[rows])
+    gm = np.zeros_like(g)
+    gm[rows] = g[rows]
+    got_m = gpu_fb(circ, "c128", x, w, gm)
+    check({"expz": got["expz"][rows], "grad_inputs": got["grad_inputs"][rows],
+           "grad_weights": got_m["grad_weights"]}, want, 1e-12, name + " c128")
+
+
+def test_workload_16q_sampled():
+    """Full batch of 1024 on the GPU; the oracle checks sampled rows. Weight
+    gradients are batch sums, so a second call zeroes grad_out outside the
+    sampled rows (the VJP is linear in grad_out)."""
+    wl = W.get("16q")
+    x, w, g = wl.inputs()
+    rows = [0, 1, 2, 255, 511, 777, 1022, 1023]
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    r = Q.Runner(circ, wl.dtype)
+    got = gpu_fb(circ, wl.dtype, x, w, g, r)
+    gm = np.zeros_like(g)
+    gm[rows] = g[rows]
+    got_m = gpu_fb(circ, wl.dtype, x, w, gm, r)
+    want = oracle.run(wl.n, wl.gates(), x[rows], w, grad_out=g[rows])
+    check({"expz": got["expz"][rows], "grad_inputs": got["grad_inputs"][rows],
+           "grad_weights": got_m["grad_weights"]}, want, TOL[wl.dtype], "16q")
+    assert np.all(np.abs(got["expz"]) <= 1 + 1e-5)
+
+
+@pytest.mark.parametrize("name", ["24q", "30q"])
+def test_workload_golden(name):
+    """Full workload on the GPU vs oracle values stored by tests/golden/make_golden.py."""
+    path = os.path.join(GOLDEN, f"{name}.npz")
+    if not os.path.exists(path):
+        pytest.skip(f"{path} not generated")
+    gold = np.load(path, allow_pickle=False)
+    wl = W.get(name)
+    x, w, g = wl.inputs()
+    import sys
+    sys.path.insert(0, GOLDEN)
+    import make_golden  # noqa: E402  (digest only)
+    assert str(gold["digest"]) == make_golden.digest(x, w, g), "golden file is stale"
+    rows = [int(v) for v in gold["rows"]]
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    r = Q.Runner(circ, wl.dtype)
+    got = gpu_fb(circ, wl.dtype, x, w, g, r)
+    if len(rows) < wl.batch:
+        gm = np.zeros_like(g)
+        gm[rows] = g[rows]
+        gw = gpu_fb(circ, wl.dtype, x, w, gm, r)["grad_weights"]
+    else:
+        gw = got["grad_weights"]
+    check({"expz": got["expz"][rows], "grad_inputs": got["grad_inputs"][rows], "grad_weights": gw},
+          {"expz": gold["expz"], "grad_inputs": gold["grad_inputs"],
+           "grad_weights": gold["grad_weights"]}, TOL[wl.dtype], name)
+    assert np.all(np.abs(got["expz"]) <= 1 + 1e-5)
+
+
+# ---------------------------------------------------------------------------
+# random circuits on every code path
+
+TILED = [
+    # n, G, B, dtype, options
+    (9, 60, 3, "c64", dict(force_tiled=1, log_regs=3, log_threads=6)),
+    (10, 80, 2, "c128", dict(force_tiled=1, log_regs=2, log_threads=6)),
+    (11, 90, 3, "c64", dict(force_tiled=1, log_regs=4, log_threads=6, low_qubits=2)),
+    (11, 90, 3, "c128", dict(force_tiled=1, log_regs=3, log_threads=7, low_qubits=3)),
+    (12, 120, 2, "c64", dict(force_tiled=1, log_regs=5, log_threads=6)),
+    (12, 120, 2, "c64", dict(force_tiled=1, log_regs=4, log_threads=6, max_gates_per_pass=1)),
+    (13, 150, 3, "c64", dict()),
+    (13, 150, 3, "c128", dict(force_tiled=1, log_regs=4, log_threads=8, max_gates_per_pass=7)),
+    (14, 200, 2, "c64", dict()),
+    (14, 200, 2, "c128", dict()),
+    (14, 160, 3, "c64", dict(log_regs=2, log_threads=8, low_qubits=1)),
+    (15, 160, 2, "c64", dict(log_regs=5, log_threads=7, wg_per_sample=3)),
+]
+
+
+@pytest.mark.parametrize("n,G,B,dtype,opts", TILED,
+                         ids=[f"n{c[0]}-{c[3]}-{'-'.join(f'{k}{v}' for k, v in c[4].items()) or 'default'}"
+                              for c in TILED])
+def test_random_tiled(n, G, B, dtype, opts):
+    F, P = 5, 7
+    gates = W.random_circuit(n, G, F, P, seed=n * 100 + G)
+    x, w, g = W.random_inputs(B, F, P, n, seed=n + G, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P, **opts)
+    info = circ.plan_info(dtype)
+    assert info["kernel"] == 1
+    got = gpu_fb(circ, dtype, x, w, g)
+    want = oracle.run(n, gates, x, w, grad_out=g)
+    check(got, want, TOL[dtype], f"tiled n={n} {dtype} {opts} passes={info['n_passes']}")
+
+
+@pytest.mark.parametrize("dtype", ["c64", "c128"])
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 7, 8, 11, 12])
+def test_random_whole_state(n, dtype):
+    if dtype == "c128" and n == 12:
+        n = 11
+    F, P = 3, 4
+    gates = W.random_circuit(n, 40 + 5 * n, F, P, seed=7 * n + 1)
+    x, w, g = W.random_inputs(5, F, P, n, seed=n, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P)
+    assert circ.plan_info(dtype)["kernel"] == 0
+    check(gpu_fb(circ, dtype, x, w, g), oracle.run(n, gates, x, w, grad_out=g), TOL[dtype],
+          f"whole n={n} {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["c64", "c128"])
+def test_degenerate_circuits(dtype):
+    """No gates, no rotations, inputs only, weights only."""
+    n, B = 13, 2
+    cases = [
+        (np.zeros((0, 5), np.int32), 0, 0),
+        (np.array([[W.H, 0, -1, 0, 0], [W.CNOT, 0, 12, 0, 0], [W.CZ, 12, 3, 0, 0]], np.int32), 0, 0),
+        (np.array([[W.RY, q, -1, W.SRC_INPUT, q % 2] for q in range(n)], np.int32), 2, 0),
+        (np.array([[W.RX, q, -1, W.SRC_WEIGHT, 0] for q in range(n)], np.int32), 0, 1),
+    ]
+    for gates, F, P in cases:
+        for opts in (dict(), dict(force_tiled=1)):
+            x, w, g = W.random_inputs(B, F, P, n, seed=3, dtype=dtype)
+            circ = Q.Circuit(n, gates, F, P, **opts)
+            got = gpu_fb(circ, dtype, x, w, g)
+            check(got, oracle.run(n, gates, x, w, grad_out=g), TOL[dtype], f"degenerate {gates.shape[0]} gates")
+
+
+def test_batch_edges():
+    """B = 1 and a B that is not a multiple of anything, on the tiled path."""
+    n, F, P = 14, 4, 6
+    gates = W.random_circuit(n, 120, F, P, seed=11)
+    circ = Q.Circuit(n, gates, F, P)
+    for B in (1, 7):
+        x, w, g = W.random_inputs(B, F, P, n, seed=B, dtype="c64")
+        check(gpu_fb(circ, "c64", x, w, g), oracle.run(n, gates, x, w, grad_out=g), 1e-5, f"B={B}")
+
+
+def test_forward_only_and_null_grads():
+    n, F, P, B = 14, 3, 5, 3
+    gates = W.random_circuit(n, 100, F, P, seed=5)
+    circ = Q.Circuit(n, gates, F, P)
+    x, w, g = W.random_inputs(B, F, P, n, seed=9, dtype="c64")
+    r = Q.Runner(circ, "c64")
+    e = r.forward(_dev(x, "c64"), _dev(w, "c64"))
+    e2, gx, gw = r.forward_backward(_dev(x, "c64"), _dev(w, "c64"), _dev(g, "c64"),
+                                    want_inputs=False, want_weights=True)
+    torch.cuda.synchronize()
+    assert gx is None
+    want = oracle.run(n, gates, x, w, grad_out=g)
+    assert np.max(np.abs(e.cpu().double().numpy() - want["expz"])) <= 1e-5
+    assert np.array_equal(e.cpu().numpy(), e2.cpu().numpy())
+    assert np.max(np.abs(gw.cpu().double().numpy() - want["grad_weights"])) <= 1e-5
+
+
+def test_deterministic():
+    """Two calls give bit-identical outputs (fixed-order fp64 reductions, no atomics)."""
+    wl = W.get("16q")
+    x, w, g = wl.inputs()
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    r = Q.Runner(circ, wl.dtype)
+    a = gpu_fb(circ, wl.dtype, x, w, g, r)
+    b = gpu_fb(circ, wl.dtype, x, w, g, r)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_plans_agree():
+    """Different tilings of one circuit agree to rounding (c128: 1e-12)."""
+    n, F, P, B = 14, 4, 6, 2
+    gates = W.random_circuit(n, 150, F, P, seed=21)
+    x, w, g = W.random_inputs(B, F, P, n, seed=22, dtype="c128")
+    ref = None
+    for opts in (dict(), dict(log_regs=2, log_threads=6), dict(max_gates_per_pass=3),
+                 dict(log_regs=3, log_threads=7, low_qubits=1)):
+        got = gpu_fb(Q.Circuit(n, gates, F, P, **opts), "c128", x, w, g)
+        if ref is None:
+            ref = got
+        else:
+            check(got, ref, 1e-12, f"plan {opts}")
+
+
+@pytest.mark.parametrize("name", ["24q", "30q"])
+def test_product_state_full_size(name):
+    """Workload circuit with its entanglers removed, at full size: every qubit
+    evolves alone, so <Z_q> and the gradients have the SO(3) closed form."""
+    wl = W.scaled(W.get(name), entangler=None)
+    x, w, g = wl.inputs()
+    gates = wl.gates()
+    circ = Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights)
+    got = gpu_fb(circ, wl.dtype, x, w, g)
+    xs, ws, gs = (a.astype(np.float64) for a in (x, w, g))
+    gw = np.zeros(wl.n_weights)
+    for b in range(wl.batch):
+        e, gx, gwb = oracle_pins.product_state_reference(wl.n, gates, xs[b], ws, gs[b])
+        gw += gwb
+        assert np.max(np.abs(got["expz"][b] - e)) <= 1e-5
+        assert np.max(np.abs(got["grad_inputs"][b] - gx)) <= 1e-5
+    assert np.max(np.abs(got["grad_weights"] - gw)) <= 1e-5
+
+
+def test_hybrid_node_closed_form():
+    """The paper's one-qubit hybrid node (H, then RY(input)): <Z> = -sin t and
+    d<Z>/dt = -cos t, on a batch of angles."""
+    t = np.linspace(-3.0, 3.0, 33)
+    gates = np.array([[W.H, 0, -1, 0, 0], [W.RY, 0, -1, W.SRC_INPUT, 0]], np.int32)
+    circ = Q.Circuit(1, gates, 1, 0)
+    got = gpu_fb(circ, "c128", t[:, None], np.zeros(0), np.ones((t.size, 1)))
+    assert np.max(np.abs(got["expz"][:, 0] + np.sin(t))) <= 1e-12
+    assert np.max(np.abs(got["grad_inputs"][:, 0] + np.cos(t))) <= 1e-12
+
+
+def test_autograd_function():
+    """The torch.autograd.Function wrapper returns the library's VJP."""
+    wl = W.get("10q")
+    x, w, g = wl.inputs()
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    r = Q.Runner(circ, wl.dtype)
+    fn = Q.quantum_layer_function()
+    xt = _dev(x, "c64").requires_grad_(True)
+    wt = _dev(w, "c64").requires_grad_(True)
+    out = fn.apply(r, xt, wt)
+    (out * _dev(g, "c64")).sum().backward()
+    torch.cuda.synchronize()
+    want = oracle.run(wl.n, wl.gates(), x, w, grad_out=g)
+    assert np.max(np.abs(out.detach().cpu().double().numpy() - want["expz"])) <= 1e-5
+    assert np.max(np.abs(xt.grad.cpu().double().numpy() - want["grad_inputs"])) <= 1e-5
+    assert np.max(np.abs(wt.grad.cpu().double().numpy() - want["grad_weights"])) <= 1e-5
+
+
+def test_shared_parameter_closed_form():
+    """The paper's compatibility example at 14 qubits (tiled path): H on every
+    qubit, RY with one shared weight; d/dt sum_i <Z_i> = -n cos t."""
+    n = 14
+    gates = np.array([[W.H, q, -1, 0, 0] for q in range(n)] +
+                     [[W.RY, q, -1, W.SRC_WEIGHT, 0] for q in range(n)], np.int32)
+    circ = Q.Circuit(n, gates, 0, 1)
+    for t in (-1.2, 0.4, 2.5):
+        got = gpu_fb(circ, "c128", np.zeros((1, 0)), np.array([t]), np.ones((1, n)))
+        assert np.max(np.abs(got["expz"][0] + math.sin(t))) <= 1e-12
+        assert abs(got["grad_weights"][0] + n * math.cos(t)) <= 1e-11
