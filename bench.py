@@ -59,6 +59,9 @@ def main():
                     help="gates in the CPU-oracle sample (0 disables it)")
     ap.add_argument("--no-timing", action="store_true",
                     help="time only the whole step (no per-kernel events)")
+    ap.add_argument("--opt", action="append", default=[],
+                    help="planner option key=value (log_regs, log_threads, low_qubits, "
+                         "max_gates_per_pass, wg_per_sample)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported; this build runs on one GPU "
@@ -71,7 +74,8 @@ def main():
 
     wl = W.get(args.workload)
     x, w, g = wl.inputs()
-    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    opts = {kv.split("=")[0]: int(kv.split("=")[1]) for kv in args.opt}
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, **opts)
     runner = Q.Runner(circ, wl.dtype)
     real = torch.float32 if wl.dtype == "c64" else torch.float64
     dev = torch.device("cuda")
@@ -118,7 +122,7 @@ def main():
         "config": {"workload": wl.name, "n_qubits": wl.n, "batch": wl.batch,
                    "gates": wl.n_gates, "weights": wl.n_weights,
                    "updates_per_step": U, "tile_passes": info["n_passes"],
-                   "tile_qubits": info["tile_qubits"]},
+                   "tile_qubits": info["tile_qubits"], "planner_options": opts},
     }
     if timing and kcnt[0] > 0:
         tile_ms = kms[0] / args.steps

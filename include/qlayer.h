@@ -89,7 +89,7 @@ enum {
  * work is split into kernel passes, never the results beyond fp rounding. */
 typedef struct {
     int32_t log_regs;           /* amplitudes per thread = 2^log_regs (2..5) */
-    int32_t log_threads;        /* threads per workgroup = 2^log_threads (6..8) */
+    int32_t log_threads;        /* threads per workgroup = 2^log_threads (6..9) */
     int32_t low_qubits;         /* qubits 0..low_qubits-1 are in every tile (1..8) */
     int32_t max_gates_per_pass; /* cap on gates per tile pass (>= 1) */
     int32_t force_tiled;        /* 1: never use the whole-state-in-LDS kernel */

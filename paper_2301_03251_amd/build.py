@@ -5,7 +5,8 @@ root and linked into ``paper_2301_03251_amd/libqlayer.so``. Every call
 recompiles (the build check runs it on a machine without a GPU; hipcc
 cross-compiles the device code).
 
-Device code is built without packed-FP32 instructions (v_pk_*_f32).
+Device code is built without packed-FP32 instructions (v_pk_*_f32), and with
+uniform control-flow regions left unstructurised.
 """
 
 from __future__ import annotations
@@ -25,7 +26,10 @@ SOURCES = ["kernels.hip", "api.cpp", "plan.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
-DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Uniform branches (the tile kernels' op dispatch) are left unstructurised so
+# the register-resident tile keeps its registers across the dispatch.
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-mllvm", "-structurizecfg-skip-uniform-regions=true"]
 
 
 def _compile(src: str) -> str:

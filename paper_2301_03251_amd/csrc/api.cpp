@@ -40,6 +40,8 @@ struct Tables {
     size_t off_pass = 0, off_phase = 0, off_ops = 0, off_gslot = 0, off_slots = 0;
     size_t off_xptr = 0, off_xslot = 0, off_wptr = 0, off_wslot = 0, off_gates = 0;
     std::vector<DevPass> passes;
+    int n_ops = 0;
+    int bwd_first = 0;
 };
 
 template <typename T>
@@ -70,16 +72,22 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
             d.fwd_begin = (int)ops.size();
             ops.insert(ops.end(), pp.fwd_ops.begin(), pp.fwd_ops.end());
             d.fwd_end = (int)ops.size();
-            d.bwd_begin = (int)ops.size();
-            ops.insert(ops.end(), pp.bwd_ops.begin(), pp.bwd_ops.end());
-            d.bwd_end = (int)ops.size();
             d.load_phase = pp.first_phase;
             d.bwd_phase = pp.last_phase;
             d.gslot_base = (int)gsl.size();
             gsl.insert(gsl.end(), pp.gslots.begin(), pp.gslots.end());
             d.n_gslots = (int)pp.gslots.size();
             d.n_exchanges = pp.n_transposes;
+            d.index = (int)passes.size();
             passes.push_back(d);
+        }
+        // backward ranges after every forward range (the binding kernel gives
+        // ops from bwd_first on the inverse rotation)
+        T.bwd_first = (int)ops.size();
+        for (size_t p = 0; p < pl.passes.size(); p++) {
+            passes[p].bwd_begin = (int)ops.size();
+            ops.insert(ops.end(), pl.passes[p].bwd_ops.begin(), pl.passes[p].bwd_ops.end());
+            passes[p].bwd_end = (int)ops.size();
         }
     }
     std::vector<SlotSrc> slots;
@@ -111,10 +119,11 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
     T.off_gates = put(T.blob, gates);
     T.blob.resize(align256(T.blob.size()), 0);
     T.passes = passes;
+    T.n_ops = (int)ops.size();
 }
 
 struct Layout {
-    size_t tables = 0, coef = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
+    size_t tables = 0, coef = 0, opc = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
     int n_wg = 1;
 };
 
@@ -166,6 +175,13 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L) 
     L.coef = off;
     if (!mul_ok((size_t)B * (size_t)std::max(1, (int)c.slot_gate.size()), amp, sz)) return fail(QL_ENOMEM, "size overflow");
     off = align256(off + sz);
+    if (!pl.whole_state) {
+        // per-sample op records (16 bytes fp32 / 32 bytes fp64) plus an end record
+        L.opc = off;
+        if (!mul_ok((size_t)B * (size_t)(h->t[dt].n_ops + 1), dt == 0 ? 16 : 32, sz))
+            return fail(QL_ENOMEM, "size overflow");
+        off = align256(off + sz);
+    }
     L.zpart = off;
     if (!mul_ok((size_t)B * (size_t)L.n_wg, (size_t)c.n * 8, sz)) return fail(QL_ENOMEM, "size overflow");
     off = align256(off + sz);
@@ -263,17 +279,33 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
     if (e != hipSuccess) return fail(QL_EHIP, std::string("table upload: ") + hipGetErrorString(e));
     Timer tm{h, stream};
 
-    BindArgs ba{};
-    ba.inputs = inputs;
-    ba.weights = weights;
-    ba.slots = (const SlotSrc*)(W + L.tables + T.off_slots);
-    ba.coef = W + L.coef;
-    ba.B = B;
-    ba.n_slots = n_slots;
-    ba.F = c.n_inputs;
-    tm.start(2);
-    e = launch_bind(dt, ba, stream);
-    tm.stop();
+    if (pl.whole_state) {
+        BindArgs ba{};
+        ba.inputs = inputs;
+        ba.weights = weights;
+        ba.slots = (const SlotSrc*)(W + L.tables + T.off_slots);
+        ba.coef = W + L.coef;
+        ba.B = B;
+        ba.n_slots = n_slots;
+        ba.F = c.n_inputs;
+        tm.start(2);
+        e = launch_bind(dt, ba, stream);
+        tm.stop();
+    } else {
+        BindTileArgs ba{};
+        ba.inputs = inputs;
+        ba.weights = weights;
+        ba.slots = (const SlotSrc*)(W + L.tables + T.off_slots);
+        ba.ops = (const DevOp*)(W + L.tables + T.off_ops);
+        ba.opc = W + L.opc;
+        ba.B = B;
+        ba.n_ops = T.n_ops;
+        ba.bwd_first = T.bwd_first;
+        ba.F = c.n_inputs;
+        tm.start(2);
+        e = launch_bind_tile(dt, ba, stream);
+        tm.stop();
+    }
     if (e != hipSuccess) return fail(QL_EHIP, std::string("k_bind: ") + hipGetErrorString(e));
 
     double* zpart = (double*)(W + L.zpart);
@@ -311,14 +343,14 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
             ta.phases = (const DevPhase*)(W + L.tables + T.off_phase);
             ta.ops = (const DevOp*)(W + L.tables + T.off_ops);
             ta.gslots = (const int32_t*)(W + L.tables + T.off_gslot) + d.gslot_base;
-            ta.coef = W + L.coef;
+            ta.opc = W + L.opc;
             ta.grad_out = grad_out;
             ta.zpart = zpart;
             ta.gpart = gpart;
             ta.B = B;
             ta.tiles = (int64_t)1 << (c.n - pl.k);
             ta.n = c.n;
-            ta.n_slots = n_slots;
+            ta.n_ops = T.n_ops;
             ta.n_wg = L.n_wg;
             ta.flags = flags;
             ta.n_gslots = (flags & PF_BWD) ? d.n_gslots : 0;

@@ -43,6 +43,50 @@ __device__ __forceinline__ double wave_sum(double v) {
     return v;
 }
 
+// DPP lane moves (gfx9 encodings): quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_half_mirror, row_mirror. Each is a VALU operand modifier, so a row-local
+// butterfly costs one instruction per step instead of an LDS-pipe permute.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+    const long long u = __builtin_bit_cast(long long, v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(u & 0xffffffff), CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(u >> 32), CTRL, 0xF, 0xF, false);
+    return __builtin_bit_cast(double, ((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Wavefront sum: butterfly inside each 16-lane row (4 DPP adds), then the four
+// row sums combined from readlanes. Returns the (uniform) total in fp64; the
+// adds run in Real, which for fp32 is a 64-term sum of per-thread partials.
+__device__ __forceinline__ double wave_total(float v) {
+    v += dpp_f32<0xB1>(v);
+    v += dpp_f32<0x4E>(v);
+    v += dpp_f32<0x141>(v);
+    v += dpp_f32<0x140>(v);
+    const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+    const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+    const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+    const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+    return ((double)a + (double)b) + ((double)c + (double)d);
+}
+__device__ __forceinline__ double wave_total(double v) {
+    v += dpp_f64<0xB1>(v);
+    v += dpp_f64<0x4E>(v);
+    v += dpp_f64<0x141>(v);
+    v += dpp_f64<0x140>(v);
+    auto lane = [&](int l) {
+        const long long u = __builtin_bit_cast(long long, v);
+        const int lo = __builtin_amdgcn_readlane((int)(u & 0xffffffff), l);
+        const int hi = __builtin_amdgcn_readlane((int)(u >> 32), l);
+        return __builtin_bit_cast(double, ((long long)hi << 32) | (unsigned int)lo);
+    };
+    return (lane(0) + lane(16)) + (lane(32) + lane(48));
+}
+
 // Scatter the low bits of x into the set bits of mask (ascending).
 __device__ __forceinline__ uint32_t deposit(uint32_t x, uint32_t mask) {
     uint32_t r = 0;
@@ -56,146 +100,7 @@ __device__ __forceinline__ uint32_t deposit(uint32_t x, uint32_t mask) {
 }
 
 // ---------------------------------------------------------------------------
-// one-qubit gates on the register bit J of a thread's 2^LOG_R amplitudes.
-// s carries the sign of the rotation: the inverse gate passes -s.
-
-template <int LOG_R, int J, typename T2, typename Real>
-__device__ __forceinline__ void reg_g1(int kind, T2* a, Real c, Real s) {
-    constexpr int R = 1 << LOG_R, M = 1 << J;
-    if (kind == K_H) {
-        const Real r = (Real)0.70710678118654752440;
-#pragma unroll
-        for (int i = 0; i < R; ++i)
-            if (!(i & M)) {
-                const T2 u = a[i], v = a[i | M];
-                a[i] = mk<T2>((u.x + v.x) * r, (u.y + v.y) * r);
-                a[i | M] = mk<T2>((u.x - v.x) * r, (u.y - v.y) * r);
-            }
-    } else if (kind == K_RX) {  // [[c, -is], [-is, c]]
-#pragma unroll
-        for (int i = 0; i < R; ++i)
-            if (!(i & M)) {
-                const T2 u = a[i], v = a[i | M];
-                a[i] = mk<T2>(c * u.x + s * v.y, c * u.y - s * v.x);
-                a[i | M] = mk<T2>(c * v.x + s * u.y, c * v.y - s * u.x);
-            }
-    } else if (kind == K_RY) {  // [[c, -s], [s, c]]
-#pragma unroll
-        for (int i = 0; i < R; ++i)
-            if (!(i & M)) {
-                const T2 u = a[i], v = a[i | M];
-                a[i] = mk<T2>(c * u.x - s * v.x, c * u.y - s * v.y);
-                a[i | M] = mk<T2>(s * u.x + c * v.x, s * u.y + c * v.y);
-            }
-    } else {  // RZ: diag(c - is, c + is)
-#pragma unroll
-        for (int i = 0; i < R; ++i) {
-            const T2 u = a[i];
-            if (i & M) a[i] = mk<T2>(c * u.x - s * u.y, c * u.y + s * u.x);
-            else a[i] = mk<T2>(c * u.x + s * u.y, c * u.y - s * u.x);
-        }
-    }
-}
-
-template <int LOG_R, typename T2, typename Real>
-__device__ __forceinline__ void reg_g1_at(int j, int kind, T2* a, Real c, Real s) {
-    switch (j) {
-        case 0: if constexpr (LOG_R > 0) reg_g1<LOG_R, 0>(kind, a, c, s); break;
-        case 1: if constexpr (LOG_R > 1) reg_g1<LOG_R, 1>(kind, a, c, s); break;
-        case 2: if constexpr (LOG_R > 2) reg_g1<LOG_R, 2>(kind, a, c, s); break;
-        case 3: if constexpr (LOG_R > 3) reg_g1<LOG_R, 3>(kind, a, c, s); break;
-        case 4: if constexpr (LOG_R > 4) reg_g1<LOG_R, 4>(kind, a, c, s); break;
-        default: break;
-    }
-}
-
-// Thread partial of Im<l | P_J | p> for the rotation generator P of `kind`.
-template <int LOG_R, int J, typename T2, typename Real>
-__device__ __forceinline__ Real reg_grad(int kind, const T2* p, const T2* l) {
-    constexpr int R = 1 << LOG_R, M = 1 << J;
-    Real acc = 0;
-    if (kind == K_RZ) {
-#pragma unroll
-        for (int i = 0; i < R; ++i) {
-            const Real t = l[i].x * p[i].y - l[i].y * p[i].x;
-            acc += (i & M) ? -t : t;
-        }
-    } else if (kind == K_RX) {
-#pragma unroll
-        for (int i = 0; i < R; ++i)
-            if (!(i & M)) {
-                const int v = i | M;
-                acc += (l[i].x * p[v].y - l[i].y * p[v].x) + (l[v].x * p[i].y - l[v].y * p[i].x);
-            }
-    } else {  // RY
-#pragma unroll
-        for (int i = 0; i < R; ++i)
-            if (!(i & M)) {
-                const int v = i | M;
-                acc += (l[v].x * p[i].x + l[v].y * p[i].y) - (l[i].x * p[v].x + l[i].y * p[v].y);
-            }
-    }
-    return acc;
-}
-
-template <int LOG_R, typename T2, typename Real>
-__device__ __forceinline__ Real reg_grad_at(int j, int kind, const T2* p, const T2* l) {
-    switch (j) {
-        case 0: if constexpr (LOG_R > 0) return reg_grad<LOG_R, 0, T2, Real>(kind, p, l); break;
-        case 1: if constexpr (LOG_R > 1) return reg_grad<LOG_R, 1, T2, Real>(kind, p, l); break;
-        case 2: if constexpr (LOG_R > 2) return reg_grad<LOG_R, 2, T2, Real>(kind, p, l); break;
-        case 3: if constexpr (LOG_R > 3) return reg_grad<LOG_R, 3, T2, Real>(kind, p, l); break;
-        case 4: if constexpr (LOG_R > 4) return reg_grad<LOG_R, 4, T2, Real>(kind, p, l); break;
-        default: break;
-    }
-    return 0;
-}
-
-// CNOT with target register bit J and control register bit m (runtime).
-template <int LOG_R, int J, typename T2>
-__device__ __forceinline__ void reg_cnot_rr(int m, T2* a) {
-    constexpr int R = 1 << LOG_R, M = 1 << J;
-#pragma unroll
-    for (int i = 0; i < R; ++i)
-        if (!(i & M) && (i >> m & 1)) {
-            const T2 t = a[i];
-            a[i] = a[i | M];
-            a[i | M] = t;
-        }
-}
-
-// CNOT with target register bit J and a per-thread control bit.
-template <int LOG_R, int J, typename T2>
-__device__ __forceinline__ void reg_cnot_sel(bool on, T2* a) {
-    constexpr int R = 1 << LOG_R, M = 1 << J;
-#pragma unroll
-    for (int i = 0; i < R; ++i)
-        if (!(i & M)) {
-            const T2 u = a[i], v = a[i | M];
-            a[i] = on ? v : u;
-            a[i | M] = on ? u : v;
-        }
-}
-
-template <int LOG_R, typename T2>
-__device__ __forceinline__ void reg_cnot_at(int j, bool reg_ctrl, int m, bool on, T2* a) {
-#define QL_CNOT_CASE(J)                                                            \
-    case J:                                                                       \
-        if constexpr (LOG_R > J) {                                                \
-            if (reg_ctrl) reg_cnot_rr<LOG_R, J>(m, a);                            \
-            else reg_cnot_sel<LOG_R, J>(on, a);                                   \
-        }                                                                         \
-        break;
-    switch (j) {
-        QL_CNOT_CASE(0)
-        QL_CNOT_CASE(1)
-        QL_CNOT_CASE(2)
-        QL_CNOT_CASE(3)
-        QL_CNOT_CASE(4)
-        default: break;
-    }
-#undef QL_CNOT_CASE
-}
+// register-tile helpers
 
 // Bank-spreading permutation of LDS slots: folds the upper nibbles of the tile
 // index into the lowest one (an involution on each aligned 2^16 block).
@@ -378,27 +283,329 @@ __global__ void __launch_bounds__(256) k_whole(const WholeArgs a) {
 
 // ---------------------------------------------------------------------------
 // k_tile: one tile pass
+//
+// Each workgroup streams tiles of 2^k amplitudes between HBM and registers and
+// applies the pass's ops there. Every op is a per-sample record (handler id,
+// argument, two coefficients) written by k_bind_tile; the op loop prefetches
+// the next record and dispatches on the handler id into a handler whose
+// register indices are compile-time constants.
+//
+// Every gate updates registers in place, so the state keeps its registers
+// through the dispatch (the library is built with uniform regions left
+// unstructurised). Rotations are exact three-shear products: a plane rotation
+// by phi of (x, y) is  x -= a y;  y += b x;  x -= a y  with a = tan(phi/2),
+// b = sin(phi). RY(theta) rotates (re u, re v) and (im u, im v) by theta/2; RX
+// rotates (re u, im v) by -theta/2 and (im u, re v) by theta/2; RZ rotates
+// each amplitude's (re, im) by -theta/2 (bit 0) or theta/2 (bit 1). Angles are
+// reduced to [-pi, pi] first (a sign common to psi and lambda, which cancels in
+// <Z> and in Im<lambda|P|psi>), so |a| <= 1.
 
-template <int LOG_R, typename T2>
-__device__ __forceinline__ void lds_exchange(T2* a, T2* lds, const DevPhase& from,
-                                             const DevPhase& to, uint32_t& tb, int tid) {
+template <typename Real> struct XOp;
+template <> struct XOp<float> {
+    uint32_t h, arg;
+    float a, b;
+};
+template <> struct XOp<double> {
+    uint32_t h, arg;
+    double a, b;
+    uint64_t pad;
+};
+
+// Offset of register i in tile-index bits (or amplitude-index bits) of a phase:
+// the OR of the masks of i's set bits (compile-time i, uniform masks).
+template <int LOG_R>
+__device__ __forceinline__ uint32_t reg_offset(int i, const uint32_t* mask) {
+    uint32_t r = 0;
+#pragma unroll
+    for (int m = 0; m < LOG_R; ++m)
+        if (i >> m & 1) r |= mask[m];
+    return r;
+}
+
+// Plane rotation of (x, y) by phi, in place: a = tan(phi/2), b = sin(phi).
+template <typename Real>
+__device__ __forceinline__ void shear(Real& x, Real& y, Real a, Real b) {
+    x = fma(-a, y, x);
+    y = fma(b, x, y);
+    x = fma(-a, y, x);
+}
+
+// One-qubit gate (KIND: 0 H, 1 RX, 2 RY, 3 RZ) on register bit J, in place.
+template <int LOG_R, int KIND, int J, typename T2, typename Real>
+__device__ __forceinline__ void g1(T2* s, Real a, Real b) {
+    constexpr int R = 1 << LOG_R, M = 1 << J;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        if (KIND == 3) {  // RZ: rotate (re, im) by -+theta/2
+            if (i & M) shear(s[i].x, s[i].y, a, b);
+            else shear(s[i].x, s[i].y, -a, -b);
+            continue;
+        }
+        if (i & M) continue;
+        T2& u = s[i];
+        T2& v = s[i | M];
+        if (KIND == 0) {  // H: (u + v, u - v) / sqrt2
+            const Real r = (Real)0.70710678118654752440;
+            u.x += v.x;
+            u.y += v.y;
+            v.x = fma((Real)-2, v.x, u.x);
+            v.y = fma((Real)-2, v.y, u.y);
+            u.x *= r;
+            u.y *= r;
+            v.x *= r;
+            v.y *= r;
+        } else if (KIND == 1) {  // RX
+            shear(u.x, v.y, -a, -b);
+            shear(u.y, v.x, a, b);
+        } else {  // RY
+            shear(u.x, v.x, a, b);
+            shear(u.y, v.y, a, b);
+        }
+    }
+}
+
+// Thread partial of Im<l | P_J | p> for the generator P of rotation KIND.
+template <int LOG_R, int KIND, int J, typename T2, typename Real>
+__device__ __forceinline__ Real gpart(const T2* p, const T2* l) {
+    constexpr int R = 1 << LOG_R, M = 1 << J;
+    Real acc = 0;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        if (KIND == 3) {
+            const Real t = l[i].x * p[i].y - l[i].y * p[i].x;
+            acc += (i & M) ? -t : t;
+            continue;
+        }
+        if (i & M) continue;
+        const int v = i | M;
+        if (KIND == 1)
+            acc += (l[i].x * p[v].y - l[i].y * p[v].x) + (l[v].x * p[i].y - l[v].y * p[i].x);
+        else
+            acc += (l[v].x * p[i].x + l[v].y * p[i].y) - (l[i].x * p[v].x + l[i].y * p[v].y);
+    }
+    return acc;
+}
+
+// Accumulator g of a wavefront lives in lane (g & 63) of acc[g >> 6].
+template <int NA>
+__device__ __forceinline__ void slot_add(double (&acc)[NA], uint32_t g, double v, int lane) {
+    const bool mine = lane == (int)(g & 63);
+    const uint32_t r = g >> 6;
+#pragma unroll
+    for (int k = 0; k < NA; ++k) acc[k] += (mine && (uint32_t)k == r) ? v : 0.0;
+}
+
+template <int LOG_R, int J, int MC, typename T2>
+__device__ __forceinline__ void cnot_rr(T2* a) {
+    constexpr int R = 1 << LOG_R, M = 1 << J, C = 1 << MC;
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+        if (!(i & M) && (i & C)) {
+            const T2 t = a[i];
+            a[i] = a[i | M];
+            a[i | M] = t;
+        }
+}
+
+// swap every pair across register bit J (X on that bit)
+template <int LOG_R, int J, typename T2>
+__device__ __forceinline__ void swap_all(T2* a) {
+    constexpr int R = 1 << LOG_R, M = 1 << J;
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+        if (!(i & M)) {
+            const T2 t = a[i];
+            a[i] = a[i | M];
+            a[i | M] = t;
+        }
+}
+
+template <int LOG_R, int J, typename T2>
+__device__ __forceinline__ void cnot_sel(T2* a, bool on) {
+    constexpr int R = 1 << LOG_R, M = 1 << J;
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+        if (!(i & M)) {
+            const T2 u = a[i], v = a[i | M];
+            a[i] = on ? v : u;
+            a[i | M] = on ? u : v;
+        }
+}
+
+template <int LOG_R, int A, int B, typename T2>
+__device__ __forceinline__ void cz_rr(T2* a) {
+    constexpr int R = 1 << LOG_R, MA = 1 << A, MB = 1 << B;
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+        if ((i & MA) && (i & MB)) {
+            a[i].x = -a[i].x;
+            a[i].y = -a[i].y;
+        }
+}
+
+// negate the amplitudes with register bit A set (all when A < 0) where on
+template <int LOG_R, int A, typename T2>
+__device__ __forceinline__ void cz_sel(T2* a, bool on) {
     constexpr int R = 1 << LOG_R;
 #pragma unroll
-    for (int i = 0; i < R; ++i) lds[lds_slot(tb | from.reg_off[i])] = a[i];
-    __syncthreads();
-    tb = deposit((uint32_t)tid, to.thr_mask);
+    for (int i = 0; i < R; ++i)
+        if (A < 0 || (i >> A & 1)) {
+            a[i].x = on ? -a[i].x : a[i].x;
+            a[i].y = on ? -a[i].y : a[i].y;
+        }
+}
+
+// RZ on a thread bit or fixed qubit `bit`.
+template <int LOG_R, typename T2, typename Real>
+__device__ __forceinline__ void rz_u(T2* s, Real a, Real b, bool bit) {
+    const Real sa = bit ? a : -a, sb = bit ? b : -b;
 #pragma unroll
-    for (int i = 0; i < R; ++i) a[i] = lds[lds_slot(tb | to.reg_off[i])];
+    for (int i = 0; i < (1 << LOG_R); ++i) shear(s[i].x, s[i].y, sa, sb);
+}
+
+// Exchange the tile through LDS from layout `from` to layout `to`. lds_slot is
+// linear over GF(2) and thread and register bits are disjoint, so the slot of
+// (thread bits | register bits) is lds_slot(thread bits) ^ lds_slot(register bits).
+template <int LOG_R, typename T2>
+__device__ __forceinline__ void lds_exchange(T2* a, T2* lds, const DevPhase& from,
+                                             const DevPhase& to, uint32_t tb_from, uint32_t tb_to) {
+    constexpr int R = 1 << LOG_R;
+    uint32_t fb = lds_slot(tb_from);
+#pragma unroll
+    for (int i = 0; i < R; ++i) lds[fb ^ lds_slot(reg_offset<LOG_R>(i, from.reg_tmask))] = a[i];
+    __syncthreads();
+    fb = lds_slot(tb_to);
+#pragma unroll
+    for (int i = 0; i < R; ++i) a[i] = lds[fb ^ lds_slot(reg_offset<LOG_R>(i, to.reg_tmask))];
     __syncthreads();
 }
 
-template <typename Real, int LOG_R, bool BWD>
-__global__ void __launch_bounds__(256) k_tile(const TileArgs a) {
+// bit of an operand location word (thread bit or fixed qubit)
+__device__ __forceinline__ bool loc_bit(uint32_t w, uint32_t tb, uint32_t gb) {
+    const uint32_t pos = w & 0xff;
+    return (((w >> 8) & 3) == LOC_THR ? (tb >> pos) : (gb >> pos)) & 1u;
+}
+
+// Per-thread tile state shared by the handlers.
+struct TileCtx {
+    uint32_t tb;  // tile-index bits of this thread (current phase)
+    uint32_t gb;  // amplitude-index bits of the qubits outside the tile
+    int ph;       // current phase
+};
+
+// Apply one op. BWD: inverse on psi and lambda, after the gradient term of a
+// rotation (Im<lambda|P|psi> into the wavefront's accumulator).
+template <int LOG_R, bool BWD, typename T2, typename Real, int NA>
+__device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
+                                       TileCtx& cx, T2* lds, const DevPhase* phases,
+                                       double (&accg)[NA], int lane, int tid) {
+#define QL_G1_CASE(KIND, J)                                                                 \
+    case H_G1 + KIND * 5 + J:                                                               \
+        if constexpr (J < LOG_R) {                                                          \
+            if constexpr (BWD) {                                                            \
+                if (KIND != 0) {                                                            \
+                    const double d = wave_total(gpart<LOG_R, KIND, J, T2, Real>(ps, lm));   \
+                    slot_add(accg, arg, d, lane);                                           \
+                }                                                                           \
+                g1<LOG_R, KIND, J, T2, Real>(lm, ca, cb);                                   \
+            }                                                                               \
+            g1<LOG_R, KIND, J, T2, Real>(ps, ca, cb);                                       \
+        }                                                                                   \
+        break;
+#define QL_G1_J(J) QL_G1_CASE(0, J) QL_G1_CASE(1, J) QL_G1_CASE(2, J) QL_G1_CASE(3, J)
+#define QL_CNOT_RR(J, M)                                                                    \
+    case H_CNOT_RR + J * 5 + M:                                                             \
+        if constexpr (J < LOG_R && M < LOG_R && J != M) {                                   \
+            cnot_rr<LOG_R, J, M>(ps);                                                       \
+            if constexpr (BWD) cnot_rr<LOG_R, J, M>(lm);                                    \
+        }                                                                                   \
+        break;
+#define QL_CNOT_RR_J(J) QL_CNOT_RR(J, 0) QL_CNOT_RR(J, 1) QL_CNOT_RR(J, 2) QL_CNOT_RR(J, 3) QL_CNOT_RR(J, 4)
+#define QL_CNOT_X(J)                                                                        \
+    case H_CNOT_T + J:                                                                      \
+        if constexpr (J < LOG_R) {                                                          \
+            const bool on = (cx.tb >> arg) & 1u;                                            \
+            cnot_sel<LOG_R, J>(ps, on);                                                     \
+            if constexpr (BWD) cnot_sel<LOG_R, J>(lm, on);                                  \
+        }                                                                                   \
+        break;                                                                              \
+    case H_CNOT_F + J:                                                                      \
+        if constexpr (J < LOG_R) {                                                          \
+            if ((cx.gb >> arg) & 1u) {                                                      \
+                swap_all<LOG_R, J>(ps);                                                     \
+                if constexpr (BWD) swap_all<LOG_R, J>(lm);                                  \
+            }                                                                               \
+        }                                                                                   \
+        break;
+#define QL_CZ_RR(A, B)                                                                      \
+    case H_CZ_RR + A * 5 + B:                                                               \
+        if constexpr (A < LOG_R && B < LOG_R && A != B) {                                   \
+            cz_rr<LOG_R, A, B>(ps);                                                         \
+            if constexpr (BWD) cz_rr<LOG_R, A, B>(lm);                                      \
+        }                                                                                   \
+        break;
+#define QL_CZ_RR_A(A) QL_CZ_RR(A, 0) QL_CZ_RR(A, 1) QL_CZ_RR(A, 2) QL_CZ_RR(A, 3) QL_CZ_RR(A, 4)
+#define QL_CZ_RX(A)                                                                         \
+    case H_CZ_RX + A:                                                                       \
+        if constexpr (A < LOG_R) {                                                          \
+            const bool on = loc_bit(arg, cx.tb, cx.gb);                                     \
+            cz_sel<LOG_R, A>(ps, on);                                                       \
+            if constexpr (BWD) cz_sel<LOG_R, A>(lm, on);                                    \
+        }                                                                                   \
+        break;
+    switch (h) {
+        QL_G1_J(0) QL_G1_J(1) QL_G1_J(2) QL_G1_J(3) QL_G1_J(4)
+        QL_CNOT_RR_J(0) QL_CNOT_RR_J(1) QL_CNOT_RR_J(2) QL_CNOT_RR_J(3) QL_CNOT_RR_J(4)
+        QL_CNOT_X(0) QL_CNOT_X(1) QL_CNOT_X(2) QL_CNOT_X(3) QL_CNOT_X(4)
+        QL_CZ_RR_A(0) QL_CZ_RR_A(1) QL_CZ_RR_A(2) QL_CZ_RR_A(3) QL_CZ_RR_A(4)
+        QL_CZ_RX(0) QL_CZ_RX(1) QL_CZ_RX(2) QL_CZ_RX(3) QL_CZ_RX(4)
+        case H_RZU: {
+            const bool bit = loc_bit(arg, cx.tb, cx.gb);
+            if constexpr (BWD) {
+                Real acc = 0;
+#pragma unroll
+                for (int i = 0; i < (1 << LOG_R); ++i) acc += lm[i].x * ps[i].y - lm[i].y * ps[i].x;
+                const double d = wave_total(bit ? -acc : acc);
+                slot_add(accg, arg >> 16, d, lane);
+                rz_u<LOG_R>(lm, ca, cb, bit);
+            }
+            rz_u<LOG_R>(ps, ca, cb, bit);
+        } break;
+        case H_CZ_XX: {
+            const bool on = loc_bit(arg & 0xffff, cx.tb, cx.gb) && loc_bit(arg >> 16, cx.tb, cx.gb);
+            cz_sel<LOG_R, -1>(ps, on);
+            if constexpr (BWD) cz_sel<LOG_R, -1>(lm, on);
+        } break;
+        case H_TRANSPOSE: {
+            const uint32_t tb_to = deposit((uint32_t)tid, phases[arg].thr_mask);
+            lds_exchange<LOG_R>(ps, lds, phases[cx.ph], phases[arg], cx.tb, tb_to);
+            if constexpr (BWD) lds_exchange<LOG_R>(lm, lds, phases[cx.ph], phases[arg], cx.tb, tb_to);
+            cx.tb = tb_to;
+            cx.ph = (int)arg;
+        } break;
+        default:
+            __builtin_unreachable();
+    }
+#undef QL_G1_CASE
+#undef QL_G1_J
+#undef QL_CNOT_RR
+#undef QL_CNOT_RR_J
+#undef QL_CNOT_X
+#undef QL_CZ_RR
+#undef QL_CZ_RR_A
+#undef QL_CZ_RX
+}
+
+template <typename Real, int LOG_R, bool BWD, int MAXT>
+__global__ void __launch_bounds__(MAXT) __attribute__((amdgpu_waves_per_eu(2)))
+k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __restrict__ phases,
+       const XOp<Real>* __restrict__ xops_all, const Real* __restrict__ gout_all,
+       const int32_t* __restrict__ gslots) {
     using T2 = typename Cx<Real>::T;
     constexpr int R = 1 << LOG_R;
+    constexpr int NA = MAX_GSLOTS / 64;
     extern __shared__ __align__(16) unsigned char smem[];
-    const DevPass& P = *a.pass;
-    const DevPhase* phases = a.phases;
+    const DevPass& P = *pass;
     const int tid = threadIdx.x, nt = blockDim.x, NW = nt >> 6;
     const int wave = tid >> 6, lane = tid & 63;
     const int flags = a.flags;
@@ -406,95 +613,63 @@ __global__ void __launch_bounds__(256) k_tile(const TileArgs a) {
     const int w = (int)(blockIdx.x - b * a.n_wg);
     const int n = a.n, k = P.k;
     T2* lds = (T2*)smem;
-    double* accz = (double*)(smem + a.lds_tile_bytes);  // [n][NW]
-    double* accg = accz + n * NW;                       // [n_gslots][NW]
-    for (int i = tid; i < (n + a.n_gslots) * NW; i += nt) accz[i] = 0.0;
-    __syncthreads();
+    double* red = (double*)(smem + a.lds_tile_bytes);  // [n + n_gslots][NW]
 
     const size_t dim = (size_t)1 << n;
     T2* psi_s = (T2*)a.psi + b * dim;
     T2* lam_s = (T2*)a.lam + b * dim;
-    const T2* coef = (const T2*)a.coef + b * a.n_slots;
-    const Real* gout = (const Real*)a.grad_out + b * n;
+    const XOp<Real>* xops = xops_all + b * (a.n_ops + 1);
+    const Real* gout = gout_all + b * n;
+
+    double accg[NA], accz = 0.0;
+#pragma unroll
+    for (int i = 0; i < NA; ++i) accg[i] = 0.0;
 
     T2 ps[R], lm[R];
     for (int64_t tile = w; tile < a.tiles; tile += a.n_wg) {
-        uint32_t gb = 0;  // amplitude index bits of the qubits outside the tile
-        for (int i = 0; i < P.n_fixed; ++i) gb |= (uint32_t)((tile >> i) & 1) << P.fixed_qubit[i];
-        int ph = (flags & PF_FWD) ? P.load_phase : P.bwd_phase;
-        uint32_t tb = deposit((uint32_t)tid, phases[ph].thr_mask);
+        TileCtx cx;
+        cx.gb = 0;
+        for (int i = 0; i < P.n_fixed; ++i) cx.gb |= (uint32_t)((tile >> i) & 1) << P.fixed_qubit[i];
+        cx.ph = (flags & PF_FWD) ? P.load_phase : P.bwd_phase;
+        cx.tb = deposit((uint32_t)tid, phases[cx.ph].thr_mask);
 
+        // amplitude index of (thread bits tbits) in this tile
         auto gaddr_thr = [&](uint32_t tbits) {
             uint32_t g = 0;
             for (int j = 0; j < k; ++j) g |= ((tbits >> j) & 1u) << P.tile_qubit[j];
-            return gb | g;
+            return cx.gb | g;
         };
 
         if (flags & PF_INIT) {
 #pragma unroll
             for (int i = 0; i < R; ++i) ps[i] = mk<T2>((Real)0, (Real)0);
-            if (gb == 0 && tb == 0) ps[0] = mk<T2>((Real)1, (Real)0);
+            if (cx.gb == 0 && cx.tb == 0) ps[0] = mk<T2>((Real)1, (Real)0);
         } else {
-            const uint32_t base = gaddr_thr(tb);
+            const DevPhase& F = phases[cx.ph];
+            const T2* src = psi_s + gaddr_thr(cx.tb);
 #pragma unroll
-            for (int i = 0; i < R; ++i) ps[i] = psi_s[base + phases[ph].greg_off[i]];
+            for (int i = 0; i < R; ++i) ps[i] = src[reg_offset<LOG_R>(i, F.reg_qmask)];
             if (BWD && (flags & PF_LOAD_LAM)) {
+                const T2* lsrc = lam_s + gaddr_thr(cx.tb);
 #pragma unroll
-                for (int i = 0; i < R; ++i) lm[i] = lam_s[base + phases[ph].greg_off[i]];
+                for (int i = 0; i < R; ++i) lm[i] = lsrc[reg_offset<LOG_R>(i, F.reg_qmask)];
             }
         }
 
         // ---- forward ops
         if (flags & PF_FWD) {
+            XOp<Real> cur = xops[P.fwd_begin];
             for (int o = P.fwd_begin; o < P.fwd_end; ++o) {
-                const DevOp op = a.ops[o];
-                Real c = 1, s = 0;
-                if (op.slot >= 0) {
-                    const T2 cs = coef[op.slot];
-                    c = cs.x;
-                    s = cs.y;
-                }
-                switch (op.code) {
-                    case OP_G1:
-                        reg_g1_at<LOG_R>(op.a_pos, op.kind, ps, c, s);
-                        break;
-                    case OP_RZ_U: {
-                        const uint32_t bit = op.a_type == LOC_THR ? (tb >> op.a_pos) & 1u
-                                                                  : (gb >> op.a_pos) & 1u;
-                        const Real ss = bit ? s : -s;
-#pragma unroll
-                        for (int i = 0; i < R; ++i)
-                            ps[i] = mk<T2>(c * ps[i].x - ss * ps[i].y, c * ps[i].y + ss * ps[i].x);
-                    } break;
-                    case OP_CNOT: {
-                        const bool rc = op.b_type == LOC_REG;
-                        const bool on = op.b_type == LOC_THR ? ((tb >> op.b_pos) & 1u)
-                                                             : ((gb >> op.b_pos) & 1u);
-                        reg_cnot_at<LOG_R>(op.a_pos, rc, op.b_pos, on, ps);
-                    } break;
-                    case OP_CZ: {
-                        uint32_t rm = 0;
-                        bool on = true;
-                        if (op.a_type == LOC_REG) rm |= 1u << op.a_pos;
-                        else on = on && ((op.a_type == LOC_THR ? tb : gb) >> op.a_pos & 1u);
-                        if (op.b_type == LOC_REG) rm |= 1u << op.b_pos;
-                        else on = on && ((op.b_type == LOC_THR ? tb : gb) >> op.b_pos & 1u);
-                        const Real sg = on ? (Real)-1 : (Real)1;
-#pragma unroll
-                        for (int i = 0; i < R; ++i)
-                            if ((i & rm) == rm) ps[i] = mk<T2>(sg * ps[i].x, sg * ps[i].y);
-                    } break;
-                    default: {  // OP_TRANSPOSE
-                        lds_exchange<LOG_R>(ps, lds, phases[ph], phases[op.arg], tb, tid);
-                        ph = op.arg;
-                    } break;
-                }
+                const XOp<Real> nxt = xops[o + 1];
+                run_op<LOG_R, false>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, accg,
+                                     lane, tid);
+                cur = nxt;
             }
         }
 
         // ---- <Z_q> partials over this tile
         if (flags & PF_ZPART) {
-            const DevPhase& F = phases[ph];
+            const DevPhase& F = phases[cx.ph];
             Real pt = 0, dm[LOG_R];
 #pragma unroll
             for (int m = 0; m < LOG_R; ++m) dm[m] = 0;
@@ -505,34 +680,33 @@ __global__ void __launch_bounds__(256) k_tile(const TileArgs a) {
 #pragma unroll
                 for (int m = 0; m < LOG_R; ++m) dm[m] += (i >> m & 1) ? -p : p;
             }
-            const double wp = wave_sum((double)pt);
+            const double wp = wave_total(pt);
             for (int j = 0; j < k; ++j) {
-                Real v = (tb >> j & 1u) ? -pt : pt;
+                Real v = (cx.tb >> j & 1u) ? -pt : pt;
 #pragma unroll
                 for (int m = 0; m < LOG_R; ++m)
                     if ((int)F.reg_bit[m] == j) v = dm[m];
-                const double d = wave_sum((double)v);
-                if (lane == 0) accz[P.tile_qubit[j] * NW + wave] += d;
+                const double d = wave_total(v);
+                accz += (lane == P.tile_qubit[j]) ? d : 0.0;
             }
-            if (lane == 0)
-                for (int i = 0; i < P.n_fixed; ++i) {
-                    const int q = P.fixed_qubit[i];
-                    accz[q * NW + wave] += (gb >> q & 1u) ? -wp : wp;
-                }
+            for (int i = 0; i < P.n_fixed; ++i) {
+                const int q = P.fixed_qubit[i];
+                accz += (lane == q) ? ((cx.gb >> q & 1u) ? -wp : wp) : 0.0;
+            }
         }
 
         if constexpr (BWD) {
             // ---- lambda = (sum_q g_q Z_q) psi
             if (flags & PF_SEED) {
-                const DevPhase& F = phases[ph];
+                const DevPhase& F = phases[cx.ph];
                 Real gs = 0, sfix = 0, sthr = 0, gm[LOG_R];
                 for (int q = 0; q < n; ++q) gs += gout[q];
                 for (int i = 0; i < P.n_fixed; ++i) {
                     const int q = P.fixed_qubit[i];
-                    if (gb >> q & 1u) sfix += gout[q];
+                    if (cx.gb >> q & 1u) sfix += gout[q];
                 }
                 for (int j = 0; j < k; ++j)
-                    if ((F.thr_mask >> j & 1u) && (tb >> j & 1u)) sthr += gout[P.tile_qubit[j]];
+                    if ((F.thr_mask >> j & 1u) && (cx.tb >> j & 1u)) sthr += gout[P.tile_qubit[j]];
 #pragma unroll
                 for (int m = 0; m < LOG_R; ++m) gm[m] = gout[P.tile_qubit[F.reg_bit[m]]];
 #pragma unroll
@@ -546,100 +720,93 @@ __global__ void __launch_bounds__(256) k_tile(const TileArgs a) {
                 }
             }
 
-            // ---- backward ops: gradient, then un-apply on psi and lambda
+            // ---- backward ops
             if (flags & PF_BWD) {
+                XOp<Real> cur = xops[P.bwd_begin];
                 for (int o = P.bwd_begin; o < P.bwd_end; ++o) {
-                    const DevOp op = a.ops[o];
-                    Real c = 1, s = 0;
-                    if (op.slot >= 0) {
-                        const T2 cs = coef[op.slot];
-                        c = cs.x;
-                        s = -cs.y;  // inverse rotation
-                    }
-                    switch (op.code) {
-                        case OP_G1:
-                            if (op.gslot >= 0) {
-                                const double d = wave_sum(
-                                    (double)reg_grad_at<LOG_R, T2, Real>(op.a_pos, op.kind, ps, lm));
-                                if (lane == 0) accg[op.gslot * NW + wave] += d;
-                            }
-                            reg_g1_at<LOG_R>(op.a_pos, op.kind, ps, c, s);
-                            reg_g1_at<LOG_R>(op.a_pos, op.kind, lm, c, s);
-                            break;
-                        case OP_RZ_U: {
-                            const uint32_t bit = op.a_type == LOC_THR ? (tb >> op.a_pos) & 1u
-                                                                      : (gb >> op.a_pos) & 1u;
-                            Real acc = 0;
-#pragma unroll
-                            for (int i = 0; i < R; ++i) acc += lm[i].x * ps[i].y - lm[i].y * ps[i].x;
-                            const double d = wave_sum((double)(bit ? -acc : acc));
-                            if (lane == 0) accg[op.gslot * NW + wave] += d;
-                            const Real ss = bit ? s : -s;
-#pragma unroll
-                            for (int i = 0; i < R; ++i) {
-                                ps[i] = mk<T2>(c * ps[i].x - ss * ps[i].y, c * ps[i].y + ss * ps[i].x);
-                                lm[i] = mk<T2>(c * lm[i].x - ss * lm[i].y, c * lm[i].y + ss * lm[i].x);
-                            }
-                        } break;
-                        case OP_CNOT: {
-                            const bool rc = op.b_type == LOC_REG;
-                            const bool on = op.b_type == LOC_THR ? ((tb >> op.b_pos) & 1u)
-                                                                 : ((gb >> op.b_pos) & 1u);
-                            reg_cnot_at<LOG_R>(op.a_pos, rc, op.b_pos, on, ps);
-                            reg_cnot_at<LOG_R>(op.a_pos, rc, op.b_pos, on, lm);
-                        } break;
-                        case OP_CZ: {
-                            uint32_t rm = 0;
-                            bool on = true;
-                            if (op.a_type == LOC_REG) rm |= 1u << op.a_pos;
-                            else on = on && ((op.a_type == LOC_THR ? tb : gb) >> op.a_pos & 1u);
-                            if (op.b_type == LOC_REG) rm |= 1u << op.b_pos;
-                            else on = on && ((op.b_type == LOC_THR ? tb : gb) >> op.b_pos & 1u);
-                            const Real sg = on ? (Real)-1 : (Real)1;
-#pragma unroll
-                            for (int i = 0; i < R; ++i)
-                                if ((i & rm) == rm) {
-                                    ps[i] = mk<T2>(sg * ps[i].x, sg * ps[i].y);
-                                    lm[i] = mk<T2>(sg * lm[i].x, sg * lm[i].y);
-                                }
-                        } break;
-                        default: {  // OP_TRANSPOSE
-                            uint32_t tb0 = tb;
-                            lds_exchange<LOG_R>(ps, lds, phases[ph], phases[op.arg], tb, tid);
-                            lds_exchange<LOG_R>(lm, lds, phases[ph], phases[op.arg], tb0, tid);
-                            ph = op.arg;
-                        } break;
-                    }
+                    const XOp<Real> nxt = xops[o + 1];
+                    run_op<LOG_R, true>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, accg,
+                                        lane, tid);
+                    cur = nxt;
                 }
             }
         }
 
         if (flags & (PF_STORE_PSI | PF_STORE_LAM)) {
-            const uint32_t base = gaddr_thr(tb);
+            const DevPhase& F = phases[cx.ph];
+            const uint32_t base = gaddr_thr(cx.tb);
             if (flags & PF_STORE_PSI) {
+                T2* dst = psi_s + base;
 #pragma unroll
-                for (int i = 0; i < R; ++i) psi_s[base + phases[ph].greg_off[i]] = ps[i];
+                for (int i = 0; i < R; ++i) dst[reg_offset<LOG_R>(i, F.reg_qmask)] = ps[i];
             }
             if (BWD && (flags & PF_STORE_LAM)) {
+                T2* dst = lam_s + base;
 #pragma unroll
-                for (int i = 0; i < R; ++i) lam_s[base + phases[ph].greg_off[i]] = lm[i];
+                for (int i = 0; i < R; ++i) dst[reg_offset<LOG_R>(i, F.reg_qmask)] = lm[i];
             }
         }
     }
 
+    // combine the wavefronts' accumulators (fixed order) and write the partials
+    if (flags & PF_ZPART) {
+        if (lane < n) red[lane * NW + wave] = accz;
+    }
+    if (BWD && (flags & PF_BWD)) {
+#pragma unroll
+        for (int r = 0; r < NA; ++r) {
+            const int g = r * 64 + lane;
+            if (g < a.n_gslots) red[(n + g) * NW + wave] = accg[r];
+        }
+    }
     __syncthreads();
     if (flags & PF_ZPART)
         for (int q = tid; q < n; q += nt) {
             double t = 0;
-            for (int v = 0; v < NW; ++v) t += accz[q * NW + v];
+            for (int v = 0; v < NW; ++v) t += red[q * NW + v];
             a.zpart[((size_t)b * a.n_wg + w) * n + q] = t;
         }
     if (BWD && (flags & PF_BWD))
         for (int g = tid; g < a.n_gslots; g += nt) {
             double t = 0;
-            for (int v = 0; v < NW; ++v) t += accg[g * NW + v];
-            a.gpart[((size_t)a.gslots[g] * a.B + b) * a.n_wg + w] = t;
+            for (int v = 0; v < NW; ++v) t += red[(n + g) * NW + v];
+            a.gpart[((size_t)gslots[g] * a.B + b) * a.n_wg + w] = t;
         }
+}
+
+// ---------------------------------------------------------------------------
+// k_bind_tile: per-sample op records of every tile op (one thread per
+// (sample, op)); shear coefficients in fp64, rounded once. The inverse of a
+// rotation (backward ops) negates both coefficients.
+
+template <typename Real>
+__global__ void k_bind_tile(const BindTileArgs a) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t per = (int64_t)a.n_ops + 1;
+    if (t >= a.B * per) return;
+    const int64_t b = t / per;
+    const int o = (int)(t - b * per);
+    XOp<Real> e{};
+    if (o == a.n_ops) {  // the record after the last op (read by the op-loop prefetch)
+        e.h = H_END;
+        ((XOp<Real>*)a.opc)[t] = e;
+        return;
+    }
+    const DevOp op = a.ops[o];
+    e.h = op.h;
+    e.arg = op.arg;
+    if (op.slot >= 0) {
+        const SlotSrc src = a.slots[op.slot];
+        double th = src.src == S_INPUT ? (double)((const Real*)a.inputs)[b * a.F + src.index]
+                                       : (double)((const Real*)a.weights)[src.index];
+        const double two_pi = 6.283185307179586476925;
+        th -= two_pi * rint(th / two_pi);  // [-pi, pi]; the dropped sign is common to psi and lambda
+        if (o >= a.bwd_first) th = -th;     // backward ops apply the inverse
+        // plane rotation by phi = theta/2: a = tan(phi/2), b = sin(phi)
+        e.a = (Real)tan(0.25 * th);
+        e.b = (Real)sin(0.5 * th);
+    }
+    ((XOp<Real>*)a.opc)[t] = e;
 }
 
 // ---------------------------------------------------------------------------
@@ -701,30 +868,49 @@ hipError_t launch_whole(int dtype, const WholeArgs& a, int threads, size_t lds, 
     return hipGetLastError();
 }
 
-template <typename Real, int LOG_R>
+template <typename Real, int LOG_R, int MAXT>
 static hipError_t launch_tile_t(bool bwd, const TileArgs& a, int threads, size_t lds, hipStream_t s) {
     const dim3 grid((unsigned)(a.B * a.n_wg));
-    if (bwd) hipLaunchKernelGGL((k_tile<Real, LOG_R, true>), grid, dim3(threads), lds, s, a);
-    else hipLaunchKernelGGL((k_tile<Real, LOG_R, false>), grid, dim3(threads), lds, s, a);
+    const XOp<Real>* xo = (const XOp<Real>*)a.opc;
+    const Real* gout = (const Real*)a.grad_out;
+    if (bwd)
+        hipLaunchKernelGGL((k_tile<Real, LOG_R, true, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
+                           a.phases, xo, gout, a.gslots);
+    else
+        hipLaunchKernelGGL((k_tile<Real, LOG_R, false, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
+                           a.phases, xo, gout, a.gslots);
+    return hipGetLastError();
+}
+
+hipError_t launch_bind_tile(int dtype, const BindTileArgs& a, hipStream_t s) {
+    const int64_t total = a.B * ((int64_t)a.n_ops + 1);
+    const unsigned grid = (unsigned)((total + 255) / 256);
+    if (dtype == 0) hipLaunchKernelGGL(k_bind_tile<float>, dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_bind_tile<double>, dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_tile(int dtype, int log_r, bool bwd, const TileArgs& a, int threads, size_t lds,
                        hipStream_t s) {
+    const bool big = threads > 256;
+#define QL_LT(REAL, LR)                                                                   \
+    return big ? launch_tile_t<REAL, LR, 512>(bwd, a, threads, lds, s)                    \
+               : launch_tile_t<REAL, LR, 256>(bwd, a, threads, lds, s);
     if (dtype == 0) {
         switch (log_r) {
-            case 2: return launch_tile_t<float, 2>(bwd, a, threads, lds, s);
-            case 3: return launch_tile_t<float, 3>(bwd, a, threads, lds, s);
-            case 4: return launch_tile_t<float, 4>(bwd, a, threads, lds, s);
-            case 5: return launch_tile_t<float, 5>(bwd, a, threads, lds, s);
+            case 2: QL_LT(float, 2)
+            case 3: QL_LT(float, 3)
+            case 4: QL_LT(float, 4)
+            case 5: QL_LT(float, 5)
         }
     } else {
         switch (log_r) {
-            case 2: return launch_tile_t<double, 2>(bwd, a, threads, lds, s);
-            case 3: return launch_tile_t<double, 3>(bwd, a, threads, lds, s);
-            case 4: return launch_tile_t<double, 4>(bwd, a, threads, lds, s);
+            case 2: QL_LT(double, 2)
+            case 3: QL_LT(double, 3)
+            case 4: QL_LT(double, 4)
         }
     }
+#undef QL_LT
     return hipErrorInvalidValue;
 }
 
@@ -749,20 +935,17 @@ hipError_t configure_kernels(size_t max_lds) {
                                 hipFuncAttributeMaxDynamicSharedMemorySize, v);
     QL_ATTR((k_whole<float>))
     QL_ATTR((k_whole<double>))
-    QL_ATTR((k_tile<float, 2, false>))
-    QL_ATTR((k_tile<float, 2, true>))
-    QL_ATTR((k_tile<float, 3, false>))
-    QL_ATTR((k_tile<float, 3, true>))
-    QL_ATTR((k_tile<float, 4, false>))
-    QL_ATTR((k_tile<float, 4, true>))
-    QL_ATTR((k_tile<float, 5, false>))
-    QL_ATTR((k_tile<float, 5, true>))
-    QL_ATTR((k_tile<double, 2, false>))
-    QL_ATTR((k_tile<double, 2, true>))
-    QL_ATTR((k_tile<double, 3, false>))
-    QL_ATTR((k_tile<double, 3, true>))
-    QL_ATTR((k_tile<double, 4, false>))
-    QL_ATTR((k_tile<double, 4, true>))
+#define QL_ATTR_T(REAL, LR)                                                               \
+    QL_ATTR((k_tile<REAL, LR, false, 256>)) QL_ATTR((k_tile<REAL, LR, true, 256>))          \
+    QL_ATTR((k_tile<REAL, LR, false, 512>)) QL_ATTR((k_tile<REAL, LR, true, 512>))
+    QL_ATTR_T(float, 2)
+    QL_ATTR_T(float, 3)
+    QL_ATTR_T(float, 4)
+    QL_ATTR_T(float, 5)
+    QL_ATTR_T(double, 2)
+    QL_ATTR_T(double, 3)
+    QL_ATTR_T(double, 4)
+#undef QL_ATTR_T
 #undef QL_ATTR
     return e;
 }

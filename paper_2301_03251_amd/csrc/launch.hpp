@@ -28,6 +28,19 @@ struct BindArgs {
     int32_t n_slots, F;
 };
 
+// Per-sample records of the tile ops (handler id, argument, two shear
+// coefficients of the rotation angle); ops at index >= bwd_first belong to
+// backward ranges and get the inverse rotation.
+struct BindTileArgs {
+    const void* inputs;    // [B][F] Real
+    const void* weights;   // [P] Real
+    const SlotSrc* slots;  // [n_slots]
+    const DevOp* ops;      // [n_ops]
+    void* opc;             // [B][n_ops + 1] records
+    int64_t B;
+    int32_t n_ops, bwd_first, F;
+};
+
 struct WholeArgs {
     const DevGate* gates;
     int32_t n_gates, n, n_slots;
@@ -46,13 +59,13 @@ struct TileArgs {
     const DevPhase* phases;
     const DevOp* ops;
     const int32_t* gslots;     // pass-local gradient index -> rotation slot
-    const void* coef;          // [B][n_slots]
+    const void* opc;           // [B][n_ops + 1] per-sample op records
     const void* grad_out;      // [B][n] Real
     double* zpart;             // [B][n_wg][n]
     double* gpart;             // [n_slots][B][n_wg]
     int64_t B;
     int64_t tiles;             // tiles per sample = 2^(n-k)
-    int32_t n, n_slots, n_wg, flags;
+    int32_t n, n_ops, n_wg, flags;
     int32_t n_gslots;          // gradient accumulators of this pass
     int32_t lds_tile_bytes;    // 0 when the pass needs no LDS exchange
 };
@@ -74,6 +87,7 @@ struct ReduceArgs {
 
 // dtype: 0 = complex64 / fp32, 1 = complex128 / fp64. Return hipError_t.
 hipError_t launch_bind(int dtype, const BindArgs& a, hipStream_t s);
+hipError_t launch_bind_tile(int dtype, const BindTileArgs& a, hipStream_t s);
 hipError_t launch_whole(int dtype, const WholeArgs& a, int threads, size_t lds, hipStream_t s);
 hipError_t launch_tile(int dtype, int log_r, bool bwd, const TileArgs& a, int threads, size_t lds,
                        hipStream_t s);

@@ -38,12 +38,14 @@ std::vector<int> scan(const std::vector<Gate>& gates, const std::vector<char>& d
     std::vector<int> exec;
     uint64_t blocked = 0;
     int count = __builtin_popcountll(tile);
+    int rotations = 0;
     for (int i = 0; i < (int)gates.size(); i++) {
         if (done[i]) continue;
         const Gate& g = gates[i];
         uint64_t qs = (1ull << g.q0) | (n_qubits_of(g) == 2 ? (1ull << g.q1) : 0);
         if (qs & blocked) { blocked |= qs; continue; }
         if (max_gates > 0 && (int)exec.size() >= max_gates) { blocked |= qs; continue; }
+        if (is_rotation(g.kind) && rotations >= MAX_GSLOTS) { blocked |= qs; continue; }
         int need = needed_tile_qubit(g);
         bool ok = need < 0 || (tile >> need & 1);
         if (!ok && grow && count < cap) {
@@ -51,8 +53,12 @@ std::vector<int> scan(const std::vector<Gate>& gates, const std::vector<char>& d
             count++;
             ok = true;
         }
-        if (ok) exec.push_back(i);
-        else blocked |= qs;
+        if (ok) {
+            exec.push_back(i);
+            rotations += is_rotation(g.kind);
+        } else {
+            blocked |= qs;
+        }
     }
     return exec;
 }
@@ -62,20 +68,11 @@ DevPhase make_phase(const std::vector<int>& tq, const std::vector<int>& reg_bits
     uint32_t regmask = 0;
     for (int m = 0; m < (int)reg_bits.size(); m++) {
         p.reg_bit[m] = reg_bits[m];
+        p.reg_tmask[m] = 1u << reg_bits[m];
+        p.reg_qmask[m] = 1u << tq[reg_bits[m]];
         regmask |= 1u << reg_bits[m];
     }
     p.thr_mask = ((k >= 32) ? 0xffffffffu : ((1u << k) - 1)) & ~regmask;
-    int R = 1 << reg_bits.size();
-    for (int i = 0; i < R; i++) {
-        uint32_t off = 0, goff = 0;
-        for (int m = 0; m < (int)reg_bits.size(); m++)
-            if (i >> m & 1) {
-                off |= 1u << reg_bits[m];
-                goff |= 1u << tq[reg_bits[m]];
-            }
-        p.reg_off[i] = off;
-        p.greg_off[i] = goff;
-    }
     return p;
 }
 
@@ -126,15 +123,23 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
     pp.first_phase = cur_phase;
 
     // gradient accumulators: one per rotation in this pass
-    std::vector<int> gslot_of(gates.size(), -1);
     int n_gs = 0;
 
-    auto loc = [&](int q, uint8_t& type, uint8_t& pos) {
+    // location of qubit q in the current phase
+    auto loc = [&](int q, uint32_t& type, uint32_t& pos) {
         int j = bit_of[q];
-        if (j < 0) { type = LOC_FIX; pos = (uint8_t)q; return; }
+        if (j < 0) { type = LOC_FIX; pos = (uint32_t)q; return; }
         auto it = std::find(regs.begin(), regs.end(), j);
-        if (it != regs.end()) { type = LOC_REG; pos = (uint8_t)(it - regs.begin()); }
-        else { type = LOC_THR; pos = (uint8_t)j; }
+        if (it != regs.end()) { type = LOC_REG; pos = (uint32_t)(it - regs.begin()); }
+        else { type = LOC_THR; pos = (uint32_t)j; }
+    };
+    auto make_op = [&](uint32_t h, uint32_t arg, int slot, int kind) {
+        DevOp op{};
+        op.h = h;
+        op.arg = arg;
+        op.slot = slot;
+        op.kind = (uint32_t)kind;
+        return op;
     };
     struct Rec { DevOp op; int prev_phase; };
     std::vector<Rec> recs;
@@ -149,33 +154,38 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
             bool ok = !(qs & blocked) &&
                       (b < 0 || std::find(regs.begin(), regs.end(), b) != regs.end());
             if (!ok) { blocked |= qs; rest.push_back(gi); continue; }
-            DevOp op{};
-            op.slot = g.slot;
-            op.gslot = -1;
-            op.kind = (uint8_t)g.kind;
+            uint32_t gs = NO_GSLOT;
             if (is_rotation(g.kind)) {
-                gslot_of[gi] = n_gs++;
-                op.gslot = gslot_of[gi];
+                gs = (uint32_t)n_gs++;
                 pp.gslots.push_back(g.slot);
             }
+            uint32_t ta, pa, tb, pb;
+            DevOp op{};
             switch (g.kind) {
-                case K_H: case K_RX: case K_RY:
-                    op.code = OP_G1;
-                    loc(g.q0, op.a_type, op.a_pos);
-                    break;
-                case K_RZ:
-                    loc(g.q0, op.a_type, op.a_pos);
-                    op.code = op.a_type == LOC_REG ? OP_G1 : OP_RZ_U;
+                case K_H: case K_RX: case K_RY: case K_RZ:
+                    loc(g.q0, ta, pa);
+                    if (ta == LOC_REG)
+                        op = make_op(H_G1 + (uint32_t)(g.kind * 5 + (int)pa), gs, g.slot, g.kind);
+                    else  // only RZ reaches here: diagonal, no register bit needed
+                        op = make_op(H_RZU, loc_word(ta, pa) | (gs << 16), g.slot, g.kind);
                     break;
                 case K_CNOT:
-                    op.code = OP_CNOT;
-                    loc(g.q1, op.a_type, op.a_pos);
-                    loc(g.q0, op.b_type, op.b_pos);
+                    loc(g.q1, ta, pa);  // target: always a register bit here
+                    loc(g.q0, tb, pb);
+                    if (tb == LOC_REG) op = make_op(H_CNOT_RR + pa * 5 + pb, 0, -1, K_CNOT);
+                    else if (tb == LOC_THR) op = make_op(H_CNOT_T + pa, pb, -1, K_CNOT);
+                    else op = make_op(H_CNOT_F + pa, pb, -1, K_CNOT);
                     break;
                 case K_CZ:
-                    op.code = OP_CZ;
-                    loc(g.q0, op.a_type, op.a_pos);
-                    loc(g.q1, op.b_type, op.b_pos);
+                    loc(g.q0, ta, pa);
+                    loc(g.q1, tb, pb);
+                    if (ta != LOC_REG && tb == LOC_REG) {
+                        std::swap(ta, tb);
+                        std::swap(pa, pb);
+                    }
+                    if (ta == LOC_REG && tb == LOC_REG) op = make_op(H_CZ_RR + pa * 5 + pb, 0, -1, K_CZ);
+                    else if (ta == LOC_REG) op = make_op(H_CZ_RX + pa, loc_word(tb, pb), -1, K_CZ);
+                    else op = make_op(H_CZ_XX, loc_word(ta, pa) | (loc_word(tb, pb) << 16), -1, K_CZ);
                     break;
             }
             recs.push_back({op, -1});
@@ -185,12 +195,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         regs = choose(0, regs);
         int np = (int)phases.size();
         phases.push_back(make_phase(pp.qubits, regs, k));
-        DevOp t{};
-        t.code = OP_TRANSPOSE;
-        t.arg = (uint16_t)np;
-        t.slot = -1;
-        t.gslot = -1;
-        recs.push_back({t, cur_phase});
+        recs.push_back({make_op(H_TRANSPOSE, (uint32_t)np, -1, K_H), cur_phase});
         cur_phase = np;
         pp.n_transposes++;
     }
@@ -205,12 +210,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         regs = choose(low_mask, keep);
         int np = (int)phases.size();
         phases.push_back(make_phase(pp.qubits, regs, k));
-        DevOp t{};
-        t.code = OP_TRANSPOSE;
-        t.arg = (uint16_t)np;
-        t.slot = -1;
-        t.gslot = -1;
-        recs.push_back({t, cur_phase});
+        recs.push_back({make_op(H_TRANSPOSE, (uint32_t)np, -1, K_H), cur_phase});
         cur_phase = np;
         pp.n_transposes++;
     }
@@ -218,7 +218,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
     for (auto& rc : recs) pp.fwd_ops.push_back(rc.op);
     for (int i = (int)recs.size() - 1; i >= 0; i--) {
         DevOp op = recs[i].op;
-        if (op.code == OP_TRANSPOSE) op.arg = (uint16_t)recs[i].prev_phase;
+        if (op.h == H_TRANSPOSE) op.arg = (uint32_t)recs[i].prev_phase;
         pp.bwd_ops.push_back(op);
     }
 }
@@ -268,7 +268,7 @@ std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, i
     }
     const Options& o = opts;
     if (o.log_regs && (o.log_regs < 2 || o.log_regs > MAX_LOG_R)) return "option: log_regs out of range [2, 5]";
-    if (o.log_threads && (o.log_threads < 6 || o.log_threads > 8)) return "option: log_threads out of range [6, 8]";
+    if (o.log_threads && (o.log_threads < 6 || o.log_threads > 9)) return "option: log_threads out of range [6, 9]";
     if (o.low_qubits && (o.low_qubits < 1 || o.low_qubits > 8)) return "option: low_qubits out of range [1, 8]";
     if (o.max_gates_per_pass < 0) return "option: max_gates_per_pass < 0";
     if (o.wg_per_sample < 0) return "option: wg_per_sample < 0";

@@ -34,35 +34,49 @@ struct Gate {
 // Operand location relative to the current tile phase.
 enum LocType : uint8_t { LOC_REG = 0, LOC_THR = 1, LOC_FIX = 2 };
 
-enum OpCode : uint8_t {
-    OP_G1 = 0,         // H / RX / RY / RZ on register bit a
-    OP_RZ_U = 1,       // RZ on a thread bit or fixed qubit (one phase per thread)
-    OP_CNOT = 2,       // target register bit a, control b (any location)
-    OP_CZ = 3,         // a, b any locations
-    OP_TRANSPOSE = 4,  // switch to phase `arg`
+// Handler ids of tile ops: a dense enumeration so the kernels dispatch every op
+// with one switch onto a handler whose register indices are compile-time
+// constants.
+enum HandlerId : uint32_t {
+    H_G1 = 0,          // + kind * 5 + J: H, RX, RY or RZ on register bit J; arg = gradient slot
+    H_RZU = 20,        // RZ on a thread bit or fixed qubit; arg = loc | gslot << 16
+    H_CNOT_RR = 21,    // + J * 5 + m: target register bit J, control register bit m
+    H_CNOT_T = 46,     // + J: control is a thread bit (arg = tile bit)
+    H_CNOT_F = 51,     // + J: control is a fixed qubit (arg = qubit)
+    H_CZ_RR = 56,      // + a * 5 + b: both register bits
+    H_CZ_RX = 81,      // + a: register bit a, other operand in arg (loc)
+    H_CZ_XX = 86,      // both operands thread/fixed bits: arg = loc_a | loc_b << 16
+    H_TRANSPOSE = 87,  // arg = phase index
+    H_END = 88,
 };
+// A loc in an op argument: tile bit or qubit in bits 0..7, LocType in bits 8..9.
+constexpr uint32_t loc_word(uint32_t type, uint32_t pos) { return pos | (type << 8); }
+constexpr uint32_t NO_GSLOT = 0xffffu;
 
-// Device op: 16 bytes, read with scalar loads.
+// Static op of a tile pass (the binding kernel turns it into a per-sample record).
 struct DevOp {
-    uint8_t code, kind;
-    uint8_t a_type, a_pos;   // target / first operand
-    uint8_t b_type, b_pos;   // control / second operand
-    uint16_t arg;            // TRANSPOSE: phase index (global in the plan)
-    int32_t slot;            // rotation slot (coefficient table column), -1 none
-    int32_t gslot;           // pass-local gradient accumulator index, -1 none
+    uint32_t h;      // handler id
+    uint32_t arg;    // handler argument (H_G1: gradient slot or NO_GSLOT)
+    int32_t slot;    // rotation slot (angle source), -1 none
+    uint32_t kind;   // gate kind (K_*), or K_H for non-gates
 };
 static_assert(sizeof(DevOp) == 16, "DevOp layout");
+
+// Gradient accumulators per pass (one per rotation in the pass).
+constexpr int MAX_GSLOTS = 256;
 
 constexpr int MAX_LOG_R = 5;
 constexpr int MAX_R = 1 << MAX_LOG_R;
 constexpr int MAX_TILE_BITS = 16;
 
-// Register layout of one phase.
+// Register layout of one phase: register bit m of a thread's amplitude index
+// is tile bit reg_bit[m]; the remaining tile bits (thr_mask, ascending) are the
+// thread index bits. The kernel forms per-register offsets from the masks.
 struct DevPhase {
-    uint32_t thr_mask;            // tile bits held by the thread index (ascending -> tid bits)
-    uint32_t reg_bit[MAX_LOG_R];  // register position m -> tile bit
-    uint32_t reg_off[MAX_R];      // tile-index offset of register i
-    uint32_t greg_off[MAX_R];     // amplitude offset (in the sample) of register i
+    uint32_t thr_mask;             // tile bits held by the thread index
+    uint32_t reg_bit[MAX_LOG_R];   // register bit m -> tile bit
+    uint32_t reg_tmask[MAX_LOG_R]; // 1 << reg_bit[m]
+    uint32_t reg_qmask[MAX_LOG_R]; // 1 << (qubit of tile bit reg_bit[m])
 };
 
 enum PassFlags : int32_t {
@@ -87,8 +101,10 @@ struct DevPass {
     int32_t bwd_phase;       // layout at the start of the backward ops
     int32_t gslot_base;      // first entry in the plan's gslot -> rotation-slot table
     int32_t n_exchanges;     // LDS layout changes in the forward ops
+    int32_t index;           // pass index in the plan
     int32_t tile_qubit[MAX_TILE_BITS];  // tile bit -> qubit
     int32_t fixed_qubit[32];            // ascending qubits outside the tile
+    int32_t pad[3];
 };
 
 struct Options {

@@ -67,7 +67,7 @@ def test_create_rejects(lib, gates, n, F, P, code):
 
 
 @pytest.mark.parametrize("opts", [dict(log_regs=1), dict(log_regs=6), dict(log_threads=5),
-                                  dict(log_threads=9), dict(low_qubits=9), dict(wg_per_sample=-1)])
+                                  dict(log_threads=10), dict(low_qubits=9), dict(wg_per_sample=-1)])
 def test_create_rejects_options(lib, opts):
     assert _err(lambda: Q.Circuit(14, np.array(G1, np.int32), 0, 1, **opts)) == -3
 

@@ -58,6 +58,73 @@ def check(got, want, tol, what, keys=("expz", "grad_inputs", "grad_weights")):
 
 
 # ---------------------------------------------------------------------------
+# random circuits on every code path
+
+TILED = [
+    # n, G, B, dtype, options
+    (9, 60, 3, "c64", dict(force_tiled=1, log_regs=3, log_threads=6)),
+    (10, 80, 2, "c128", dict(force_tiled=1, log_regs=2, log_threads=6)),
+    (11, 90, 3, "c64", dict(force_tiled=1, log_regs=4, log_threads=6, low_qubits=2)),
+    (11, 90, 3, "c128", dict(force_tiled=1, log_regs=3, log_threads=7, low_qubits=3)),
+    (12, 120, 2, "c64", dict(force_tiled=1, log_regs=5, log_threads=6)),
+    (12, 120, 2, "c64", dict(force_tiled=1, log_regs=4, log_threads=6, max_gates_per_pass=1)),
+    (13, 150, 3, "c64", dict()),
+    (13, 150, 3, "c128", dict(force_tiled=1, log_regs=4, log_threads=8, max_gates_per_pass=7)),
+    (14, 200, 2, "c64", dict()),
+    (14, 200, 2, "c128", dict()),
+    (14, 160, 3, "c64", dict(log_regs=2, log_threads=8, low_qubits=1)),
+    (15, 160, 2, "c64", dict(log_regs=5, log_threads=7, wg_per_sample=3)),
+]
+
+
+@pytest.mark.parametrize("n,G,B,dtype,opts", TILED,
+                         ids=[f"n{c[0]}-{c[3]}-{'-'.join(f'{k}{v}' for k, v in c[4].items()) or 'default'}"
+                              for c in TILED])
+def test_random_tiled(n, G, B, dtype, opts):
+    F, P = 5, 7
+    gates = W.random_circuit(n, G, F, P, seed=n * 100 + G)
+    x, w, g = W.random_inputs(B, F, P, n, seed=n + G, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P, **opts)
+    info = circ.plan_info(dtype)
+    assert info["kernel"] == 1
+    got = gpu_fb(circ, dtype, x, w, g)
+    want = oracle.run(n, gates, x, w, grad_out=g)
+    check(got, want, TOL[dtype], f"tiled n={n} {dtype} {opts} passes={info['n_passes']}")
+
+
+@pytest.mark.parametrize("dtype", ["c64", "c128"])
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 7, 8, 11, 12])
+def test_random_whole_state(n, dtype):
+    if dtype == "c128" and n == 12:
+        n = 11
+    F, P = 3, 4
+    gates = W.random_circuit(n, 40 + 5 * n, F, P, seed=7 * n + 1)
+    x, w, g = W.random_inputs(5, F, P, n, seed=n, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P)
+    assert circ.plan_info(dtype)["kernel"] == 0
+    check(gpu_fb(circ, dtype, x, w, g), oracle.run(n, gates, x, w, grad_out=g), TOL[dtype],
+          f"whole n={n} {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["c64", "c128"])
+def test_degenerate_circuits(dtype):
+    """No gates, no rotations, inputs only, weights only."""
+    n, B = 13, 2
+    cases = [
+        (np.zeros((0, 5), np.int32), 0, 0),
+        (np.array([[W.H, 0, -1, 0, 0], [W.CNOT, 0, 12, 0, 0], [W.CZ, 12, 3, 0, 0]], np.int32), 0, 0),
+        (np.array([[W.RY, q, -1, W.SRC_INPUT, q % 2] for q in range(n)], np.int32), 2, 0),
+        (np.array([[W.RX, q, -1, W.SRC_WEIGHT, 0] for q in range(n)], np.int32), 0, 1),
+    ]
+    for gates, F, P in cases:
+        for opts in (dict(), dict(force_tiled=1)):
+            x, w, g = W.random_inputs(B, F, P, n, seed=3, dtype=dtype)
+            circ = Q.Circuit(n, gates, F, P, **opts)
+            got = gpu_fb(circ, dtype, x, w, g)
+            check(got, oracle.run(n, gates, x, w, grad_out=g), TOL[dtype], f"degenerate {gates.shape[0]} gates")
+
+
+# ---------------------------------------------------------------------------
 # the five workloads
 
 @pytest.mark.parametrize("name", ["4q", "10q"])
@@ -132,73 +199,6 @@ def test_workload_golden(name):
           {"expz": gold["expz"], "grad_inputs": gold["grad_inputs"],
            "grad_weights": gold["grad_weights"]}, TOL[wl.dtype], name)
     assert np.all(np.abs(got["expz"]) <= 1 + 1e-5)
-
-
-# ---------------------------------------------------------------------------
-# random circuits on every code path
-
-TILED = [
-    # n, G, B, dtype, options
-    (9, 60, 3, "c64", dict(force_tiled=1, log_regs=3, log_threads=6)),
-    (10, 80, 2, "c128", dict(force_tiled=1, log_regs=2, log_threads=6)),
-    (11, 90, 3, "c64", dict(force_tiled=1, log_regs=4, log_threads=6, low_qubits=2)),
-    (11, 90, 3, "c128", dict(force_tiled=1, log_regs=3, log_threads=7, low_qubits=3)),
-    (12, 120, 2, "c64", dict(force_tiled=1, log_regs=5, log_threads=6)),
-    (12, 120, 2, "c64", dict(force_tiled=1, log_regs=4, log_threads=6, max_gates_per_pass=1)),
-    (13, 150, 3, "c64", dict()),
-    (13, 150, 3, "c128", dict(force_tiled=1, log_regs=4, log_threads=8, max_gates_per_pass=7)),
-    (14, 200, 2, "c64", dict()),
-    (14, 200, 2, "c128", dict()),
-    (14, 160, 3, "c64", dict(log_regs=2, log_threads=8, low_qubits=1)),
-    (15, 160, 2, "c64", dict(log_regs=5, log_threads=7, wg_per_sample=3)),
-]
-
-
-@pytest.mark.parametrize("n,G,B,dtype,opts", TILED,
-                         ids=[f"n{c[0]}-{c[3]}-{'-'.join(f'{k}{v}' for k, v in c[4].items()) or 'default'}"
-                              for c in TILED])
-def test_random_tiled(n, G, B, dtype, opts):
-    F, P = 5, 7
-    gates = W.random_circuit(n, G, F, P, seed=n * 100 + G)
-    x, w, g = W.random_inputs(B, F, P, n, seed=n + G, dtype=dtype)
-    circ = Q.Circuit(n, gates, F, P, **opts)
-    info = circ.plan_info(dtype)
-    assert info["kernel"] == 1
-    got = gpu_fb(circ, dtype, x, w, g)
-    want = oracle.run(n, gates, x, w, grad_out=g)
-    check(got, want, TOL[dtype], f"tiled n={n} {dtype} {opts} passes={info['n_passes']}")
-
-
-@pytest.mark.parametrize("dtype", ["c64", "c128"])
-@pytest.mark.parametrize("n", [1, 2, 3, 5, 7, 8, 11, 12])
-def test_random_whole_state(n, dtype):
-    if dtype == "c128" and n == 12:
-        n = 11
-    F, P = 3, 4
-    gates = W.random_circuit(n, 40 + 5 * n, F, P, seed=7 * n + 1)
-    x, w, g = W.random_inputs(5, F, P, n, seed=n, dtype=dtype)
-    circ = Q.Circuit(n, gates, F, P)
-    assert circ.plan_info(dtype)["kernel"] == 0
-    check(gpu_fb(circ, dtype, x, w, g), oracle.run(n, gates, x, w, grad_out=g), TOL[dtype],
-          f"whole n={n} {dtype}")
-
-
-@pytest.mark.parametrize("dtype", ["c64", "c128"])
-def test_degenerate_circuits(dtype):
-    """No gates, no rotations, inputs only, weights only."""
-    n, B = 13, 2
-    cases = [
-        (np.zeros((0, 5), np.int32), 0, 0),
-        (np.array([[W.H, 0, -1, 0, 0], [W.CNOT, 0, 12, 0, 0], [W.CZ, 12, 3, 0, 0]], np.int32), 0, 0),
-        (np.array([[W.RY, q, -1, W.SRC_INPUT, q % 2] for q in range(n)], np.int32), 2, 0),
-        (np.array([[W.RX, q, -1, W.SRC_WEIGHT, 0] for q in range(n)], np.int32), 0, 1),
-    ]
-    for gates, F, P in cases:
-        for opts in (dict(), dict(force_tiled=1)):
-            x, w, g = W.random_inputs(B, F, P, n, seed=3, dtype=dtype)
-            circ = Q.Circuit(n, gates, F, P, **opts)
-            got = gpu_fb(circ, dtype, x, w, g)
-            check(got, oracle.run(n, gates, x, w, grad_out=g), TOL[dtype], f"degenerate {gates.shape[0]} gates")
 
 
 def test_batch_edges():
