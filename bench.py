@@ -15,6 +15,7 @@ whole state; the batch/state sharding design is documented separately).
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -29,6 +30,36 @@ import workloads as W  # noqa: E402
 
 METRIC = "amplitude-gate updates/s (batched fwd+adjoint grad); % of HBM peak BW"
 HBM_PEAK_GBS = 8000.0
+# fp32 FMA without packed-FP32 instructions: 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz
+ALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+# Algorithmic flops per amplitude: a rotation (RX/RY/RZ) is a real plane rotation
+# of each amplitude pair's components, 6 flops per amplitude; H is 4; CNOT/CZ
+# are permutations/signs (0). One step applies every gate once (forward) and
+# un-applies it on psi and lambda (backward); each rotation also takes a
+# gradient term Im<lambda|P|psi> (4 flops per amplitude).
+FLOPS_FWD = {W.H: 4, W.RX: 6, W.RY: 6, W.RZ: 6, W.CNOT: 0, W.CZ: 0}
+FLOPS_GRAD = 4
+
+
+def algorithmic_flops(wl) -> float:
+    per_amp = 0
+    for g in wl.gates():
+        k = int(g[0])
+        per_amp += 3 * FLOPS_FWD[k] + (FLOPS_GRAD if k in W.ROTATIONS else 0)
+    return float(per_amp) * wl.batch * (1 << wl.n)
+
+
+def profiled_traffic(wl):
+    """Calibrated HBM bytes per step of the tile kernel from the committed
+    rocprofv3 summary, if it was taken with the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"k_tile_{wl.name}_b{wl.batch}_{wl.dtype}.txt")
+    if not os.path.exists(path):
+        return None
+    fields = dict(l.split(": ", 1) for l in open(path).read().splitlines() if ": " in l and not l.startswith("#"))
+    src = os.path.join(ROOT, "paper_2301_03251_amd", "csrc", "kernels.hip")
+    if fields.get("kernels_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    return float(fields["traffic_bytes_per_step"])
 
 
 def cpu_baseline(wl, n_gates: int):
@@ -59,6 +90,9 @@ def main():
                     help="gates in the CPU-oracle sample (0 disables it)")
     ap.add_argument("--no-timing", action="store_true",
                     help="time only the whole step (no per-kernel events)")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="run one 1 GiB device-to-device copy first (a plain copy kernel of known "
+                         "size, to scale hardware byte counters)")
     ap.add_argument("--opt", action="append", default=[],
                     help="planner option key=value (log_regs, log_threads, low_qubits, "
                          "max_gates_per_pass, wg_per_sample)")
@@ -86,6 +120,13 @@ def main():
             torch.empty((wl.batch, wl.n_inputs), dtype=real, device=dev),
             torch.empty(wl.n_weights, dtype=real, device=dev))
     runner.workspace(wl.batch, Q.MODE_FWD_BWD)
+    if args.calibrate:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         runner.forward_backward(xt, wt, gt, outs=outs)
@@ -127,19 +168,29 @@ def main():
     if timing and kcnt[0] > 0:
         tile_ms = kms[0] / args.steps
         state_bytes = circ.state_bytes(wl.dtype, wl.batch)
-        achieved = state_bytes / (tile_ms / 1e3) / 1e9
-        line["roofline"] = {"bound": "hbm", "kernel": "k_tile", "achieved": achieved,
-                            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                            "traffic": None,
-                            "launches_per_step": kcnt[0] / args.steps,
+        hbm = state_bytes / (tile_ms / 1e3) / 1e9
+        flops = algorithmic_flops(wl)
+        alu = flops / (tile_ms / 1e3) / 1e12
+        traffic = profiled_traffic(wl)
+        launches = kcnt[0] / args.steps
+        line["roofline"] = {"bound": "alu", "kernel": "k_tile", "achieved": alu,
+                            "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": alu / ALU_PEAK_TFLOPS,
+                            "traffic": None if traffic is None else traffic / launches,
+                            "traffic_unit": "bytes per launch",
+                            "launches_per_step": launches,
                             "kernel_ms_per_step": tile_ms,
-                            "algorithmic_bytes_per_step": state_bytes}
+                            "algorithmic_flops_per_step": flops,
+                            "algorithmic_bytes_per_step": state_bytes,
+                            "hbm": {"achieved": hbm, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                    "frac": hbm / HBM_PEAK_GBS}}
         line["kernel_ms_per_step"] = {"k_tile": kms[0] / args.steps, "k_whole": kms[1] / args.steps,
                                       "k_bind": kms[2] / args.steps, "k_reduce": kms[3] / args.steps}
     elif timing and kcnt[1] > 0:
-        line["roofline"] = {"bound": "alu", "kernel": "k_whole", "achieved": None, "peak": None,
-                            "unit": None, "frac": None, "traffic": None,
-                            "kernel_ms_per_step": kms[1] / args.steps}
+        whole_ms = kms[1] / args.steps
+        alu = algorithmic_flops(wl) / (whole_ms / 1e3) / 1e12
+        line["roofline"] = {"bound": "alu", "kernel": "k_whole", "achieved": alu,
+                            "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": alu / ALU_PEAK_TFLOPS,
+                            "traffic": None, "kernel_ms_per_step": whole_ms}
     if args.cpu_gates > 0:
         line["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_gates, wl.n_gates))
     print(json.dumps(line), flush=True)
