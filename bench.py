@@ -52,7 +52,7 @@ def algorithmic_flops(wl) -> float:
 def profiled_traffic(wl):
     """Calibrated HBM bytes per step of the tile kernel from the committed
     rocprofv3 summary, if it was taken with the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"k_tile_{wl.name}_b{wl.batch}_{wl.dtype}.txt")
+    path = os.path.join(ROOT, "profiles", f"k_tile_{wl.name}.txt")
     if not os.path.exists(path):
         return None
     fields = dict(l.split(": ", 1) for l in open(path).read().splitlines() if ": " in l and not l.startswith("#"))
