@@ -295,10 +295,17 @@ __global__ void __launch_bounds__(256) k_whole(const WholeArgs a) {
 // unstructurised). Rotations are exact three-shear products: a plane rotation
 // by phi of (x, y) is  x -= a y;  y += b x;  x -= a y  with a = tan(phi/2),
 // b = sin(phi). RY(theta) rotates (re u, re v) and (im u, im v) by theta/2; RX
-// rotates (re u, im v) by -theta/2 and (im u, re v) by theta/2; RZ rotates
-// each amplitude's (re, im) by -theta/2 (bit 0) or theta/2 (bit 1). Angles are
+// rotates (re u, im v) by -theta/2 and (im u, re v) by theta/2. Angles are
 // reduced to [-pi, pi] first (a sign common to psi and lambda, which cancels in
 // <Z> and in Im<lambda|P|psi>), so |a| <= 1.
+//
+// RZ(theta) = exp(-i theta/2) diag(1, exp(i theta)). On a register bit the
+// kernel applies diag(1, exp(i theta)) only: the dropped factor is a global
+// phase applied identically to psi and lambda (lambda is seeded from psi and
+// both are un-applied by the same inverses), so it cancels in <Z> and in every
+// Im<lambda|P|psi>. Only the bit-1 amplitudes are rotated, by theta reduced to
+// [-pi/2, pi/2]; when the reduction moved theta by pi the rotated amplitudes
+// are also negated (handler H_RZN, chosen per sample by k_bind_tile).
 
 template <typename Real> struct XOp;
 template <> struct XOp<float> {
@@ -330,15 +337,26 @@ __device__ __forceinline__ void shear(Real& x, Real& y, Real a, Real b) {
     x = fma(-a, y, x);
 }
 
+// -(rotation by phi) of (x, y), in place; the negations are operand modifiers.
+template <typename Real>
+__device__ __forceinline__ void shear_neg(Real& x, Real& y, Real a, Real b) {
+    x = fma(-a, y, x);
+    y = fma(-b, x, -y);
+    x = fma(-a, y, -x);
+}
+
 // One-qubit gate (KIND: 0 H, 1 RX, 2 RY, 3 RZ) on register bit J, in place.
-template <int LOG_R, int KIND, int J, typename T2, typename Real>
+// RZ applies diag(1, exp(i phi)) (a, b from phi; NEG: diag(1, -exp(i phi))).
+template <int LOG_R, int KIND, int J, typename T2, typename Real, bool NEG = false>
 __device__ __forceinline__ void g1(T2* s, Real a, Real b) {
     constexpr int R = 1 << LOG_R, M = 1 << J;
 #pragma unroll
     for (int i = 0; i < R; ++i) {
-        if (KIND == 3) {  // RZ: rotate (re, im) by -+theta/2
-            if (i & M) shear(s[i].x, s[i].y, a, b);
-            else shear(s[i].x, s[i].y, -a, -b);
+        if (KIND == 3) {  // RZ: phase on the bit-1 amplitudes only
+            if (i & M) {
+                if (NEG) shear_neg(s[i].x, s[i].y, a, b);
+                else shear(s[i].x, s[i].y, a, b);
+            }
             continue;
         }
         if (i & M) continue;
@@ -364,35 +382,88 @@ __device__ __forceinline__ void g1(T2* s, Real a, Real b) {
     }
 }
 
-// Thread partial of Im<l | P_J | p> for the generator P of rotation KIND.
+// Thread partial of Im<l | P_J | p> for the generator P of rotation KIND, as
+// two interleaved FMA chains.
 template <int LOG_R, int KIND, int J, typename T2, typename Real>
 __device__ __forceinline__ Real gpart(const T2* p, const T2* l) {
     constexpr int R = 1 << LOG_R, M = 1 << J;
-    Real acc = 0;
+    Real acc[2] = {0, 0};
 #pragma unroll
     for (int i = 0; i < R; ++i) {
-        if (KIND == 3) {
-            const Real t = l[i].x * p[i].y - l[i].y * p[i].x;
-            acc += (i & M) ? -t : t;
+        if (KIND == 3) {  // Z: (l.x p.y - l.y p.x), negated where bit J is set
+            Real& c = acc[i & 1];
+            if (i & M) {
+                c = fma(-l[i].x, p[i].y, c);
+                c = fma(l[i].y, p[i].x, c);
+            } else {
+                c = fma(l[i].x, p[i].y, c);
+                c = fma(-l[i].y, p[i].x, c);
+            }
             continue;
         }
         if (i & M) continue;
         const int v = i | M;
-        if (KIND == 1)
-            acc += (l[i].x * p[v].y - l[i].y * p[v].x) + (l[v].x * p[i].y - l[v].y * p[i].x);
-        else
-            acc += (l[v].x * p[i].x + l[v].y * p[i].y) - (l[i].x * p[v].x + l[i].y * p[v].y);
+        Real& c = acc[(i >> (J == 0 ? 1 : 0)) & 1];
+        if (KIND == 1) {  // X
+            c = fma(l[i].x, p[v].y, c);
+            c = fma(-l[i].y, p[v].x, c);
+            c = fma(l[v].x, p[i].y, c);
+            c = fma(-l[v].y, p[i].x, c);
+        } else {  // Y
+            c = fma(l[v].x, p[i].x, c);
+            c = fma(l[v].y, p[i].y, c);
+            c = fma(-l[i].x, p[v].x, c);
+            c = fma(-l[i].y, p[v].y, c);
+        }
     }
-    return acc;
+    return acc[0] + acc[1];
 }
 
-// Accumulator g of a wavefront lives in lane (g & 63) of acc[g >> 6].
-template <int NA>
-__device__ __forceinline__ void slot_add(double (&acc)[NA], uint32_t g, double v, int lane) {
-    const bool mine = lane == (int)(g & 63);
-    const uint32_t r = g >> 6;
-#pragma unroll
-    for (int k = 0; k < NA; ++k) acc[k] += (mine && (uint32_t)k == r) ? v : 0.0;
+// DPP row broadcast (row_bcast:15 into rows 1 and 3, row_bcast:31 into rows 2
+// and 3); lanes of the other rows read 0.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float bcast_f32(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                 ROWS, 0xF, false));
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double bcast_f64(double v) {
+    const long long u = __builtin_bit_cast(long long, v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(u & 0xffffffff), CTRL, ROWS, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(u >> 32), CTRL, ROWS, 0xF, false);
+    return __builtin_bit_cast(double, ((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Wavefront sum left in lane 63 (other lanes hold partial sums): the row
+// butterfly, then rows 0+1 and 2+3, then all four. Fixed order.
+__device__ __forceinline__ float wave_to_last(float v) {
+    v += dpp_f32<0xB1>(v);
+    v += dpp_f32<0x4E>(v);
+    v += dpp_f32<0x141>(v);
+    v += dpp_f32<0x140>(v);
+    v += bcast_f32<0x142, 0xA>(v);
+    v += bcast_f32<0x143, 0xC>(v);
+    return v;
+}
+__device__ __forceinline__ double wave_to_last(double v) {
+    v += dpp_f64<0xB1>(v);
+    v += dpp_f64<0x4E>(v);
+    v += dpp_f64<0x141>(v);
+    v += dpp_f64<0x140>(v);
+    v += bcast_f64<0x142, 0xA>(v);
+    v += bcast_f64<0x143, 0xC>(v);
+    return v;
+}
+
+// Add the wavefront's gradient partial to its LDS accumulator gacc[g][wave].
+// Only lane 63 of this wavefront ever touches that word, so the sum is in
+// program order (deterministic); the add has no return value.
+template <typename Real>
+__device__ __forceinline__ void grad_add(Real* gacc, uint32_t g, Real part, int lane, int wave, int nw) {
+    const Real w = wave_to_last(part);
+    if (lane == 63)
+        __hip_atomic_fetch_add(gacc + g * (uint32_t)nw + (uint32_t)wave, w, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 template <int LOG_R, int J, int MC, typename T2>
@@ -495,21 +566,29 @@ struct TileCtx {
 
 // Apply one op. BWD: inverse on psi and lambda, after the gradient term of a
 // rotation (Im<lambda|P|psi> into the wavefront's accumulator).
-template <int LOG_R, bool BWD, typename T2, typename Real, int NA>
+template <int LOG_R, bool BWD, typename T2, typename Real>
 __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
-                                       TileCtx& cx, T2* lds, const DevPhase* phases,
-                                       double (&accg)[NA], int lane, int tid) {
+                                       TileCtx& cx, T2* lds, const DevPhase* phases, Real* gacc,
+                                       int lane, int wave, int nw, int tid) {
 #define QL_G1_CASE(KIND, J)                                                                 \
     case H_G1 + KIND * 5 + J:                                                               \
         if constexpr (J < LOG_R) {                                                          \
             if constexpr (BWD) {                                                            \
-                if (KIND != 0) {                                                            \
-                    const double d = wave_total(gpart<LOG_R, KIND, J, T2, Real>(ps, lm));   \
-                    slot_add(accg, arg, d, lane);                                           \
-                }                                                                           \
+                if (KIND != 0)                                                              \
+                    grad_add(gacc, arg, gpart<LOG_R, KIND, J, T2, Real>(ps, lm), lane, wave, nw); \
                 g1<LOG_R, KIND, J, T2, Real>(lm, ca, cb);                                   \
             }                                                                               \
             g1<LOG_R, KIND, J, T2, Real>(ps, ca, cb);                                       \
+        }                                                                                   \
+        break;
+#define QL_RZN_CASE(J)                                                                      \
+    case H_RZN + J:                                                                         \
+        if constexpr (J < LOG_R) {                                                          \
+            if constexpr (BWD) {                                                            \
+                grad_add(gacc, arg, gpart<LOG_R, 3, J, T2, Real>(ps, lm), lane, wave, nw);  \
+                g1<LOG_R, 3, J, T2, Real, true>(lm, ca, cb);                                \
+            }                                                                               \
+            g1<LOG_R, 3, J, T2, Real, true>(ps, ca, cb);                                    \
         }                                                                                   \
         break;
 #define QL_G1_J(J) QL_G1_CASE(0, J) QL_G1_CASE(1, J) QL_G1_CASE(2, J) QL_G1_CASE(3, J)
@@ -559,14 +638,18 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         QL_CNOT_X(0) QL_CNOT_X(1) QL_CNOT_X(2) QL_CNOT_X(3) QL_CNOT_X(4)
         QL_CZ_RR_A(0) QL_CZ_RR_A(1) QL_CZ_RR_A(2) QL_CZ_RR_A(3) QL_CZ_RR_A(4)
         QL_CZ_RX(0) QL_CZ_RX(1) QL_CZ_RX(2) QL_CZ_RX(3) QL_CZ_RX(4)
+        QL_RZN_CASE(0) QL_RZN_CASE(1) QL_RZN_CASE(2) QL_RZN_CASE(3) QL_RZN_CASE(4)
         case H_RZU: {
             const bool bit = loc_bit(arg, cx.tb, cx.gb);
             if constexpr (BWD) {
-                Real acc = 0;
+                Real acc[2] = {0, 0};
 #pragma unroll
-                for (int i = 0; i < (1 << LOG_R); ++i) acc += lm[i].x * ps[i].y - lm[i].y * ps[i].x;
-                const double d = wave_total(bit ? -acc : acc);
-                slot_add(accg, arg >> 16, d, lane);
+                for (int i = 0; i < (1 << LOG_R); ++i) {
+                    acc[i & 1] = fma(lm[i].x, ps[i].y, acc[i & 1]);
+                    acc[i & 1] = fma(-lm[i].y, ps[i].x, acc[i & 1]);
+                }
+                const Real t = acc[0] + acc[1];
+                grad_add(gacc, arg >> 16, bit ? -t : t, lane, wave, nw);
                 rz_u<LOG_R>(lm, ca, cb, bit);
             }
             rz_u<LOG_R>(ps, ca, cb, bit);
@@ -587,6 +670,7 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
             __builtin_unreachable();
     }
 #undef QL_G1_CASE
+#undef QL_RZN_CASE
 #undef QL_G1_J
 #undef QL_CNOT_RR
 #undef QL_CNOT_RR_J
@@ -603,7 +687,6 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
        const int32_t* __restrict__ gslots) {
     using T2 = typename Cx<Real>::T;
     constexpr int R = 1 << LOG_R;
-    constexpr int NA = MAX_GSLOTS / 64;
     extern __shared__ __align__(16) unsigned char smem[];
     const DevPass& P = *pass;
     const int tid = threadIdx.x, nt = blockDim.x, NW = nt >> 6;
@@ -613,7 +696,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     const int w = (int)(blockIdx.x - b * a.n_wg);
     const int n = a.n, k = P.k;
     T2* lds = (T2*)smem;
-    double* red = (double*)(smem + a.lds_tile_bytes);  // [n + n_gslots][NW]
+    double* red = (double*)(smem + a.lds_tile_bytes);  // [n][NW]
+    Real* gacc = (Real*)(red + (size_t)n * NW);        // [n_gslots][NW]
 
     const size_t dim = (size_t)1 << n;
     T2* psi_s = (T2*)a.psi + b * dim;
@@ -621,9 +705,11 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     const XOp<Real>* xops = xops_all + b * (a.n_ops + 1);
     const Real* gout = gout_all + b * n;
 
-    double accg[NA], accz = 0.0;
-#pragma unroll
-    for (int i = 0; i < NA; ++i) accg[i] = 0.0;
+    double accz = 0.0;
+    if (BWD && (flags & PF_BWD)) {
+        for (int i = tid; i < a.n_gslots * NW; i += nt) gacc[i] = (Real)0;
+        __syncthreads();
+    }
 
     T2 ps[R], lm[R];
     for (int64_t tile = w; tile < a.tiles; tile += a.n_wg) {
@@ -661,8 +747,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
             XOp<Real> cur = xops[P.fwd_begin];
             for (int o = P.fwd_begin; o < P.fwd_end; ++o) {
                 const XOp<Real> nxt = xops[o + 1];
-                run_op<LOG_R, false>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, accg,
-                                     lane, tid);
+                run_op<LOG_R, false>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, gacc,
+                                     lane, wave, NW, tid);
                 cur = nxt;
             }
         }
@@ -725,8 +811,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 XOp<Real> cur = xops[P.bwd_begin];
                 for (int o = P.bwd_begin; o < P.bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
-                    run_op<LOG_R, true>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, accg,
-                                        lane, tid);
+                    run_op<LOG_R, true>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, gacc,
+                                        lane, wave, NW, tid);
                     cur = nxt;
                 }
             }
@@ -752,13 +838,6 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     if (flags & PF_ZPART) {
         if (lane < n) red[lane * NW + wave] = accz;
     }
-    if (BWD && (flags & PF_BWD)) {
-#pragma unroll
-        for (int r = 0; r < NA; ++r) {
-            const int g = r * 64 + lane;
-            if (g < a.n_gslots) red[(n + g) * NW + wave] = accg[r];
-        }
-    }
     __syncthreads();
     if (flags & PF_ZPART)
         for (int q = tid; q < n; q += nt) {
@@ -769,7 +848,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     if (BWD && (flags & PF_BWD))
         for (int g = tid; g < a.n_gslots; g += nt) {
             double t = 0;
-            for (int v = 0; v < NW; ++v) t += red[(n + g) * NW + v];
+            for (int v = 0; v < NW; ++v) t += (double)gacc[g * NW + v];
             a.gpart[((size_t)gslots[g] * a.B + b) * a.n_wg + w] = t;
         }
 }
@@ -802,9 +881,21 @@ __global__ void k_bind_tile(const BindTileArgs a) {
         const double two_pi = 6.283185307179586476925;
         th -= two_pi * rint(th / two_pi);  // [-pi, pi]; the dropped sign is common to psi and lambda
         if (o >= a.bwd_first) th = -th;     // backward ops apply the inverse
-        // plane rotation by phi = theta/2: a = tan(phi/2), b = sin(phi)
-        e.a = (Real)tan(0.25 * th);
-        e.b = (Real)sin(0.5 * th);
+        if (op.h >= H_G1 + 15 && op.h < H_G1 + 20) {
+            // RZ on a register bit: phase exp(i phi) on the bit-1 amplitudes,
+            // phi = theta moved into [-pi/2, pi/2] (a move by pi negates them)
+            const double half_pi = 1.570796326794896619231;
+            double phi = th;
+            if (phi > half_pi) phi -= 2.0 * half_pi;
+            else if (phi < -half_pi) phi += 2.0 * half_pi;
+            if (phi != th) e.h = H_RZN + (op.h - (H_G1 + 15));
+            e.a = (Real)tan(0.5 * phi);
+            e.b = (Real)sin(phi);
+        } else {
+            // plane rotation by phi = theta/2: a = tan(phi/2), b = sin(phi)
+            e.a = (Real)tan(0.25 * th);
+            e.b = (Real)sin(0.5 * th);
+        }
     }
     ((XOp<Real>*)a.opc)[t] = e;
 }

@@ -47,7 +47,9 @@ enum HandlerId : uint32_t {
     H_CZ_RX = 81,      // + a: register bit a, other operand in arg (loc)
     H_CZ_XX = 86,      // both operands thread/fixed bits: arg = loc_a | loc_b << 16
     H_TRANSPOSE = 87,  // arg = phase index
-    H_END = 88,
+    H_RZN = 88,        // + J: RZ on register bit J whose phase on bit 1 is negated (set per sample
+                       //      by the binding kernel in place of H_G1 + 15 + J)
+    H_END = 93,
 };
 // A loc in an op argument: tile bit or qubit in bits 0..7, LocType in bits 8..9.
 constexpr uint32_t loc_word(uint32_t type, uint32_t pos) { return pos | (type << 8); }
