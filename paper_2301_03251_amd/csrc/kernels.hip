@@ -466,16 +466,30 @@ __device__ __forceinline__ void grad_add(Real* gacc, uint32_t g, Real part, int 
                                __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
+// Exchange two values in place (their registers keep their roles, so the
+// state's register assignment is the same before and after the op).
+__device__ __forceinline__ void xswap(float& x, float& y) {
+    asm("v_swap_b32 %0, %1" : "+v"(x), "+v"(y));
+}
+__device__ __forceinline__ void xswap(double& x, double& y) {
+    uint2 a = __builtin_bit_cast(uint2, x), b = __builtin_bit_cast(uint2, y);
+    asm("v_swap_b32 %0, %1" : "+v"(a.x), "+v"(b.x));
+    asm("v_swap_b32 %0, %1" : "+v"(a.y), "+v"(b.y));
+    x = __builtin_bit_cast(double, a);
+    y = __builtin_bit_cast(double, b);
+}
+template <typename T2>
+__device__ __forceinline__ void xswap2(T2& u, T2& v) {
+    xswap(u.x, v.x);
+    xswap(u.y, v.y);
+}
+
 template <int LOG_R, int J, int MC, typename T2>
 __device__ __forceinline__ void cnot_rr(T2* a) {
     constexpr int R = 1 << LOG_R, M = 1 << J, C = 1 << MC;
 #pragma unroll
     for (int i = 0; i < R; ++i)
-        if (!(i & M) && (i & C)) {
-            const T2 t = a[i];
-            a[i] = a[i | M];
-            a[i | M] = t;
-        }
+        if (!(i & M) && (i & C)) xswap2(a[i], a[i | M]);
 }
 
 // swap every pair across register bit J (X on that bit)
@@ -484,23 +498,13 @@ __device__ __forceinline__ void swap_all(T2* a) {
     constexpr int R = 1 << LOG_R, M = 1 << J;
 #pragma unroll
     for (int i = 0; i < R; ++i)
-        if (!(i & M)) {
-            const T2 t = a[i];
-            a[i] = a[i | M];
-            a[i | M] = t;
-        }
+        if (!(i & M)) xswap2(a[i], a[i | M]);
 }
 
+// swap_all in the lanes where `on` holds
 template <int LOG_R, int J, typename T2>
 __device__ __forceinline__ void cnot_sel(T2* a, bool on) {
-    constexpr int R = 1 << LOG_R, M = 1 << J;
-#pragma unroll
-    for (int i = 0; i < R; ++i)
-        if (!(i & M)) {
-            const T2 u = a[i], v = a[i | M];
-            a[i] = on ? v : u;
-            a[i | M] = on ? u : v;
-        }
+    if (on) swap_all<LOG_R, J>(a);
 }
 
 template <int LOG_R, int A, int B, typename T2>
