@@ -32,12 +32,14 @@ METRIC = "amplitude-gate updates/s (batched fwd+adjoint grad); % of HBM peak BW"
 HBM_PEAK_GBS = 8000.0
 # fp32 FMA without packed-FP32 instructions: 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz
 ALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
-# Algorithmic flops per amplitude: a rotation (RX/RY/RZ) is a real plane rotation
-# of each amplitude pair's components, 6 flops per amplitude; H is 4; CNOT/CZ
-# are permutations/signs (0). One step applies every gate once (forward) and
-# un-applies it on psi and lambda (backward); each rotation also takes a
-# gradient term Im<lambda|P|psi> (4 flops per amplitude).
-FLOPS_FWD = {W.H: 4, W.RX: 6, W.RY: 6, W.RZ: 6, W.CNOT: 0, W.CZ: 0}
+# Algorithmic flops per amplitude, each gate in its cheapest exact form: RX/RY
+# rotate a real plane per pair of components, 6 flops per amplitude; RZ is, up
+# to a global phase, a complex multiply of the bit-1 half of the amplitudes,
+# 3 flops per amplitude; H is 4; CNOT/CZ are permutations/signs (0). One step
+# applies every gate once (forward) and un-applies it on psi and lambda
+# (backward); each rotation also takes a gradient term Im<lambda|P|psi>
+# (4 flops per amplitude).
+FLOPS_FWD = {W.H: 4, W.RX: 6, W.RY: 6, W.RZ: 3, W.CNOT: 0, W.CZ: 0}
 FLOPS_GRAD = 4
 
 

@@ -568,6 +568,24 @@ struct TileCtx {
     int ph;       // current phase
 };
 
+// An empty asm that reads every amplitude of a register tile: the compiler
+// waits for the tile's pending loads here, once, instead of before the first
+// use of each register inside every op handler.
+template <int R>
+__device__ __forceinline__ void tile_ready(const float2* t) {
+#pragma unroll
+    for (int i = 0; i < R; i += 4)
+        asm volatile("" ::"v"(t[i].x), "v"(t[i].y), "v"(t[i + 1].x), "v"(t[i + 1].y), "v"(t[i + 2].x),
+                     "v"(t[i + 2].y), "v"(t[i + 3].x), "v"(t[i + 3].y));
+}
+template <int R>
+__device__ __forceinline__ void tile_ready(const double2* t) {
+#pragma unroll
+    for (int i = 0; i < R; i += 4)
+        asm volatile("" ::"v"(t[i].x), "v"(t[i].y), "v"(t[i + 1].x), "v"(t[i + 1].y), "v"(t[i + 2].x),
+                     "v"(t[i + 2].y), "v"(t[i + 3].x), "v"(t[i + 3].y));
+}
+
 // Apply one op. BWD: inverse on psi and lambda, after the gradient term of a
 // rotation (Im<lambda|P|psi> into the wavefront's accumulator).
 template <int LOG_R, bool BWD, typename T2, typename Real>
@@ -699,6 +717,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     const int64_t b = blockIdx.x / a.n_wg;
     const int w = (int)(blockIdx.x - b * a.n_wg);
     const int n = a.n, k = P.k;
+    const int fwd_begin = P.fwd_begin, fwd_end = P.fwd_end;
+    const int bwd_begin = P.bwd_begin, bwd_end = P.bwd_end;
     T2* lds = (T2*)smem;
     double* red = (double*)(smem + a.lds_tile_bytes);  // [n][NW]
     Real* gacc = (Real*)(red + (size_t)n * NW);        // [n_gslots][NW]
@@ -715,13 +735,32 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
         __syncthreads();
     }
 
+    // The first phase's thread bits and the per-register offsets are the same
+    // for every tile; only the fixed (out-of-tile) qubit bits change.
+    const int ph0 = (flags & PF_FWD) ? P.load_phase : P.bwd_phase;
+    const uint32_t tb0 = deposit((uint32_t)tid, phases[ph0].thr_mask);
+    uint32_t toff = 0;  // amplitude-index bits of this thread's tile bits
+    for (int j = 0; j < k; ++j) toff |= ((tb0 >> j) & 1u) << P.tile_qubit[j];
+    auto fixed_bits = [&](int64_t tile) {
+        uint32_t gb = 0;
+        for (int i = 0; i < P.n_fixed; ++i) gb |= (uint32_t)((tile >> i) & 1) << P.fixed_qubit[i];
+        return gb;
+    };
+    const bool load = !(flags & PF_INIT);
+    const bool load_lam = BWD && (flags & PF_LOAD_LAM);
+    auto load_tile = [&](T2* dst, const T2* state, uint32_t gb) {
+        const DevPhase& F = phases[ph0];
+        const T2* src = state + (gb | toff);
+#pragma unroll
+        for (int i = 0; i < R; ++i) dst[i] = src[reg_offset<LOG_R>(i, F.reg_qmask)];
+    };
+
     T2 ps[R], lm[R];
     for (int64_t tile = w; tile < a.tiles; tile += a.n_wg) {
         TileCtx cx;
-        cx.gb = 0;
-        for (int i = 0; i < P.n_fixed; ++i) cx.gb |= (uint32_t)((tile >> i) & 1) << P.fixed_qubit[i];
-        cx.ph = (flags & PF_FWD) ? P.load_phase : P.bwd_phase;
-        cx.tb = deposit((uint32_t)tid, phases[cx.ph].thr_mask);
+        cx.gb = fixed_bits(tile);
+        cx.ph = ph0;
+        cx.tb = tb0;
 
         // amplitude index of (thread bits tbits) in this tile
         auto gaddr_thr = [&](uint32_t tbits) {
@@ -730,26 +769,21 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
             return cx.gb | g;
         };
 
-        if (flags & PF_INIT) {
+        if (!load) {
 #pragma unroll
             for (int i = 0; i < R; ++i) ps[i] = mk<T2>((Real)0, (Real)0);
             if (cx.gb == 0 && cx.tb == 0) ps[0] = mk<T2>((Real)1, (Real)0);
         } else {
-            const DevPhase& F = phases[cx.ph];
-            const T2* src = psi_s + gaddr_thr(cx.tb);
-#pragma unroll
-            for (int i = 0; i < R; ++i) ps[i] = src[reg_offset<LOG_R>(i, F.reg_qmask)];
-            if (BWD && (flags & PF_LOAD_LAM)) {
-                const T2* lsrc = lam_s + gaddr_thr(cx.tb);
-#pragma unroll
-                for (int i = 0; i < R; ++i) lm[i] = lsrc[reg_offset<LOG_R>(i, F.reg_qmask)];
-            }
+            load_tile(ps, psi_s, cx.gb);
+            if (load_lam) load_tile(lm, lam_s, cx.gb);
+            tile_ready<R>(ps);
+            if (load_lam) tile_ready<R>(lm);
         }
 
         // ---- forward ops
         if (flags & PF_FWD) {
-            XOp<Real> cur = xops[P.fwd_begin];
-            for (int o = P.fwd_begin; o < P.fwd_end; ++o) {
+            XOp<Real> cur = xops[fwd_begin];
+            for (int o = fwd_begin; o < fwd_end; ++o) {
                 const XOp<Real> nxt = xops[o + 1];
                 run_op<LOG_R, false>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, gacc,
                                      lane, wave, NW, tid);
@@ -812,8 +846,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
 
             // ---- backward ops
             if (flags & PF_BWD) {
-                XOp<Real> cur = xops[P.bwd_begin];
-                for (int o = P.bwd_begin; o < P.bwd_end; ++o) {
+                XOp<Real> cur = xops[bwd_begin];
+                for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
                     run_op<LOG_R, true>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, gacc,
                                         lane, wave, NW, tid);
