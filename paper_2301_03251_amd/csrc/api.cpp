@@ -354,9 +354,10 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
             ta.n_wg = L.n_wg;
             ta.flags = flags;
             ta.n_gslots = (flags & PF_BWD) ? d.n_gslots : 0;
-            ta.lds_tile_bytes = d.n_exchanges > 0 ? (int)(((size_t)1 << pl.k) * amp) : 0;
-            const size_t lds = (size_t)ta.lds_tile_bytes + (size_t)(c.n + ta.n_gslots) * NW * 8;
-            if (lds > g_lds_limit) return fail(QL_EUNSUPPORTED, "tile pass needs more LDS than available");
+            // dynamic LDS: <Z> and gradient scratch (the exchange buffer is static)
+            const size_t lds = (size_t)(c.n + ta.n_gslots) * NW * 8;
+            if (lds + tile_static_lds(dt, pl.log_r, threads) > g_lds_limit)
+                return fail(QL_EUNSUPPORTED, "tile pass needs more LDS than available");
             tm.start(0);
             hipError_t le = launch_tile(dt, pl.log_r, (flags & PF_BWD) != 0, ta, threads, lds, stream);
             tm.stop();

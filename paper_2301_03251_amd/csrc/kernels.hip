@@ -87,27 +87,6 @@ __device__ __forceinline__ double wave_total(double v) {
     return (lane(0) + lane(16)) + (lane(32) + lane(48));
 }
 
-// Scatter the low bits of x into the set bits of mask (ascending).
-__device__ __forceinline__ uint32_t deposit(uint32_t x, uint32_t mask) {
-    uint32_t r = 0;
-    for (int j = 0; j < MAX_TILE_BITS; ++j) {
-        if (mask >> j & 1u) {
-            r |= (x & 1u) << j;
-            x >>= 1;
-        }
-    }
-    return r;
-}
-
-// ---------------------------------------------------------------------------
-// register-tile helpers
-
-// Bank-spreading permutation of LDS slots: folds the upper nibbles of the tile
-// index into the lowest one (an involution on each aligned 2^16 block).
-__device__ __forceinline__ uint32_t lds_slot(uint32_t t) {
-    return t ^ (((t >> 4) ^ (t >> 8) ^ (t >> 12)) & 15u);
-}
-
 // ---------------------------------------------------------------------------
 // k_bind
 
@@ -318,17 +297,6 @@ template <> struct XOp<double> {
     uint64_t pad;
 };
 
-// Offset of register i in tile-index bits (or amplitude-index bits) of a phase:
-// the OR of the masks of i's set bits (compile-time i, uniform masks).
-template <int LOG_R>
-__device__ __forceinline__ uint32_t reg_offset(int i, const uint32_t* mask) {
-    uint32_t r = 0;
-#pragma unroll
-    for (int m = 0; m < LOG_R; ++m)
-        if (i >> m & 1) r |= mask[m];
-    return r;
-}
-
 // Plane rotation of (x, y) by phi, in place: a = tan(phi/2), b = sin(phi).
 template <typename Real>
 __device__ __forceinline__ void shear(Real& x, Real& y, Real a, Real b) {
@@ -538,20 +506,49 @@ __device__ __forceinline__ void rz_u(T2* s, Real a, Real b, bool bit) {
     for (int i = 0; i < (1 << LOG_R); ++i) shear(s[i].x, s[i].y, sa, sb);
 }
 
-// Exchange the tile through LDS from layout `from` to layout `to`. lds_slot is
-// linear over GF(2) and thread and register bits are disjoint, so the slot of
-// (thread bits | register bits) is lds_slot(thread bits) ^ lds_slot(register bits).
+// Tile bits `tb` and LDS byte offset `ts` of thread `tid` in phase F: every
+// thread-index bit contributes its tile bit and its (precomputed) slot offset.
+// Thread-index bits at or above log2(threads) are zero.
+template <int LOG_T>
+__device__ __forceinline__ void thread_layout(uint32_t tid, const DevPhase& F, uint32_t& tb, uint32_t& ts) {
+    tb = 0;
+    ts = 0;
+#pragma unroll
+    for (int b = 0; b < LOG_T; ++b) {
+        const uint32_t on = (tid >> b) & 1u;
+        tb |= on << F.thr_bit[b];
+        ts ^= on ? F.thr_slot[b] : 0u;
+    }
+}
+
+// Exchange the tile through LDS from layout `from` to layout `to`. The slot map
+// is linear over GF(2) and thread and register bits are disjoint, so the byte
+// offset of (thread, register i) is the thread's offset XOR the register's, and
+// the register's is the XOR of its bits' columns reg_slot[1 << m]. Registers
+// are visited in Gray-code order, so each access costs one XOR.
 template <int LOG_R, typename T2>
-__device__ __forceinline__ void lds_exchange(T2* a, T2* lds, const DevPhase& from,
-                                             const DevPhase& to, uint32_t tb_from, uint32_t tb_to) {
+__device__ __forceinline__ void lds_exchange(T2* a, unsigned char* lds, const DevPhase& from,
+                                             const DevPhase& to, uint32_t ts_from, uint32_t ts_to) {
     constexpr int R = 1 << LOG_R;
-    uint32_t fb = lds_slot(tb_from);
+    uint32_t cf[LOG_R], ct[LOG_R];
 #pragma unroll
-    for (int i = 0; i < R; ++i) lds[fb ^ lds_slot(reg_offset<LOG_R>(i, from.reg_tmask))] = a[i];
+    for (int m = 0; m < LOG_R; ++m) {
+        cf[m] = from.reg_slot[1 << m];
+        ct[m] = to.reg_slot[1 << m];
+    }
+    uint32_t ad = ts_from;
+#pragma unroll
+    for (int g = 0; g < R; ++g) {
+        *(T2*)(lds + ad) = a[g ^ (g >> 1)];
+        if (g + 1 < R) ad ^= cf[__builtin_ctz(g + 1)];
+    }
     __syncthreads();
-    fb = lds_slot(tb_to);
+    ad = ts_to;
 #pragma unroll
-    for (int i = 0; i < R; ++i) a[i] = lds[fb ^ lds_slot(reg_offset<LOG_R>(i, to.reg_tmask))];
+    for (int g = 0; g < R; ++g) {
+        a[g ^ (g >> 1)] = *(const T2*)(lds + ad);
+        if (g + 1 < R) ad ^= ct[__builtin_ctz(g + 1)];
+    }
     __syncthreads();
 }
 
@@ -564,6 +561,7 @@ __device__ __forceinline__ bool loc_bit(uint32_t w, uint32_t tb, uint32_t gb) {
 // Per-thread tile state shared by the handlers.
 struct TileCtx {
     uint32_t tb;  // tile-index bits of this thread (current phase)
+    uint32_t ts;  // LDS byte offset of this thread's slots (current phase)
     uint32_t gb;  // amplitude-index bits of the qubits outside the tile
     int ph;       // current phase
 };
@@ -588,10 +586,10 @@ __device__ __forceinline__ void tile_ready(const double2* t) {
 
 // Apply one op. BWD: inverse on psi and lambda, after the gradient term of a
 // rotation (Im<lambda|P|psi> into the wavefront's accumulator).
-template <int LOG_R, bool BWD, typename T2, typename Real>
+template <int LOG_R, int LOG_T, bool BWD, typename T2, typename Real>
 __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
-                                       TileCtx& cx, T2* lds, const DevPhase* phases, Real* gacc,
-                                       int lane, int wave, int nw, int tid) {
+                                       TileCtx& cx, unsigned char* lds, const DevPhase* phases,
+                                       Real* gacc, int lane, int wave, int nw, int tid) {
 #define QL_G1_CASE(KIND, J)                                                                 \
     case H_G1 + KIND * 5 + J:                                                               \
         if constexpr (J < LOG_R) {                                                          \
@@ -682,10 +680,13 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
             if constexpr (BWD) cz_sel<LOG_R, -1>(lm, on);
         } break;
         case H_TRANSPOSE: {
-            const uint32_t tb_to = deposit((uint32_t)tid, phases[arg].thr_mask);
-            lds_exchange<LOG_R>(ps, lds, phases[cx.ph], phases[arg], cx.tb, tb_to);
-            if constexpr (BWD) lds_exchange<LOG_R>(lm, lds, phases[cx.ph], phases[arg], cx.tb, tb_to);
+            const DevPhase& to = phases[arg];
+            uint32_t tb_to, ts_to;
+            thread_layout<LOG_T>((uint32_t)tid, to, tb_to, ts_to);
+            lds_exchange<LOG_R>(ps, lds, phases[cx.ph], to, cx.ts, ts_to);
+            if constexpr (BWD) lds_exchange<LOG_R>(lm, lds, phases[cx.ph], to, cx.ts, ts_to);
             cx.tb = tb_to;
+            cx.ts = ts_to;
             cx.ph = (int)arg;
         } break;
         default:
@@ -702,6 +703,17 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
 #undef QL_CZ_RX
 }
 
+// OR over the 64 lanes (every lane gets the result): row butterfly by DPP,
+// then the four row results from readlanes.
+__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);
+    return (uint32_t)(__builtin_amdgcn_readlane((int)v, 0) | __builtin_amdgcn_readlane((int)v, 16) |
+                      __builtin_amdgcn_readlane((int)v, 32) | __builtin_amdgcn_readlane((int)v, 48));
+}
+
 template <typename Real, int LOG_R, bool BWD, int MAXT>
 __global__ void __launch_bounds__(MAXT) __attribute__((amdgpu_waves_per_eu(2)))
 k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __restrict__ phases,
@@ -709,6 +721,11 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
        const int32_t* __restrict__ gslots) {
     using T2 = typename Cx<Real>::T;
     constexpr int R = 1 << LOG_R;
+    constexpr int LOG_T = MAXT == 512 ? 9 : 8;
+    // The tile exchange buffer is static (its LDS address is a compile-time
+    // constant, so exchange addresses need no base add); the reduction
+    // scratch is dynamic and follows it.
+    __shared__ __align__(16) unsigned char tile_lds[tile_lds_bytes<Real, LOG_R, MAXT>()];
     extern __shared__ __align__(16) unsigned char smem[];
     const DevPass& P = *pass;
     const int tid = threadIdx.x, nt = blockDim.x, NW = nt >> 6;
@@ -716,11 +733,11 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     const int flags = a.flags;
     const int64_t b = blockIdx.x / a.n_wg;
     const int w = (int)(blockIdx.x - b * a.n_wg);
-    const int n = a.n, k = P.k;
+    const int n = a.n, k = P.k, n_fixed = P.n_fixed;
     const int fwd_begin = P.fwd_begin, fwd_end = P.fwd_end;
     const int bwd_begin = P.bwd_begin, bwd_end = P.bwd_end;
-    T2* lds = (T2*)smem;
-    double* red = (double*)(smem + a.lds_tile_bytes);  // [n][NW]
+    unsigned char* lds = tile_lds;
+    double* red = (double*)smem;                       // [n][NW]
     Real* gacc = (Real*)(red + (size_t)n * NW);        // [n_gslots][NW]
 
     const size_t dim = (size_t)1 << n;
@@ -729,45 +746,80 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     const XOp<Real>* xops = xops_all + b * (a.n_ops + 1);
     const Real* gout = gout_all + b * n;
 
-    double accz = 0.0;
     if (BWD && (flags & PF_BWD)) {
         for (int i = tid; i < a.n_gslots * NW; i += nt) gacc[i] = (Real)0;
         __syncthreads();
     }
 
-    // The first phase's thread bits and the per-register offsets are the same
-    // for every tile; only the fixed (out-of-tile) qubit bits change.
-    const int ph0 = (flags & PF_FWD) ? P.load_phase : P.bwd_phase;
-    const uint32_t tb0 = deposit((uint32_t)tid, phases[ph0].thr_mask);
-    uint32_t toff = 0;  // amplitude-index bits of this thread's tile bits
-    for (int j = 0; j < k; ++j) toff |= ((tb0 >> j) & 1u) << P.tile_qubit[j];
-    auto fixed_bits = [&](int64_t tile) {
-        uint32_t gb = 0;
-        for (int i = 0; i < P.n_fixed; ++i) gb |= (uint32_t)((tile >> i) & 1) << P.fixed_qubit[i];
-        return gb;
+    // Phases are the same for every tile: the pass loads in ph0, stores in
+    // ph_st (the backward ops walk the forward layouts back to the first one),
+    // and takes <Z> and the lambda seed in the last forward layout. Only the
+    // fixed (out-of-tile) qubit bits change from tile to tile.
+    auto amp_offset = [&](uint32_t tb) {  // amplitude-index bits of tile bits tb
+        uint32_t g = 0;
+        for (int j = 0; j < k; ++j) g |= ((tb >> j) & 1u) << P.tile_qubit[j];
+        return g;
     };
+    const int ph0 = (flags & PF_FWD) ? P.load_phase : P.bwd_phase;
+    const int ph_st = (BWD && (flags & PF_BWD)) ? P.load_phase : P.bwd_phase;
+    uint32_t tb0, ts0, tb_st, ts_st;
+    thread_layout<LOG_T>((uint32_t)tid, phases[ph0], tb0, ts0);
+    thread_layout<LOG_T>((uint32_t)tid, phases[ph_st], tb_st, ts_st);
+    const uint32_t toff0 = amp_offset(tb0), toff_st = amp_offset(tb_st);
+    // lane i < n_fixed holds fixed qubit i: a tile's fixed bits are the OR
+    // over lanes of (bit i of the tile index) << qubit
+    const uint32_t fq_lane = lane < n_fixed ? (uint32_t)P.fixed_qubit[lane] : 0u;
+
+    // <Z> and seed constants of the last forward layout: the qubit of each
+    // register bit and of each thread-index bit
+    uint32_t tbz = 0, qreg[LOG_R], qthr[LOG_T];
+    Real seed_base = 0, gm[LOG_R], gfix = 0;
+    double accz = 0.0, accf = 0.0;  // lane q: <Z_q> of tile qubit q; lane i: of fixed qubit i
+#pragma unroll
+    for (int m = 0; m < LOG_R; ++m) {
+        gm[m] = 0;
+        qreg[m] = 0;
+    }
+#pragma unroll
+    for (int t = 0; t < LOG_T; ++t) qthr[t] = 0;
+    if (flags & (PF_ZPART | PF_SEED)) {
+        const DevPhase& F = phases[P.bwd_phase];
+        uint32_t tsz;
+        thread_layout<LOG_T>((uint32_t)tid, F, tbz, tsz);
+#pragma unroll
+        for (int m = 0; m < LOG_R; ++m) qreg[m] = (uint32_t)P.tile_qubit[F.reg_bit[m]];
+#pragma unroll
+        for (int t = 0; t < LOG_T; ++t)  // 64 (no lane) for thread bits this launch does not have
+            qthr[t] = t < P.log_t ? (uint32_t)P.tile_qubit[F.thr_bit[t]] : 64u;
+        if (BWD && (flags & PF_SEED)) {
+            Real gs = 0, sthr = 0;
+            for (int q = 0; q < n; ++q) gs += gout[q];
+            for (int j = 0; j < k; ++j)
+                if ((F.thr_mask >> j & 1u) && (tbz >> j & 1u)) sthr += gout[P.tile_qubit[j]];
+            seed_base = gs - (Real)2 * sthr;
+#pragma unroll
+            for (int m = 0; m < LOG_R; ++m) gm[m] = gout[P.tile_qubit[F.reg_bit[m]]];
+            gfix = lane < n_fixed ? gout[fq_lane] : (Real)0;
+        }
+    }
+
     const bool load = !(flags & PF_INIT);
     const bool load_lam = BWD && (flags & PF_LOAD_LAM);
     auto load_tile = [&](T2* dst, const T2* state, uint32_t gb) {
         const DevPhase& F = phases[ph0];
-        const T2* src = state + (gb | toff);
+        const T2* src = state + (gb | toff0);
 #pragma unroll
-        for (int i = 0; i < R; ++i) dst[i] = src[reg_offset<LOG_R>(i, F.reg_qmask)];
+        for (int i = 0; i < R; ++i) dst[i] = src[F.reg_qoff[i]];
     };
 
     T2 ps[R], lm[R];
     for (int64_t tile = w; tile < a.tiles; tile += a.n_wg) {
+        const uint32_t tbit = lane < n_fixed ? (((uint32_t)tile >> lane) & 1u) : 0u;
         TileCtx cx;
-        cx.gb = fixed_bits(tile);
+        cx.gb = wave_or(tbit << fq_lane);
         cx.ph = ph0;
         cx.tb = tb0;
-
-        // amplitude index of (thread bits tbits) in this tile
-        auto gaddr_thr = [&](uint32_t tbits) {
-            uint32_t g = 0;
-            for (int j = 0; j < k; ++j) g |= ((tbits >> j) & 1u) << P.tile_qubit[j];
-            return cx.gb | g;
-        };
+        cx.ts = ts0;
 
         if (!load) {
 #pragma unroll
@@ -785,15 +837,16 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
             XOp<Real> cur = xops[fwd_begin];
             for (int o = fwd_begin; o < fwd_end; ++o) {
                 const XOp<Real> nxt = xops[o + 1];
-                run_op<LOG_R, false>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, gacc,
-                                     lane, wave, NW, tid);
+                run_op<LOG_R, LOG_T, false>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases,
+                                            gacc, lane, wave, NW, tid);
                 cur = nxt;
             }
         }
 
-        // ---- <Z_q> partials over this tile
+        // ---- <Z_q> partials over this tile: register bits from the signed
+        // register sums, lane bits from lane-signed wavefront sums, wavefront
+        // bits and fixed bits from the tile total with a uniform sign
         if (flags & PF_ZPART) {
-            const DevPhase& F = phases[cx.ph];
             Real pt = 0, dm[LOG_R];
 #pragma unroll
             for (int m = 0; m < LOG_R; ++m) dm[m] = 0;
@@ -804,42 +857,34 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
 #pragma unroll
                 for (int m = 0; m < LOG_R; ++m) dm[m] += (i >> m & 1) ? -p : p;
             }
-            const double wp = wave_total(pt);
-            for (int j = 0; j < k; ++j) {
-                Real v = (cx.tb >> j & 1u) ? -pt : pt;
 #pragma unroll
-                for (int m = 0; m < LOG_R; ++m)
-                    if ((int)F.reg_bit[m] == j) v = dm[m];
-                const double d = wave_total(v);
-                accz += (lane == P.tile_qubit[j]) ? d : 0.0;
+            for (int m = 0; m < LOG_R; ++m) {
+                const double d = wave_total(dm[m]);
+                accz += (lane == (int)qreg[m]) ? d : 0.0;
             }
-            for (int i = 0; i < P.n_fixed; ++i) {
-                const int q = P.fixed_qubit[i];
-                accz += (lane == q) ? ((cx.gb >> q & 1u) ? -wp : wp) : 0.0;
+#pragma unroll
+            for (int t = 0; t < 6; ++t) {
+                const double d = wave_total((lane >> t & 1) ? -pt : pt);
+                accz += (lane == (int)qthr[t]) ? d : 0.0;
             }
+            const double wp = wave_total(pt);
+#pragma unroll
+            for (int t = 6; t < LOG_T; ++t) accz += (lane == (int)qthr[t]) ? ((wave >> (t - 6) & 1) ? -wp : wp) : 0.0;
+            accf += tbit ? -wp : wp;
         }
 
         if constexpr (BWD) {
             // ---- lambda = (sum_q g_q Z_q) psi
             if (flags & PF_SEED) {
-                const DevPhase& F = phases[cx.ph];
-                Real gs = 0, sfix = 0, sthr = 0, gm[LOG_R];
-                for (int q = 0; q < n; ++q) gs += gout[q];
-                for (int i = 0; i < P.n_fixed; ++i) {
-                    const int q = P.fixed_qubit[i];
-                    if (cx.gb >> q & 1u) sfix += gout[q];
-                }
-                for (int j = 0; j < k; ++j)
-                    if ((F.thr_mask >> j & 1u) && (cx.tb >> j & 1u)) sthr += gout[P.tile_qubit[j]];
-#pragma unroll
-                for (int m = 0; m < LOG_R; ++m) gm[m] = gout[P.tile_qubit[F.reg_bit[m]]];
+                const Real sfix = (Real)wave_total(tbit ? gfix : (Real)0);
+                const Real base = seed_base - (Real)2 * sfix;
 #pragma unroll
                 for (int i = 0; i < R; ++i) {
                     Real sr = 0;
 #pragma unroll
                     for (int m = 0; m < LOG_R; ++m)
                         if (i >> m & 1) sr += gm[m];
-                    const Real d = gs - (Real)2 * (sfix + sthr + sr);
+                    const Real d = base - (Real)2 * sr;
                     lm[i] = mk<T2>(d * ps[i].x, d * ps[i].y);
                 }
             }
@@ -849,32 +894,35 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 XOp<Real> cur = xops[bwd_begin];
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
-                    run_op<LOG_R, true>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases, gacc,
-                                        lane, wave, NW, tid);
+                    run_op<LOG_R, LOG_T, true>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases,
+                                               gacc, lane, wave, NW, tid);
                     cur = nxt;
                 }
             }
         }
 
         if (flags & (PF_STORE_PSI | PF_STORE_LAM)) {
-            const DevPhase& F = phases[cx.ph];
-            const uint32_t base = gaddr_thr(cx.tb);
+            const DevPhase& F = phases[ph_st];
+            const uint32_t base = cx.gb | toff_st;
             if (flags & PF_STORE_PSI) {
                 T2* dst = psi_s + base;
 #pragma unroll
-                for (int i = 0; i < R; ++i) dst[reg_offset<LOG_R>(i, F.reg_qmask)] = ps[i];
+                for (int i = 0; i < R; ++i) dst[F.reg_qoff[i]] = ps[i];
             }
             if (BWD && (flags & PF_STORE_LAM)) {
                 T2* dst = lam_s + base;
 #pragma unroll
-                for (int i = 0; i < R; ++i) dst[reg_offset<LOG_R>(i, F.reg_qmask)] = lm[i];
+                for (int i = 0; i < R; ++i) dst[F.reg_qoff[i]] = lm[i];
             }
         }
     }
 
     // combine the wavefronts' accumulators (fixed order) and write the partials
     if (flags & PF_ZPART) {
+        // two stores from one wavefront land in order: a fixed qubit's slot
+        // first gets 0 from accz, then its own sum
         if (lane < n) red[lane * NW + wave] = accz;
+        if (lane < n_fixed) red[fq_lane * NW + wave] = accf;
     }
     __syncthreads();
     if (flags & PF_ZPART)
@@ -1055,18 +1103,29 @@ hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+size_t tile_static_lds(int dtype, int log_r, int threads) {
+    const size_t maxt = threads > 256 ? 512 : 256;
+    return maxt * ((size_t)1 << log_r) * 2 * (dtype == 0 ? sizeof(float) : sizeof(double));
+}
+
 hipError_t configure_kernels(size_t max_lds) {
-    const int v = (int)max_lds;
     hipError_t e = hipSuccess;
-#define QL_ATTR(fn)                                                                      \
+#define QL_ATTR_V(fn, v)                                                                 \
     if (e == hipSuccess)                                                                 \
         e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),                       \
-                                hipFuncAttributeMaxDynamicSharedMemorySize, v);
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)(v));
+#define QL_ATTR(fn) QL_ATTR_V(fn, max_lds)
     QL_ATTR((k_whole<float>))
     QL_ATTR((k_whole<double>))
+    // tile kernels: what the static exchange buffer leaves
+#define QL_ATTR_TK(REAL, LR, BW, MT)                                                      \
+    {                                                                                     \
+        const size_t st = tile_lds_bytes<REAL, LR, MT>();                                 \
+        if (st < max_lds) QL_ATTR_V((k_tile<REAL, LR, BW, MT>), max_lds - st)             \
+    }
 #define QL_ATTR_T(REAL, LR)                                                               \
-    QL_ATTR((k_tile<REAL, LR, false, 256>)) QL_ATTR((k_tile<REAL, LR, true, 256>))          \
-    QL_ATTR((k_tile<REAL, LR, false, 512>)) QL_ATTR((k_tile<REAL, LR, true, 512>))
+    QL_ATTR_TK(REAL, LR, false, 256) QL_ATTR_TK(REAL, LR, true, 256)                      \
+    QL_ATTR_TK(REAL, LR, false, 512) QL_ATTR_TK(REAL, LR, true, 512)
     QL_ATTR_T(float, 2)
     QL_ATTR_T(float, 3)
     QL_ATTR_T(float, 4)
@@ -1075,7 +1134,9 @@ hipError_t configure_kernels(size_t max_lds) {
     QL_ATTR_T(double, 3)
     QL_ATTR_T(double, 4)
 #undef QL_ATTR_T
+#undef QL_ATTR_TK
 #undef QL_ATTR
+#undef QL_ATTR_V
     return e;
 }
 

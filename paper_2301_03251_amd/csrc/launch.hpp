@@ -67,7 +67,6 @@ struct TileArgs {
     int64_t tiles;             // tiles per sample = 2^(n-k)
     int32_t n, n_ops, n_wg, flags;
     int32_t n_gslots;          // gradient accumulators of this pass
-    int32_t lds_tile_bytes;    // 0 when the pass needs no LDS exchange
 };
 
 struct ReduceArgs {
@@ -84,6 +83,14 @@ struct ReduceArgs {
     int32_t n, n_wg, F, P, n_slots;
     int32_t grads;         // 1: reduce gradients too
 };
+
+// Static LDS of a tile kernel: the exchange buffer for a whole tile of
+// MAXT threads x 2^LOG_R amplitudes.
+template <typename Real, int LOG_R, int MAXT>
+constexpr size_t tile_lds_bytes() {
+    return (size_t)MAXT * ((size_t)1 << LOG_R) * 2 * sizeof(Real);
+}
+size_t tile_static_lds(int dtype, int log_r, int threads);
 
 // dtype: 0 = complex64 / fp32, 1 = complex128 / fp64. Return hipError_t.
 hipError_t launch_bind(int dtype, const BindArgs& a, hipStream_t s);

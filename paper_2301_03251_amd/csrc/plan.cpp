@@ -63,22 +63,41 @@ std::vector<int> scan(const std::vector<Gate>& gates, const std::vector<char>& d
     return exec;
 }
 
-DevPhase make_phase(const std::vector<int>& tq, const std::vector<int>& reg_bits, int k) {
+// `amp` is the size of one amplitude in bytes (LDS offsets are in bytes).
+DevPhase make_phase(const std::vector<int>& tq, const std::vector<int>& reg_bits, int k, uint32_t amp) {
     DevPhase p{};
     uint32_t regmask = 0;
-    for (int m = 0; m < (int)reg_bits.size(); m++) {
+    const int r = (int)reg_bits.size();
+    for (int m = 0; m < r; m++) {
         p.reg_bit[m] = reg_bits[m];
         p.reg_tmask[m] = 1u << reg_bits[m];
         p.reg_qmask[m] = 1u << tq[reg_bits[m]];
         regmask |= 1u << reg_bits[m];
     }
     p.thr_mask = ((k >= 32) ? 0xffffffffu : ((1u << k) - 1)) & ~regmask;
+    int b = 0;
+    for (int j = 0; j < k && b < MAX_THREAD_BITS; j++)
+        if (p.thr_mask >> j & 1) {
+            p.thr_bit[b] = (uint32_t)j;
+            p.thr_slot[b] = lds_slot(1u << j) * amp;
+            b++;
+        }
+    for (int i = 0; i < (1 << r); i++) {
+        uint32_t t = 0, q = 0;
+        for (int m = 0; m < r; m++)
+            if (i >> m & 1) {
+                t |= p.reg_tmask[m];
+                q |= p.reg_qmask[m];
+            }
+        p.reg_slot[i] = lds_slot(t) * amp;
+        p.reg_qoff[i] = q;
+    }
     return p;
 }
 
 // Schedule the gates of one pass onto register phases.
 void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_r, int low,
-                   std::vector<DevPhase>& phases) {
+                   uint32_t amp, std::vector<DevPhase>& phases) {
     const int r = log_r;
     std::vector<int> bit_of(64, -1);  // qubit -> tile bit
     for (int j = 0; j < k; j++) bit_of[pp.qubits[j]] = j;
@@ -119,7 +138,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
 
     std::vector<int> regs = choose(low_mask, {});
     int cur_phase = (int)phases.size();
-    phases.push_back(make_phase(pp.qubits, regs, k));
+    phases.push_back(make_phase(pp.qubits, regs, k, amp));
     pp.first_phase = cur_phase;
 
     // gradient accumulators: one per rotation in this pass
@@ -194,7 +213,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         if (pending.empty()) break;
         regs = choose(0, regs);
         int np = (int)phases.size();
-        phases.push_back(make_phase(pp.qubits, regs, k));
+        phases.push_back(make_phase(pp.qubits, regs, k, amp));
         recs.push_back({make_op(H_TRANSPOSE, (uint32_t)np, -1, K_H), cur_phase});
         cur_phase = np;
         pp.n_transposes++;
@@ -209,7 +228,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         pending.clear();
         regs = choose(low_mask, keep);
         int np = (int)phases.size();
-        phases.push_back(make_phase(pp.qubits, regs, k));
+        phases.push_back(make_phase(pp.qubits, regs, k, amp));
         recs.push_back({make_op(H_TRANSPOSE, (uint32_t)np, -1, K_H), cur_phase});
         cur_phase = np;
         pp.n_transposes++;
@@ -335,7 +354,7 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         pp.gates = best;
         for (int gi : best) done[gi] = 1;
         remaining -= (int)best.size();
-        schedule_pass(c.gates, pp, k, log_r, low, pl.phases);
+        schedule_pass(c.gates, pp, k, log_r, low, dtype == 0 ? 8u : 16u, pl.phases);
         pl.passes.push_back(std::move(pp));
         if (G == 0) break;
     }

@@ -71,15 +71,31 @@ constexpr int MAX_LOG_R = 5;
 constexpr int MAX_R = 1 << MAX_LOG_R;
 constexpr int MAX_TILE_BITS = 16;
 
+constexpr int MAX_THREAD_BITS = 12;
+
 // Register layout of one phase: register bit m of a thread's amplitude index
 // is tile bit reg_bit[m]; the remaining tile bits (thr_mask, ascending) are the
-// thread index bits. The kernel forms per-register offsets from the masks.
+// thread index bits. Every per-register and per-thread-bit offset the kernel
+// needs is precomputed here, so a layout change costs one XOR per access.
+//
+// LDS: the amplitude with tile index t sits in slot lds_slot(t) (a GF(2)-linear
+// bank-spreading permutation), so the byte offset of (thread, register i) is
+// XOR(thr_slot[b] for set bits b of the thread index) ^ reg_slot[i].
 struct DevPhase {
-    uint32_t thr_mask;             // tile bits held by the thread index
-    uint32_t reg_bit[MAX_LOG_R];   // register bit m -> tile bit
-    uint32_t reg_tmask[MAX_LOG_R]; // 1 << reg_bit[m]
-    uint32_t reg_qmask[MAX_LOG_R]; // 1 << (qubit of tile bit reg_bit[m])
+    uint32_t thr_mask;                   // tile bits held by the thread index
+    uint32_t reg_bit[MAX_LOG_R];         // register bit m -> tile bit
+    uint32_t reg_tmask[MAX_LOG_R];       // 1 << reg_bit[m]
+    uint32_t reg_qmask[MAX_LOG_R];       // 1 << (qubit of tile bit reg_bit[m])
+    uint32_t thr_bit[MAX_THREAD_BITS];   // thread-index bit b -> tile bit
+    uint32_t thr_slot[MAX_THREAD_BITS];  // LDS byte offset of thread-index bit b
+    uint32_t reg_slot[MAX_R];            // LDS byte offset of register i's tile bits
+    uint32_t reg_qoff[MAX_R];            // amplitude-index offset of register i's tile bits
 };
+
+// Bank-spreading permutation of LDS slots: folds the upper nibbles of the tile
+// index into the lowest one. Linear over GF(2), an involution on each aligned
+// block of 2^16 slots.
+constexpr uint32_t lds_slot(uint32_t t) { return t ^ (((t >> 4) ^ (t >> 8) ^ (t >> 12)) & 15u); }
 
 enum PassFlags : int32_t {
     PF_INIT = 1,        // start from |0..0> instead of loading psi
