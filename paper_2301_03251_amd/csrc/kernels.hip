@@ -560,10 +560,11 @@ __device__ __forceinline__ bool loc_bit(uint32_t w, uint32_t tb, uint32_t gb) {
 
 // Per-thread tile state shared by the handlers.
 struct TileCtx {
-    uint32_t tb;  // tile-index bits of this thread (current phase)
-    uint32_t ts;  // LDS byte offset of this thread's slots (current phase)
-    uint32_t gb;  // amplitude-index bits of the qubits outside the tile
-    int ph;       // current phase
+    uint32_t tb;   // tile-index bits of this thread (current phase)
+    uint32_t ts;   // LDS byte offset of this thread's slots (current phase)
+    uint32_t gb;   // amplitude-index bits of the qubits outside the tile (ps)
+    uint32_t gb2;  // the same for the tile in lm (equal to gb unless two tiles)
+    int ph;        // current phase
 };
 
 // An empty asm that reads every amplitude of a register tile: the compiler
@@ -584,30 +585,33 @@ __device__ __forceinline__ void tile_ready(const double2* t) {
                      "v"(t[i + 2].y), "v"(t[i + 3].x), "v"(t[i + 3].y));
 }
 
-// Apply one op. BWD: inverse on psi and lambda, after the gradient term of a
-// rotation (Im<lambda|P|psi> into the wavefront's accumulator).
-template <int LOG_R, int LOG_T, bool BWD, typename T2, typename Real>
+// Apply one op. OPM selects the register arrays it acts on:
+//   OP_ONE  -- ps only (one forward tile);
+//   OP_PAIR -- ps and lm, two forward tiles that differ in their fixed bits
+//              (cx.gb for ps, cx.gb2 for lm);
+//   OP_BWD  -- the gradient term Im<lambda|P|psi> of a rotation into the
+//              wavefront's accumulator, then the op (its inverse, from the
+//              binding) on psi (ps) and lambda (lm) of one tile.
+enum { OP_ONE = 0, OP_PAIR = 1, OP_BWD = 2 };
+template <int LOG_R, int LOG_T, int OPM, typename T2, typename Real>
 __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
                                        TileCtx& cx, unsigned char* lds, const DevPhase* phases,
                                        Real* gacc, int lane, int wave, int nw, int tid) {
 #define QL_G1_CASE(KIND, J)                                                                 \
     case H_G1 + KIND * 5 + J:                                                               \
         if constexpr (J < LOG_R) {                                                          \
-            if constexpr (BWD) {                                                            \
-                if (KIND != 0)                                                              \
-                    grad_add(gacc, arg, gpart<LOG_R, KIND, J, T2, Real>(ps, lm), lane, wave, nw); \
-                g1<LOG_R, KIND, J, T2, Real>(lm, ca, cb);                                   \
-            }                                                                               \
+            if constexpr (OPM == OP_BWD && KIND != 0)                                       \
+                grad_add(gacc, arg, gpart<LOG_R, KIND, J, T2, Real>(ps, lm), lane, wave, nw); \
+            if constexpr (OPM != OP_ONE) g1<LOG_R, KIND, J, T2, Real>(lm, ca, cb);            \
             g1<LOG_R, KIND, J, T2, Real>(ps, ca, cb);                                       \
         }                                                                                   \
         break;
 #define QL_RZN_CASE(J)                                                                      \
     case H_RZN + J:                                                                         \
         if constexpr (J < LOG_R) {                                                          \
-            if constexpr (BWD) {                                                            \
+            if constexpr (OPM == OP_BWD)                                                    \
                 grad_add(gacc, arg, gpart<LOG_R, 3, J, T2, Real>(ps, lm), lane, wave, nw);  \
-                g1<LOG_R, 3, J, T2, Real, true>(lm, ca, cb);                                \
-            }                                                                               \
+            if constexpr (OPM != OP_ONE) g1<LOG_R, 3, J, T2, Real, true>(lm, ca, cb);         \
             g1<LOG_R, 3, J, T2, Real, true>(ps, ca, cb);                                    \
         }                                                                                   \
         break;
@@ -616,7 +620,7 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
     case H_CNOT_RR + J * 5 + M:                                                             \
         if constexpr (J < LOG_R && M < LOG_R && J != M) {                                   \
             cnot_rr<LOG_R, J, M>(ps);                                                       \
-            if constexpr (BWD) cnot_rr<LOG_R, J, M>(lm);                                    \
+            if constexpr (OPM != OP_ONE) cnot_rr<LOG_R, J, M>(lm);                          \
         }                                                                                   \
         break;
 #define QL_CNOT_RR_J(J) QL_CNOT_RR(J, 0) QL_CNOT_RR(J, 1) QL_CNOT_RR(J, 2) QL_CNOT_RR(J, 3) QL_CNOT_RR(J, 4)
@@ -625,31 +629,29 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         if constexpr (J < LOG_R) {                                                          \
             const bool on = (cx.tb >> arg) & 1u;                                            \
             cnot_sel<LOG_R, J>(ps, on);                                                     \
-            if constexpr (BWD) cnot_sel<LOG_R, J>(lm, on);                                  \
+            if constexpr (OPM != OP_ONE) cnot_sel<LOG_R, J>(lm, on);                        \
         }                                                                                   \
         break;                                                                              \
     case H_CNOT_F + J:                                                                      \
         if constexpr (J < LOG_R) {                                                          \
-            if ((cx.gb >> arg) & 1u) {                                                      \
-                swap_all<LOG_R, J>(ps);                                                     \
-                if constexpr (BWD) swap_all<LOG_R, J>(lm);                                  \
-            }                                                                               \
+            if ((cx.gb >> arg) & 1u) swap_all<LOG_R, J>(ps);                                \
+            if constexpr (OPM != OP_ONE)                                                    \
+                if ((cx.gb2 >> arg) & 1u) swap_all<LOG_R, J>(lm);                           \
         }                                                                                   \
         break;
 #define QL_CZ_RR(A, B)                                                                      \
     case H_CZ_RR + A * 5 + B:                                                               \
         if constexpr (A < LOG_R && B < LOG_R && A != B) {                                   \
             cz_rr<LOG_R, A, B>(ps);                                                         \
-            if constexpr (BWD) cz_rr<LOG_R, A, B>(lm);                                      \
+            if constexpr (OPM != OP_ONE) cz_rr<LOG_R, A, B>(lm);                            \
         }                                                                                   \
         break;
 #define QL_CZ_RR_A(A) QL_CZ_RR(A, 0) QL_CZ_RR(A, 1) QL_CZ_RR(A, 2) QL_CZ_RR(A, 3) QL_CZ_RR(A, 4)
 #define QL_CZ_RX(A)                                                                         \
     case H_CZ_RX + A:                                                                       \
         if constexpr (A < LOG_R) {                                                          \
-            const bool on = loc_bit(arg, cx.tb, cx.gb);                                     \
-            cz_sel<LOG_R, A>(ps, on);                                                       \
-            if constexpr (BWD) cz_sel<LOG_R, A>(lm, on);                                    \
+            cz_sel<LOG_R, A>(ps, loc_bit(arg, cx.tb, cx.gb));                               \
+            if constexpr (OPM != OP_ONE) cz_sel<LOG_R, A>(lm, loc_bit(arg, cx.tb, cx.gb2));   \
         }                                                                                   \
         break;
     switch (h) {
@@ -661,7 +663,7 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         QL_RZN_CASE(0) QL_RZN_CASE(1) QL_RZN_CASE(2) QL_RZN_CASE(3) QL_RZN_CASE(4)
         case H_RZU: {
             const bool bit = loc_bit(arg, cx.tb, cx.gb);
-            if constexpr (BWD) {
+            if constexpr (OPM == OP_BWD) {
                 Real acc[2] = {0, 0};
 #pragma unroll
                 for (int i = 0; i < (1 << LOG_R); ++i) {
@@ -671,20 +673,23 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
                 const Real t = acc[0] + acc[1];
                 grad_add(gacc, arg >> 16, bit ? -t : t, lane, wave, nw);
                 rz_u<LOG_R>(lm, ca, cb, bit);
+            } else if constexpr (OPM == OP_PAIR) {
+                rz_u<LOG_R>(lm, ca, cb, loc_bit(arg, cx.tb, cx.gb2));
             }
             rz_u<LOG_R>(ps, ca, cb, bit);
         } break;
         case H_CZ_XX: {
             const bool on = loc_bit(arg & 0xffff, cx.tb, cx.gb) && loc_bit(arg >> 16, cx.tb, cx.gb);
             cz_sel<LOG_R, -1>(ps, on);
-            if constexpr (BWD) cz_sel<LOG_R, -1>(lm, on);
+            if constexpr (OPM != OP_ONE)
+                cz_sel<LOG_R, -1>(lm, loc_bit(arg & 0xffff, cx.tb, cx.gb2) && loc_bit(arg >> 16, cx.tb, cx.gb2));
         } break;
         case H_TRANSPOSE: {
             const DevPhase& to = phases[arg];
             uint32_t tb_to, ts_to;
             thread_layout<LOG_T>((uint32_t)tid, to, tb_to, ts_to);
             lds_exchange<LOG_R>(ps, lds, phases[cx.ph], to, cx.ts, ts_to);
-            if constexpr (BWD) lds_exchange<LOG_R>(lm, lds, phases[cx.ph], to, cx.ts, ts_to);
+            if constexpr (OPM != OP_ONE) lds_exchange<LOG_R>(lm, lds, phases[cx.ph], to, cx.ts, ts_to);
             cx.tb = tb_to;
             cx.ts = ts_to;
             cx.ph = (int)arg;
@@ -703,6 +708,41 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
 #undef QL_CZ_RX
 }
 
+// <Z_q> partials of one tile held in registers t: register bits from the
+// signed register sums, lane bits from lane-signed wavefront sums, wavefront
+// bits and fixed bits (tbit: this lane's fixed-qubit bit of the tile) from the
+// tile total with a uniform sign. Lane q of accz collects tile qubit q; lane i
+// of accf collects fixed qubit i.
+template <int LOG_R, int LOG_T, typename Real, typename T2>
+__device__ __forceinline__ void zpart_tile(const T2* t, uint32_t tbit, const uint32_t* qreg,
+                                           const uint32_t* qthr, int lane, int wave, double& accz,
+                                           double& accf) {
+    Real pt = 0, dm[LOG_R];
+#pragma unroll
+    for (int m = 0; m < LOG_R; ++m) dm[m] = 0;
+#pragma unroll
+    for (int i = 0; i < (1 << LOG_R); ++i) {
+        const Real p = t[i].x * t[i].x + t[i].y * t[i].y;
+        pt += p;
+#pragma unroll
+        for (int m = 0; m < LOG_R; ++m) dm[m] += (i >> m & 1) ? -p : p;
+    }
+#pragma unroll
+    for (int m = 0; m < LOG_R; ++m) {
+        const double d = wave_total(dm[m]);
+        accz += (lane == (int)qreg[m]) ? d : 0.0;
+    }
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+        const double d = wave_total((lane >> b & 1) ? -pt : pt);
+        accz += (lane == (int)qthr[b]) ? d : 0.0;
+    }
+    const double wp = wave_total(pt);
+#pragma unroll
+    for (int b = 6; b < LOG_T; ++b) accz += (lane == (int)qthr[b]) ? ((wave >> (b - 6) & 1) ? -wp : wp) : 0.0;
+    accf += tbit ? -wp : wp;
+}
+
 // OR over the 64 lanes (every lane gets the result): row butterfly by DPP,
 // then the four row results from readlanes.
 __device__ __forceinline__ uint32_t wave_or(uint32_t v) {
@@ -714,12 +754,18 @@ __device__ __forceinline__ uint32_t wave_or(uint32_t v) {
                       __builtin_amdgcn_readlane((int)v, 32) | __builtin_amdgcn_readlane((int)v, 48));
 }
 
-template <typename Real, int LOG_R, bool BWD, int MAXT>
+// Kernel modes: one forward tile per iteration, two forward tiles per
+// iteration (the tile index and the same index with its top bit set), or the
+// backward sweep (psi and lambda of one tile).
+enum { KM_FWD1 = 0, KM_FWD2 = 1, KM_BWD = 2 };
+
+template <typename Real, int LOG_R, int KM, int MAXT>
 __global__ void __launch_bounds__(MAXT) __attribute__((amdgpu_waves_per_eu(2)))
 k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __restrict__ phases,
        const XOp<Real>* __restrict__ xops_all, const Real* __restrict__ gout_all,
        const int32_t* __restrict__ gslots) {
     using T2 = typename Cx<Real>::T;
+    constexpr bool BWD = KM == KM_BWD, PAIR = KM == KM_FWD2;
     constexpr int R = 1 << LOG_R;
     constexpr int LOG_T = MAXT == 512 ? 9 : 8;
     // The tile exchange buffer is static (its LDS address is a compile-time
@@ -812,11 +858,16 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
         for (int i = 0; i < R; ++i) dst[i] = src[F.reg_qoff[i]];
     };
 
+    // two-tile mode: the second tile has the top tile-index bit set, i.e. the
+    // highest fixed qubit
+    const int64_t tiles = PAIR ? a.tiles >> 1 : a.tiles;
+    const uint32_t top_fixed = (PAIR && n_fixed > 0) ? 1u << P.fixed_qubit[n_fixed - 1] : 0u;
     T2 ps[R], lm[R];
-    for (int64_t tile = w; tile < a.tiles; tile += a.n_wg) {
+    for (int64_t tile = w; tile < tiles; tile += a.n_wg) {
         const uint32_t tbit = lane < n_fixed ? (((uint32_t)tile >> lane) & 1u) : 0u;
         TileCtx cx;
         cx.gb = wave_or(tbit << fq_lane);
+        cx.gb2 = cx.gb | top_fixed;
         cx.ph = ph0;
         cx.tb = tb0;
         cx.ts = ts0;
@@ -825,11 +876,16 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
 #pragma unroll
             for (int i = 0; i < R; ++i) ps[i] = mk<T2>((Real)0, (Real)0);
             if (cx.gb == 0 && cx.tb == 0) ps[0] = mk<T2>((Real)1, (Real)0);
+            if constexpr (PAIR) {  // the second tile never holds amplitude 0
+#pragma unroll
+                for (int i = 0; i < R; ++i) lm[i] = mk<T2>((Real)0, (Real)0);
+            }
         } else {
             load_tile(ps, psi_s, cx.gb);
-            if (load_lam) load_tile(lm, lam_s, cx.gb);
+            if (PAIR) load_tile(lm, psi_s, cx.gb2);
+            else if (load_lam) load_tile(lm, lam_s, cx.gb);
             tile_ready<R>(ps);
-            if (load_lam) tile_ready<R>(lm);
+            if (PAIR || load_lam) tile_ready<R>(lm);
         }
 
         // ---- forward ops
@@ -837,8 +893,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
             XOp<Real> cur = xops[fwd_begin];
             for (int o = fwd_begin; o < fwd_end; ++o) {
                 const XOp<Real> nxt = xops[o + 1];
-                run_op<LOG_R, LOG_T, false>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases,
-                                            gacc, lane, wave, NW, tid);
+                run_op<LOG_R, LOG_T, PAIR ? OP_PAIR : OP_ONE>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx,
+                                                              lds, phases, gacc, lane, wave, NW, tid);
                 cur = nxt;
             }
         }
@@ -847,30 +903,10 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
         // register sums, lane bits from lane-signed wavefront sums, wavefront
         // bits and fixed bits from the tile total with a uniform sign
         if (flags & PF_ZPART) {
-            Real pt = 0, dm[LOG_R];
-#pragma unroll
-            for (int m = 0; m < LOG_R; ++m) dm[m] = 0;
-#pragma unroll
-            for (int i = 0; i < R; ++i) {
-                const Real p = ps[i].x * ps[i].x + ps[i].y * ps[i].y;
-                pt += p;
-#pragma unroll
-                for (int m = 0; m < LOG_R; ++m) dm[m] += (i >> m & 1) ? -p : p;
-            }
-#pragma unroll
-            for (int m = 0; m < LOG_R; ++m) {
-                const double d = wave_total(dm[m]);
-                accz += (lane == (int)qreg[m]) ? d : 0.0;
-            }
-#pragma unroll
-            for (int t = 0; t < 6; ++t) {
-                const double d = wave_total((lane >> t & 1) ? -pt : pt);
-                accz += (lane == (int)qthr[t]) ? d : 0.0;
-            }
-            const double wp = wave_total(pt);
-#pragma unroll
-            for (int t = 6; t < LOG_T; ++t) accz += (lane == (int)qthr[t]) ? ((wave >> (t - 6) & 1) ? -wp : wp) : 0.0;
-            accf += tbit ? -wp : wp;
+            zpart_tile<LOG_R, LOG_T, Real>(ps, tbit, qreg, qthr, lane, wave, accz, accf);
+            if constexpr (PAIR)
+                zpart_tile<LOG_R, LOG_T, Real>(lm, tbit | (uint32_t)(lane == n_fixed - 1), qreg, qthr, lane,
+                                               wave, accz, accf);
         }
 
         if constexpr (BWD) {
@@ -894,8 +930,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 XOp<Real> cur = xops[bwd_begin];
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
-                    run_op<LOG_R, LOG_T, true>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases,
-                                               gacc, lane, wave, NW, tid);
+                    run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases,
+                                                 gacc, lane, wave, NW, tid);
                     cur = nxt;
                 }
             }
@@ -908,6 +944,11 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 T2* dst = psi_s + base;
 #pragma unroll
                 for (int i = 0; i < R; ++i) dst[F.reg_qoff[i]] = ps[i];
+                if constexpr (PAIR) {
+                    T2* dst2 = psi_s + (cx.gb2 | toff_st);
+#pragma unroll
+                    for (int i = 0; i < R; ++i) dst2[F.reg_qoff[i]] = lm[i];
+                }
             }
             if (BWD && (flags & PF_STORE_LAM)) {
                 T2* dst = lam_s + base;
@@ -1051,10 +1092,13 @@ static hipError_t launch_tile_t(bool bwd, const TileArgs& a, int threads, size_t
     const XOp<Real>* xo = (const XOp<Real>*)a.opc;
     const Real* gout = (const Real*)a.grad_out;
     if (bwd)
-        hipLaunchKernelGGL((k_tile<Real, LOG_R, true, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
+        hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_BWD, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
+                           a.phases, xo, gout, a.gslots);
+    else if (a.tiles >= 2)  // forward passes carry two tiles per iteration when there are two
+        hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_FWD2, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
                            a.phases, xo, gout, a.gslots);
     else
-        hipLaunchKernelGGL((k_tile<Real, LOG_R, false, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
+        hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_FWD1, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
                            a.phases, xo, gout, a.gslots);
     return hipGetLastError();
 }
@@ -1124,8 +1168,9 @@ hipError_t configure_kernels(size_t max_lds) {
         if (st < max_lds) QL_ATTR_V((k_tile<REAL, LR, BW, MT>), max_lds - st)             \
     }
 #define QL_ATTR_T(REAL, LR)                                                               \
-    QL_ATTR_TK(REAL, LR, false, 256) QL_ATTR_TK(REAL, LR, true, 256)                      \
-    QL_ATTR_TK(REAL, LR, false, 512) QL_ATTR_TK(REAL, LR, true, 512)
+    QL_ATTR_TK(REAL, LR, KM_FWD1, 256) QL_ATTR_TK(REAL, LR, KM_FWD2, 256)                  \
+    QL_ATTR_TK(REAL, LR, KM_BWD, 256) QL_ATTR_TK(REAL, LR, KM_FWD1, 512)                   \
+    QL_ATTR_TK(REAL, LR, KM_FWD2, 512) QL_ATTR_TK(REAL, LR, KM_BWD, 512)
     QL_ATTR_T(float, 2)
     QL_ATTR_T(float, 3)
     QL_ATTR_T(float, 4)
