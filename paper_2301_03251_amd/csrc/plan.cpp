@@ -107,9 +107,27 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         int q = needed_tile_qubit(g);
         return q < 0 ? -1 : bit_of[q];
     };
-    // choose up to r register bits by a virtual ordered scan; `forbid` masks
-    // tile bits that may not be chosen.
-    auto choose = [&](uint32_t forbid, const std::vector<int>& keep) {
+    const uint32_t low_bits = (low >= 32) ? 0xffffffffu : ((1u << low) - 1);
+    // gates of `pending` that one phase with register bits `regmask` runs (the
+    // same ordered scan the phase itself makes)
+    auto phase_gates = [&](uint32_t regmask) {
+        uint64_t blocked = 0;
+        int cnt = 0;
+        for (int gi : pending) {
+            const Gate& g = gates[gi];
+            uint64_t qs = (1ull << g.q0) | (n_qubits_of(g) == 2 ? (1ull << g.q1) : 0);
+            int b = need_bit(g);
+            if (!(qs & blocked) && (b < 0 || (regmask >> b & 1))) cnt++;
+            else blocked |= qs;
+        }
+        return cnt;
+    };
+    // Register bits of the next phase: the r allowed tile bits that let the
+    // most pending gates run in that phase (all r-subsets are tried); ties
+    // prefer sets without the low (coalesced) bits, so a pass more often ends
+    // in a layout it can store, then the ordered-scan choice below. `forbid`
+    // masks tile bits that may not be chosen.
+    auto choose_scan = [&](uint32_t forbid, const std::vector<int>& keep) {
         std::vector<int> chosen;
         uint64_t blocked = 0;
         for (int gi : pending) {
@@ -134,7 +152,28 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         std::sort(chosen.begin(), chosen.end());
         return chosen;
     };
-    const uint32_t low_mask = (low >= 32) ? 0xffffffffu : ((1u << low) - 1);
+    auto choose = [&](uint32_t forbid, const std::vector<int>& keep) {
+        std::vector<int> chosen = choose_scan(forbid, keep);
+        uint32_t best = 0;
+        for (int b : chosen) best |= 1u << b;
+        int best_n = phase_gates(best);
+        bool best_low = (best & low_bits) != 0;
+        for (uint32_t m = 0; m < (1u << k); m++) {
+            if (__builtin_popcount(m) != r || (m & forbid)) continue;
+            const int c = phase_gates(m);
+            const bool lw = (m & low_bits) != 0;
+            if (c > best_n || (c == best_n && best_low && !lw)) {
+                best = m;
+                best_n = c;
+                best_low = lw;
+            }
+        }
+        chosen.clear();
+        for (int b = 0; b < k; b++)
+            if (best >> b & 1) chosen.push_back(b);
+        return chosen;
+    };
+    const uint32_t low_mask = low_bits;
 
     std::vector<int> regs = choose(low_mask, {});
     int cur_phase = (int)phases.size();
