@@ -351,8 +351,10 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         pl.k = c.n;
         return "";
     }
-    int log_r = o.log_regs ? o.log_regs : (dtype == 0 ? 5 : 4);
-    int log_t = o.log_threads ? o.log_threads : 8;
+    // complex64: 16 amplitudes per thread and 512 threads (a 2^13-amplitude
+    // tile, four wavefronts per SIMD); complex128: 16 per thread, 256 threads
+    int log_r = o.log_regs ? o.log_regs : 4;
+    int log_t = o.log_threads ? o.log_threads : (dtype == 0 ? 9 : 8);
     while (log_r + log_t > c.n && log_t > 6) log_t--;
     while (log_r + log_t > c.n && log_r > 2) log_r--;
     if (log_r + log_t > c.n) return "circuit too small for the tile kernel";
