@@ -26,8 +26,10 @@
  *
  * Precision: QL_C64 states are complex64 (fp32 real/imag), angles, grad_out
  * and all outputs are fp32; QL_C128 uses complex128 and fp64 throughout.
- * Every reduction (over amplitudes, workgroups and the batch) accumulates in
- * fp64 in a fixed order, so results are bit-reproducible run to run.
+ * Every reduction runs in a fixed order, so results are bit-reproducible run
+ * to run. For QL_C64, sums over one wavefront and over the tiles of one
+ * workgroup are fp32; sums across wavefronts, workgroups and the batch are
+ * fp64.
  *
  * Memory: all array arguments of ql_forward / ql_forward_backward are DEVICE
  * pointers on the current HIP device, row-major and contiguous, owned by the
@@ -130,6 +132,29 @@ int ql_forward_backward(const ql_circuit* c, ql_dtype dtype, int64_t batch,
                         const void* inputs, const void* weights, const void* grad_out,
                         void* expz, void* grad_inputs, void* grad_weights,
                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ---- parameter-shift gradients -------------------------------------------
+ *
+ * The same VJP as ql_forward_backward, computed with the two-term
+ * parameter-shift rule instead of the adjoint sweep. The paper's hybrid example
+ * (appendix, class Hybrid) differentiates its quantum node this way, by
+ * re-running the circuit with the angle shifted by +pi/2 and -pi/2; for
+ * exp(-i t P / 2) gates d<Z_i>/dt = (<Z_i>(t + pi/2) - <Z_i>(t - pi/2)) / 2 is
+ * exact (the paper's own expression omits the 1/2). Every rotation occurrence
+ * s of every sample b gives two shifted circuits; together with the unshifted
+ * one these are B * (2S + 1) circuits for S rotation gates, run as extra
+ * samples of batched forward passes in chunks of at most max_chunk circuits
+ * (0 = all at once). Arguments, outputs, layout and errors are those of
+ * ql_forward_backward; grad_out is required. The workspace must hold
+ * ql_param_shift_workspace_bytes(c, dtype, batch, max_chunk) bytes; it grows
+ * with the chunk (one state per circuit of a chunk) and with B * (2S + 1)
+ * fp64 values. Results are deterministic. */
+int ql_param_shift_workspace_bytes(const ql_circuit* c, ql_dtype dtype, int64_t batch,
+                                   int64_t max_chunk, size_t* out);
+int ql_param_shift(const ql_circuit* c, ql_dtype dtype, int64_t batch, const void* inputs,
+                   const void* weights, const void* grad_out, void* expz, void* grad_inputs,
+                   void* grad_weights, int64_t max_chunk, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* ql_last_error(void);

@@ -247,78 +247,84 @@ struct Timer {
     }
 };
 
-int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* inputs,
-        const void* weights, const void* grad_out, void* expz, void* grad_inputs,
-        void* grad_weights, void* ws, size_t ws_bytes, hipStream_t stream) {
-    if (!hc) return fail(QL_EINVAL, "circuit is NULL");
-    ql_circuit* h = const_cast<ql_circuit*>(hc);  // only the timing state is touched
-    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
-    const int dt = (int)dtype;
-    const Circuit& c = h->c;
-    const Plan& pl = c.plan[dt];
-    const Tables& T = h->t[dt];
-    const bool bwd = mode == QL_MODE_FWD_BWD;
+// One call's device context: the plan tables of its dtype, the workspace
+// layout and the stream.
+struct Ctx {
+    ql_circuit* h;
+    int dt;
+    const Circuit& c;
+    const Plan& pl;
+    const Tables& T;
+    uint8_t* W;
     Layout L;
-    int rc = compute_layout(h, dt, B, mode, L);
-    if (rc) return rc;
-    if (!expz) return fail(QL_EINVAL, "expz is NULL");
-    if (c.n_inputs > 0 && !inputs) return fail(QL_EINVAL, "inputs is NULL");
-    if (c.n_weights > 0 && !weights) return fail(QL_EINVAL, "weights is NULL");
-    if (bwd && !grad_out) return fail(QL_EINVAL, "grad_out is NULL");
-    if (!ws) return fail(QL_EINVAL, "workspace is NULL");
-    if (ws_bytes < L.total)
-        return fail(QL_ENOMEM, "workspace too small: need " + std::to_string(L.total) + " bytes, got " +
-                                   std::to_string(ws_bytes));
-    rc = ensure_device();
-    if (rc) return rc;
+    hipStream_t stream;
+    Timer tm;
+};
 
-    const size_t amp = dt == 0 ? 8 : 16;
-    uint8_t* W = (uint8_t*)ws;
-    const int n_slots = (int)c.slot_gate.size();
-    hipError_t e = hipMemcpyAsync(W + L.tables, T.blob.data(), T.blob.size(), hipMemcpyHostToDevice, stream);
-    if (e != hipSuccess) return fail(QL_EHIP, std::string("table upload: ") + hipGetErrorString(e));
-    Timer tm{h, stream};
+int upload_tables(Ctx& x) {
+    hipError_t e = hipMemcpyAsync(x.W + x.L.tables, x.T.blob.data(), x.T.blob.size(), hipMemcpyHostToDevice,
+                                  x.stream);
+    return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("table upload: ") + hipGetErrorString(e));
+}
 
-    if (pl.whole_state) {
+// Angle binding for B circuits. With vper > 0 the circuits are the shifted
+// copies of a parameter-shift chunk: circuit i is virtual circuit v = v0 + i,
+// sample v / vper, and v % vper = 2s+1 (2s+2) shifts rotation slot s by
+// +pi/2 (-pi/2).
+int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0, int32_t vper) {
+    hipError_t e;
+    if (x.pl.whole_state) {
         BindArgs ba{};
         ba.inputs = inputs;
         ba.weights = weights;
-        ba.slots = (const SlotSrc*)(W + L.tables + T.off_slots);
-        ba.coef = W + L.coef;
+        ba.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
+        ba.coef = x.W + x.L.coef;
         ba.B = B;
-        ba.n_slots = n_slots;
-        ba.F = c.n_inputs;
-        tm.start(2);
-        e = launch_bind(dt, ba, stream);
-        tm.stop();
+        ba.n_slots = (int)x.c.slot_gate.size();
+        ba.F = x.c.n_inputs;
+        ba.v0 = v0;
+        ba.vper = vper;
+        x.tm.start(2);
+        e = launch_bind(x.dt, ba, x.stream);
+        x.tm.stop();
     } else {
         BindTileArgs ba{};
         ba.inputs = inputs;
         ba.weights = weights;
-        ba.slots = (const SlotSrc*)(W + L.tables + T.off_slots);
-        ba.ops = (const DevOp*)(W + L.tables + T.off_ops);
-        ba.opc = W + L.opc;
+        ba.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
+        ba.ops = (const DevOp*)(x.W + x.L.tables + x.T.off_ops);
+        ba.opc = x.W + x.L.opc;
         ba.B = B;
-        ba.n_ops = T.n_ops;
-        ba.bwd_first = T.bwd_first;
-        ba.F = c.n_inputs;
-        tm.start(2);
-        e = launch_bind_tile(dt, ba, stream);
-        tm.stop();
+        ba.n_ops = x.T.n_ops;
+        ba.bwd_first = x.T.bwd_first;
+        ba.F = x.c.n_inputs;
+        ba.v0 = v0;
+        ba.vper = vper;
+        x.tm.start(2);
+        e = launch_bind_tile(x.dt, ba, x.stream);
+        x.tm.stop();
     }
-    if (e != hipSuccess) return fail(QL_EHIP, std::string("k_bind: ") + hipGetErrorString(e));
+    return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("k_bind: ") + hipGetErrorString(e));
+}
 
-    double* zpart = (double*)(W + L.zpart);
-    double* gpart = bwd ? (double*)(W + L.gpart) : nullptr;
+// The state passes of B circuits: the whole-state kernel, or the forward tile
+// passes, the fused pass and (bwd) the backward passes. Writes the <Z> partials
+// (and, bwd, the gradient partials) of the workspace.
+int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out) {
+    const Circuit& c = x.c;
+    const Plan& pl = x.pl;
+    const size_t amp = x.dt == 0 ? 8 : 16;
+    double* zpart = (double*)(x.W + x.L.zpart);
+    double* gpart = bwd ? (double*)(x.W + x.L.gpart) : nullptr;
     if (pl.whole_state) {
         WholeArgs wa{};
-        wa.gates = (const DevGate*)(W + L.tables + T.off_gates);
+        wa.gates = (const DevGate*)(x.W + x.L.tables + x.T.off_gates);
         wa.n_gates = (int)c.gates.size();
         wa.n = c.n;
-        wa.n_slots = n_slots;
+        wa.n_slots = (int)c.slot_gate.size();
         wa.bwd = bwd ? 1 : 0;
         wa.B = B;
-        wa.coef = W + L.coef;
+        wa.coef = x.W + x.L.coef;
         wa.grad_out = grad_out;
         wa.zpart = zpart;
         wa.gpart = gpart;
@@ -326,81 +332,207 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
         const int threads = std::max(64, std::min(256, dim / 4));
         const size_t lds = 2 * (size_t)dim * amp + (size_t)c.n * (threads / 64) * 8 + 64;
         if (lds > g_lds_limit) return fail(QL_EUNSUPPORTED, "state does not fit in LDS");
-        tm.start(1);
-        e = launch_whole(dt, wa, threads, lds, stream);
-        tm.stop();
-        if (e != hipSuccess) return fail(QL_EHIP, std::string("k_whole: ") + hipGetErrorString(e));
-    } else {
-        const int m = (int)pl.passes.size();
-        const int threads = 1 << pl.log_t;
-        const int NW = threads / 64;
-        auto launch_pass = [&](int p, int flags) -> int {
-            const DevPass& d = T.passes[p];
-            TileArgs ta{};
-            ta.psi = L.psi ? (void*)(W + L.psi) : nullptr;
-            ta.lam = L.lam ? (void*)(W + L.lam) : nullptr;
-            ta.pass = (const DevPass*)(W + L.tables + T.off_pass) + p;
-            ta.phases = (const DevPhase*)(W + L.tables + T.off_phase);
-            ta.ops = (const DevOp*)(W + L.tables + T.off_ops);
-            ta.gslots = (const int32_t*)(W + L.tables + T.off_gslot) + d.gslot_base;
-            ta.opc = W + L.opc;
-            ta.grad_out = grad_out;
-            ta.zpart = zpart;
-            ta.gpart = gpart;
-            ta.B = B;
-            ta.tiles = (int64_t)1 << (c.n - pl.k);
-            ta.n = c.n;
-            ta.n_ops = T.n_ops;
-            ta.n_wg = L.n_wg;
-            ta.flags = flags;
-            ta.n_gslots = (flags & PF_BWD) ? d.n_gslots : 0;
-            // dynamic LDS: <Z> and gradient scratch (the exchange buffer is static)
-            const size_t lds = (size_t)(c.n + ta.n_gslots) * NW * 8;
-            if (lds + tile_static_lds(dt, pl.log_r, threads) > g_lds_limit)
-                return fail(QL_EUNSUPPORTED, "tile pass needs more LDS than available");
-            tm.start(0);
-            hipError_t le = launch_tile(dt, pl.log_r, (flags & PF_BWD) != 0, ta, threads, lds, stream);
-            tm.stop();
-            if (le != hipSuccess) return fail(QL_EHIP, std::string("k_tile: ") + hipGetErrorString(le));
-            return QL_OK;
-        };
-        for (int p = 0; p + 1 < m; p++) {
-            rc = launch_pass(p, (p == 0 ? PF_INIT : 0) | PF_FWD | PF_STORE_PSI);
+        x.tm.start(1);
+        hipError_t e = launch_whole(x.dt, wa, threads, lds, x.stream);
+        x.tm.stop();
+        return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("k_whole: ") + hipGetErrorString(e));
+    }
+    const int m = (int)pl.passes.size();
+    const int threads = 1 << pl.log_t;
+    const int NW = threads / 64;
+    auto launch_pass = [&](int p, int flags) -> int {
+        const DevPass& d = x.T.passes[p];
+        TileArgs ta{};
+        ta.psi = x.L.psi ? (void*)(x.W + x.L.psi) : nullptr;
+        ta.lam = x.L.lam ? (void*)(x.W + x.L.lam) : nullptr;
+        ta.pass = (const DevPass*)(x.W + x.L.tables + x.T.off_pass) + p;
+        ta.phases = (const DevPhase*)(x.W + x.L.tables + x.T.off_phase);
+        ta.ops = (const DevOp*)(x.W + x.L.tables + x.T.off_ops);
+        ta.gslots = (const int32_t*)(x.W + x.L.tables + x.T.off_gslot) + d.gslot_base;
+        ta.opc = x.W + x.L.opc;
+        ta.grad_out = grad_out;
+        ta.zpart = zpart;
+        ta.gpart = gpart;
+        ta.B = B;
+        ta.tiles = (int64_t)1 << (c.n - pl.k);
+        ta.n = c.n;
+        ta.n_ops = x.T.n_ops;
+        ta.n_wg = x.L.n_wg;
+        ta.flags = flags;
+        ta.n_gslots = (flags & PF_BWD) ? d.n_gslots : 0;
+        // dynamic LDS: <Z> and gradient scratch (the exchange buffer is static)
+        const size_t lds = (size_t)(c.n + ta.n_gslots) * NW * 8;
+        if (lds + tile_static_lds(x.dt, pl.log_r, threads) > g_lds_limit)
+            return fail(QL_EUNSUPPORTED, "tile pass needs more LDS than available");
+        x.tm.start(0);
+        hipError_t le = launch_tile(x.dt, pl.log_r, (flags & PF_BWD) != 0, ta, threads, lds, x.stream);
+        x.tm.stop();
+        if (le != hipSuccess) return fail(QL_EHIP, std::string("k_tile: ") + hipGetErrorString(le));
+        return QL_OK;
+    };
+    int rc;
+    for (int p = 0; p + 1 < m; p++) {
+        rc = launch_pass(p, (p == 0 ? PF_INIT : 0) | PF_FWD | PF_STORE_PSI);
+        if (rc) return rc;
+    }
+    int last = (m == 1 ? PF_INIT : 0) | PF_FWD | PF_ZPART;
+    if (bwd) last |= PF_SEED | PF_BWD | (m > 1 ? (PF_STORE_PSI | PF_STORE_LAM) : 0);
+    rc = launch_pass(m - 1, last);
+    if (rc) return rc;
+    if (bwd)
+        for (int p = m - 2; p >= 0; p--) {
+            rc = launch_pass(p, PF_LOAD_LAM | PF_BWD | (p > 0 ? (PF_STORE_PSI | PF_STORE_LAM) : 0));
             if (rc) return rc;
         }
-        int last = (m == 1 ? PF_INIT : 0) | PF_FWD | PF_ZPART;
-        if (bwd) last |= PF_SEED | PF_BWD | (m > 1 ? (PF_STORE_PSI | PF_STORE_LAM) : 0);
-        rc = launch_pass(m - 1, last);
-        if (rc) return rc;
-        if (bwd)
-            for (int p = m - 2; p >= 0; p--) {
-                rc = launch_pass(p, PF_LOAD_LAM | PF_BWD | (p > 0 ? (PF_STORE_PSI | PF_STORE_LAM) : 0));
-                if (rc) return rc;
-            }
-    }
+    return QL_OK;
+}
 
+// Final fixed-order reductions of the partials into expz (and gradients).
+int reduce(Ctx& x, int64_t B, bool grads, void* expz, void* grad_inputs, void* grad_weights) {
     ReduceArgs ra{};
-    ra.zpart = zpart;
-    ra.gpart = gpart;
+    ra.zpart = (const double*)(x.W + x.L.zpart);
+    ra.gpart = grads ? (const double*)(x.W + x.L.gpart) : nullptr;
     ra.expz = expz;
     ra.grad_inputs = grad_inputs;
     ra.grad_weights = grad_weights;
-    ra.x_ptr = (const int32_t*)(W + L.tables + T.off_xptr);
-    ra.x_slot = (const int32_t*)(W + L.tables + T.off_xslot);
-    ra.w_ptr = (const int32_t*)(W + L.tables + T.off_wptr);
-    ra.w_slot = (const int32_t*)(W + L.tables + T.off_wslot);
+    ra.x_ptr = (const int32_t*)(x.W + x.L.tables + x.T.off_xptr);
+    ra.x_slot = (const int32_t*)(x.W + x.L.tables + x.T.off_xslot);
+    ra.w_ptr = (const int32_t*)(x.W + x.L.tables + x.T.off_wptr);
+    ra.w_slot = (const int32_t*)(x.W + x.L.tables + x.T.off_wslot);
     ra.B = B;
-    ra.n = c.n;
-    ra.n_wg = L.n_wg;
-    ra.F = c.n_inputs;
-    ra.P = c.n_weights;
-    ra.n_slots = n_slots;
-    ra.grads = bwd ? 1 : 0;
-    tm.start(3);
-    e = launch_reduce(dt, ra, stream);
-    tm.stop();
-    if (e != hipSuccess) return fail(QL_EHIP, std::string("k_reduce: ") + hipGetErrorString(e));
+    ra.n = x.c.n;
+    ra.n_wg = x.L.n_wg;
+    ra.F = x.c.n_inputs;
+    ra.P = x.c.n_weights;
+    ra.n_slots = (int)x.c.slot_gate.size();
+    ra.grads = grads ? 1 : 0;
+    x.tm.start(3);
+    hipError_t e = launch_reduce(x.dt, ra, x.stream);
+    x.tm.stop();
+    return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("k_reduce: ") + hipGetErrorString(e));
+}
+
+int check_args(const Circuit& c, const void* inputs, const void* weights, const void* expz, bool need_g,
+               const void* grad_out, const void* ws) {
+    if (!expz) return fail(QL_EINVAL, "expz is NULL");
+    if (c.n_inputs > 0 && !inputs) return fail(QL_EINVAL, "inputs is NULL");
+    if (c.n_weights > 0 && !weights) return fail(QL_EINVAL, "weights is NULL");
+    if (need_g && !grad_out) return fail(QL_EINVAL, "grad_out is NULL");
+    if (!ws) return fail(QL_EINVAL, "workspace is NULL");
     return QL_OK;
+}
+
+int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* inputs,
+        const void* weights, const void* grad_out, void* expz, void* grad_inputs,
+        void* grad_weights, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (!hc) return fail(QL_EINVAL, "circuit is NULL");
+    ql_circuit* h = const_cast<ql_circuit*>(hc);  // only the timing state is touched
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    const int dt = (int)dtype;
+    const bool bwd = mode == QL_MODE_FWD_BWD;
+    Layout L;
+    int rc = compute_layout(h, dt, B, mode, L);
+    if (rc) return rc;
+    rc = check_args(h->c, inputs, weights, expz, bwd, grad_out, ws);
+    if (rc) return rc;
+    if (ws_bytes < L.total)
+        return fail(QL_ENOMEM, "workspace too small: need " + std::to_string(L.total) + " bytes, got " +
+                                   std::to_string(ws_bytes));
+    rc = ensure_device();
+    if (rc) return rc;
+    Ctx x{h, dt, h->c, h->c.plan[dt], h->t[dt], (uint8_t*)ws, L, stream, Timer{h, stream}};
+    if ((rc = upload_tables(x))) return rc;
+    if ((rc = bind(x, B, inputs, weights, 0, 0))) return rc;
+    if ((rc = state_passes(x, B, bwd, grad_out))) return rc;
+    return reduce(x, B, bwd, expz, grad_inputs, grad_weights);
+}
+
+// Workspace of a parameter-shift call: the forward layout of one chunk of
+// C shifted circuits, then the chunk's <Z> values [C][n] (Real) and the VJP
+// of every shifted circuit [B * (2S+1)] (fp64).
+struct ShiftLayout {
+    Layout L;
+    int64_t chunk = 0, total = 0;
+    size_t ev = 0, dv = 0, bytes = 0;
+};
+
+int shift_layout(const ql_circuit* h, int dt, int64_t B, int64_t max_chunk, ShiftLayout& S) {
+    if (B < 1) return fail(QL_EINVAL, "batch must be >= 1");
+    if (max_chunk < 0) return fail(QL_EINVAL, "max_chunk must be >= 0");
+    const int64_t V = 2 * (int64_t)h->c.slot_gate.size() + 1;
+    if (B > ((int64_t)1 << 40) / V) return fail(QL_EINVAL, "batch too large");
+    S.total = B * V;
+    S.chunk = max_chunk > 0 ? std::min<int64_t>(max_chunk, S.total) : S.total;
+    int rc = compute_layout(h, dt, S.chunk, QL_MODE_FWD, S.L);
+    if (rc) return rc;
+    const size_t real = dt == 0 ? 4 : 8;
+    size_t off = S.L.total, sz;
+    S.ev = off;
+    if (!mul_ok((size_t)S.chunk, (size_t)h->c.n * real, sz)) return fail(QL_ENOMEM, "size overflow");
+    off = align256(off + sz);
+    S.dv = off;
+    if (!mul_ok((size_t)S.total, 8, sz)) return fail(QL_ENOMEM, "size overflow");
+    S.bytes = align256(off + sz);
+    return QL_OK;
+}
+
+int param_shift(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs,
+                const void* weights, const void* grad_out, void* expz, void* grad_inputs,
+                void* grad_weights, int64_t max_chunk, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (!hc) return fail(QL_EINVAL, "circuit is NULL");
+    ql_circuit* h = const_cast<ql_circuit*>(hc);
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    const int dt = (int)dtype;
+    ShiftLayout S;
+    int rc = shift_layout(h, dt, B, max_chunk, S);
+    if (rc) return rc;
+    rc = check_args(h->c, inputs, weights, expz, true, grad_out, ws);
+    if (rc) return rc;
+    if (ws_bytes < S.bytes)
+        return fail(QL_ENOMEM, "workspace too small: need " + std::to_string(S.bytes) + " bytes, got " +
+                                   std::to_string(ws_bytes));
+    rc = ensure_device();
+    if (rc) return rc;
+    Ctx x{h, dt, h->c, h->c.plan[dt], h->t[dt], (uint8_t*)ws, S.L, stream, Timer{h, stream}};
+    if ((rc = upload_tables(x))) return rc;
+    const int32_t V = (int32_t)(2 * h->c.slot_gate.size() + 1);
+    void* ev = x.W + S.ev;
+    double* dv = (double*)(x.W + S.dv);
+    for (int64_t v0 = 0; v0 < S.total; v0 += S.chunk) {
+        const int64_t cb = std::min(S.chunk, S.total - v0);
+        if ((rc = bind(x, cb, inputs, weights, v0, V))) return rc;
+        if ((rc = state_passes(x, cb, false, nullptr))) return rc;
+        if ((rc = reduce(x, cb, false, ev, nullptr, nullptr))) return rc;
+        ShiftDotArgs sa{};
+        sa.ev = ev;
+        sa.grad_out = grad_out;
+        sa.expz = expz;
+        sa.dv = dv;
+        sa.v0 = v0;
+        sa.count = cb;
+        sa.vper = V;
+        sa.n = h->c.n;
+        x.tm.start(3);
+        hipError_t e = launch_shift_dot(dt, sa, stream);
+        x.tm.stop();
+        if (e != hipSuccess) return fail(QL_EHIP, std::string("k_shift_dot: ") + hipGetErrorString(e));
+    }
+    ShiftGradArgs ga{};
+    ga.dv = dv;
+    ga.grad_inputs = grad_inputs;
+    ga.grad_weights = grad_weights;
+    ga.x_ptr = (const int32_t*)(x.W + x.L.tables + x.T.off_xptr);
+    ga.x_slot = (const int32_t*)(x.W + x.L.tables + x.T.off_xslot);
+    ga.w_ptr = (const int32_t*)(x.W + x.L.tables + x.T.off_wptr);
+    ga.w_slot = (const int32_t*)(x.W + x.L.tables + x.T.off_wslot);
+    ga.B = B;
+    ga.vper = V;
+    ga.F = h->c.n_inputs;
+    ga.P = h->c.n_weights;
+    x.tm.start(3);
+    hipError_t e = launch_shift_grad(dt, ga, stream);
+    x.tm.stop();
+    return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("k_shift_grad: ") + hipGetErrorString(e));
 }
 
 Options to_options(const ql_options* o) {
@@ -484,6 +616,26 @@ int ql_forward_backward(const ql_circuit* h, ql_dtype dtype, int64_t batch, cons
                         void* grad_weights, void* ws, size_t ws_bytes, hipStream_t stream) {
     int rc = run(h, dtype, batch, QL_MODE_FWD_BWD, inputs, weights, grad_out, expz, grad_inputs,
                  grad_weights, ws, ws_bytes, stream);
+    if (rc == QL_OK) g_err.clear();
+    return rc;
+}
+
+int ql_param_shift_workspace_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, int64_t max_chunk,
+                                   size_t* out) {
+    if (!h || !out) return fail(QL_EINVAL, "NULL argument");
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    ShiftLayout S;
+    int rc = shift_layout(h, (int)dtype, batch, max_chunk, S);
+    if (rc) return rc;
+    *out = S.bytes;
+    return QL_OK;
+}
+
+int ql_param_shift(const ql_circuit* h, ql_dtype dtype, int64_t batch, const void* inputs,
+                   const void* weights, const void* grad_out, void* expz, void* grad_inputs,
+                   void* grad_weights, int64_t max_chunk, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int rc = param_shift(h, dtype, batch, inputs, weights, grad_out, expz, grad_inputs, grad_weights,
+                         max_chunk, ws, ws_bytes, stream);
     if (rc == QL_OK) g_err.clear();
     return rc;
 }

@@ -88,6 +88,31 @@ __device__ __forceinline__ double wave_total(double v) {
 }
 
 // ---------------------------------------------------------------------------
+// angle sources (shared by the binding kernels)
+
+// The bound angle of rotation slot `s` for circuit b. In a parameter-shift
+// chunk (vper > 0) circuit b is virtual circuit v = v0 + b of sample v / vper.
+template <typename Real>
+__device__ __forceinline__ Real angle_of(const void* inputs, const void* weights, int F, const SlotSrc src,
+                                         int64_t b, int64_t v0, int32_t vper, int s, int64_t& bs) {
+    (void)s;
+    bs = vper > 0 ? (v0 + b) / vper : b;
+    return src.src == S_INPUT ? ((const Real*)inputs)[bs * F + src.index] : ((const Real*)weights)[src.index];
+}
+
+// Parameter-shift offset of slot s in circuit b: v % vper = 2s+1 adds pi/2,
+// 2s+2 subtracts it (the two-term rule of exp(-i t P / 2) gates).
+__device__ __forceinline__ double shift_of(int64_t b, int64_t v0, int32_t vper, int s) {
+    if (vper <= 0) return 0.0;
+    const int64_t v = v0 + b;
+    const int j = (int)(v - (v / vper) * vper);
+    const double half_pi = 1.570796326794896619231;
+    if (j == 2 * s + 1) return half_pi;
+    if (j == 2 * s + 2) return -half_pi;
+    return 0.0;
+}
+
+// ---------------------------------------------------------------------------
 // k_bind
 
 template <typename Real>
@@ -98,9 +123,9 @@ __global__ void k_bind(const BindArgs a) {
     const int64_t b = t / a.n_slots;
     const int s = (int)(t - b * a.n_slots);
     const SlotSrc src = a.slots[s];
-    const double th = src.src == S_INPUT
-                          ? (double)((const Real*)a.inputs)[b * a.F + src.index]
-                          : (double)((const Real*)a.weights)[src.index];
+    int64_t bs = b;
+    const double th = (double)angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, s, bs) +
+                      shift_of(b, a.v0, a.vper, s);
     double sn, cs;
     sincos(0.5 * th, &sn, &cs);
     ((T2*)a.coef)[t] = mk<T2>((Real)cs, (Real)sn);
@@ -1003,8 +1028,9 @@ __global__ void k_bind_tile(const BindTileArgs a) {
     e.arg = op.arg;
     if (op.slot >= 0) {
         const SlotSrc src = a.slots[op.slot];
-        double th = src.src == S_INPUT ? (double)((const Real*)a.inputs)[b * a.F + src.index]
-                                       : (double)((const Real*)a.weights)[src.index];
+        int64_t bs;
+        double th = (double)angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, op.slot, bs) +
+                    shift_of(b, a.v0, a.vper, op.slot);
         const double two_pi = 6.283185307179586476925;
         th -= two_pi * rint(th / two_pi);  // [-pi, pi]; the dropped sign is common to psi and lambda
         if (o >= a.bwd_first) th = -th;     // backward ops apply the inverse
@@ -1060,6 +1086,58 @@ __global__ void __launch_bounds__(256) k_reduce(const ReduceArgs a) {
         for (int i = a.w_ptr[p]; i < a.w_ptr[p + 1]; ++i) {
             const double* src = a.gpart + (size_t)a.w_slot[i] * per;
             for (int64_t j = lane; j < per; j += 64) acc += src[j];
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) ((Real*)a.grad_weights)[p] = (Real)acc;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// parameter shift: per-circuit VJP, then the two-term differences
+
+template <typename Real>
+__global__ void __launch_bounds__(256) k_shift_dot(const ShiftDotArgs a) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= a.count) return;
+    const int64_t v = a.v0 + i;
+    const int64_t b = v / a.vper;
+    const Real* e = (const Real*)a.ev + i * a.n;
+    const Real* g = (const Real*)a.grad_out + b * a.n;
+    double d = 0;
+    for (int q = 0; q < a.n; ++q) d += (double)g[q] * (double)e[q];
+    a.dv[v] = d;
+    if (v - b * a.vper == 0)
+        for (int q = 0; q < a.n; ++q) ((Real*)a.expz)[b * a.n + q] = e[q];
+}
+
+// One wavefront per output element: input gradient (b, f) or weight p.
+template <typename Real>
+__global__ void __launch_bounds__(256) k_shift_grad(const ShiftGradArgs a) {
+    const int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    const int64_t nx = a.grad_inputs ? a.B * a.F : 0;
+    const int64_t nw = a.grad_weights ? a.P : 0;
+    double acc = 0;
+    if (e < nx) {
+        const int64_t b = e / a.F;
+        const int f = (int)(e - b * a.F);
+        const int cnt = a.x_ptr[f + 1] - a.x_ptr[f];
+        for (int i = lane; i < cnt; i += 64) {
+            const int s = a.x_slot[a.x_ptr[f] + i];
+            const double* d = a.dv + b * a.vper;
+            acc += 0.5 * (d[2 * s + 1] - d[2 * s + 2]);
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) ((Real*)a.grad_inputs)[e] = (Real)acc;
+    } else if (e < nx + nw) {
+        const int p = (int)(e - nx);
+        const int cnt = a.w_ptr[p + 1] - a.w_ptr[p];
+        const int64_t per = (int64_t)cnt * a.B;
+        for (int64_t j = lane; j < per; j += 64) {
+            const int64_t b = j / cnt;
+            const int s = a.w_slot[a.w_ptr[p] + (int)(j - b * cnt)];
+            const double* d = a.dv + b * a.vper;
+            acc += 0.5 * (d[2 * s + 1] - d[2 * s + 2]);
         }
         acc = wave_sum(acc);
         if (lane == 0) ((Real*)a.grad_weights)[p] = (Real)acc;
@@ -1150,6 +1228,23 @@ hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s) {
 size_t tile_static_lds(int dtype, int log_r, int threads) {
     const size_t maxt = threads > 256 ? 512 : 256;
     return maxt * ((size_t)1 << log_r) * 2 * (dtype == 0 ? sizeof(float) : sizeof(double));
+}
+
+hipError_t launch_shift_dot(int dtype, const ShiftDotArgs& a, hipStream_t s) {
+    if (a.count == 0) return hipSuccess;
+    const unsigned grid = (unsigned)((a.count + 255) / 256);
+    if (dtype == 0) hipLaunchKernelGGL(k_shift_dot<float>, dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_shift_dot<double>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s) {
+    const int64_t waves = (a.grad_inputs ? a.B * a.F : 0) + (a.grad_weights ? a.P : 0);
+    if (waves == 0) return hipSuccess;
+    const unsigned grid = (unsigned)((waves + 3) / 4);
+    if (dtype == 0) hipLaunchKernelGGL(k_shift_grad<float>, dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_shift_grad<double>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
 }
 
 hipError_t configure_kernels(size_t max_lds) {

@@ -26,6 +26,8 @@ struct BindArgs {
     void* coef;           // [B][n_slots] complex (cos, sin) of theta/2
     int64_t B;
     int32_t n_slots, F;
+    int64_t v0;           // parameter-shift chunks: first virtual circuit
+    int32_t vper;         // circuits per sample (2 * n_slots + 1), 0 = plain batch
 };
 
 // Per-sample records of the tile ops (handler id, argument, two shear
@@ -39,6 +41,34 @@ struct BindTileArgs {
     void* opc;             // [B][n_ops + 1] records
     int64_t B;
     int32_t n_ops, bwd_first, F;
+    int64_t v0;            // parameter-shift chunks: first virtual circuit
+    int32_t vper;          // circuits per sample (2 * n_slots + 1), 0 = plain batch
+};
+
+// Parameter shift: per shifted circuit v of a chunk, d[v] = sum_i grad_out[b][i]
+// * ev[v - v0][i] in fp64 (b = v / vper); the unshifted circuit (v % vper == 0)
+// also writes expz[b].
+struct ShiftDotArgs {
+    const void* ev;        // [count][n] Real: <Z> of the chunk's circuits
+    const void* grad_out;  // [B][n] Real
+    void* expz;            // [B][n] Real
+    double* dv;            // [B * vper]
+    int64_t v0, count;
+    int32_t vper, n;
+};
+
+// grad of rotation slot s of sample b = (d[b, 2s+1] - d[b, 2s+2]) / 2, summed
+// over each input's / weight's slots (and over the batch for weights).
+struct ShiftGradArgs {
+    const double* dv;      // [B * vper]
+    void* grad_inputs;     // [B][F] Real or null
+    void* grad_weights;    // [P] Real or null
+    const int32_t* x_ptr;
+    const int32_t* x_slot;
+    const int32_t* w_ptr;
+    const int32_t* w_slot;
+    int64_t B;
+    int32_t vper, F, P;
 };
 
 struct WholeArgs {
@@ -99,6 +129,8 @@ hipError_t launch_whole(int dtype, const WholeArgs& a, int threads, size_t lds, 
 hipError_t launch_tile(int dtype, int log_r, bool bwd, const TileArgs& a, int threads, size_t lds,
                        hipStream_t s);
 hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s);
+hipError_t launch_shift_dot(int dtype, const ShiftDotArgs& a, hipStream_t s);
+hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s);
 
 // Raise the dynamic-LDS limit of every kernel on the current device.
 hipError_t configure_kernels(size_t max_lds);

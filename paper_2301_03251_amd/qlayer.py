@@ -43,6 +43,7 @@ class _PlanInfo(ctypes.Structure):
 _lib = None
 EXPORTS = ("ql_circuit_create", "ql_circuit_create_ex", "ql_circuit_destroy",
            "ql_workspace_bytes", "ql_forward", "ql_forward_backward", "ql_last_error",
+           "ql_param_shift_workspace_bytes", "ql_param_shift",
            "ql_plan_info_get", "ql_plan_schedule", "ql_plan_state_bytes",
            "ql_timing_enable", "ql_timing_read")
 
@@ -65,6 +66,8 @@ def load():
     lib.ql_workspace_bytes.argtypes = [P, ctypes.c_int, I64, ctypes.c_int, ctypes.POINTER(SZ)]
     lib.ql_forward.argtypes = [P, ctypes.c_int, I64, P, P, P, P, SZ, P]
     lib.ql_forward_backward.argtypes = [P, ctypes.c_int, I64, P, P, P, P, P, P, P, SZ, P]
+    lib.ql_param_shift_workspace_bytes.argtypes = [P, ctypes.c_int, I64, I64, ctypes.POINTER(SZ)]
+    lib.ql_param_shift.argtypes = [P, ctypes.c_int, I64, P, P, P, P, P, P, I64, P, SZ, P]
     lib.ql_last_error.argtypes = []
     lib.ql_last_error.restype = ctypes.c_char_p
     lib.ql_plan_info_get.argtypes = [P, ctypes.c_int, ctypes.POINTER(_PlanInfo)]
@@ -74,7 +77,8 @@ def load():
     lib.ql_timing_enable.argtypes = [P, ctypes.c_int]
     lib.ql_timing_read.argtypes = [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]
     for name in ("ql_circuit_create", "ql_circuit_create_ex", "ql_workspace_bytes", "ql_forward",
-                 "ql_forward_backward", "ql_plan_info_get", "ql_plan_schedule",
+                 "ql_forward_backward", "ql_param_shift_workspace_bytes", "ql_param_shift",
+                 "ql_plan_info_get", "ql_plan_schedule",
                  "ql_plan_state_bytes", "ql_timing_enable", "ql_timing_read"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -153,6 +157,12 @@ class Circuit:
         _check(load().ql_timing_read(self._h, ms, cnt))
         return list(ms), list(cnt)
 
+    def param_shift_workspace_bytes(self, dtype, batch, max_chunk=0) -> int:
+        out = ctypes.c_size_t()
+        _check(load().ql_param_shift_workspace_bytes(self._h, _dt(dtype), int(batch), int(max_chunk),
+                                                     ctypes.byref(out)))
+        return out.value
+
     # raw entry points: device pointers as ints, stream as int (hipStream_t)
     def forward_raw(self, dtype, batch, inputs, weights, expz, ws, ws_bytes, stream):
         _check(load().ql_forward(self._h, _dt(dtype), int(batch), inputs, weights, expz, ws,
@@ -163,6 +173,12 @@ class Circuit:
         _check(load().ql_forward_backward(self._h, _dt(dtype), int(batch), inputs, weights,
                                           grad_out, expz, grad_inputs, grad_weights, ws,
                                           int(ws_bytes), stream))
+
+    def param_shift_raw(self, dtype, batch, inputs, weights, grad_out, expz, grad_inputs,
+                        grad_weights, max_chunk, ws, ws_bytes, stream):
+        _check(load().ql_param_shift(self._h, _dt(dtype), int(batch), inputs, weights, grad_out,
+                                     expz, grad_inputs, grad_weights, int(max_chunk), ws,
+                                     int(ws_bytes), stream))
 
 
 # ---------------------------------------------------------------------------
@@ -233,6 +249,33 @@ class Runner:
             self.dtype, B, _ptr(x) if self.c.n_inputs else None, _ptr(w) if self.c.n_weights else None,
             _ptr(grad_out), _ptr(expz), _ptr(gx) if (gx is not None and self.c.n_inputs) else None,
             _ptr(gw) if (gw is not None and self.c.n_weights) else None, _ptr(ws), ws.numel(),
+            ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
+        return expz, gx, gw
+
+
+    def param_shift(self, inputs, weights, grad_out, max_chunk=0, want_inputs=True, want_weights=True,
+                    outs=None):
+        """The VJP of forward_backward by the two-term parameter-shift rule
+        (shifted circuits folded into the batch, in chunks of max_chunk)."""
+        torch = _torch()
+        B = int(inputs.shape[0])
+        x, w = self._args(inputs, weights, B)
+        if grad_out.dtype != self.real or not grad_out.is_contiguous():
+            raise ValueError("grad_out must be a contiguous tensor of the layer's real dtype")
+        if outs is None:
+            expz = torch.empty((B, self.c.n), dtype=self.real, device=self.device)
+            gx = torch.empty((B, self.c.n_inputs), dtype=self.real, device=self.device) if want_inputs else None
+            gw = torch.empty(self.c.n_weights, dtype=self.real, device=self.device) if want_weights else None
+        else:
+            expz, gx, gw = outs
+        need = self.c.param_shift_workspace_bytes(self.dtype, B, max_chunk)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        ws = self._ws
+        self.c.param_shift_raw(
+            self.dtype, B, _ptr(x) if self.c.n_inputs else None, _ptr(w) if self.c.n_weights else None,
+            _ptr(grad_out), _ptr(expz), _ptr(gx) if (gx is not None and self.c.n_inputs) else None,
+            _ptr(gw) if (gw is not None and self.c.n_weights) else None, max_chunk, _ptr(ws), ws.numel(),
             ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
         return expz, gx, gw
 

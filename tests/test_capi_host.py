@@ -99,6 +99,30 @@ def test_call_validation_before_launch(lib):
     assert _err(lambda: c.workspace_bytes("c64", 1 << 31)) == -1
 
 
+def test_param_shift_validation_and_workspace(lib):
+    """Parameter-shift entry point: errors before launch and workspace size
+    (one chunk's forward layout + its <Z> values + one fp64 per circuit)."""
+    wl = W.get("10q")
+    c = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    S = c.plan_info("c64")["n_param_gates"]
+    B = 4
+    total = B * (2 * S + 1)
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    need = c.param_shift_workspace_bytes("c64", B, 64)
+    assert _err(lambda: c.param_shift_raw("c64", B, fake, fake, None, fake, None, None, 64, fake,
+                                          need, None)) == -1           # grad_out NULL
+    assert _err(lambda: c.param_shift_raw("c64", B, fake, fake, fake, fake, None, None, 64, fake,
+                                          need - 1, None)) == -2       # workspace too small
+    assert _err(lambda: c.param_shift_raw("c64", B, fake, fake, fake, fake, None, None, -1, fake,
+                                          need, None)) == -1           # negative chunk
+    assert _err(lambda: c.param_shift_workspace_bytes("c64", 0, 0)) == -1
+    chunk64 = c.workspace_bytes("c64", 64, Q.MODE_FWD)
+    assert chunk64 + 64 * wl.n * 4 + total * 8 <= need <= chunk64 + 64 * wl.n * 4 + total * 8 + 512
+    # chunk 0 means all circuits at once
+    assert c.param_shift_workspace_bytes("c64", B, 0) == c.param_shift_workspace_bytes("c64", B, total)
+    assert c.param_shift_workspace_bytes("c64", B, 10 * total) == c.param_shift_workspace_bytes("c64", B, 0)
+
+
 def test_workspace_arithmetic(lib):
     wl = W.get("30q")
     c = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)

@@ -314,3 +314,75 @@ def test_shared_parameter_closed_form():
         got = gpu_fb(circ, "c128", np.zeros((1, 0)), np.array([t]), np.ones((1, n)))
         assert np.max(np.abs(got["expz"][0] + math.sin(t))) <= 1e-12
         assert abs(got["grad_weights"][0] + n * math.cos(t)) <= 1e-11
+
+
+# ---------------------------------------------------------------------------
+# parameter-shift gradients (the paper's rule, shifted circuits batched)
+
+def gpu_shift(circ, dtype, x, w, g, max_chunk=0, runner=None):
+    r = runner or Q.Runner(circ, dtype)
+    e, gx, gw = r.param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), max_chunk=max_chunk)
+    torch.cuda.synchronize()
+    return {"expz": e.cpu().double().numpy(), "grad_inputs": gx.cpu().double().numpy(),
+            "grad_weights": gw.cpu().double().numpy()}
+
+
+SHIFT_CASES = [
+    # n, G, B, dtype, options, max_chunk
+    (5, 40, 3, "c128", dict(), 0),
+    (8, 60, 2, "c64", dict(), 7),
+    (11, 70, 2, "c128", dict(), 0),
+    (13, 80, 2, "c64", dict(), 0),
+    (14, 90, 2, "c64", dict(), 33),
+    (14, 60, 2, "c128", dict(), 0),
+]
+
+
+@pytest.mark.parametrize("n,G,B,dtype,opts,chunk", SHIFT_CASES,
+                         ids=[f"n{c[0]}-{c[3]}-chunk{c[5]}" for c in SHIFT_CASES])
+def test_param_shift_vs_oracle(n, G, B, dtype, opts, chunk):
+    """GPU parameter shift against the oracle's parameter shift (expz from the
+    unshifted circuits against the oracle forward)."""
+    F, P = 4, 6
+    gates = W.random_circuit(n, G, F, P, seed=500 + n * 7 + G)
+    x, w, g = W.random_inputs(B, F, P, n, seed=600 + n, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P, **opts)
+    got = gpu_shift(circ, dtype, x, w, g, max_chunk=chunk)
+    gx, gw = oracle.param_shift(n, gates, x, w, g)
+    want = {"expz": oracle.run(n, gates, x, w)["expz"], "grad_inputs": gx, "grad_weights": gw}
+    check(got, want, TOL[dtype], f"shift n={n} {dtype} chunk={chunk}")
+
+
+@pytest.mark.parametrize("name", ["4q", "10q"])
+def test_param_shift_equals_adjoint_on_workloads(name):
+    """Two gradient methods, one answer: parameter shift and the adjoint sweep
+    on the small workloads at full batch."""
+    wl = W.get(name)
+    x, w, g = wl.inputs()
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    r = Q.Runner(circ, wl.dtype)
+    adj = gpu_fb(circ, wl.dtype, x, w, g, r)
+    sh = gpu_shift(circ, wl.dtype, x, w, g, max_chunk=4096, runner=r)
+    check(sh, adj, 2 * TOL[wl.dtype], f"{name} shift vs adjoint")
+
+
+def test_param_shift_chunks_agree():
+    """Chunk size only changes how the shifted circuits are grouped."""
+    n, F, P, B = 14, 3, 5, 2
+    gates = W.random_circuit(n, 70, F, P, seed=77)
+    x, w, g = W.random_inputs(B, F, P, n, seed=78, dtype="c128")
+    circ = Q.Circuit(n, gates, F, P)
+    ref = gpu_shift(circ, "c128", x, w, g, max_chunk=0)
+    for chunk in (1, 5, 64):
+        check(gpu_shift(circ, "c128", x, w, g, max_chunk=chunk), ref, 1e-12, f"chunk {chunk}")
+
+
+def test_param_shift_hybrid_node():
+    """The paper's one-qubit hybrid node (H, then RY(input)) differentiated by
+    the paper's own rule: d<Z>/dt = -cos t."""
+    t = np.linspace(-3.0, 3.0, 17)
+    gates = np.array([[W.H, 0, -1, 0, 0], [W.RY, 0, -1, W.SRC_INPUT, 0]], np.int32)
+    circ = Q.Circuit(1, gates, 1, 0)
+    got = gpu_shift(circ, "c128", t[:, None], np.zeros(0), np.ones((t.size, 1)))
+    assert np.max(np.abs(got["expz"][:, 0] + np.sin(t))) <= 1e-12
+    assert np.max(np.abs(got["grad_inputs"][:, 0] + np.cos(t))) <= 1e-12
