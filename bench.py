@@ -51,6 +51,19 @@ def algorithmic_flops(wl) -> float:
     return float(per_amp) * wl.batch * (1 << wl.n)
 
 
+def shift_circuits(wl) -> int:
+    """Circuits one parameter-shift VJP runs: per sample the unshifted circuit
+    and two shifted copies per rotation gate."""
+    rot = sum(1 for g in wl.gates() if int(g[0]) in W.ROTATIONS)
+    return wl.batch * (2 * rot + 1)
+
+
+def shift_flops(wl) -> float:
+    """Algorithmic flops of one parameter-shift VJP: forward passes only."""
+    per_amp = sum(FLOPS_FWD[int(g[0])] for g in wl.gates())
+    return float(per_amp) * shift_circuits(wl) * (1 << wl.n)
+
+
 def profiled_traffic(wl):
     """Calibrated HBM bytes per step of the tile kernel from the committed
     rocprofv3 summary, if it was taken with the current kernel source."""
@@ -95,6 +108,11 @@ def main():
     ap.add_argument("--calibrate", action="store_true",
                     help="run one 1 GiB device-to-device copy first (a plain copy kernel of known "
                          "size, to scale hardware byte counters)")
+    ap.add_argument("--grad", choices=("adjoint", "shift"), default="adjoint",
+                    help="gradient method timed: the adjoint sweep (the headline metric) or the "
+                         "batched parameter-shift rule")
+    ap.add_argument("--shift-chunk", type=int, default=0,
+                    help="shifted circuits per chunk (0: as many as 8 GiB of states hold)")
     ap.add_argument("--opt", action="append", default=[],
                     help="planner option key=value (log_regs, log_threads, low_qubits, "
                          "max_gates_per_pass, wg_per_sample)")
@@ -121,7 +139,14 @@ def main():
     outs = (torch.empty((wl.batch, wl.n), dtype=real, device=dev),
             torch.empty((wl.batch, wl.n_inputs), dtype=real, device=dev),
             torch.empty(wl.n_weights, dtype=real, device=dev))
-    runner.workspace(wl.batch, Q.MODE_FWD_BWD)
+    shift = args.grad == "shift"
+    amp = 8 if wl.dtype == "c64" else 16
+    chunk = args.shift_chunk or max(1, min(shift_circuits(wl), (8 << 30) // ((1 << wl.n) * amp)))
+    if shift:
+        step = lambda: runner.param_shift(xt, wt, gt, max_chunk=chunk, outs=outs)  # noqa: E731
+    else:
+        runner.workspace(wl.batch, Q.MODE_FWD_BWD)
+        step = lambda: runner.forward_backward(xt, wt, gt, outs=outs)  # noqa: E731
     if args.calibrate:
         src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
@@ -131,7 +156,7 @@ def main():
         del src, dst
 
     for _ in range(args.warmup):
-        runner.forward_backward(xt, wt, gt, outs=outs)
+        step()
     torch.cuda.synchronize()
 
     timing = not args.no_timing
@@ -140,7 +165,7 @@ def main():
     torch.cuda.synchronize()
     start.record()
     for _ in range(args.steps):
-        runner.forward_backward(xt, wt, gt, outs=outs)
+        step()
     end.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / args.steps
@@ -149,8 +174,12 @@ def main():
 
     info = circ.plan_info(wl.dtype)
     U = wl.updates()
+    if shift:
+        # amplitude-gate updates the parameter-shift VJP performs
+        U = shift_circuits(wl) * wl.n_gates * (1 << wl.n)
     line = {
-        "metric": METRIC,
+        "metric": METRIC if not shift else
+        "amplitude-gate updates/s (batched parameter-shift grad)",
         "value": U / (ms_step / 1e3),
         "unit": "amplitude-gate updates/s",
         "n_gpus": 1,
@@ -167,13 +196,22 @@ def main():
                    "updates_per_step": U, "tile_passes": info["n_passes"],
                    "tile_qubits": info["tile_qubits"], "planner_options": opts},
     }
+    if shift:
+        line["config"].update({"grad": "parameter shift", "circuits_per_step": shift_circuits(wl),
+                               "chunk": chunk})
+        line["vjp_per_s"] = 1e3 / ms_step
     if timing and kcnt[0] > 0:
         tile_ms = kms[0] / args.steps
-        state_bytes = circ.state_bytes(wl.dtype, wl.batch)
+        if shift:
+            state_bytes = circ.state_bytes(wl.dtype, shift_circuits(wl), Q.MODE_FWD)
+            flops = shift_flops(wl)
+            traffic = None
+        else:
+            state_bytes = circ.state_bytes(wl.dtype, wl.batch)
+            flops = algorithmic_flops(wl)
+            traffic = profiled_traffic(wl)
         hbm = state_bytes / (tile_ms / 1e3) / 1e9
-        flops = algorithmic_flops(wl)
         alu = flops / (tile_ms / 1e3) / 1e12
-        traffic = profiled_traffic(wl)
         launches = kcnt[0] / args.steps
         line["roofline"] = {"bound": "alu", "kernel": "k_tile", "achieved": alu,
                             "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": alu / ALU_PEAK_TFLOPS,
@@ -189,7 +227,7 @@ def main():
                                       "k_bind": kms[2] / args.steps, "k_reduce": kms[3] / args.steps}
     elif timing and kcnt[1] > 0:
         whole_ms = kms[1] / args.steps
-        alu = algorithmic_flops(wl) / (whole_ms / 1e3) / 1e12
+        alu = (shift_flops(wl) if shift else algorithmic_flops(wl)) / (whole_ms / 1e3) / 1e12
         line["roofline"] = {"bound": "alu", "kernel": "k_whole", "achieved": alu,
                             "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": alu / ALU_PEAK_TFLOPS,
                             "traffic": None, "kernel_ms_per_step": whole_ms}
