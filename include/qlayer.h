@@ -94,7 +94,10 @@ typedef struct {
     int32_t log_threads;        /* threads per workgroup = 2^log_threads (6..9) */
     int32_t low_qubits;         /* qubits 0..low_qubits-1 are in every tile (1..8) */
     int32_t max_gates_per_pass; /* cap on gates per tile pass (>= 1) */
-    int32_t force_tiled;        /* 1: never use the whole-state-in-LDS kernel */
+    int32_t force_tiled;        /* kernel choice: 0 library default (register tiles for
+                                   n >= 8, whole state in LDS below), 1 register tiles,
+                                   -1 whole state in LDS whenever it fits (n <= 12 for
+                                   QL_C64, n <= 11 for QL_C128) */
     int32_t wg_per_sample;      /* workgroups per sample in a tile pass */
 } ql_options;
 

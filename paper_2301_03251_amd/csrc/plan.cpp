@@ -342,7 +342,10 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
     pl.n = c.n;
     pl.n_slots = (int)c.slot_gate.size();
     const Options& o = c.opts;
-    if (c.n < 8 || (!o.force_tiled && c.n <= whole_state_max_qubits(dtype))) {
+    // The register-tile kernel needs at least 2^8 amplitudes per tile; below
+    // that, or when asked (force_tiled < 0) and the state fits in LDS, the
+    // whole state of a sample lives in one workgroup's LDS.
+    if (c.n < 8 || (o.force_tiled < 0 && c.n <= whole_state_max_qubits(dtype))) {
         pl.whole_state = true;
         PassPlan pp;
         for (int i = 0; i < (int)c.gates.size(); i++) pp.gates.push_back(i);

@@ -166,10 +166,12 @@ def test_workload_plans(lib, name):
         _check_schedule(c, wl.gates(), dt)
         info = c.plan_info(dt)
         assert info["n_param_gates"] == sum(1 for g in wl.gates() if g[0] in W.ROTATIONS)
-        if wl.n <= (12 if dt == "c64" else 11):
+        if wl.n < 8:  # below one minimal register tile: whole state in LDS
             assert info["kernel"] == 0 and info["n_passes"] == 1
         else:
             assert info["kernel"] == 1 and info["tile_qubits"] == info["log_regs"] + info["log_threads"]
+        whole = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, force_tiled=-1).plan_info(dt)
+        assert whole["kernel"] == (0 if wl.n <= (12 if dt == "c64" else 11) else 1)
 
 
 @pytest.mark.parametrize("seed", range(6))

@@ -100,7 +100,7 @@ def test_random_whole_state(n, dtype):
     F, P = 3, 4
     gates = W.random_circuit(n, 40 + 5 * n, F, P, seed=7 * n + 1)
     x, w, g = W.random_inputs(5, F, P, n, seed=n, dtype=dtype)
-    circ = Q.Circuit(n, gates, F, P)
+    circ = Q.Circuit(n, gates, F, P, force_tiled=-1)
     assert circ.plan_info(dtype)["kernel"] == 0
     check(gpu_fb(circ, dtype, x, w, g), oracle.run(n, gates, x, w, grad_out=g), TOL[dtype],
           f"whole n={n} {dtype}")
