@@ -48,6 +48,8 @@ def _bind(path):
     lib.oracle_param_shift.argtypes = [ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
                                        ctypes.c_int, ctypes.c_int, P, P, P, P, P]
     lib.oracle_param_shift.restype = ctypes.c_int
+    lib.oracle_sample.argtypes = [ctypes.c_int, ctypes.c_int, P, ctypes.c_int64, P, P]
+    lib.oracle_sample.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     return lib
@@ -83,6 +85,9 @@ class Oracle:
 
     def param_shift(self, n, gates, inputs, weights, grad_out):
         return _param_shift(self.lib, n, gates, inputs, weights, grad_out)
+
+    def sample(self, n, states, uniforms):
+        return _sample(self.lib, n, states, uniforms)
 
 
 def default() -> "Oracle":
@@ -151,6 +156,24 @@ def _param_shift(lib, n, gates, inputs, weights, grad_out):
     if rc != 0:
         raise ValueError(f"oracle_param_shift failed with code {rc}")
     return gi, gw
+
+
+def sample(n, states, uniforms):
+    """See ``_sample``; uses the default oracle library."""
+    return _sample(_load(), n, states, uniforms)
+
+
+def _sample(lib, n, states, uniforms):
+    """Shots by the inverse CDF: ``states[B, 2^n]`` (complex), ``uniforms[B, shots]``
+    in [0, 1) -> amplitude indices ``[B, shots]`` (int64)."""
+    st = np.ascontiguousarray(np.asarray(states, dtype=np.complex128).reshape(-1, 1 << n))
+    B = st.shape[0]
+    u = np.ascontiguousarray(np.asarray(uniforms, dtype=np.float64).reshape(B, -1))
+    out = np.zeros(u.shape, dtype=np.int64)
+    rc = lib.oracle_sample(n, B, _ptr(st.view(np.float64)), u.shape[1], _ptr(u), _ptr(out))
+    if rc != 0:
+        raise ValueError(f"oracle_sample failed with code {rc}")
+    return out
 
 
 def num_threads() -> int:

@@ -346,6 +346,46 @@ int oracle_param_shift(int n, const int32_t* gates, int G, int B, int F, int P,
     return 0;
 }
 
+/*
+ * Shot sampling: the paper's measurement is Monte Carlo (a finite number of
+ * shots turned into probabilities, Sec. "Quantum Node" and the appendix
+ * examples). A shot draws one basis state j with probability |psi_j|^2.
+ * Definition by the inverse CDF: with C(j) = sum_{i <= j} |psi_i|^2 the
+ * running sum in index order (fp64) and u in [0, 1) passed in, the shot
+ * returns the smallest j with C(j) > u * C(2^n - 1). A zero-probability
+ * index is never returned. States: psi[B][2^n]; uniforms u[B][shots];
+ * out[B][shots] (amplitude index = bitstring, qubit q = bit q). Returns -1 on
+ * bad arguments or a state with zero norm.
+ */
+int oracle_sample(int n, int B, const double* psi_ri, int64_t shots, const double* u, int64_t* out)
+{
+    if (n < 0 || n > 34 || B < 0 || shots < 0 || (B > 0 && shots > 0 && (!psi_ri || !u || !out))) return -1;
+    const int64_t dim = (int64_t)1 << n;
+    double* cdf = (double*)malloc(sizeof(double) * (size_t)dim);
+    if (!cdf) return -2;
+    for (int b = 0; b < B; b++) {
+        const double* p = psi_ri + (size_t)b * (size_t)dim * 2;
+        double acc = 0.0;
+        for (int64_t j = 0; j < dim; j++) {
+            acc += p[2 * j] * p[2 * j] + p[2 * j + 1] * p[2 * j + 1];
+            cdf[j] = acc;
+        }
+        if (!(acc > 0.0)) { free(cdf); return -1; }
+        for (int64_t s = 0; s < shots; s++) {
+            const double r = u[(size_t)b * (size_t)shots + (size_t)s] * acc;
+            int64_t lo = 0, hi = dim - 1;  /* smallest j with cdf[j] > r; cdf[dim-1] = acc > r */
+            while (lo < hi) {
+                const int64_t mid = lo + (hi - lo) / 2;
+                if (cdf[mid] > r) hi = mid;
+                else lo = mid + 1;
+            }
+            out[(size_t)b * (size_t)shots + (size_t)s] = lo;
+        }
+    }
+    free(cdf);
+    return 0;
+}
+
 /* Number of OpenMP threads the parallel loops use (1 without OpenMP). */
 int oracle_num_threads(void)
 {

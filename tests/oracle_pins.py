@@ -376,9 +376,52 @@ def pin_cyclic_shift(orc):
            tol=1e-12, what="shift gw")
 
 
+def pin_sampling(orc):
+    """Shot sampling against what the definition of sampling fixes, without
+    re-deriving the CDF: a basis state always returns itself; a uniform
+    superposition with stratified uniforms (i + 1/2) / 2^n returns i; one RY(t)
+    qubit returns 0 exactly for u < cos^2(t/2); u = 0 returns the first index of
+    nonzero probability (never a zero-probability one); a state and twice that
+    state give the same shots; and the frequencies of many shots of a random
+    state match |psi|^2 within five standard errors."""
+    n = 4
+    dim = 1 << n
+    for j in (0, 5, dim - 1):
+        e = np.zeros((1, dim), np.complex128)
+        e[0, j] = 1.0
+        got = orc.sample(n, e, np.linspace(0.0, 0.999, 9)[None, :])
+        assert np.all(got == j), f"basis state {j}: {got}"
+    uni = np.full((1, dim), 1.0 / np.sqrt(dim), np.complex128)
+    got = orc.sample(n, uni, ((np.arange(dim) + 0.5) / dim)[None, :])
+    assert np.array_equal(got[0], np.arange(dim)), f"stratified uniform: {got}"
+    for t in (0.3, 1.7, 2.9):
+        st = orc.run(1, _arr([_g(W.RY, 0, src=W.SRC_WEIGHT)]), np.zeros((1, 0)), [t], want_state=True)["state"]
+        p0 = np.cos(t / 2) ** 2
+        u = np.array([[p0 - 1e-9, p0 + 1e-9, 0.0, 0.999999]])
+        got = orc.sample(1, st, u)[0]
+        assert list(got) == [0, 1, 0, 1], f"RY({t}) threshold: {got}"
+    st = np.zeros((1, dim), np.complex128)
+    st[0, 3] = 0.6
+    st[0, 9] = 0.8j
+    got = orc.sample(n, st, np.array([[0.0, 0.35, 0.36, 0.999]]))[0]
+    assert list(got) == [3, 3, 9, 9], f"zero-probability skip: {got}"
+    gates, x, w, _ = _random_case(n, 30, seed=44, B=1)
+    psi = orc.run(n, gates, x, w, want_state=True)["state"]
+    p = np.abs(psi[0]) ** 2
+    rng = np.random.default_rng(45)
+    shots = 200000
+    got = orc.sample(n, psi, rng.random((1, shots)))[0]
+    # scale invariance: sampling reads |psi|^2 relative to the state's norm
+    us = rng.random((1, 64))
+    assert np.array_equal(orc.sample(n, 2.0 * psi, us), orc.sample(n, psi, us)), "norm-dependent shots"
+    freq = np.bincount(got, minlength=dim) / shots
+    se = np.sqrt(p * (1 - p) / shots) + 1e-12
+    assert np.all(np.abs(freq - p) <= 5 * se + 1e-9), "shot frequencies do not follow |psi|^2"
+
+
 ALL_PINS = [
     pin_rotations_on_zero, pin_rotation_axes, pin_h_rz_h, pin_hybrid_node,
     pin_shared_parameter, pin_cnot_truth_table, pin_cnot_chain_parity, pin_cz_kickback,
     pin_bell, pin_brute_force, pin_unitarity, pin_param_shift, pin_finite_difference,
-    pin_vjp_structure, pin_product_states, pin_cyclic_shift,
+    pin_vjp_structure, pin_product_states, pin_cyclic_shift, pin_sampling,
 ]

@@ -1,7 +1,7 @@
 """Plant plausible mistakes in copies of the oracle (CPU only) and check that the
 pin battery catches every one of them: evidence that the pins constrain each
 part of the oracle (gate matrices, orientation, expectation, adjoint sweep,
-gradient accumulation, parameter shift)."""
+gradient accumulation, parameter shift, shot sampling)."""
 
 import os
 import shutil
@@ -49,6 +49,13 @@ MUTANTS = [
      "                apply_gate(psi, dim, gk, th, 0);"),
     ("shift_without_half", "double d = 0.5 * (fp - fm);", "double d = (fp - fm);"),
     ("lambda_not_unapplied", "            apply_gate(lam, dim, gk, th, 1);\n", "\n"),
+    ("sample_ge_instead_of_gt", "if (cdf[mid] > r) hi = mid;", "if (cdf[mid] >= r) hi = mid;"),
+    ("sample_off_by_one", "out[(size_t)b * (size_t)shots + (size_t)s] = lo;",
+     "out[(size_t)b * (size_t)shots + (size_t)s] = lo > 0 ? lo - 1 : 0;"),
+    ("sample_amplitude_not_squared", "acc += p[2 * j] * p[2 * j] + p[2 * j + 1] * p[2 * j + 1];",
+     "acc += fabs(p[2 * j]) + fabs(p[2 * j + 1]);"),
+    ("sample_unscaled_uniform", "const double r = u[(size_t)b * (size_t)shots + (size_t)s] * acc;",
+     "const double r = u[(size_t)b * (size_t)shots + (size_t)s];"),
 ]
 
 
