@@ -159,6 +159,42 @@ int ql_param_shift(const ql_circuit* c, ql_dtype dtype, int64_t batch, const voi
                    void* grad_weights, int64_t max_chunk, void* workspace,
                    size_t workspace_bytes, hipStream_t stream);
 
+/* ---- final states and shot sampling --------------------------------------
+ *
+ * The paper's quantum node measures its circuit with a finite number of shots
+ * (Sec. "Quantum Node"; the appendix examples measure 100 shots and turn the
+ * counts into probabilities). These calls expose that measurement: ql_state
+ * writes the final state of every sample, and ql_sample draws shots from
+ * states with caller-supplied uniforms.
+ *
+ * ql_state: same inputs as ql_forward; psi[batch][2^n_qubits] receives the
+ * final state (interleaved complex: float2 for QL_C64, double2 for QL_C128),
+ * a caller-owned device buffer that also serves as the working state (the
+ * workspace then holds no state). Workspace from ql_state_workspace_bytes. */
+int ql_state_workspace_bytes(const ql_circuit* c, ql_dtype dtype, int64_t batch, size_t* out);
+int ql_state(const ql_circuit* c, ql_dtype dtype, int64_t batch, const void* inputs,
+             const void* weights, void* psi, void* workspace, size_t workspace_bytes,
+             hipStream_t stream);
+
+/* ql_sample: psi[batch][2^n_qubits] (device, the layout of ql_state) and
+ * uniforms[batch][shots] (device, fp64 in [0, 1)); samples[batch][shots]
+ * (device, int64) receives, for shot s of sample b, the smallest basis index j
+ * whose running sum of |psi_i|^2 (i <= j, in index order) exceeds
+ * uniforms[b][s] times the state's total |psi|^2 -- the inverse-CDF draw, so
+ * the index's bits are the measured qubits (qubit q = bit q) and no
+ * zero-probability index is returned. The sums run in fp64 in a fixed
+ * (blocked) order; when a uniform falls within rounding of a CDF boundary the
+ * neighbouring index may be returned. zhat[batch][n_qubits] (device, fp32 for
+ * QL_C64, fp64 for QL_C128; may be NULL) receives the shot estimate of <Z_q>:
+ * (shots with bit q = 0 minus shots with bit q = 1) / shots. The states need
+ * not be normalised. shots = 0 writes nothing. Workspace:
+ * ql_sample_workspace_bytes(n_qubits, batch) bytes (one fp64 per 4096
+ * amplitudes). n_qubits in [1, 32] (QL_C128: [1, 31]). */
+int ql_sample_workspace_bytes(int32_t n_qubits, int64_t batch, size_t* out);
+int ql_sample(ql_dtype dtype, int32_t n_qubits, int64_t batch, const void* psi, int64_t shots,
+              const double* uniforms, int64_t* samples, void* zhat, void* workspace,
+              size_t workspace_bytes, hipStream_t stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* ql_last_error(void);
 

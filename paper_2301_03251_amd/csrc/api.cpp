@@ -150,7 +150,9 @@ struct ql_circuit {
 
 namespace {
 
-int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L) {
+// own_psi = false: the caller's state buffer holds psi (ql_state), so the
+// workspace has none.
+int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, bool own_psi = true) {
     const Circuit& c = h->c;
     const Plan& pl = c.plan[dt];
     const size_t amp = dt == 0 ? 8 : 16;
@@ -191,7 +193,7 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L) 
             return fail(QL_ENOMEM, "size overflow");
         off = align256(off + sz);
     }
-    if (!pl.whole_state && pl.passes.size() > 1) {
+    if (own_psi && !pl.whole_state && pl.passes.size() > 1) {
         size_t st;
         if (!mul_ok((size_t)B, ((size_t)1 << c.n) * amp, st)) return fail(QL_ENOMEM, "size overflow");
         L.psi = off;
@@ -310,7 +312,7 @@ int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0,
 // The state passes of B circuits: the whole-state kernel, or the forward tile
 // passes, the fused pass and (bwd) the backward passes. Writes the <Z> partials
 // (and, bwd, the gradient partials) of the workspace.
-int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out) {
+int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ext = nullptr) {
     const Circuit& c = x.c;
     const Plan& pl = x.pl;
     const size_t amp = x.dt == 0 ? 8 : 16;
@@ -328,6 +330,7 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out) {
         wa.grad_out = grad_out;
         wa.zpart = zpart;
         wa.gpart = gpart;
+        wa.psi_out = psi_ext;
         const int dim = 1 << c.n;
         const int threads = std::max(64, std::min(256, dim / 4));
         const size_t lds = 2 * (size_t)dim * amp + (size_t)c.n * (threads / 64) * 8 + 64;
@@ -343,7 +346,7 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out) {
     auto launch_pass = [&](int p, int flags) -> int {
         const DevPass& d = x.T.passes[p];
         TileArgs ta{};
-        ta.psi = x.L.psi ? (void*)(x.W + x.L.psi) : nullptr;
+        ta.psi = psi_ext ? psi_ext : (x.L.psi ? (void*)(x.W + x.L.psi) : nullptr);
         ta.lam = x.L.lam ? (void*)(x.W + x.L.lam) : nullptr;
         ta.pass = (const DevPass*)(x.W + x.L.tables + x.T.off_pass) + p;
         ta.phases = (const DevPhase*)(x.W + x.L.tables + x.T.off_phase);
@@ -375,7 +378,7 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out) {
         rc = launch_pass(p, (p == 0 ? PF_INIT : 0) | PF_FWD | PF_STORE_PSI);
         if (rc) return rc;
     }
-    int last = (m == 1 ? PF_INIT : 0) | PF_FWD | PF_ZPART;
+    int last = (m == 1 ? PF_INIT : 0) | PF_FWD | (psi_ext ? PF_STORE_PSI : PF_ZPART);
     if (bwd) last |= PF_SEED | PF_BWD | (m > 1 ? (PF_STORE_PSI | PF_STORE_LAM) : 0);
     rc = launch_pass(m - 1, last);
     if (rc) return rc;
@@ -535,6 +538,60 @@ int param_shift(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inp
     return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("k_shift_grad: ") + hipGetErrorString(e));
 }
 
+int state(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs, const void* weights,
+          void* psi, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (!hc) return fail(QL_EINVAL, "circuit is NULL");
+    ql_circuit* h = const_cast<ql_circuit*>(hc);
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    const int dt = (int)dtype;
+    Layout L;
+    int rc = compute_layout(h, dt, B, QL_MODE_FWD, L, false);
+    if (rc) return rc;
+    if (!psi) return fail(QL_EINVAL, "psi is NULL");
+    rc = check_args(h->c, inputs, weights, psi, false, nullptr, ws);
+    if (rc) return rc;
+    if (ws_bytes < L.total)
+        return fail(QL_ENOMEM, "workspace too small: need " + std::to_string(L.total) + " bytes, got " +
+                                   std::to_string(ws_bytes));
+    rc = ensure_device();
+    if (rc) return rc;
+    Ctx x{h, dt, h->c, h->c.plan[dt], h->t[dt], (uint8_t*)ws, L, stream, Timer{h, stream}};
+    if ((rc = upload_tables(x))) return rc;
+    if ((rc = bind(x, B, inputs, weights, 0, 0))) return rc;
+    if ((rc = state_passes(x, B, false, nullptr, psi))) return rc;
+    if (x.pl.whole_state) return QL_OK;  // exact gates: no phase to undo
+    BindTileArgs ba{};
+    ba.inputs = inputs;
+    ba.weights = weights;
+    ba.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
+    ba.ops = (const DevOp*)(x.W + x.L.tables + x.T.off_ops);
+    ba.B = B;
+    ba.n_ops = x.T.n_ops;
+    ba.bwd_first = x.T.bwd_first;
+    ba.F = h->c.n_inputs;
+    hipError_t e = launch_state_phase(dt, ba, (double*)(x.W + x.L.zpart), psi, h->c.n, stream);
+    return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("state phase: ") + hipGetErrorString(e));
+}
+
+// Blocks of 2^bb amplitudes for shot sampling.
+int sample_blocks(int n, int& bb, int64_t& nblk) {
+    if (n < 1 || n > QL_MAX_QUBITS_C64) return fail(QL_EINVAL, "n_qubits out of range [1, 32]");
+    bb = std::min(n, 12);
+    nblk = (int64_t)1 << (n - bb);
+    return QL_OK;
+}
+
+int sample_bytes(int n, int64_t B, size_t& out) {
+    int bb;
+    int64_t nblk;
+    int rc = sample_blocks(n, bb, nblk);
+    if (rc) return rc;
+    if (B < 1) return fail(QL_EINVAL, "batch must be >= 1");
+    if (!mul_ok((size_t)B, (size_t)nblk * 8, out)) return fail(QL_ENOMEM, "size overflow");
+    out = align256(out);
+    return QL_OK;
+}
+
 Options to_options(const ql_options* o) {
     Options r;
     if (o) {
@@ -638,6 +695,68 @@ int ql_param_shift(const ql_circuit* h, ql_dtype dtype, int64_t batch, const voi
                          max_chunk, ws, ws_bytes, stream);
     if (rc == QL_OK) g_err.clear();
     return rc;
+}
+
+int ql_state_workspace_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, size_t* out) {
+    if (!h || !out) return fail(QL_EINVAL, "NULL argument");
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    Layout L;
+    int rc = compute_layout(h, (int)dtype, batch, QL_MODE_FWD, L, false);
+    if (rc) return rc;
+    *out = L.total;
+    return QL_OK;
+}
+
+int ql_state(const ql_circuit* h, ql_dtype dtype, int64_t batch, const void* inputs, const void* weights,
+             void* psi, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int rc = state(h, dtype, batch, inputs, weights, psi, ws, ws_bytes, stream);
+    if (rc == QL_OK) g_err.clear();
+    return rc;
+}
+
+int ql_sample_workspace_bytes(int32_t n_qubits, int64_t batch, size_t* out) {
+    if (!out) return fail(QL_EINVAL, "NULL argument");
+    size_t b;
+    int rc = sample_bytes(n_qubits, batch, b);
+    if (rc) return rc;
+    *out = b;
+    g_err.clear();
+    return QL_OK;
+}
+
+int ql_sample(ql_dtype dtype, int32_t n_qubits, int64_t batch, const void* psi, int64_t shots,
+              const double* uniforms, int64_t* samples, void* zhat, void* ws, size_t ws_bytes,
+              hipStream_t stream) {
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    if (dtype == QL_C128 && n_qubits > QL_MAX_QUBITS_C128) return fail(QL_EUNSUPPORTED, "too many qubits for this dtype");
+    size_t need;
+    int rc = sample_bytes(n_qubits, batch, need);
+    if (rc) return rc;
+    if (shots < 0) return fail(QL_EINVAL, "shots must be >= 0");
+    if (!psi) return fail(QL_EINVAL, "psi is NULL");
+    if (shots > 0 && (!uniforms || !samples)) return fail(QL_EINVAL, "uniforms or samples is NULL");
+    if (!ws) return fail(QL_EINVAL, "workspace is NULL");
+    if (ws_bytes < need)
+        return fail(QL_ENOMEM, "workspace too small: need " + std::to_string(need) + " bytes, got " +
+                                   std::to_string(ws_bytes));
+    if (batch > ((int64_t)1 << 40) / std::max<int64_t>(shots, 1)) return fail(QL_EINVAL, "batch * shots too large");
+    rc = ensure_device();
+    if (rc) return rc;
+    SampleArgs a{};
+    a.psi = psi;
+    a.uniforms = uniforms;
+    a.samples = samples;
+    a.zhat = shots > 0 ? zhat : nullptr;
+    a.bsum = (double*)ws;
+    a.B = batch;
+    a.shots = shots;
+    a.n = n_qubits;
+    rc = sample_blocks(n_qubits, a.bb, a.nblk);
+    if (rc) return rc;
+    hipError_t e = launch_sample((int)dtype, a, stream);
+    if (e != hipSuccess) return fail(QL_EHIP, std::string("sampling: ") + hipGetErrorString(e));
+    g_err.clear();
+    return QL_OK;
 }
 
 const char* ql_last_error(void) { return g_err.c_str(); }

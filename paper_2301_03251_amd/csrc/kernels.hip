@@ -18,6 +18,8 @@
 //               <Z_q>, input gradients and (batch-summed) weight gradients
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "launch.hpp"
 
 namespace qlayer {
@@ -239,6 +241,8 @@ __global__ void __launch_bounds__(256) k_whole(const WholeArgs a) {
         lds_gate(psi, g, c, s, n, tid, nt);
         __syncthreads();
     }
+    if (a.psi_out)
+        for (int j = tid; j < dim; j += nt) ((T2*)a.psi_out)[b * dim + j] = psi[j];
     for (int q = 0; q < n; ++q) {
         Real acc = 0;
         for (int j = tid; j < dim; j += nt) {
@@ -1144,6 +1148,195 @@ __global__ void __launch_bounds__(256) k_shift_grad(const ShiftGradArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// exact final states of the tile path
+//
+// The tile kernel applies each rotation with its angle reduced to [-pi, pi]
+// (a factor (-1)^k per rotation whose angle moved by 2 pi k) and an RZ on a
+// register bit as diag(1, exp(i t)) (dropping exp(-i t / 2)); both are global
+// phases per sample. k_state_phase sums them over the forward ops, from the
+// same angle sources and reduction as k_bind_tile; k_phase_fix multiplies the
+// state by the inverse phase.
+
+template <typename Real>
+__global__ void k_state_phase(const BindTileArgs a, double* phase) {
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= a.B) return;
+    const double pi = 3.141592653589793238463, two_pi = 2.0 * pi;
+    double ph = 0.0;
+    for (int o = 0; o < a.bwd_first; ++o) {
+        const DevOp op = a.ops[o];
+        if (op.slot < 0) continue;
+        const SlotSrc src = a.slots[op.slot];
+        int64_t bs;
+        const double th = (double)angle_of<Real>(a.inputs, a.weights, a.F, src, b, 0, 0, op.slot, bs);
+        const double k = rint(th / two_pi);
+        ph += pi * k;
+        if (op.h >= H_G1 + 15 && op.h < H_G1 + 20) ph += 0.5 * (th - two_pi * k);
+    }
+    phase[b] = ph;
+}
+
+template <typename T2>
+__global__ void k_phase_fix(void* psi, const double* phase, int64_t B, int n) {
+    const int64_t total = B << n;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        double sn, cs;
+        sincos(-phase[i >> n], &sn, &cs);
+        T2 v = ((T2*)psi)[i];
+        const double x = (double)v.x, y = (double)v.y;
+        v.x = (decltype(v.x))(x * cs - y * sn);
+        v.y = (decltype(v.y))(x * sn + y * cs);
+        ((T2*)psi)[i] = v;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// shot sampling (inverse CDF). A block of 2^bb amplitudes is 64 lane chunks
+// of consecutive amplitudes; every block quantity below comes from one
+// function (chunk sums, then a fixed-order lane scan), so the block totals and
+// the in-block search see bitwise the same numbers.
+
+template <typename T2>
+__device__ __forceinline__ double chunk_sum(const T2* p, int64_t base, int64_t lo, int64_t cnt) {
+    double acc = 0.0;
+    for (int64_t j = lo; j < lo + cnt; ++j) {
+        const T2 v = p[base + j];
+        acc += (double)v.x * (double)v.x + (double)v.y * (double)v.y;
+    }
+    return acc;
+}
+
+// Inclusive scan over the 64 lanes, Hillis-Steele, fixed order.
+__device__ __forceinline__ double lane_scan(double v, int lane) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const double t = __shfl_up(v, off, 64);
+        if (lane >= off) v += t;
+    }
+    return v;
+}
+
+// Chunk geometry of a block: lane l covers [l * csz, l * csz + cnt_l).
+__device__ __forceinline__ void chunk_of(int bb, int lane, int64_t& lo, int64_t& cnt) {
+    const int64_t bs = (int64_t)1 << bb;
+    const int64_t csz = bs >= 64 ? bs / 64 : 1;
+    lo = (int64_t)lane * csz;
+    cnt = lo < bs ? csz : 0;
+}
+
+// One wavefront per (sample, block): block total into bsum.
+template <typename T2>
+__global__ void __launch_bounds__(256) k_block_sums(const SampleArgs a) {
+    const int64_t wv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    if (wv >= a.B * a.nblk) return;
+    const int64_t b = wv / a.nblk, blk = wv - b * a.nblk;
+    int64_t lo, cnt;
+    chunk_of(a.bb, lane, lo, cnt);
+    const int64_t base = (b << a.n) + (blk << a.bb);
+    const double s = lane_scan(chunk_sum((const T2*)a.psi, base, lo, cnt), lane);
+    if (lane == 63) a.bsum[wv] = s;
+}
+
+// One workgroup per sample: inclusive prefix of the block totals, in place,
+// fixed order (contiguous thread ranges, then the range offsets in order).
+__global__ void __launch_bounds__(256) k_block_scan(const SampleArgs a) {
+    __shared__ double off[256];
+    const int64_t b = blockIdx.x;
+    const int t = threadIdx.x, nt = blockDim.x;
+    double* s = a.bsum + b * a.nblk;
+    const int64_t per = (a.nblk + nt - 1) / nt;
+    const int64_t lo = t * per, hi = lo + per < a.nblk ? lo + per : a.nblk;
+    double acc = 0.0;
+    for (int64_t i = lo; i < hi; ++i) acc += s[i];
+    off[t] = acc;
+    __syncthreads();
+    if (t == 0) {
+        double run = 0.0;
+        for (int i = 0; i < nt; ++i) {
+            const double v = off[i];
+            off[i] = run;
+            run += v;
+        }
+    }
+    __syncthreads();
+    double run = off[t];
+    for (int64_t i = lo; i < hi; ++i) {
+        run += s[i];
+        s[i] = run;
+    }
+}
+
+// One wavefront per shot: the block (binary search over the prefix), the lane
+// chunk (ballot over the lane scan), then the amplitude (running sum in the
+// chunk). The index is the first one whose running total exceeds u * total.
+template <typename T2>
+__global__ void __launch_bounds__(256) k_shots(const SampleArgs a) {
+    const int64_t wv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    if (wv >= a.B * a.shots) return;
+    const int64_t b = wv / a.shots;
+    const double* pre = a.bsum + b * a.nblk;
+    const double total = pre[a.nblk - 1];
+    const double r = a.uniforms[wv] * total;
+    int64_t lo = 0, hi = a.nblk - 1;  // first block with pre > r (pre[nblk-1] = total > r)
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (pre[mid] > r) hi = mid;
+        else lo = mid + 1;
+    }
+    const int64_t blk = lo;
+    const double before = blk > 0 ? pre[blk - 1] : 0.0;
+    int64_t clo, ccnt;
+    chunk_of(a.bb, lane, clo, ccnt);
+    const int64_t base = (b << a.n) + (blk << a.bb);
+    const T2* p = (const T2*)a.psi;
+    const double incl = lane_scan(chunk_sum(p, base, clo, ccnt), lane);
+    // shuffle with every lane active, then select (a shuffle inside the
+    // conditional would read lane 0 while it is switched off)
+    const double up = __shfl_up(incl, 1, 64);
+    const double prev = lane > 0 ? up : 0.0;
+    const uint64_t hit = __ballot(before + incl > r && ccnt > 0);
+    int L = hit ? (int)__builtin_ctzll(hit) : -1;
+    if (L < 0) {  // rounding left r above the block: last lane with amplitudes
+        const uint64_t has = __ballot(ccnt > 0);
+        L = 63 - (int)__builtin_clzll(has);
+    }
+    const double start = before + __shfl(prev, L, 64);
+    int64_t lL, cL;
+    chunk_of(a.bb, L, lL, cL);
+    int64_t idx = -1, last_nz = lL;
+    if (lane == 0) {
+        double run = start;
+        for (int64_t j = lL; j < lL + cL; ++j) {
+            const T2 v = p[base + j];
+            const double q = (double)v.x * (double)v.x + (double)v.y * (double)v.y;
+            if (q > 0.0) last_nz = j;
+            run += q;
+            if (run > r && q > 0.0) {
+                idx = j;
+                break;
+            }
+        }
+        if (idx < 0) idx = last_nz;  // rounding: the chunk's last amplitude of nonzero probability
+        a.samples[wv] = (blk << a.bb) + idx;
+    }
+}
+
+// <Z_q> from the shots: one thread per (sample, qubit), exact integer counts.
+template <typename Real>
+__global__ void __launch_bounds__(256) k_shot_z(const SampleArgs a) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= a.B * a.n) return;
+    const int64_t b = t / a.n;
+    const int q = (int)(t - b * a.n);
+    int64_t ones = 0;
+    for (int64_t s = 0; s < a.shots; ++s) ones += (a.samples[b * a.shots + s] >> q) & 1;
+    ((Real*)a.zhat)[t] = a.shots > 0 ? (Real)((double)(a.shots - 2 * ones) / (double)a.shots) : (Real)0;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -1244,6 +1437,38 @@ hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s) {
     const unsigned grid = (unsigned)((waves + 3) / 4);
     if (dtype == 0) hipLaunchKernelGGL(k_shift_grad<float>, dim3(grid), dim3(256), 0, s, a);
     else hipLaunchKernelGGL(k_shift_grad<double>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, void* psi, int n,
+                              hipStream_t s) {
+    const unsigned g1 = (unsigned)((a.B + 255) / 256);
+    const int64_t total = a.B << n;
+    const unsigned g2 = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
+    if (dtype == 0) {
+        hipLaunchKernelGGL(k_state_phase<float>, dim3(g1), dim3(256), 0, s, a, phase);
+        hipLaunchKernelGGL(k_phase_fix<float2>, dim3(g2), dim3(256), 0, s, psi, (const double*)phase, a.B, n);
+    } else {
+        hipLaunchKernelGGL(k_state_phase<double>, dim3(g1), dim3(256), 0, s, a, phase);
+        hipLaunchKernelGGL(k_phase_fix<double2>, dim3(g2), dim3(256), 0, s, psi, (const double*)phase, a.B, n);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_sample(int dtype, const SampleArgs& a, hipStream_t s) {
+    const int64_t wb = a.B * a.nblk, ws = a.B * a.shots;
+    if (dtype == 0) hipLaunchKernelGGL(k_block_sums<float2>, dim3((unsigned)((wb + 3) / 4)), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_block_sums<double2>, dim3((unsigned)((wb + 3) / 4)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_block_scan, dim3((unsigned)a.B), dim3(256), 0, s, a);
+    if (ws > 0) {
+        if (dtype == 0) hipLaunchKernelGGL(k_shots<float2>, dim3((unsigned)((ws + 3) / 4)), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL(k_shots<double2>, dim3((unsigned)((ws + 3) / 4)), dim3(256), 0, s, a);
+    }
+    if (a.zhat) {
+        const int64_t t = a.B * a.n;
+        if (dtype == 0) hipLaunchKernelGGL(k_shot_z<float>, dim3((unsigned)((t + 255) / 256)), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL(k_shot_z<double>, dim3((unsigned)((t + 255) / 256)), dim3(256), 0, s, a);
+    }
     return hipGetLastError();
 }
 

@@ -80,6 +80,19 @@ struct WholeArgs {
     const void* grad_out; // [B][n] Real
     double* zpart;        // [B][n]           (one workgroup per sample)
     double* gpart;        // [n_slots][B]
+    void* psi_out;        // [B][2^n] complex: the final state, or null
+};
+
+// Shot sampling from states psi[B][2^n]: blocks of 2^bb amplitudes, each
+// split into 64 lane chunks.
+struct SampleArgs {
+    const void* psi;        // [B][2^n] complex
+    const double* uniforms; // [B][shots] in [0, 1)
+    int64_t* samples;       // [B][shots]
+    void* zhat;             // [B][n] Real or null: <Z_q> estimated from the shots
+    double* bsum;           // [B][nblk]: block sums, then their inclusive prefix
+    int64_t B, shots, nblk;
+    int32_t n, bb;
 };
 
 struct TileArgs {
@@ -130,6 +143,11 @@ hipError_t launch_tile(int dtype, int log_r, bool bwd, const TileArgs& a, int th
                        hipStream_t s);
 hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_shift_dot(int dtype, const ShiftDotArgs& a, hipStream_t s);
+hipError_t launch_sample(int dtype, const SampleArgs& a, hipStream_t s);
+// Undo the per-sample global phase the tile kernel leaves on final states
+// (phase: [B] fp64 scratch).
+hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, void* psi, int n,
+                              hipStream_t s);
 hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s);
 
 // Raise the dynamic-LDS limit of every kernel on the current device.

@@ -43,7 +43,8 @@ class _PlanInfo(ctypes.Structure):
 _lib = None
 EXPORTS = ("ql_circuit_create", "ql_circuit_create_ex", "ql_circuit_destroy",
            "ql_workspace_bytes", "ql_forward", "ql_forward_backward", "ql_last_error",
-           "ql_param_shift_workspace_bytes", "ql_param_shift",
+           "ql_param_shift_workspace_bytes", "ql_param_shift", "ql_state_workspace_bytes",
+           "ql_state", "ql_sample_workspace_bytes", "ql_sample",
            "ql_plan_info_get", "ql_plan_schedule", "ql_plan_state_bytes",
            "ql_timing_enable", "ql_timing_read")
 
@@ -68,6 +69,10 @@ def load():
     lib.ql_forward_backward.argtypes = [P, ctypes.c_int, I64, P, P, P, P, P, P, P, SZ, P]
     lib.ql_param_shift_workspace_bytes.argtypes = [P, ctypes.c_int, I64, I64, ctypes.POINTER(SZ)]
     lib.ql_param_shift.argtypes = [P, ctypes.c_int, I64, P, P, P, P, P, P, I64, P, SZ, P]
+    lib.ql_state_workspace_bytes.argtypes = [P, ctypes.c_int, I64, ctypes.POINTER(SZ)]
+    lib.ql_state.argtypes = [P, ctypes.c_int, I64, P, P, P, P, SZ, P]
+    lib.ql_sample_workspace_bytes.argtypes = [I32, I64, ctypes.POINTER(SZ)]
+    lib.ql_sample.argtypes = [ctypes.c_int, I32, I64, P, I64, P, P, P, P, SZ, P]
     lib.ql_last_error.argtypes = []
     lib.ql_last_error.restype = ctypes.c_char_p
     lib.ql_plan_info_get.argtypes = [P, ctypes.c_int, ctypes.POINTER(_PlanInfo)]
@@ -78,6 +83,7 @@ def load():
     lib.ql_timing_read.argtypes = [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]
     for name in ("ql_circuit_create", "ql_circuit_create_ex", "ql_workspace_bytes", "ql_forward",
                  "ql_forward_backward", "ql_param_shift_workspace_bytes", "ql_param_shift",
+                 "ql_state_workspace_bytes", "ql_state", "ql_sample_workspace_bytes", "ql_sample",
                  "ql_plan_info_get", "ql_plan_schedule",
                  "ql_plan_state_bytes", "ql_timing_enable", "ql_timing_read"):
         getattr(lib, name).restype = ctypes.c_int
@@ -162,6 +168,15 @@ class Circuit:
         _check(load().ql_param_shift_workspace_bytes(self._h, _dt(dtype), int(batch), int(max_chunk),
                                                      ctypes.byref(out)))
         return out.value
+
+    def state_workspace_bytes(self, dtype, batch) -> int:
+        out = ctypes.c_size_t()
+        _check(load().ql_state_workspace_bytes(self._h, _dt(dtype), int(batch), ctypes.byref(out)))
+        return out.value
+
+    def state_raw(self, dtype, batch, inputs, weights, psi, ws, ws_bytes, stream):
+        _check(load().ql_state(self._h, _dt(dtype), int(batch), inputs, weights, psi, ws,
+                               int(ws_bytes), stream))
 
     # raw entry points: device pointers as ints, stream as int (hipStream_t)
     def forward_raw(self, dtype, batch, inputs, weights, expz, ws, ws_bytes, stream):
@@ -278,6 +293,55 @@ class Runner:
             _ptr(gw) if (gw is not None and self.c.n_weights) else None, max_chunk, _ptr(ws), ws.numel(),
             ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
         return expz, gx, gw
+
+
+    def state(self, inputs, weights):
+        """Final states [B, 2^n] (complex64 / complex128) of the batch."""
+        torch = _torch()
+        B = int(inputs.shape[0])
+        x, w = self._args(inputs, weights, B)
+        cdt = torch.complex64 if self.real == torch.float32 else torch.complex128
+        psi = torch.empty((B, 1 << self.c.n), dtype=cdt, device=self.device)
+        need = self.c.state_workspace_bytes(self.dtype, B)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        self.c.state_raw(self.dtype, B, _ptr(x) if self.c.n_inputs else None,
+                         _ptr(w) if self.c.n_weights else None, _ptr(psi), _ptr(self._ws),
+                         self._ws.numel(), ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
+        return psi
+
+
+def sample_workspace_bytes(n_qubits, batch) -> int:
+    out = ctypes.c_size_t()
+    _check(load().ql_sample_workspace_bytes(int(n_qubits), int(batch), ctypes.byref(out)))
+    return out.value
+
+
+def sample_raw(dtype, n_qubits, batch, psi, shots, uniforms, samples, zhat, ws, ws_bytes, stream):
+    _check(load().ql_sample(_dt(dtype), int(n_qubits), int(batch), psi, int(shots), uniforms, samples,
+                            zhat, ws, int(ws_bytes), stream))
+
+
+def sample(psi, uniforms, want_z=True):
+    """Shots from states ``psi[B, 2^n]`` (complex CUDA tensor) with uniforms
+    ``[B, shots]`` (float64 CUDA tensor): returns (indices[B, shots] int64,
+    <Z_q> shot estimates [B, n] or None)."""
+    torch = _torch()
+    B, dim = int(psi.shape[0]), int(psi.shape[1])
+    n = dim.bit_length() - 1
+    if dim != 1 << n or not psi.is_contiguous() or psi.dtype not in (torch.complex64, torch.complex128):
+        raise ValueError("psi must be a contiguous complex tensor [B, 2^n]")
+    if uniforms.dtype != torch.float64 or not uniforms.is_contiguous() or int(uniforms.shape[0]) != B:
+        raise ValueError("uniforms must be a contiguous float64 tensor [B, shots]")
+    shots = int(uniforms.shape[1])
+    dtype = "c64" if psi.dtype == torch.complex64 else "c128"
+    real = torch.float32 if dtype == "c64" else torch.float64
+    out = torch.empty((B, shots), dtype=torch.int64, device=psi.device)
+    zhat = torch.empty((B, n), dtype=real, device=psi.device) if want_z else None
+    ws = torch.empty(max(sample_workspace_bytes(n, B), 256), dtype=torch.uint8, device=psi.device)
+    sample_raw(dtype, n, B, _ptr(psi), shots, _ptr(uniforms), _ptr(out), _ptr(zhat), _ptr(ws), ws.numel(),
+               ctypes.c_void_p(torch.cuda.current_stream(psi.device).cuda_stream))
+    return out, zhat
 
 
 def quantum_layer_function():

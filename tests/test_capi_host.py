@@ -123,6 +123,28 @@ def test_param_shift_validation_and_workspace(lib):
     assert c.param_shift_workspace_bytes("c64", B, 10 * total) == c.param_shift_workspace_bytes("c64", B, 0)
 
 
+def test_state_and_sample_validation(lib):
+    """ql_state / ql_sample: errors before launch and workspace sizes."""
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    c = Q.Circuit(14, W.random_circuit(14, 40, 0, 1, seed=3), 0, 1, max_gates_per_pass=5)
+    need = c.state_workspace_bytes("c64", 2)
+    # the caller's state buffer is the working state: the workspace holds none
+    assert need + 2 * (1 << 14) * 8 == c.workspace_bytes("c64", 2, Q.MODE_FWD)
+    assert _err(lambda: c.state_raw("c64", 2, None, fake, None, fake, need, None)) == -1
+    assert _err(lambda: c.state_raw("c64", 2, None, fake, fake, fake, need - 1, None)) == -2
+    assert Q.sample_workspace_bytes(30, 3) == 3 * (1 << 18) * 8   # one fp64 per 4096 amplitudes
+    assert Q.sample_workspace_bytes(5, 1) == 256
+    assert _err(lambda: Q.sample_workspace_bytes(0, 1)) == -1
+    assert _err(lambda: Q.sample_workspace_bytes(33, 1)) == -1
+    ws = Q.sample_workspace_bytes(10, 2)
+    raw = Q.qlayer.sample_raw
+    assert _err(lambda: raw("c64", 10, 2, None, 4, fake, fake, None, fake, ws, None)) == -1  # psi NULL
+    assert _err(lambda: raw("c64", 10, 2, fake, 4, None, fake, None, fake, ws, None)) == -1  # uniforms NULL
+    assert _err(lambda: raw("c64", 10, 2, fake, -1, fake, fake, None, fake, ws, None)) == -1  # shots < 0
+    assert _err(lambda: raw("c64", 10, 2, fake, 4, fake, fake, None, fake, ws - 1, None)) == -2
+    assert _err(lambda: raw("c128", 32, 1, fake, 4, fake, fake, None, fake, 1 << 30, None)) == -3
+
+
 def test_workspace_arithmetic(lib):
     wl = W.get("30q")
     c = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)

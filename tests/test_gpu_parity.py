@@ -386,3 +386,80 @@ def test_param_shift_hybrid_node():
     got = gpu_shift(circ, "c128", t[:, None], np.zeros(0), np.ones((t.size, 1)))
     assert np.max(np.abs(got["expz"][:, 0] + np.sin(t))) <= 1e-12
     assert np.max(np.abs(got["grad_inputs"][:, 0] + np.cos(t))) <= 1e-12
+
+
+# ---------------------------------------------------------------------------
+# final states and shot sampling (the paper's Monte Carlo measurement)
+
+STATE_CASES = [(3, "c128"), (6, "c64"), (9, "c64"), (10, "c128"), (13, "c64"), (14, "c128"), (16, "c64")]
+
+
+@pytest.mark.parametrize("n,dtype", STATE_CASES, ids=[f"n{c[0]}-{c[1]}" for c in STATE_CASES])
+def test_state_vs_oracle(n, dtype):
+    F, P, B = 3, 5, 3
+    gates = W.random_circuit(n, 12 * n, F, P, seed=900 + n)
+    x, w, _ = W.random_inputs(B, F, P, n, seed=901 + n, dtype=dtype)
+    r = Q.Runner(Q.Circuit(n, gates, F, P), dtype)
+    psi = r.state(_dev(x, dtype), _dev(w, dtype))
+    torch.cuda.synchronize()
+    want = oracle.run(n, gates, x, w, want_state=True)["state"]
+    err = float(np.max(np.abs(psi.cpu().numpy().astype(np.complex128) - want)))
+    assert err <= TOL[dtype], f"state n={n} {dtype}: {err:.3e}"
+
+
+def _valid_near_tie(psi_row, u, idx, tol=1e-12):
+    """A shot that differs from the oracle must sit on a CDF boundary of the same state."""
+    p = np.abs(psi_row) ** 2
+    cdf = np.cumsum(p)
+    r = u * cdf[-1]
+    lo = cdf[idx - 1] if idx > 0 else 0.0
+    return p[idx] > 0 and lo - tol * cdf[-1] <= r <= cdf[idx] + tol * cdf[-1]
+
+
+SAMPLE_CASES = [(3, "c64"), (7, "c128"), (10, "c64"), (14, "c64"), (16, "c128")]
+
+
+@pytest.mark.parametrize("n,dtype", SAMPLE_CASES, ids=[f"n{c[0]}-{c[1]}" for c in SAMPLE_CASES])
+def test_sample_vs_oracle(n, dtype):
+    """Shots from the GPU's own states: the kernel's indices against the
+    oracle sampler on the same states and uniforms (integers, so exact; a
+    uniform on a CDF boundary within rounding may pick the neighbour, which is
+    then checked to be valid). zhat equals the count formula of the indices."""
+    F, P, B, shots = 3, 5, 2, 4096
+    gates = W.random_circuit(n, 10 * n, F, P, seed=950 + n)
+    x, w, _ = W.random_inputs(B, F, P, n, seed=951 + n, dtype=dtype)
+    r = Q.Runner(Q.Circuit(n, gates, F, P), dtype)
+    psi = r.state(_dev(x, dtype), _dev(w, dtype))
+    u = np.random.default_rng(952 + n).random((B, shots))
+    idx, zhat = Q.sample(psi, torch.from_numpy(u).to("cuda"))
+    torch.cuda.synchronize()
+    st = psi.cpu().numpy().astype(np.complex128)
+    got = idx.cpu().numpy()
+    want = oracle.sample(n, st, u)
+    bad = np.argwhere(got != want)
+    assert len(bad) <= 2, f"{len(bad)} shots differ from the oracle"
+    for b, s_ in bad:
+        assert _valid_near_tie(st[b], u[b, s_], int(got[b, s_])), f"invalid shot {b},{s_}"
+    bits = (got[:, :, None] >> np.arange(n)) & 1
+    zc = (shots - 2 * bits.sum(axis=1)) / shots
+    assert np.array_equal(zhat.cpu().double().numpy(), zc.astype(np.float32 if dtype == "c64" else np.float64).astype(np.float64))
+
+
+def test_sample_statistics_and_scale():
+    """Many shots estimate <Z_q> within five standard errors of the exact value;
+    scaling the state leaves the shots unchanged; zero shots writes nothing."""
+    wl = W.scaled(W.get("16q"), batch=2, layers=2)
+    x, w, _ = wl.inputs()
+    r = Q.Runner(Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights), wl.dtype)
+    psi = r.state(_dev(x, wl.dtype), _dev(w, wl.dtype))
+    exact = oracle.run(wl.n, wl.gates(), x, w)["expz"]
+    shots = 200000
+    u = torch.from_numpy(np.random.default_rng(5).random((wl.batch, shots))).to("cuda")
+    idx, zhat = Q.sample(psi, u)
+    idx2, _ = Q.sample((psi * 2).contiguous(), u)  # a power of two scales every sum exactly
+    torch.cuda.synchronize()
+    se = np.sqrt(np.maximum(1 - exact ** 2, 1e-12) / shots)
+    assert np.all(np.abs(zhat.cpu().double().numpy() - exact) <= 5 * se + 1e-6)
+    assert torch.equal(idx, idx2)
+    empty, ez = Q.sample(psi, torch.empty((wl.batch, 0), dtype=torch.float64, device="cuda"))
+    assert empty.shape == (wl.batch, 0)
