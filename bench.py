@@ -111,6 +111,9 @@ def main():
     ap.add_argument("--grad", choices=("adjoint", "shift"), default="adjoint",
                     help="gradient method timed: the adjoint sweep (the headline metric) or the "
                          "batched parameter-shift rule")
+    ap.add_argument("--shots", type=int, default=0,
+                    help="time measurement by shots instead of a gradient step: final states "
+                         "(ql_state) plus this many shots per sample (ql_sample)")
     ap.add_argument("--shift-chunk", type=int, default=0,
                     help="shifted circuits per chunk (0: as many as 8 GiB of states hold)")
     ap.add_argument("--opt", action="append", default=[],
@@ -142,7 +145,10 @@ def main():
     shift = args.grad == "shift"
     amp = 8 if wl.dtype == "c64" else 16
     chunk = args.shift_chunk or max(1, min(shift_circuits(wl), (8 << 30) // ((1 << wl.n) * amp)))
-    if shift:
+    if args.shots > 0:
+        uni = torch.from_numpy(np.random.default_rng(7).random((wl.batch, args.shots))).to(dev)
+        step = lambda: Q.sample(runner.state(xt, wt), uni)  # noqa: E731
+    elif shift:
         step = lambda: runner.param_shift(xt, wt, gt, max_chunk=chunk, outs=outs)  # noqa: E731
     else:
         runner.workspace(wl.batch, Q.MODE_FWD_BWD)
@@ -177,9 +183,11 @@ def main():
     if shift:
         # amplitude-gate updates the parameter-shift VJP performs
         U = shift_circuits(wl) * wl.n_gates * (1 << wl.n)
+    if args.shots > 0:
+        U = wl.n_gates * wl.batch * (1 << wl.n)  # forward only
     line = {
-        "metric": METRIC if not shift else
-        "amplitude-gate updates/s (batched parameter-shift grad)",
+        "metric": ("amplitude-gate updates/s (final states + shot sampling)" if args.shots > 0 else
+                   "amplitude-gate updates/s (batched parameter-shift grad)" if shift else METRIC),
         "value": U / (ms_step / 1e3),
         "unit": "amplitude-gate updates/s",
         "n_gpus": 1,
@@ -196,13 +204,20 @@ def main():
                    "updates_per_step": U, "tile_passes": info["n_passes"],
                    "tile_qubits": info["tile_qubits"], "planner_options": opts},
     }
-    if shift:
+    if args.shots > 0:
+        line["config"].update({"measurement": "shots", "shots": args.shots})
+        line["shots_per_s"] = args.shots * wl.batch * 1e3 / ms_step
+    elif shift:
         line["config"].update({"grad": "parameter shift", "circuits_per_step": shift_circuits(wl),
                                "chunk": chunk})
         line["vjp_per_s"] = 1e3 / ms_step
     if timing and kcnt[0] > 0:
         tile_ms = kms[0] / args.steps
-        if shift:
+        if args.shots > 0:
+            state_bytes = circ.state_bytes(wl.dtype, wl.batch, Q.MODE_FWD) + (1 << wl.n) * wl.batch * amp
+            flops = sum(FLOPS_FWD[int(g_[0])] for g_ in wl.gates()) * wl.batch * float(1 << wl.n)
+            traffic = None
+        elif shift:
             state_bytes = circ.state_bytes(wl.dtype, shift_circuits(wl), Q.MODE_FWD)
             flops = shift_flops(wl)
             traffic = None
