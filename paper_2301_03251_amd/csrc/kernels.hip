@@ -416,6 +416,24 @@ __device__ __forceinline__ Real gpart(const T2* p, const T2* l) {
     return acc[0] + acc[1];
 }
 
+// Sum over this thread's registers of Im(conj(l) p) = l.x p.y - l.y p.x, over
+// all registers (ALL) or those with register bit J set. The full sum is
+// invariant under every op inside one register layout: each acts unitarily on
+// the thread's registers, or multiplies psi and lambda by the same phase.
+template <int LOG_R, int J, typename T2, typename Real>
+__device__ __forceinline__ Real im_sum(const T2* p, const T2* l) {
+    constexpr int R = 1 << LOG_R;
+    Real acc[2] = {0, 0};
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        if (J >= 0 && !(i >> (J < 0 ? 0 : J) & 1)) continue;
+        Real& c = acc[i & 1];
+        c = fma(l[i].x, p[i].y, c);
+        c = fma(-l[i].y, p[i].x, c);
+    }
+    return acc[0] + acc[1];
+}
+
 // DPP row broadcast (row_bcast:15 into rows 1 and 3, row_bcast:31 into rows 2
 // and 3); lanes of the other rows read 0.
 template <int CTRL, int ROWS>
@@ -622,14 +640,23 @@ __device__ __forceinline__ void tile_ready(const double2* t) {
 //              wavefront's accumulator, then the op (its inverse, from the
 //              binding) on psi (ps) and lambda (lm) of one tile.
 enum { OP_ONE = 0, OP_PAIR = 1, OP_BWD = 2 };
+//
+// In OP_BWD, `ival` holds the thread's full Im(conj(lambda) psi) sum of the
+// current layout (refreshed after each exchange), so the Z-generator term of
+// an RZ is ival - 2 * (the bit-1 half), and of an RZ on a thread or fixed bit
+// +-ival.
 template <int LOG_R, int LOG_T, int OPM, typename T2, typename Real>
 __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
-                                       TileCtx& cx, unsigned char* lds, const DevPhase* phases,
-                                       Real* gacc, int lane, int wave, int nw, int tid) {
+                                       TileCtx& cx, Real& ival, unsigned char* lds,
+                                       const DevPhase* phases, Real* gacc, int lane, int wave, int nw,
+                                       int tid) {
 #define QL_G1_CASE(KIND, J)                                                                 \
     case H_G1 + KIND * 5 + J:                                                               \
         if constexpr (J < LOG_R) {                                                          \
-            if constexpr (OPM == OP_BWD && KIND != 0)                                       \
+            if constexpr (OPM == OP_BWD && KIND == 3)                                       \
+                grad_add(gacc, arg, fma((Real)-2, im_sum<LOG_R, J, T2, Real>(ps, lm), ival),  \
+                         lane, wave, nw);                                                   \
+            else if constexpr (OPM == OP_BWD && KIND != 0)                                  \
                 grad_add(gacc, arg, gpart<LOG_R, KIND, J, T2, Real>(ps, lm), lane, wave, nw); \
             if constexpr (OPM != OP_ONE) g1<LOG_R, KIND, J, T2, Real>(lm, ca, cb);            \
             g1<LOG_R, KIND, J, T2, Real>(ps, ca, cb);                                       \
@@ -639,7 +666,8 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
     case H_RZN + J:                                                                         \
         if constexpr (J < LOG_R) {                                                          \
             if constexpr (OPM == OP_BWD)                                                    \
-                grad_add(gacc, arg, gpart<LOG_R, 3, J, T2, Real>(ps, lm), lane, wave, nw);  \
+                grad_add(gacc, arg, fma((Real)-2, im_sum<LOG_R, J, T2, Real>(ps, lm), ival),  \
+                         lane, wave, nw);                                                   \
             if constexpr (OPM != OP_ONE) g1<LOG_R, 3, J, T2, Real, true>(lm, ca, cb);         \
             g1<LOG_R, 3, J, T2, Real, true>(ps, ca, cb);                                    \
         }                                                                                   \
@@ -693,14 +721,7 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         case H_RZU: {
             const bool bit = loc_bit(arg, cx.tb, cx.gb);
             if constexpr (OPM == OP_BWD) {
-                Real acc[2] = {0, 0};
-#pragma unroll
-                for (int i = 0; i < (1 << LOG_R); ++i) {
-                    acc[i & 1] = fma(lm[i].x, ps[i].y, acc[i & 1]);
-                    acc[i & 1] = fma(-lm[i].y, ps[i].x, acc[i & 1]);
-                }
-                const Real t = acc[0] + acc[1];
-                grad_add(gacc, arg >> 16, bit ? -t : t, lane, wave, nw);
+                grad_add(gacc, arg >> 16, bit ? -ival : ival, lane, wave, nw);
                 rz_u<LOG_R>(lm, ca, cb, bit);
             } else if constexpr (OPM == OP_PAIR) {
                 rz_u<LOG_R>(lm, ca, cb, loc_bit(arg, cx.tb, cx.gb2));
@@ -719,6 +740,7 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
             thread_layout<LOG_T>((uint32_t)tid, to, tb_to, ts_to);
             lds_exchange<LOG_R>(ps, lds, phases[cx.ph], to, cx.ts, ts_to);
             if constexpr (OPM != OP_ONE) lds_exchange<LOG_R>(lm, lds, phases[cx.ph], to, cx.ts, ts_to);
+            if constexpr (OPM == OP_BWD) ival = im_sum<LOG_R, -1, T2, Real>(ps, lm);
             cx.tb = tb_to;
             cx.ts = ts_to;
             cx.ph = (int)arg;
@@ -892,6 +914,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     const int64_t tiles = PAIR ? a.tiles >> 1 : a.tiles;
     const uint32_t top_fixed = (PAIR && n_fixed > 0) ? 1u << P.fixed_qubit[n_fixed - 1] : 0u;
     T2 ps[R], lm[R];
+    Real ival = 0;  // see run_op
     for (int64_t tile = w; tile < tiles; tile += a.n_wg) {
         const uint32_t tbit = lane < n_fixed ? (((uint32_t)tile >> lane) & 1u) : 0u;
         TileCtx cx;
@@ -923,7 +946,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
             for (int o = fwd_begin; o < fwd_end; ++o) {
                 const XOp<Real> nxt = xops[o + 1];
                 run_op<LOG_R, LOG_T, PAIR ? OP_PAIR : OP_ONE>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx,
-                                                              lds, phases, gacc, lane, wave, NW, tid);
+                                                              ival, lds, phases, gacc, lane, wave, NW,
+                                                              tid);
                 cur = nxt;
             }
         }
@@ -956,11 +980,12 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
 
             // ---- backward ops
             if (flags & PF_BWD) {
+                ival = im_sum<LOG_R, -1, T2, Real>(ps, lm);
                 XOp<Real> cur = xops[bwd_begin];
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
-                    run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, lds, phases,
-                                                 gacc, lane, wave, NW, tid);
+                    run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, ival, lds,
+                                                 phases, gacc, lane, wave, NW, tid);
                     cur = nxt;
                 }
             }
