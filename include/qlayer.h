@@ -209,6 +209,8 @@ typedef struct {
     int32_t low_qubits;    /* contiguous low qubits in every tile */
     int32_t n_transposes;  /* LDS layout changes summed over the forward passes */
     int32_t n_param_gates; /* rotation gates (gradient slots) */
+    int32_t n_lane_swaps;  /* in-register layout changes (register bit <-> lane bit) summed
+                              over the forward passes */
 } ql_plan_info;
 
 int ql_plan_info_get(const ql_circuit* c, ql_dtype dtype, ql_plan_info* out);

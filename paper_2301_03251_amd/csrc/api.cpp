@@ -772,7 +772,10 @@ int ql_plan_info_get(const ql_circuit* h, ql_dtype dtype, ql_plan_info* out) {
     r.log_regs = pl.log_r;
     r.log_threads = pl.log_t;
     r.low_qubits = pl.low;
-    for (const auto& pp : pl.passes) r.n_transposes += pp.n_transposes;
+    for (const auto& pp : pl.passes) {
+        r.n_transposes += pp.n_transposes;
+        r.n_lane_swaps += pp.n_lane_swaps;
+    }
     r.n_param_gates = (int)h->c.slot_gate.size();
     *out = r;
     return QL_OK;

@@ -599,6 +599,50 @@ __device__ __forceinline__ void lds_exchange(T2* a, unsigned char* lds, const De
     __syncthreads();
 }
 
+// Exchange register bit M with lane bit B (4 or 5) of a register tile: the
+// amplitude at (lane L, register i) moves to (lane L with bit B := bit M of
+// i, register i with bit M := bit B of L). For each register pair (lo: bit M
+// = 0, hi: bit M = 1) the lanes with bit B = 1 of lo trade places with the
+// lanes with bit B = 0 of hi, which is what the gfx950 permlane swaps do in
+// one instruction per 32-bit register pair.
+template <int B>
+__device__ __forceinline__ void lane_swap_u32(uint32_t& lo, uint32_t& hi) {
+    static_assert(B == 4 || B == 5, "lane swaps exist for lane bits 4 and 5");
+    if constexpr (B == 5) {
+        const auto r = __builtin_amdgcn_permlane32_swap(lo, hi, false, false);
+        lo = r[0];
+        hi = r[1];
+    } else {
+        const auto r = __builtin_amdgcn_permlane16_swap(lo, hi, false, false);
+        lo = r[0];
+        hi = r[1];
+    }
+}
+template <int B>
+__device__ __forceinline__ void lane_swap_real(float& lo, float& hi) {
+    uint32_t l = __builtin_bit_cast(uint32_t, lo), h = __builtin_bit_cast(uint32_t, hi);
+    lane_swap_u32<B>(l, h);
+    lo = __builtin_bit_cast(float, l);
+    hi = __builtin_bit_cast(float, h);
+}
+template <int B>
+__device__ __forceinline__ void lane_swap_real(double& lo, double& hi) {
+    uint2 l = __builtin_bit_cast(uint2, lo), h = __builtin_bit_cast(uint2, hi);
+    lane_swap_u32<B>(l.x, h.x);
+    lane_swap_u32<B>(l.y, h.y);
+    lo = __builtin_bit_cast(double, l);
+    hi = __builtin_bit_cast(double, h);
+}
+template <int LOG_R, int M, int B, typename T2>
+__device__ __forceinline__ void lane_swap(T2* a) {
+#pragma unroll
+    for (int i = 0; i < (1 << LOG_R); ++i)
+        if (!(i >> M & 1)) {
+            lane_swap_real<B>(a[i].x, a[i | (1 << M)].x);
+            lane_swap_real<B>(a[i].y, a[i | (1 << M)].y);
+        }
+}
+
 // bit of an operand location word (thread bit or fixed qubit)
 __device__ __forceinline__ bool loc_bit(uint32_t w, uint32_t tb, uint32_t gb) {
     const uint32_t pos = w & 0xff;
@@ -704,6 +748,24 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         }                                                                                   \
         break;
 #define QL_CZ_RR_A(A) QL_CZ_RR(A, 0) QL_CZ_RR(A, 1) QL_CZ_RR(A, 2) QL_CZ_RR(A, 3) QL_CZ_RR(A, 4)
+// A lane swap moves one tile bit x off lane bit B and tile bit y onto it: the
+// threads with lane bit B set trade x for y in their tile bits and in their
+// LDS offset (linear in the tile bits).
+#define QL_LSWAP(M, B)                                                                      \
+    case H_LSWAP + M * 6 + B:                                                               \
+        if constexpr (M < LOG_R && B < LOG_T) {                                             \
+            lane_swap<LOG_R, M, B>(ps);                                                     \
+            if constexpr (OPM != OP_ONE) lane_swap<LOG_R, M, B>(lm);                        \
+            cx.ph = (int)(arg & 0xfffff);                                                   \
+            const uint32_t dtb = (1u << ((arg >> 20) & 31)) | (1u << (arg >> 25));         \
+            if ((lane >> B) & 1) {                                                          \
+                cx.tb ^= dtb;                                                               \
+                cx.ts ^= lds_slot(dtb) * (uint32_t)sizeof(T2);                              \
+            }                                                                               \
+            if constexpr (OPM == OP_BWD) ival = im_sum<LOG_R, -1, T2, Real>(ps, lm);        \
+        }                                                                                   \
+        break;
+#define QL_LSWAP_M(M) QL_LSWAP(M, 4) QL_LSWAP(M, 5)
 #define QL_CZ_RX(A)                                                                         \
     case H_CZ_RX + A:                                                                       \
         if constexpr (A < LOG_R) {                                                          \
@@ -718,6 +780,7 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         QL_CZ_RR_A(0) QL_CZ_RR_A(1) QL_CZ_RR_A(2) QL_CZ_RR_A(3) QL_CZ_RR_A(4)
         QL_CZ_RX(0) QL_CZ_RX(1) QL_CZ_RX(2) QL_CZ_RX(3) QL_CZ_RX(4)
         QL_RZN_CASE(0) QL_RZN_CASE(1) QL_RZN_CASE(2) QL_RZN_CASE(3) QL_RZN_CASE(4)
+        QL_LSWAP_M(0) QL_LSWAP_M(1) QL_LSWAP_M(2) QL_LSWAP_M(3) QL_LSWAP_M(4)
         case H_RZU: {
             const bool bit = loc_bit(arg, cx.tb, cx.gb);
             if constexpr (OPM == OP_BWD) {
@@ -757,6 +820,8 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
 #undef QL_CZ_RR
 #undef QL_CZ_RR_A
 #undef QL_CZ_RX
+#undef QL_LSWAP
+#undef QL_LSWAP_M
 }
 
 // <Z_q> partials of one tile held in registers t: register bits from the

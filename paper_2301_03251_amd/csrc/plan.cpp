@@ -63,25 +63,24 @@ std::vector<int> scan(const std::vector<Gate>& gates, const std::vector<char>& d
     return exec;
 }
 
-// `amp` is the size of one amplitude in bytes (LDS offsets are in bytes).
-DevPhase make_phase(const std::vector<int>& tq, const std::vector<int>& reg_bits, int k, uint32_t amp) {
+// Layout: reg_bits[m] is the tile bit of register bit m, thr_bits[b] the tile
+// bit of thread-index bit b. `amp` is the size of one amplitude in bytes (LDS
+// offsets are in bytes).
+DevPhase make_phase(const std::vector<int>& tq, const std::vector<int>& reg_bits,
+                    const std::vector<int>& thr_bits, uint32_t amp) {
     DevPhase p{};
-    uint32_t regmask = 0;
     const int r = (int)reg_bits.size();
     for (int m = 0; m < r; m++) {
         p.reg_bit[m] = reg_bits[m];
         p.reg_tmask[m] = 1u << reg_bits[m];
         p.reg_qmask[m] = 1u << tq[reg_bits[m]];
-        regmask |= 1u << reg_bits[m];
     }
-    p.thr_mask = ((k >= 32) ? 0xffffffffu : ((1u << k) - 1)) & ~regmask;
-    int b = 0;
-    for (int j = 0; j < k && b < MAX_THREAD_BITS; j++)
-        if (p.thr_mask >> j & 1) {
-            p.thr_bit[b] = (uint32_t)j;
-            p.thr_slot[b] = lds_slot(1u << j) * amp;
-            b++;
-        }
+    for (int b = 0; b < (int)thr_bits.size() && b < MAX_THREAD_BITS; b++) {
+        const int j = thr_bits[b];
+        p.thr_mask |= 1u << j;
+        p.thr_bit[b] = (uint32_t)j;
+        p.thr_slot[b] = lds_slot(1u << j) * amp;
+    }
     for (int i = 0; i < (1 << r); i++) {
         uint32_t t = 0, q = 0;
         for (int m = 0; m < r; m++)
@@ -175,15 +174,92 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
     };
     const uint32_t low_mask = low_bits;
 
+    // ---- layouts. A layout is the tile bit of every register bit (`regs`,
+    // by register bit) and of every thread-index bit (`thr`; bits 0-5 are lane
+    // bits, the rest wavefront bits). A layout change that brings only
+    // tile bits from lane bits 4 and 5 into the registers is a sequence of
+    // lane swaps done in the registers (H_LSWAP, one permlane swap per
+    // register pair); any other change goes through LDS (H_TRANSPOSE). Loads
+    // and stores need the low tile bits on their own thread bits (thr[j] = j
+    // for j < low), so lanes cover contiguous memory.
+    const int log_t = k - r;
+    const int home = std::min(low, log_t);
+    auto swap_lane = [&](int slot) { return (slot == 4 || slot == 5) && slot < log_t; };
+    auto next_use = [&](int bit) {
+        int pos = 0;
+        for (int gi : pending) {
+            if (need_bit(gates[gi]) == bit) return pos;
+            pos++;
+        }
+        return 1 << 30;
+    };
+    // thread bits for register set R after an LDS exchange: the low tile bits
+    // on their own thread bits; the bits needed soonest on the swap lanes
+    // (4, 5), the rest in order of use
+    auto fresh_thr = [&](const std::vector<int>& R) {
+        std::vector<int> thr(log_t, -1), rest;
+        for (int j = 0; j < k; j++) {
+            if (std::find(R.begin(), R.end(), j) != R.end()) continue;
+            if (j < home) thr[j] = j;
+            else rest.push_back(j);
+        }
+        std::stable_sort(rest.begin(), rest.end(), [&](int x, int y) { return next_use(x) < next_use(y); });
+        size_t ri = 0;
+        for (int sl : {4, 5})
+            if (swap_lane(sl) && thr[sl] < 0 && ri < rest.size()) thr[sl] = rest[ri++];
+        for (int sl = 0; sl < log_t; sl++)
+            if (thr[sl] < 0 && ri < rest.size()) thr[sl] = rest[ri++];
+        return thr;
+    };
+    auto slot_of = [](const std::vector<int>& v, int bit) {
+        return (int)(std::find(v.begin(), v.end(), bit) - v.begin());
+    };
+
     std::vector<int> regs = choose(low_mask, {});
+    std::vector<int> thr = fresh_thr(regs);
+    // register sets reachable by lane swaps only: every incoming bit on a
+    // swap lane
+    auto reachable = [&](uint32_t m) {
+        for (int j = 0; j < k; j++)
+            if ((m >> j & 1) && std::find(regs.begin(), regs.end(), j) == regs.end() &&
+                !swap_lane(slot_of(thr, j)))
+                return false;
+        return true;
+    };
+    // next register set: the best set the lane swaps reach, if it runs any
+    // gate (a lane swap costs a few VALU operations per register pair, an LDS
+    // exchange the whole tile's LDS traffic and two barriers); else the best
+    // set overall
+    auto choose_next = [&]() {
+        std::vector<int> best = choose(0, regs);
+        uint32_t bm = 0;
+        for (int x : best) bm |= 1u << x;
+        if (reachable(bm)) return best;
+        int rn = 0;
+        uint32_t rm = 0;
+        for (uint32_t m = 0; m < (1u << k); m++) {
+            if (__builtin_popcount(m) != r || !reachable(m)) continue;
+            const int c = phase_gates(m);
+            if (c > rn) {
+                rn = c;
+                rm = m;
+            }
+        }
+        if (rn == 0) return best;
+        std::vector<int> out;
+        for (int j = 0; j < k; j++)
+            if (rm >> j & 1) out.push_back(j);
+        return out;
+    };
+
     int cur_phase = (int)phases.size();
-    phases.push_back(make_phase(pp.qubits, regs, k, amp));
+    phases.push_back(make_phase(pp.qubits, regs, thr, amp));
     pp.first_phase = cur_phase;
 
     // gradient accumulators: one per rotation in this pass
     int n_gs = 0;
 
-    // location of qubit q in the current phase
+    // location of qubit q in the current layout
     auto loc = [&](int q, uint32_t& type, uint32_t& pos) {
         int j = bit_of[q];
         if (j < 0) { type = LOC_FIX; pos = (uint32_t)q; return; }
@@ -199,8 +275,53 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         op.kind = (uint32_t)kind;
         return op;
     };
-    struct Rec { DevOp op; int prev_phase; };
+    // bwd_arg: the argument of the op's backward form (a layout change takes
+    // the backward sweep back to the previous layout)
+    struct Rec { DevOp op; uint32_t bwd_arg; };
     std::vector<Rec> recs;
+
+    // layout changes; the backward op list takes each one back to the previous layout
+    auto new_phase = [&]() {
+        phases.push_back(make_phase(pp.qubits, regs, thr, amp));
+        return (int)phases.size() - 1;
+    };
+    // lane swap of register bit m and lane bit b; the argument carries the new
+    // phase and the tile bits lane bit b leaves (x) and takes (y)
+    auto lane_swap = [&](int m, int b) {
+        const uint32_t x = (uint32_t)thr[b], y = (uint32_t)regs[m];
+        std::swap(regs[m], thr[b]);
+        const int np = new_phase();
+        recs.push_back({make_op(H_LSWAP + (uint32_t)(m * 6 + b), lswap_arg((uint32_t)np, x, y), -1, K_H),
+                        lswap_arg((uint32_t)cur_phase, y, x)});
+        cur_phase = np;
+        pp.n_lane_swaps++;
+    };
+    auto lds_exchange_to = [&](const std::vector<int>& R, const std::vector<int>& T) {
+        regs = R;
+        thr = T;
+        const int np = new_phase();
+        recs.push_back({make_op(H_TRANSPOSE, (uint32_t)np, -1, K_H), (uint32_t)cur_phase});
+        cur_phase = np;
+        pp.n_transposes++;
+    };
+    // move to register set R2: lane swaps when every incoming bit is on a
+    // swap lane, else one LDS exchange
+    auto change_to = [&](const std::vector<int>& R2) {
+        std::vector<int> in, out;
+        for (int x : R2)
+            if (std::find(regs.begin(), regs.end(), x) == regs.end()) in.push_back(x);
+        for (int x : regs)
+            if (std::find(R2.begin(), R2.end(), x) == R2.end()) out.push_back(x);
+        bool lanes = true;
+        for (int x : in) lanes &= swap_lane(slot_of(thr, x));
+        if (!lanes) {
+            std::vector<int> R = regs;  // kept bits stay on their register bits
+            for (size_t i = 0; i < out.size(); i++) R[slot_of(R, out[i])] = in[i];
+            lds_exchange_to(R, fresh_thr(R));
+            return;
+        }
+        for (size_t i = 0; i < in.size(); i++) lane_swap(slot_of(regs, out[i]), slot_of(thr, in[i]));
+    };
 
     while (!pending.empty()) {
         uint64_t blocked = 0;
@@ -246,37 +367,29 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
                     else op = make_op(H_CZ_XX, loc_word(ta, pa) | (loc_word(tb, pb) << 16), -1, K_CZ);
                     break;
             }
-            recs.push_back({op, -1});
+            recs.push_back({op, op.arg});
         }
         pending.swap(rest);
         if (pending.empty()) break;
-        regs = choose(0, regs);
-        int np = (int)phases.size();
-        phases.push_back(make_phase(pp.qubits, regs, k, amp));
-        recs.push_back({make_op(H_TRANSPOSE, (uint32_t)np, -1, K_H), cur_phase});
-        cur_phase = np;
-        pp.n_transposes++;
+        change_to(choose_next());
     }
-    // end in a layout whose register bits avoid the low (contiguous) tile
-    // bits, so the store and the next load are coalesced
-    bool low_in_regs = false;
-    for (int b : regs) low_in_regs |= (b < low);
-    if (low_in_regs) {
+    // end in a store layout: the low tile bits back on their own thread bits
+    // (through LDS if any has left them)
+    bool fits = true;
+    for (int j = 0; j < home; j++) fits &= thr[j] == j;
+    if (!fits) {
         std::vector<int> keep;
-        for (int b : regs) if (b >= low) keep.push_back(b);
+        for (int x : regs)
+            if (x >= home) keep.push_back(x);
         pending.clear();
-        regs = choose(low_mask, keep);
-        int np = (int)phases.size();
-        phases.push_back(make_phase(pp.qubits, regs, k, amp));
-        recs.push_back({make_op(H_TRANSPOSE, (uint32_t)np, -1, K_H), cur_phase});
-        cur_phase = np;
-        pp.n_transposes++;
+        std::vector<int> R = choose_scan(low_mask, keep);
+        lds_exchange_to(R, fresh_thr(R));
     }
     pp.last_phase = cur_phase;
     for (auto& rc : recs) pp.fwd_ops.push_back(rc.op);
     for (int i = (int)recs.size() - 1; i >= 0; i--) {
         DevOp op = recs[i].op;
-        if (op.h == H_TRANSPOSE) op.arg = (uint32_t)recs[i].prev_phase;
+        op.arg = recs[i].bwd_arg;
         pp.bwd_ops.push_back(op);
     }
 }

@@ -49,8 +49,16 @@ enum HandlerId : uint32_t {
     H_TRANSPOSE = 87,  // arg = phase index
     H_RZN = 88,        // + J: RZ on register bit J whose phase on bit 1 is negated (set per sample
                        //      by the binding kernel in place of H_G1 + 15 + J)
-    H_END = 93,
+    H_LSWAP = 93,      // + m * 6 + b: exchange register bit m with lane bit b (4 or 5) by
+                       //      permlane swaps; arg = lswap_arg(new phase, tile bit lane b
+                       //      leaves, tile bit it takes)
+    H_END = 123,
 };
+// Argument of a lane swap: the new phase (< 2^20) and the tile bits x (leaving
+// the lane bit for the registers) and y (taking its place).
+constexpr uint32_t lswap_arg(uint32_t phase, uint32_t x, uint32_t y) {
+    return phase | x << 20 | y << 25;
+}
 // A loc in an op argument: tile bit or qubit in bits 0..7, LocType in bits 8..9.
 constexpr uint32_t loc_word(uint32_t type, uint32_t pos) { return pos | (type << 8); }
 constexpr uint32_t NO_GSLOT = 0xffffu;
@@ -74,9 +82,10 @@ constexpr int MAX_TILE_BITS = 16;
 constexpr int MAX_THREAD_BITS = 12;
 
 // Register layout of one phase: register bit m of a thread's amplitude index
-// is tile bit reg_bit[m]; the remaining tile bits (thr_mask, ascending) are the
-// thread index bits. Every per-register and per-thread-bit offset the kernel
-// needs is precomputed here, so a layout change costs one XOR per access.
+// is tile bit reg_bit[m]; thread-index bit b is tile bit thr_bit[b] (bits 0-5
+// are lane bits, the rest wavefront bits). Every per-register and
+// per-thread-bit offset the kernel needs is precomputed here, so a layout
+// change costs one XOR per access.
 //
 // LDS: the amplitude with tile index t sits in slot lds_slot(t) (a GF(2)-linear
 // bank-spreading permutation), so the byte offset of (thread, register i) is
@@ -139,7 +148,8 @@ struct PassPlan {
     std::vector<int> gslots;          // pass-local gradient accumulator -> rotation slot
     int first_phase = 0;              // phase index at pass start (forward)
     int last_phase = 0;               // phase index at pass end (forward)
-    int n_transposes = 0;
+    int n_transposes = 0;             // layout changes through LDS
+    int n_lane_swaps = 0;             // layout changes inside the registers
 };
 
 struct Plan {

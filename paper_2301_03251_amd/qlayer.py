@@ -37,7 +37,7 @@ class _Options(ctypes.Structure):
 class _PlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "n_passes", "tile_qubits", "log_regs",
                                               "log_threads", "low_qubits", "n_transposes",
-                                              "n_param_gates")]
+                                              "n_param_gates", "n_lane_swaps")]
 
 
 _lib = None
