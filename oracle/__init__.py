@@ -7,6 +7,11 @@ path never does, and the two share no code.
 
 Angles are consumed as float64. For complex64 workloads callers pass the
 float32 values the GPU receives, upcast exactly.
+
+Gate kinds: H 0, RX 1, RY 2, RZ 3, CNOT 4, CZ 5, CRX 6, CRY 7, CRZ 8 (q0 control,
+q1 target) and PAULI 9 (a Pauli-channel trajectory: its uniform is input
+feature ``index``, its probabilities the next row of ``pauli_p``). Embeddings
+``embed = (kind, first)``: kind 0 none (|0...0>), 1 basis, 2 amplitude.
 """
 
 from __future__ import annotations
@@ -48,6 +53,11 @@ def _bind(path):
     lib.oracle_param_shift.argtypes = [ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
                                        ctypes.c_int, ctypes.c_int, P, P, P, P, P]
     lib.oracle_param_shift.restype = ctypes.c_int
+    ci = ctypes.c_int
+    lib.oracle_run_ext.argtypes = [ci, P, ci, ci, ci, ci, ci, ci, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_run_ext.restype = ci
+    lib.oracle_param_shift_ext.argtypes = [ci, P, ci, ci, ci, ci, ci, ci, P, P, P, P, P, P]
+    lib.oracle_param_shift_ext.restype = ci
     lib.oracle_sample.argtypes = [ctypes.c_int, ctypes.c_int, P, ctypes.c_int64, P, P]
     lib.oracle_sample.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
@@ -80,11 +90,13 @@ class Oracle:
     def __init__(self, path):
         self.lib = _bind(path)
 
-    def run(self, n, gates, inputs, weights, grad_out=None, want_state=False, want_back=False):
-        return _run(self.lib, n, gates, inputs, weights, grad_out, want_state, want_back)
+    def run(self, n, gates, inputs, weights, grad_out=None, want_state=False, want_back=False,
+            embed=None, pauli_p=None):
+        return _run(self.lib, n, gates, inputs, weights, grad_out, want_state, want_back, embed,
+                    pauli_p)
 
-    def param_shift(self, n, gates, inputs, weights, grad_out):
-        return _param_shift(self.lib, n, gates, inputs, weights, grad_out)
+    def param_shift(self, n, gates, inputs, weights, grad_out, embed=None, pauli_p=None):
+        return _param_shift(self.lib, n, gates, inputs, weights, grad_out, embed, pauli_p)
 
     def sample(self, n, states, uniforms):
         return _sample(self.lib, n, states, uniforms)
@@ -95,23 +107,32 @@ def default() -> "Oracle":
     return _default
 
 
-def run(n, gates, inputs, weights, grad_out=None, want_state=False, want_back=False):
+def run(n, gates, inputs, weights, grad_out=None, want_state=False, want_back=False, embed=None,
+        pauli_p=None):
     """See ``_run``; uses the default oracle library."""
-    return _run(_load(), n, gates, inputs, weights, grad_out, want_state, want_back)
+    return _run(_load(), n, gates, inputs, weights, grad_out, want_state, want_back, embed, pauli_p)
 
 
-def param_shift(n, gates, inputs, weights, grad_out):
+def param_shift(n, gates, inputs, weights, grad_out, embed=None, pauli_p=None):
     """See ``_param_shift``; uses the default oracle library."""
-    return _param_shift(_load(), n, gates, inputs, weights, grad_out)
+    return _param_shift(_load(), n, gates, inputs, weights, grad_out, embed, pauli_p)
 
 
-def _run(lib, n, gates, inputs, weights, grad_out=None, want_state=False, want_back=False):
+def _ext(embed, pauli_p):
+    kind, first = (0, 0) if embed is None else (int(embed[0]), int(embed[1]))
+    pp = None if pauli_p is None else np.ascontiguousarray(np.asarray(pauli_p, np.float64).reshape(-1, 3))
+    return kind, first, pp
+
+
+def _run(lib, n, gates, inputs, weights, grad_out=None, want_state=False, want_back=False,
+         embed=None, pauli_p=None):
     """Forward (+ adjoint VJP when ``grad_out`` is given) over a batch.
 
     Returns a dict with ``expz[B,n]`` and, with ``grad_out``, ``grad_inputs[B,F]``
     and ``grad_weights[P]``; ``state[B,2^n]`` (complex128) with ``want_state``;
     ``back_psi[B,2^n]`` and ``back_lam0[B]`` (psi and lambda[0] after the
-    reverse sweep un-applied every gate) with ``want_back``.
+    reverse sweep un-applied every gate) with ``want_back``. ``embed`` and
+    ``pauli_p`` as in the module docstring.
     """
     inputs = np.asarray(inputs)
     B = inputs.shape[0]
@@ -135,15 +156,18 @@ def _run(lib, n, gates, inputs, weights, grad_out=None, want_state=False, want_b
         out["back_psi"], out["back_lam0"] = bp, bl
     if st is not None:
         out["state"] = st
-    rc = lib.oracle_run(n, _ptr(gates), gates.shape[0], B, F, P, _ptr(x), _ptr(w), _ptr(g),
-                        _ptr(expz), _ptr(gi), _ptr(gw), _ptr(st), _ptr(bp), _ptr(bl))
+    kind, first, pp = _ext(embed, pauli_p)
+    rc = lib.oracle_run_ext(n, _ptr(gates), gates.shape[0], B, F, P, kind, first, _ptr(pp), _ptr(x),
+                            _ptr(w), _ptr(g), _ptr(expz), _ptr(gi), _ptr(gw), _ptr(st), _ptr(bp),
+                            _ptr(bl))
     if rc != 0:
         raise ValueError(f"oracle_run failed with code {rc}")
     return out
 
 
-def _param_shift(lib, n, gates, inputs, weights, grad_out):
-    """Parameter-shift VJP: ``(grad_inputs[B,F], grad_weights[P])``."""
+def _param_shift(lib, n, gates, inputs, weights, grad_out, embed=None, pauli_p=None):
+    """Parameter-shift VJP: ``(grad_inputs[B,F], grad_weights[P])`` (two-term rule,
+    four-term for controlled rotations; amplitude-embedding features get none)."""
     inputs = np.asarray(inputs)
     B = inputs.shape[0]
     gates, x, w = _prep(gates, inputs, weights, B)
@@ -151,8 +175,9 @@ def _param_shift(lib, n, gates, inputs, weights, grad_out):
     g = np.ascontiguousarray(np.asarray(grad_out, dtype=np.float64).reshape(B, n))
     gi = np.zeros((B, F), dtype=np.float64)
     gw = np.zeros(P, dtype=np.float64)
-    rc = lib.oracle_param_shift(n, _ptr(gates), gates.shape[0], B, F, P, _ptr(x), _ptr(w),
-                                _ptr(g), _ptr(gi), _ptr(gw))
+    kind, first, pp = _ext(embed, pauli_p)
+    rc = lib.oracle_param_shift_ext(n, _ptr(gates), gates.shape[0], B, F, P, kind, first, _ptr(pp),
+                                    _ptr(x), _ptr(w), _ptr(g), _ptr(gi), _ptr(gw))
     if rc != 0:
         raise ValueError(f"oracle_param_shift failed with code {rc}")
     return gi, gw

@@ -419,9 +419,270 @@ def pin_sampling(orc):
     assert np.all(np.abs(freq - p) <= 5 * se + 1e-9), "shot frequencies do not follow |psi|^2"
 
 
+# --------------------------------------------------------------------------
+# controlled rotations (the quantum autoencoder's controlled gates)
+
+def _wrap_crz(kind):
+    """CRZ acts on the phase; H before and after turns it into a population change."""
+    return ([_g(W.H, 1)], [_g(W.H, 1)]) if kind == W.CRZ else ([], [])
+
+
+def pin_controlled_rotation_closed_forms(orc):
+    """Control |0>: the target keeps <Z> = 1 and the gradient is 0. Control |1>
+    (prepared by RY(pi)): CRX(t), CRY(t) and H CRZ(t) H give <Z_t> = cos t with
+    derivative -sin t. Control |+> (H): <Z_t> = (1 + cos t) / 2, derivative
+    -sin(t) / 2, and the control keeps <Z> = 0."""
+    for kind in W.CONTROLLED:
+        pre, post = _wrap_crz(kind)
+        cr = [_g(kind, 0, 1, W.SRC_WEIGHT, 0)]
+        for t in THETAS:
+            name = W.KIND_NAMES[kind]
+            r = orc.run(2, _arr(pre + cr + post), np.zeros((1, 1)), [t], grad_out=[[0.0, 1.0]])
+            _close(r["expz"][0, 1], 1.0, what=f"{name} control 0")
+            _close(r["grad_weights"][0], 0.0, what=f"{name} control 0 grad")
+            r = orc.run(2, _arr([_g(W.RY, 0, -1, W.SRC_INPUT, 0)] + pre + cr + post),
+                        np.array([[math.pi]]), [t], grad_out=[[0.0, 1.0]])
+            _close(r["expz"][0, 1], math.cos(t), what=f"{name} control 1")
+            _close(r["grad_weights"][0], -math.sin(t), what=f"{name} control 1 grad")
+            r = orc.run(2, _arr([_g(W.H, 0)] + pre + cr + post), np.zeros((1, 1)), [t],
+                        grad_out=[[0.0, 1.0]])
+            _close(r["expz"][0], [0.0, 0.5 * (1 + math.cos(t))], what=f"{name} control +")
+            _close(r["grad_weights"][0], -0.5 * math.sin(t), what=f"{name} control + grad")
+
+
+def pin_controlled_rotation_brute_force(orc):
+    """Random circuits with controlled rotations on 2..4 qubits: states, <Z_i>
+    and gradients equal the dense model P0 (x) I + P1 (x) exp(-i t P / 2)."""
+    kinds = (W.H, W.RY, W.RZ, W.CNOT, W.CRX, W.CRY, W.CRZ)
+    for n in (2, 3, 4):
+        for seed in range(2):
+            gates = W.random_circuit(n, 16, 3, 4, 500 * n + seed, kinds=kinds)
+            x, w, g = W.random_inputs(2, 3, 4, n, 500 * n + seed + 7)
+            r = orc.run(n, gates, x, w, grad_out=g, want_state=True)
+            b = brute.run(n, gates, x, w, grad_out=g)
+            _close(r["state"], b["state"], what=f"crot brute state n={n}")
+            _close(r["expz"], b["expz"], what=f"crot brute expz n={n}")
+            _close(r["grad_inputs"], b["grad_inputs"], what=f"crot brute grad_x n={n}")
+            _close(r["grad_weights"], b["grad_weights"], what=f"crot brute grad_w n={n}")
+
+
+def pin_controlled_rotation_decomposition(orc):
+    """CRY(t) = RY(t/2) CNOT RY(-t/2) CNOT, CRZ likewise with RZ, and CRX(t) =
+    RX(t/2) CZ RX(-t/2) CZ (X RY(a) X = RY(-a), X RZ(a) X = RZ(-a), Z RX(a) Z =
+    RX(-a)): the same final states inside a random circuit, and the gradient of
+    t equals (g(t/2) - g(-t/2)) / 2 from the two half-angle rotations."""
+    n = 3
+    for kind, rot, ent in ((W.CRX, W.RX, W.CZ), (W.CRY, W.RY, W.CNOT), (W.CRZ, W.RZ, W.CNOT)):
+        pre = W.random_circuit(n, 8, 1, 2, 61 + kind, kinds=(W.H, W.RX, W.RY, W.CNOT)).tolist()
+        post = W.random_circuit(n, 8, 1, 2, 71 + kind, kinds=(W.H, W.RZ, W.RY, W.CZ)).tolist()
+        t = 1.234
+        x, w, g = W.random_inputs(1, 1, 2, n, 81)
+        wc = np.concatenate([w, [t]])
+        full = _arr(pre + [_g(kind, 2, 0, W.SRC_WEIGHT, 2)] + post)
+        wd = np.concatenate([w, [0.5 * t, -0.5 * t]])
+        dec = _arr(pre + [_g(rot, 0, -1, W.SRC_WEIGHT, 2), _g(ent, 2, 0), _g(rot, 0, -1, W.SRC_WEIGHT, 3),
+                          _g(ent, 2, 0)] + post)
+        rc = orc.run(n, full, x, wc, grad_out=g, want_state=True)
+        rd = orc.run(n, dec, x, wd, grad_out=g, want_state=True)
+        _close(rc["state"], rd["state"], what=f"{W.KIND_NAMES[kind]} decomposition state")
+        _close(rc["grad_weights"][2], 0.5 * (rd["grad_weights"][2] - rd["grad_weights"][3]),
+               what=f"{W.KIND_NAMES[kind]} decomposition grad")
+        _close(rc["grad_weights"][:2], rd["grad_weights"][:2], what="other weights")
+
+
+def pin_controlled_rotation_shift_and_fd(orc):
+    """Adjoint gradients of circuits with controlled rotations equal the
+    four-term parameter-shift rule for generators with eigenvalues {0, +-1/2}
+    (Anselmetti et al. 2021) and central differences (h = 1e-5)."""
+    n = 3
+    kinds = (W.H, W.RX, W.CNOT, W.CRX, W.CRY, W.CRZ)
+    gates = W.random_circuit(n, 20, 2, 3, 91, kinds=kinds)
+    x, w, g = W.random_inputs(2, 2, 3, n, 92)
+    r = orc.run(n, gates, x, w, grad_out=g)
+    gi, gw = orc.param_shift(n, gates, x, w, g)
+    _close(r["grad_inputs"], gi, tol=1e-12, what="crot shift grad_x")
+    _close(r["grad_weights"], gw, tol=1e-12, what="crot shift grad_w")
+    h = 1e-5
+    for p in range(w.size):
+        wp, wm = w.copy(), w.copy()
+        wp[p] += h
+        wm[p] -= h
+        fd = (np.sum(g * orc.run(n, gates, x, wp)["expz"]) - np.sum(g * orc.run(n, gates, x, wm)["expz"])) / (2 * h)
+        _close(fd, r["grad_weights"][p], tol=1e-8, what="crot fd w")
+
+
+# --------------------------------------------------------------------------
+# initial-state embeddings (Sec. "Quantum Data")
+
+def pin_basis_embedding(orc):
+    """Basis embedding: qubit q is 1 where feature first + q is >= 0.5 (0.5
+    itself counts as 1, just below does not); <Z_q> = 1 - 2 bit_q, and a
+    circuit after it acts as on the basis state prepared by RY(pi) gates
+    (RY(pi)|0> = |1> exactly)."""
+    n = 4
+    feats = np.array([[7.0, 0.5, 0.49999999, 1.0, 0.0, 3.0],
+                      [7.0, 0.0, 1.0, 0.2, 0.7, 3.0]])
+    bits = [[1, 0, 1, 0], [0, 1, 0, 1]]
+    r = orc.run(n, _arr([]), feats, [], embed=(W.EMBED_BASIS, 1), want_state=True)
+    for b in range(2):
+        idx = sum(bits[b][q] << q for q in range(n))
+        e = np.zeros(1 << n)
+        e[idx] = 1
+        _close(r["state"][b], e, what="basis state")
+        _close(r["expz"][b], [1 - 2 * bits[b][q] for q in range(n)], what="basis <Z>")
+    circ = W.random_circuit(n, 20, 1, 3, 33)
+    x, w, g = W.random_inputs(2, 1, 3, n, 34)
+    xe = np.concatenate([x, feats], axis=1)
+    circ_e = circ.copy()
+    r = orc.run(n, circ_e, xe, w, grad_out=g, embed=(W.EMBED_BASIS, 2), want_state=True)
+    for b in range(2):
+        prep = [_g(W.RY, q, -1, W.SRC_WEIGHT, 3) for q in range(n) if bits[b][q]]
+        rb = orc.run(n, _arr(prep + circ.tolist()), x[b:b + 1], np.concatenate([w, [math.pi]]),
+                     grad_out=g[b:b + 1], want_state=True)
+        _close(r["state"][b], rb["state"][0], what="basis embedding then circuit")
+        _close(r["grad_inputs"][b, :1], rb["grad_inputs"][0], what="basis embedding grad_x")
+        _close(r["grad_inputs"][b, 1:], 0.0, what="no gradient for embedded bits")
+
+
+def pin_amplitude_embedding(orc):
+    """Amplitude embedding: psi_0 = x / |x| (so <Z_q> = sum x_j^2 (1 - 2 bit_q(j)) / |x|^2
+    with no gates); with a circuit after it, states, <Z> and rotation gradients
+    equal the dense model started from x / |x|; the zero vector gives <Z> = 0."""
+    n = 3
+    dim = 1 << n
+    rng = np.random.default_rng(5)
+    feats = rng.standard_normal((2, dim + 2))
+    r = orc.run(n, _arr([]), feats, [], embed=(W.EMBED_AMPLITUDE, 1), want_state=True)
+    for b in range(2):
+        v = feats[b, 1:1 + dim]
+        _close(r["state"][b], v / np.linalg.norm(v), what="amplitude state")
+        want = [np.sum(v ** 2 * np.where((np.arange(dim) >> q) & 1, -1.0, 1.0)) / np.sum(v ** 2)
+                for q in range(n)]
+        _close(r["expz"][b], want, what="amplitude <Z>")
+    circ = W.random_circuit(n, 24, 2, 3, 35)
+    x, w, g = W.random_inputs(2, 2, 3, n, 36)
+    xe = np.concatenate([x, feats], axis=1)
+    r = orc.run(n, circ, xe, w, grad_out=g, embed=(W.EMBED_AMPLITUDE, 3), want_state=True)
+    b_ = brute.run(n, circ, xe, w, grad_out=g, embed=(W.EMBED_AMPLITUDE, 3))
+    _close(r["state"], b_["state"], what="amplitude brute state")
+    _close(r["expz"], b_["expz"], what="amplitude brute expz")
+    _close(r["grad_weights"], b_["grad_weights"], what="amplitude brute grad_w")
+    _close(r["grad_inputs"][:, :2], b_["grad_inputs"][:, :2], what="amplitude brute grad_x (angles)")
+    z = np.zeros((1, dim))
+    r0 = orc.run(n, circ, np.concatenate([x[:1], z], axis=1), w, embed=(W.EMBED_AMPLITUDE, 2))
+    _close(r0["expz"], 0.0, what="zero vector")
+
+
+def pin_amplitude_embedding_gradient(orc):
+    """Gradient with respect to the embedded features: central differences
+    (h = 1e-6); f is invariant under x -> c x, so sum_j x_j df/dx_j = 0 (Euler)
+    and the gradient of 3x is a third of that of x."""
+    n = 3
+    dim = 1 << n
+    circ = W.random_circuit(n, 20, 1, 3, 37)
+    x, w, g = W.random_inputs(2, 1, 3, n, 38)
+    rng = np.random.default_rng(39)
+    xe = np.concatenate([x, rng.standard_normal((2, dim))], axis=1)
+    emb = (W.EMBED_AMPLITUDE, 1)
+    r = orc.run(n, circ, xe, w, grad_out=g, embed=emb)
+    h = 1e-6
+
+    def f(xx):
+        return float(np.sum(g * orc.run(n, circ, xx, w, embed=emb)["expz"]))
+
+    for b in range(2):
+        for j in range(1, 1 + dim):
+            xp, xm = xe.copy(), xe.copy()
+            xp[b, j] += h
+            xm[b, j] -= h
+            _close((f(xp) - f(xm)) / (2 * h), r["grad_inputs"][b, j], tol=1e-8, what="amplitude fd")
+        _close(np.dot(xe[b, 1:], r["grad_inputs"][b, 1:]), 0.0, tol=1e-12, what="Euler homogeneity")
+    x3 = xe.copy()
+    x3[:, 1:] *= 3.0
+    r3 = orc.run(n, circ, x3, w, grad_out=g, embed=emb)
+    _close(r3["grad_inputs"][:, 1:], r["grad_inputs"][:, 1:] / 3.0, what="gradient of 3x")
+    _close(r3["expz"], r["expz"], what="scale invariance")
+
+
+# --------------------------------------------------------------------------
+# Pauli-channel trajectories (noise-inclusive simulation)
+
+def pin_pauli_trajectory_choices(orc):
+    """With probabilities (1/8, 1/4, 3/8) a uniform below 1/8 applies X, [1/8, 3/8)
+    Y, [3/8, 3/4) Z and the rest nothing (edges belong to the next bin): on |0>,
+    X|0> = |1>, Y|0> = i|1>; on |+> (H), Z gives |->. The channel's uniform
+    feature gets no gradient."""
+    pp = [[0.125, 0.25, 0.375]]
+    cases = [(0.0, 1), (0.124, 1), (0.125, 2), (0.374, 2), (0.375, 3), (0.749, 3), (0.75, 0), (0.99, 0)]
+    for u, which in cases:
+        r = orc.run(1, _arr([_g(W.PAULI, 0, -1, W.SRC_INPUT, 0)]), np.array([[u]]), [], want_state=True,
+                    pauli_p=pp)
+        want = {0: [1, 0], 1: [0, 1], 2: [0, 1j], 3: [1, 0]}[which]
+        _close(r["state"][0], want, what=f"pauli u={u} on |0>")
+        r = orc.run(1, _arr([_g(W.H, 0), _g(W.PAULI, 0, -1, W.SRC_INPUT, 0)]), np.array([[u]]), [],
+                    want_state=True, pauli_p=pp)
+        s2 = 1 / math.sqrt(2)
+        want = {0: [s2, s2], 1: [s2, s2], 2: [-1j * s2, 1j * s2], 3: [s2, -s2]}[which]
+        _close(r["state"][0], want, what=f"pauli u={u} on |+>")
+    gates = _arr([_g(W.RY, 0, -1, W.SRC_WEIGHT, 0), _g(W.PAULI, 0, -1, W.SRC_INPUT, 0)])
+    r = orc.run(1, gates, np.array([[0.2]]), [0.4], grad_out=[[1.0]], pauli_p=pp)
+    _close(r["grad_inputs"], 0.0, what="no gradient for the uniform")
+    _close(r["expz"][0, 0], -math.cos(0.4), what="Y flips <Z>")
+    _close(r["grad_weights"][0], math.sin(0.4), what="gradient through the flip")
+
+
+def _density_reference(n, gates, x_b, w, pauli_p):
+    """<Z_q> of the channel-averaged state: rho -> U rho U^dag per gate and
+    rho -> sum_k p_k P_k rho P_k + (1 - sum p) rho per channel."""
+    dim = 1 << n
+    rho = np.zeros((dim, dim), np.complex128)
+    rho[0, 0] = 1
+    ch = 0
+    th = brute.angles(gates, x_b, w, [[0, 0, 0]] * len(pauli_p))
+    for gt, t in zip(gates, th):
+        if int(gt[0]) == W.PAULI:
+            p = pauli_p[ch]
+            ch += 1
+            acc = (1 - sum(p)) * rho
+            for k in range(3):
+                P = brute.embed(n, {int(gt[1]): brute.PAULIS[k + 1]})
+                acc = acc + p[k] * P @ rho @ P.conj().T
+            rho = acc
+        else:
+            U = brute.gate_unitary(n, gt, t)
+            rho = U @ rho @ U.conj().T
+    return np.array([np.real(np.trace(brute.z_observable(n, q) @ rho)) for q in range(n)])
+
+
+def pin_pauli_channel_average(orc):
+    """Averaging the trajectories over every outcome of two channels, weighted by
+    the outcome probabilities, gives the density-matrix expectation exactly."""
+    n = 3
+    base = W.random_circuit(n, 12, 1, 3, 95, kinds=(W.H, W.RX, W.RY, W.CNOT, W.CRY)).tolist()
+    gates = _arr(base[:6] + [_g(W.PAULI, 1, -1, W.SRC_INPUT, 1)] + base[6:] +
+                 [_g(W.PAULI, 2, -1, W.SRC_INPUT, 2)])
+    pp = [[0.1, 0.05, 0.2], [0.02, 0.3, 0.08]]
+    x, w, _ = W.random_inputs(1, 1, 3, n, 96)
+    mid = []  # a uniform inside each outcome's bin, and the outcome probability
+    for p in pp:
+        e = np.cumsum([0.0] + list(p) + [1 - sum(p)])
+        mid.append([(0.5 * (e[k] + e[k + 1]), e[k + 1] - e[k]) for k in range(4)])
+    avg = np.zeros(n)
+    for a in range(4):
+        for b in range(4):
+            u = np.array([[x[0, 0], mid[0][a][0], mid[1][b][0]]])
+            avg += mid[0][a][1] * mid[1][b][1] * orc.run(n, gates, u, w, pauli_p=pp)["expz"][0]
+    xb = np.array([x[0, 0], 0.0, 0.0])
+    _close(avg, _density_reference(n, gates, xb, w, pp), what="trajectory average vs density matrix")
+
+
 ALL_PINS = [
     pin_rotations_on_zero, pin_rotation_axes, pin_h_rz_h, pin_hybrid_node,
     pin_shared_parameter, pin_cnot_truth_table, pin_cnot_chain_parity, pin_cz_kickback,
     pin_bell, pin_brute_force, pin_unitarity, pin_param_shift, pin_finite_difference,
     pin_vjp_structure, pin_product_states, pin_cyclic_shift, pin_sampling,
+    pin_controlled_rotation_closed_forms, pin_controlled_rotation_brute_force,
+    pin_controlled_rotation_decomposition, pin_controlled_rotation_shift_and_fd,
+    pin_basis_embedding, pin_amplitude_embedding, pin_amplitude_embedding_gradient,
+    pin_pauli_trajectory_choices, pin_pauli_channel_average,
 ]

@@ -1,7 +1,8 @@
 """Plant plausible mistakes in copies of the oracle (CPU only) and check that the
 pin battery catches every one of them: evidence that the pins constrain each
 part of the oracle (gate matrices, orientation, expectation, adjoint sweep,
-gradient accumulation, parameter shift, shot sampling)."""
+gradient accumulation, parameter shift, shot sampling, controlled rotations,
+embeddings, Pauli-channel trajectories)."""
 
 import os
 import shutil
@@ -28,8 +29,8 @@ MUTANTS = [
     ("transposed_operand", "psi[j] = m[0] * a + m[1] * b;\n        psi[j | bit] = m[2] * a + m[3] * b;",
      "psi[j] = m[0] * a + m[2] * b;\n        psi[j | bit] = m[1] * a + m[3] * b;"),
     ("expect_sign", "return (j & c->bit) ? -p : p;", "return (j & c->bit) ? p : -p;"),
-    ("expect_wrong_qubit", "term_ctx c = { psi, NULL, (int64_t)1 << q, 0 };",
-     "term_ctx c = { psi, NULL, (int64_t)1 << (q ^ 1), 0 };"),
+    ("expect_wrong_qubit", "term_ctx c = { psi, NULL, (int64_t)1 << q, 0, 0, NULL };",
+     "term_ctx c = { psi, NULL, (int64_t)1 << (q ^ 1), 0, 0, NULL };"),
     ("no_dagger", "if (dagger) { adjoint2(m, a);", "if (0) { adjoint2(m, a);"),
     ("dagger_without_transpose", "a[0] = conj(m[0]); a[1] = conj(m[2]);\n    a[2] = conj(m[1]);",
      "a[0] = conj(m[0]); a[1] = conj(m[1]);\n    a[2] = conj(m[2]);"),
@@ -43,12 +44,12 @@ MUTANTS = [
     # psi one gate behind lambda in the inner product (un-applying both first
     # would be equivalent: a rotation commutes with its own generator)
     ("psi_lambda_misaligned",
-     "double v = im_inner(lam, psi, dim, gk->q0, gk->kind);",
-     "apply_gate(psi, dim, gk, th, 1);\n"
-     "                double v = im_inner(lam, psi, dim, gk->q0, gk->kind);\n"
-     "                apply_gate(psi, dim, gk, th, 0);"),
-    ("shift_without_half", "double d = 0.5 * (fp - fm);", "double d = (fp - fm);"),
-    ("lambda_not_unapplied", "            apply_gate(lam, dim, gk, th, 1);\n", "\n"),
+     "double v = im_inner(lam, psi, dim, gk);",
+     "apply_gate(psi, dim, gk, th, 0, 1);\n"
+     "                double v = im_inner(lam, psi, dim, gk);\n"
+     "                apply_gate(psi, dim, gk, th, 0, 0);"),
+    ("shift_without_half", "d = 0.5 * (f[0] - f[1]);", "d = (f[0] - f[1]);"),
+    ("lambda_not_unapplied", "            apply_gate(lam, dim, gk, th, which, 1);\n", "\n"),
     ("sample_ge_instead_of_gt", "if (cdf[mid] > r) hi = mid;", "if (cdf[mid] >= r) hi = mid;"),
     ("sample_off_by_one", "out[(size_t)b * (size_t)shots + (size_t)s] = lo;",
      "out[(size_t)b * (size_t)shots + (size_t)s] = lo > 0 ? lo - 1 : 0;"),
@@ -56,6 +57,24 @@ MUTANTS = [
      "acc += fabs(p[2 * j]) + fabs(p[2 * j + 1]);"),
     ("sample_unscaled_uniform", "const double r = u[(size_t)b * (size_t)shots + (size_t)s] * acc;",
      "const double r = u[(size_t)b * (size_t)shots + (size_t)s];"),
+    ("crot_ignores_control", "if ((j & bit) || (j & cmask) != cmask) continue;", "if (j & bit) continue;"),
+    ("crot_grad_all_amplitudes", "    if (c->cbit && !(j & c->cbit)) return 0.0;\n", ""),
+    ("crot_control_target_swapped", "apply_matrix(psi, dim, (int64_t)1 << g->q0, g->q1, m);",
+     "apply_matrix(psi, dim, (int64_t)1 << g->q1, g->q0, m);"),
+    ("crot_two_term_shift", "const int ns = is_crot(g[k].kind) ? 4 : 2;", "const int ns = 2;"),
+    ("four_term_second_sign", "- (r2 - 1) / (4 * r2) * (f[2] - f[3]);", "+ (r2 - 1) / (4 * r2) * (f[2] - f[3]);"),
+    ("pauli_y_sign", "else if (which == 2) { psi[j] = -I * b; psi[j | bit] = I * a; }",
+     "else if (which == 2) { psi[j] = I * b; psi[j | bit] = -I * a; }"),
+    ("pauli_x_as_z", "if (u < c1) return 1;", "if (u < c1) return 3;"),
+    ("pauli_edge_in_lower_bin", "if (u < c1) return 1;", "if (u <= c1) return 1;"),
+    ("pauli_z_on_bit0", "else psi[j | bit] = -b;", "else psi[j] = -a;"),
+    ("pauli_cumulative_missing", "const double c1 = p[0], c2 = c1 + p[1], c3 = c2 + p[2];",
+     "const double c1 = p[0], c2 = p[1], c3 = p[2];"),
+    ("basis_threshold_strict", "if (x_b[first + q] >= 0.5) idx", "if (x_b[first + q] > 0.5) idx"),
+    ("amplitude_unnormalised", "for (int64_t j = 0; j < dim; j++) psi[j] = x_b[first + j] / r;",
+     "for (int64_t j = 0; j < dim; j++) psi[j] = x_b[first + j];"),
+    ("amplitude_grad_no_projection", "2.0 / r * (creal(lam[j]) - creal(psi[j]) * L);", "2.0 / r * creal(lam[j]);"),
+    ("amplitude_grad_half", "2.0 / r * (creal(lam[j])", "1.0 / r * (creal(lam[j])"),
 ]
 
 

@@ -8,12 +8,19 @@ other.
 A circuit is an ``int32`` array of shape ``[G, 5]``; each row is one gate
 ``(kind, q0, q1, src, index)``:
 
-* ``kind``  -- ``H=0, RX=1, RY=2, RZ=3, CNOT=4, CZ=5``;
-* ``q0, q1`` -- qubits; ``q1 = -1`` for one-qubit gates, CNOT uses
-  ``q0 = control, q1 = target``;
+* ``kind``  -- ``H=0, RX=1, RY=2, RZ=3, CNOT=4, CZ=5``, controlled rotations
+  ``CRX=6, CRY=7, CRZ=8`` and Pauli-channel trajectories ``PAULI=9``;
+* ``q0, q1`` -- qubits; ``q1 = -1`` for one-qubit gates, CNOT and the
+  controlled rotations use ``q0 = control, q1 = target``;
 * ``src``   -- where a rotation angle comes from: ``NONE=0`` (H, CNOT, CZ),
   ``INPUT=1`` (feature ``index`` of the sample), ``WEIGHT=2`` (trainable
-  weight ``index``, shared by every sample).
+  weight ``index``, shared by every sample). A Pauli channel reads its
+  trajectory uniform from input feature ``index``; its probabilities
+  ``(p_x, p_y, p_z)`` are given beside the circuit, one row per channel.
+
+Initial-state embeddings: ``EMBED_NONE=0`` (|0...0>), ``EMBED_BASIS=1``
+(qubit q is 1 where feature ``first + q`` is >= 0.5), ``EMBED_AMPLITUDE=2``
+(the 2^n features from ``first`` on, normalised).
 
 The gate set and the binding of rotation angles to input features or
 trainable weights follow the quantum node of the paper (Sec. "Quantum Node":
@@ -37,9 +44,13 @@ import math
 import numpy as np
 
 H, RX, RY, RZ, CNOT, CZ = 0, 1, 2, 3, 4, 5
+CRX, CRY, CRZ, PAULI = 6, 7, 8, 9
 SRC_NONE, SRC_INPUT, SRC_WEIGHT = 0, 1, 2
-KIND_NAMES = {H: "H", RX: "RX", RY: "RY", RZ: "RZ", CNOT: "CNOT", CZ: "CZ"}
+EMBED_NONE, EMBED_BASIS, EMBED_AMPLITUDE = 0, 1, 2
+KIND_NAMES = {H: "H", RX: "RX", RY: "RY", RZ: "RZ", CNOT: "CNOT", CZ: "CZ", CRX: "CRX",
+              CRY: "CRY", CRZ: "CRZ", PAULI: "PAULI"}
 ROTATIONS = (RX, RY, RZ)
+CONTROLLED = (CRX, CRY, CRZ)
 
 
 def _g(kind, q0, q1=-1, src=SRC_NONE, index=0):
@@ -183,16 +194,23 @@ def random_circuit(n: int, n_gates: int, n_inputs: int, n_weights: int, seed: in
     gates = []
     for _ in range(n_gates):
         kind = int(kinds[rng.integers(len(kinds))])
-        if kind in (CNOT, CZ):
+        if kind in (CNOT, CZ) + CONTROLLED:
             if n < 2:
                 kind = H
             else:
                 a, b = rng.choice(n, size=2, replace=False)
-                gates.append(_g(kind, int(a), int(b)))
+                if kind in (CNOT, CZ):
+                    gates.append(_g(kind, int(a), int(b)))
+                elif n_inputs > 0 and (n_weights == 0 or rng.random() < 0.4):
+                    gates.append(_g(kind, int(a), int(b), SRC_INPUT, int(rng.integers(n_inputs))))
+                else:
+                    gates.append(_g(kind, int(a), int(b), SRC_WEIGHT, int(rng.integers(n_weights))))
                 continue
         q = int(rng.integers(n))
         if kind == H:
             gates.append(_g(H, q))
+        elif kind == PAULI:
+            gates.append(_g(PAULI, q, -1, SRC_INPUT, int(rng.integers(n_inputs))))
         else:
             use_input = n_inputs > 0 and (n_weights == 0 or rng.random() < 0.4)
             if use_input:
