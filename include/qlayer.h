@@ -58,18 +58,58 @@
 extern "C" {
 #endif
 
-/* Gate kinds. */
-enum { QL_H = 0, QL_RX = 1, QL_RY = 2, QL_RZ = 3, QL_CNOT = 4, QL_CZ = 5 };
+/* Gate kinds.
+ *
+ * QL_CRX/QL_CRY/QL_CRZ (q0 = control, q1 = target): the rotation of the
+ * target on the amplitudes whose control bit is 1, |0><0| (x) I + |1><1| (x)
+ * R(t) -- the controlled rotations of the paper's quantum autoencoder
+ * (appendix "Quantum Autoencoder"). Their gradient is exact (generator
+ * |1><1| (x) P).
+ *
+ * QL_PAULI (q0, q1 = -1, src = QL_SRC_INPUT): one quantum trajectory of a
+ * Pauli channel, the noise model of the paper's noise-inclusive simulator
+ * (Sec. "Unification of Classical and Quantum Machine"). With the channel's
+ * probabilities (p_x, p_y, p_z) (ql_circuit_desc.pauli_p) and the sample's
+ * uniform u = inputs[b][index] in [0, 1), it applies X if u < p_x, else Y if
+ * u < p_x + p_y, else Z if u < p_x + p_y + p_z, else nothing (fp64 sums in that
+ * order). The mean of <Z> over samples with independent uniforms estimates
+ * the noisy expectation; the uniform gets no gradient. */
+enum { QL_H = 0, QL_RX = 1, QL_RY = 2, QL_RZ = 3, QL_CNOT = 4, QL_CZ = 5,
+       QL_CRX = 6, QL_CRY = 7, QL_CRZ = 8, QL_PAULI = 9 };
 
-/* Where a rotation angle comes from: H/CNOT/CZ use QL_SRC_NONE; RX/RY/RZ use
- * QL_SRC_INPUT (feature `index` of each sample) or QL_SRC_WEIGHT (trainable
- * weight `index`). */
+/* Where a rotation angle comes from: H/CNOT/CZ use QL_SRC_NONE; RX/RY/RZ and
+ * the controlled rotations use QL_SRC_INPUT (feature `index` of each sample)
+ * or QL_SRC_WEIGHT (trainable weight `index`). */
 enum { QL_SRC_NONE = 0, QL_SRC_INPUT = 1, QL_SRC_WEIGHT = 2 };
 
 /* One gate. One-qubit gates use q0 and set q1 = -1. */
 typedef struct {
     int32_t kind, q0, q1, src, index;
 } ql_gate;
+
+/* Initial-state embeddings (Sec. "Quantum Data": encoding classical data into
+ * the basis state or into the amplitude vector; angle encoding is rotation
+ * gates bound to inputs).
+ *   QL_EMBED_NONE       |0...0>.
+ *   QL_EMBED_BASIS      qubit q is 1 where inputs[b][first + q] >= 0.5 (a
+ *                       direct-product basis state); no gradient.
+ *   QL_EMBED_AMPLITUDE  psi_0 = x / |x| for the 2^n real features
+ *                       x = inputs[b][first .. first + 2^n - 1] (n <= 30; a
+ *                       zero vector gives the zero state: <Z> = 0, no
+ *                       gradient). grad_inputs of those features is the VJP
+ *                       through the normalisation,
+ *                       (2 / |x|) (Re lambda_0 - psi_0 Re<psi_0|lambda_0>),
+ *                       with lambda_0 the adjoint state after the sweep. */
+enum { QL_EMBED_NONE = 0, QL_EMBED_BASIS = 1, QL_EMBED_AMPLITUDE = 2 };
+
+/* Circuit extras for ql_circuit_create_desc. pauli_p[c][3] = (p_x, p_y, p_z)
+ * of the c-th QL_PAULI gate in gate order (each >= 0, sum <= 1); read during
+ * the call only. NULL when the circuit has no Pauli channels. */
+typedef struct {
+    int32_t embedding;      /* QL_EMBED_* */
+    int32_t embed_first;    /* first input feature the embedding reads */
+    const double* pauli_p;
+} ql_circuit_desc;
 
 typedef enum { QL_C64 = 0, QL_C128 = 1 } ql_dtype;
 
@@ -116,6 +156,16 @@ int ql_circuit_create_ex(int32_t n_qubits, const ql_gate* gates, int32_t n_gates
                          int32_t n_inputs, int32_t n_weights, const ql_options* opts,
                          ql_circuit** out);
 
+/* Same with an initial-state embedding and Pauli-channel probabilities (desc
+ * NULL = no embedding, no channels) and planning options (NULL = defaults).
+ * Returns QL_EINVAL also for an embedding whose features do not fit in
+ * n_inputs, amplitude embedding above 30 qubits, a QL_PAULI gate without
+ * probabilities, or probabilities < 0 or summing above 1. Every entry point
+ * honours the embedding and the channels. */
+int ql_circuit_create_desc(int32_t n_qubits, const ql_gate* gates, int32_t n_gates,
+                           int32_t n_inputs, int32_t n_weights, const ql_circuit_desc* desc,
+                           const ql_options* opts, ql_circuit** out);
+
 void ql_circuit_destroy(ql_circuit* c);
 
 /* Bytes of device workspace a call with this dtype, batch and mode needs. */
@@ -151,7 +201,15 @@ int ql_forward_backward(const ql_circuit* c, ql_dtype dtype, int64_t batch,
  * ql_forward_backward; grad_out is required. The workspace must hold
  * ql_param_shift_workspace_bytes(c, dtype, batch, max_chunk) bytes; it grows
  * with the chunk (one state per circuit of a chunk) and with B * (2S + 1)
- * fp64 values. Results are deterministic. */
+ * fp64 values. Results are deterministic.
+ *
+ * A controlled rotation CR(t) equals R(t/2) E R(-t/2) E (E = CNOT for CRY and
+ * CRZ, CZ for CRX); its two half-angle rotations are shifted separately and
+ * their differences combined with factors +-1/2, which is exact (it equals
+ * the four-term rule for the controlled generator). Pauli channels are not
+ * shifted. With QL_EMBED_AMPLITUDE, grad_inputs must be NULL
+ * (QL_EUNSUPPORTED otherwise): the shift rule gives no gradient for
+ * amplitudes. */
 int ql_param_shift_workspace_bytes(const ql_circuit* c, ql_dtype dtype, int64_t batch,
                                    int64_t max_chunk, size_t* out);
 int ql_param_shift(const ql_circuit* c, ql_dtype dtype, int64_t batch, const void* inputs,
@@ -208,7 +266,8 @@ typedef struct {
     int32_t log_threads;   /* threads per workgroup = 2^log_threads */
     int32_t low_qubits;    /* contiguous low qubits in every tile */
     int32_t n_transposes;  /* LDS layout changes summed over the forward passes */
-    int32_t n_param_gates; /* rotation gates (gradient slots) */
+    int32_t n_param_gates; /* rotation occurrences bound to inputs or weights (S of the
+                              parameter-shift count; a controlled rotation counts 2) */
     int32_t n_lane_swaps;  /* in-register layout changes (register bit <-> lane bit) summed
                               over the forward passes */
 } ql_plan_info;
@@ -216,7 +275,10 @@ typedef struct {
 int ql_plan_info_get(const ql_circuit* c, ql_dtype dtype, ql_plan_info* out);
 
 /* Forward schedule: pass_of_gate[n_gates] receives the pass that applies each
- * gate, order[n_gates] the gate indices in execution order (pass by pass). */
+ * gate, order[n_gates] the gate indices in execution order (pass by pass).
+ * A controlled rotation or Pauli channel runs as several gates; it is
+ * reported at the pass and position of the last one (a channel with all
+ * probabilities 0 applies nothing: pass -1, listed first). */
 int ql_plan_schedule(const ql_circuit* c, ql_dtype dtype, int32_t* pass_of_gate,
                      int32_t* order);
 

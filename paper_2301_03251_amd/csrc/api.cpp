@@ -91,7 +91,7 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
         }
     }
     std::vector<SlotSrc> slots;
-    for (int gi : c.slot_gate) slots.push_back({c.gates[gi].src, c.gates[gi].index});
+    for (const Slot& sl : c.slots) slots.push_back({sl.src, sl.index, sl.axis, 0, sl.scale, sl.c1, sl.c2, sl.c3});
     std::vector<int32_t> xptr(c.n_inputs + 1, 0), wptr(c.n_weights + 1, 0), xs, ws;
     for (int f = 0; f < c.n_inputs; f++) {
         for (int s = 0; s < (int)slots.size(); s++)
@@ -124,6 +124,7 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
 
 struct Layout {
     size_t tables = 0, coef = 0, opc = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
+    size_t enorm = 0, edot = 0;  // embedding: per-circuit |x| or basis index; L_b
     int n_wg = 1;
 };
 
@@ -175,7 +176,7 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
     L.tables = off;
     off = align256(off + h->t[dt].blob.size());
     L.coef = off;
-    if (!mul_ok((size_t)B * (size_t)std::max(1, (int)c.slot_gate.size()), amp, sz)) return fail(QL_ENOMEM, "size overflow");
+    if (!mul_ok((size_t)B * (size_t)std::max(1, (int)c.slots.size()), amp, sz)) return fail(QL_ENOMEM, "size overflow");
     off = align256(off + sz);
     if (!pl.whole_state) {
         // per-sample op records (16 bytes fp32 / 32 bytes fp64) plus an end record
@@ -189,19 +190,33 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
     off = align256(off + sz);
     if (bwd) {
         L.gpart = off;
-        if (!mul_ok((size_t)B * (size_t)L.n_wg, (size_t)std::max(1, (int)c.slot_gate.size()) * 8, sz))
+        if (!mul_ok((size_t)B * (size_t)L.n_wg, (size_t)std::max(1, (int)c.slots.size()) * 8, sz))
             return fail(QL_ENOMEM, "size overflow");
         off = align256(off + sz);
     }
-    if (own_psi && !pl.whole_state && pl.passes.size() > 1) {
-        size_t st;
+    // state buffers: psi between tile passes or for an embedded initial state
+    // (the caller's buffer when own_psi is false); lambda between backward
+    // passes or for the amplitude-embedding gradient (lambda_0)
+    const bool multi = !pl.whole_state && pl.passes.size() > 1;
+    const bool emb = c.embed != E_NONE, amp_bwd = bwd && c.embed == E_AMPLITUDE;
+    size_t st = 0;
+    if ((own_psi && (multi || emb)) || (bwd && multi) || amp_bwd)
         if (!mul_ok((size_t)B, ((size_t)1 << c.n) * amp, st)) return fail(QL_ENOMEM, "size overflow");
+    if (own_psi && (multi || emb)) {
         L.psi = off;
         off = align256(off + st);
-        if (bwd) {
-            L.lam = off;
-            off = align256(off + st);
-        }
+    }
+    if ((bwd && multi) || amp_bwd) {
+        L.lam = off;
+        off = align256(off + st);
+    }
+    if (emb) {
+        L.enorm = off;
+        off = align256(off + (size_t)B * 8);
+    }
+    if (amp_bwd) {
+        L.edot = off;
+        off = align256(off + (size_t)B * 8);
     }
     L.total = off;
     return QL_OK;
@@ -282,7 +297,7 @@ int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0,
         ba.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
         ba.coef = x.W + x.L.coef;
         ba.B = B;
-        ba.n_slots = (int)x.c.slot_gate.size();
+        ba.n_slots = (int)x.c.slots.size();
         ba.F = x.c.n_inputs;
         ba.v0 = v0;
         ba.vper = vper;
@@ -309,6 +324,28 @@ int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0,
     return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("k_bind: ") + hipGetErrorString(e));
 }
 
+// Initial states of B circuits for an embedding (into psi: the caller's state
+// buffer or the workspace's). Circuit i is sample i, or sample (v0 + i) / vper
+// of a parameter-shift chunk.
+int embed(Ctx& x, int64_t B, const void* inputs, void* psi, int64_t v0, int32_t vper) {
+    if (x.c.embed == E_NONE) return QL_OK;
+    EmbedArgs ea{};
+    ea.inputs = inputs;
+    ea.psi = psi;
+    ea.norm = (double*)(x.W + x.L.enorm);
+    ea.count = B;
+    ea.v0 = v0;
+    ea.vper = vper;
+    ea.kind = x.c.embed;
+    ea.first = x.c.embed_first;
+    ea.F = x.c.n_inputs;
+    ea.n = x.c.n;
+    x.tm.start(2);
+    hipError_t e = launch_embed(x.dt, ea, x.stream);
+    x.tm.stop();
+    return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("k_embed: ") + hipGetErrorString(e));
+}
+
 // The state passes of B circuits: the whole-state kernel, or the forward tile
 // passes, the fused pass and (bwd) the backward passes. Writes the <Z> partials
 // (and, bwd, the gradient partials) of the workspace.
@@ -318,12 +355,15 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
     const size_t amp = x.dt == 0 ? 8 : 16;
     double* zpart = (double*)(x.W + x.L.zpart);
     double* gpart = bwd ? (double*)(x.W + x.L.gpart) : nullptr;
+    // an embedded initial state is in the state buffer (written by embed())
+    const bool emb = c.embed != E_NONE, amp_bwd = bwd && c.embed == E_AMPLITUDE;
+    void* psi_buf = psi_ext ? psi_ext : (x.L.psi ? (void*)(x.W + x.L.psi) : nullptr);
     if (pl.whole_state) {
         WholeArgs wa{};
         wa.gates = (const DevGate*)(x.W + x.L.tables + x.T.off_gates);
         wa.n_gates = (int)c.gates.size();
         wa.n = c.n;
-        wa.n_slots = (int)c.slot_gate.size();
+        wa.n_slots = (int)c.slots.size();
         wa.bwd = bwd ? 1 : 0;
         wa.B = B;
         wa.coef = x.W + x.L.coef;
@@ -331,6 +371,8 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         wa.zpart = zpart;
         wa.gpart = gpart;
         wa.psi_out = psi_ext;
+        wa.psi_in = emb ? psi_buf : nullptr;
+        wa.lam_out = amp_bwd ? (void*)(x.W + x.L.lam) : nullptr;
         const int dim = 1 << c.n;
         const int threads = std::max(64, std::min(256, dim / 4));
         const size_t lds = 2 * (size_t)dim * amp + (size_t)c.n * (threads / 64) * 8 + 64;
@@ -346,7 +388,7 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
     auto launch_pass = [&](int p, int flags) -> int {
         const DevPass& d = x.T.passes[p];
         TileArgs ta{};
-        ta.psi = psi_ext ? psi_ext : (x.L.psi ? (void*)(x.W + x.L.psi) : nullptr);
+        ta.psi = psi_buf;
         ta.lam = x.L.lam ? (void*)(x.W + x.L.lam) : nullptr;
         ta.pass = (const DevPass*)(x.W + x.L.tables + x.T.off_pass) + p;
         ta.phases = (const DevPhase*)(x.W + x.L.tables + x.T.off_phase);
@@ -374,17 +416,22 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         return QL_OK;
     };
     int rc;
+    // the first pass starts from |0...0> in registers unless an embedding
+    // wrote the initial state; the last backward pass stores lambda_0 when the
+    // amplitude-embedding gradient needs it
+    const int init = emb ? 0 : PF_INIT;
+    const int lam0 = amp_bwd ? PF_STORE_LAM : 0;
     for (int p = 0; p + 1 < m; p++) {
-        rc = launch_pass(p, (p == 0 ? PF_INIT : 0) | PF_FWD | PF_STORE_PSI);
+        rc = launch_pass(p, (p == 0 ? init : 0) | PF_FWD | PF_STORE_PSI);
         if (rc) return rc;
     }
-    int last = (m == 1 ? PF_INIT : 0) | PF_FWD | (psi_ext ? PF_STORE_PSI : PF_ZPART);
-    if (bwd) last |= PF_SEED | PF_BWD | (m > 1 ? (PF_STORE_PSI | PF_STORE_LAM) : 0);
+    int last = (m == 1 ? init : 0) | PF_FWD | (psi_ext ? PF_STORE_PSI : PF_ZPART);
+    if (bwd) last |= PF_SEED | PF_BWD | (m > 1 ? (PF_STORE_PSI | PF_STORE_LAM) : lam0);
     rc = launch_pass(m - 1, last);
     if (rc) return rc;
     if (bwd)
         for (int p = m - 2; p >= 0; p--) {
-            rc = launch_pass(p, PF_LOAD_LAM | PF_BWD | (p > 0 ? (PF_STORE_PSI | PF_STORE_LAM) : 0));
+            rc = launch_pass(p, PF_LOAD_LAM | PF_BWD | (p > 0 ? (PF_STORE_PSI | PF_STORE_LAM) : lam0));
             if (rc) return rc;
         }
     return QL_OK;
@@ -402,12 +449,13 @@ int reduce(Ctx& x, int64_t B, bool grads, void* expz, void* grad_inputs, void* g
     ra.x_slot = (const int32_t*)(x.W + x.L.tables + x.T.off_xslot);
     ra.w_ptr = (const int32_t*)(x.W + x.L.tables + x.T.off_wptr);
     ra.w_slot = (const int32_t*)(x.W + x.L.tables + x.T.off_wslot);
+    ra.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
     ra.B = B;
     ra.n = x.c.n;
     ra.n_wg = x.L.n_wg;
     ra.F = x.c.n_inputs;
     ra.P = x.c.n_weights;
-    ra.n_slots = (int)x.c.slot_gate.size();
+    ra.n_slots = (int)x.c.slots.size();
     ra.grads = grads ? 1 : 0;
     x.tm.start(3);
     hipError_t e = launch_reduce(x.dt, ra, x.stream);
@@ -446,8 +494,26 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
     Ctx x{h, dt, h->c, h->c.plan[dt], h->t[dt], (uint8_t*)ws, L, stream, Timer{h, stream}};
     if ((rc = upload_tables(x))) return rc;
     if ((rc = bind(x, B, inputs, weights, 0, 0))) return rc;
+    if ((rc = embed(x, B, inputs, x.L.psi ? (void*)(x.W + x.L.psi) : nullptr, 0, 0))) return rc;
     if ((rc = state_passes(x, B, bwd, grad_out))) return rc;
-    return reduce(x, B, bwd, expz, grad_inputs, grad_weights);
+    if ((rc = reduce(x, B, bwd, expz, grad_inputs, grad_weights))) return rc;
+    if (bwd && grad_inputs && h->c.embed == E_AMPLITUDE) {
+        EmbedGradArgs ga{};
+        ga.inputs = inputs;
+        ga.lam = x.W + x.L.lam;
+        ga.norm = (const double*)(x.W + x.L.enorm);
+        ga.dot = (double*)(x.W + x.L.edot);
+        ga.grad_inputs = grad_inputs;
+        ga.B = B;
+        ga.first = h->c.embed_first;
+        ga.F = h->c.n_inputs;
+        ga.n = h->c.n;
+        x.tm.start(3);
+        hipError_t e = launch_embed_grad(dt, ga, stream);
+        x.tm.stop();
+        if (e != hipSuccess) return fail(QL_EHIP, std::string("k_embed_grad: ") + hipGetErrorString(e));
+    }
+    return QL_OK;
 }
 
 // Workspace of a parameter-shift call: the forward layout of one chunk of
@@ -462,7 +528,7 @@ struct ShiftLayout {
 int shift_layout(const ql_circuit* h, int dt, int64_t B, int64_t max_chunk, ShiftLayout& S) {
     if (B < 1) return fail(QL_EINVAL, "batch must be >= 1");
     if (max_chunk < 0) return fail(QL_EINVAL, "max_chunk must be >= 0");
-    const int64_t V = 2 * (int64_t)h->c.slot_gate.size() + 1;
+    const int64_t V = 2 * (int64_t)h->c.n_param_slots + 1;
     if (B > ((int64_t)1 << 40) / V) return fail(QL_EINVAL, "batch too large");
     S.total = B * V;
     S.chunk = max_chunk > 0 ? std::min<int64_t>(max_chunk, S.total) : S.total;
@@ -491,6 +557,9 @@ int param_shift(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inp
     if (rc) return rc;
     rc = check_args(h->c, inputs, weights, expz, true, grad_out, ws);
     if (rc) return rc;
+    if (grad_inputs && h->c.embed == E_AMPLITUDE)
+        return fail(QL_EUNSUPPORTED, "parameter shift gives no gradient for amplitude-embedded features "
+                                     "(pass grad_inputs = NULL, or use ql_forward_backward)");
     if (ws_bytes < S.bytes)
         return fail(QL_ENOMEM, "workspace too small: need " + std::to_string(S.bytes) + " bytes, got " +
                                    std::to_string(ws_bytes));
@@ -498,12 +567,13 @@ int param_shift(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inp
     if (rc) return rc;
     Ctx x{h, dt, h->c, h->c.plan[dt], h->t[dt], (uint8_t*)ws, S.L, stream, Timer{h, stream}};
     if ((rc = upload_tables(x))) return rc;
-    const int32_t V = (int32_t)(2 * h->c.slot_gate.size() + 1);
+    const int32_t V = (int32_t)(2 * h->c.n_param_slots + 1);
     void* ev = x.W + S.ev;
     double* dv = (double*)(x.W + S.dv);
     for (int64_t v0 = 0; v0 < S.total; v0 += S.chunk) {
         const int64_t cb = std::min(S.chunk, S.total - v0);
         if ((rc = bind(x, cb, inputs, weights, v0, V))) return rc;
+        if ((rc = embed(x, cb, inputs, x.L.psi ? (void*)(x.W + x.L.psi) : nullptr, v0, V))) return rc;
         if ((rc = state_passes(x, cb, false, nullptr))) return rc;
         if ((rc = reduce(x, cb, false, ev, nullptr, nullptr))) return rc;
         ShiftDotArgs sa{};
@@ -528,6 +598,7 @@ int param_shift(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inp
     ga.x_slot = (const int32_t*)(x.W + x.L.tables + x.T.off_xslot);
     ga.w_ptr = (const int32_t*)(x.W + x.L.tables + x.T.off_wptr);
     ga.w_slot = (const int32_t*)(x.W + x.L.tables + x.T.off_wslot);
+    ga.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
     ga.B = B;
     ga.vper = V;
     ga.F = h->c.n_inputs;
@@ -558,8 +629,12 @@ int state(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs, c
     Ctx x{h, dt, h->c, h->c.plan[dt], h->t[dt], (uint8_t*)ws, L, stream, Timer{h, stream}};
     if ((rc = upload_tables(x))) return rc;
     if ((rc = bind(x, B, inputs, weights, 0, 0))) return rc;
+    if ((rc = embed(x, B, inputs, psi, 0, 0))) return rc;
     if ((rc = state_passes(x, B, false, nullptr, psi))) return rc;
-    if (x.pl.whole_state) return QL_OK;  // exact gates: no phase to undo
+    const int n_slots = (int)h->c.slots.size();
+    // the whole-state kernel applies exact rotations: only Pauli outcomes
+    // (applied as -i P) leave a phase
+    if (x.pl.whole_state && n_slots == h->c.n_param_slots) return QL_OK;
     BindTileArgs ba{};
     ba.inputs = inputs;
     ba.weights = weights;
@@ -569,7 +644,8 @@ int state(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs, c
     ba.n_ops = x.T.n_ops;
     ba.bwd_first = x.T.bwd_first;
     ba.F = h->c.n_inputs;
-    hipError_t e = launch_state_phase(dt, ba, (double*)(x.W + x.L.zpart), psi, h->c.n, stream);
+    hipError_t e = launch_state_phase(dt, ba, x.pl.whole_state, n_slots, (double*)(x.W + x.L.zpart), psi,
+                                      h->c.n, stream);
     return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("state phase: ") + hipGetErrorString(e));
 }
 
@@ -609,16 +685,25 @@ Options to_options(const ql_options* o) {
 
 extern "C" {
 
-int ql_circuit_create_ex(int32_t n_qubits, const ql_gate* gates, int32_t n_gates, int32_t n_inputs,
-                         int32_t n_weights, const ql_options* opts, ql_circuit** out) {
+int ql_circuit_create_desc(int32_t n_qubits, const ql_gate* gates, int32_t n_gates, int32_t n_inputs,
+                           int32_t n_weights, const ql_circuit_desc* desc, const ql_options* opts,
+                           ql_circuit** out) {
     if (!out) return fail(QL_EINVAL, "out is NULL");
     *out = nullptr;
     static_assert(sizeof(ql_gate) == 5 * sizeof(int32_t), "ql_gate layout");
+    static_assert(QL_CRX == P_CRX && QL_CRY == P_CRY && QL_CRZ == P_CRZ && QL_PAULI == P_PAULI, "kinds");
+    static_assert(QL_EMBED_BASIS == E_BASIS && QL_EMBED_AMPLITUDE == E_AMPLITUDE, "embeddings");
+    Extras ext;
+    if (desc) {
+        ext.embed = desc->embedding;
+        ext.embed_first = desc->embed_first;
+        ext.pauli_p = desc->pauli_p;
+    }
     ql_circuit* h = new (std::nothrow) ql_circuit();
     if (!h) return fail(QL_ENOMEM, "host allocation failed");
     std::string err;
     try {
-        err = build_circuit(n_qubits, (const int32_t*)gates, n_gates, n_inputs, n_weights,
+        err = build_circuit(n_qubits, (const int32_t*)gates, n_gates, n_inputs, n_weights, ext,
                             to_options(opts), h->c);
         if (err.empty())
             for (int dt = 0; dt < 2; dt++) build_tables(h->c, dt, h->t[dt]);
@@ -635,9 +720,14 @@ int ql_circuit_create_ex(int32_t n_qubits, const ql_gate* gates, int32_t n_gates
     return QL_OK;
 }
 
+int ql_circuit_create_ex(int32_t n_qubits, const ql_gate* gates, int32_t n_gates, int32_t n_inputs,
+                         int32_t n_weights, const ql_options* opts, ql_circuit** out) {
+    return ql_circuit_create_desc(n_qubits, gates, n_gates, n_inputs, n_weights, nullptr, opts, out);
+}
+
 int ql_circuit_create(int32_t n_qubits, const ql_gate* gates, int32_t n_gates, int32_t n_inputs,
                       int32_t n_weights, ql_circuit** out) {
-    return ql_circuit_create_ex(n_qubits, gates, n_gates, n_inputs, n_weights, nullptr, out);
+    return ql_circuit_create_desc(n_qubits, gates, n_gates, n_inputs, n_weights, nullptr, nullptr, out);
 }
 
 void ql_circuit_destroy(ql_circuit* h) {
@@ -776,7 +866,7 @@ int ql_plan_info_get(const ql_circuit* h, ql_dtype dtype, ql_plan_info* out) {
         r.n_transposes += pp.n_transposes;
         r.n_lane_swaps += pp.n_lane_swaps;
     }
-    r.n_param_gates = (int)h->c.slot_gate.size();
+    r.n_param_gates = h->c.n_param_slots;
     *out = r;
     return QL_OK;
 }
@@ -785,16 +875,24 @@ int ql_plan_schedule(const ql_circuit* h, ql_dtype dtype, int32_t* pass_of_gate,
     if (!h || !pass_of_gate || !order) return fail(QL_EINVAL, "NULL argument");
     if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
     const Plan& pl = h->c.plan[(int)dtype];
-    const int G = (int)h->c.gates.size();
+    // a gate as given is reported at its last piece after intake (a
+    // controlled rotation or Pauli channel becomes several gates); gates with
+    // no piece (a channel with all probabilities 0) come first, with pass -1
+    const int G = h->c.n_user_gates;
+    std::vector<int> last(G, -1);
     for (int i = 0; i < G; i++) pass_of_gate[i] = -1;
     int k = 0;
     for (int p = 0; p < (int)pl.passes.size(); p++)
         for (int gi : pl.passes[p].gates) {
-            if (k < G) order[k] = gi;
-            k++;
-            pass_of_gate[gi] = p;
+            const int u = h->c.gates[gi].user;
+            last[u] = k++;
+            pass_of_gate[u] = p;
         }
-    return k == G ? QL_OK : fail(QL_EINVAL, "schedule size mismatch");
+    std::vector<std::pair<int, int>> at;
+    for (int u = 0; u < G; u++) at.push_back({last[u], u});
+    std::sort(at.begin(), at.end());
+    for (int i = 0; i < G; i++) order[i] = at[i].second;
+    return QL_OK;
 }
 
 int ql_plan_state_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, int mode, double* out) {

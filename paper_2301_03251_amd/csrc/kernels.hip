@@ -92,14 +92,21 @@ __device__ __forceinline__ double wave_total(double v) {
 // ---------------------------------------------------------------------------
 // angle sources (shared by the binding kernels)
 
-// The bound angle of rotation slot `s` for circuit b. In a parameter-shift
+// The angle (fp64) of a rotation slot for circuit b. In a parameter-shift
 // chunk (vper > 0) circuit b is virtual circuit v = v0 + b of sample v / vper.
+// Input and weight slots: scale * bound value (scale 1, or +-1/2 for the
+// halves of a controlled rotation). Pauli-channel slots: pi when the
+// trajectory uniform selects the slot's axis, else 0 (the comparisons are in
+// fp64 against cumulative sums formed on the host).
 template <typename Real>
-__device__ __forceinline__ Real angle_of(const void* inputs, const void* weights, int F, const SlotSrc src,
-                                         int64_t b, int64_t v0, int32_t vper, int s, int64_t& bs) {
-    (void)s;
+__device__ __forceinline__ double angle_of(const void* inputs, const void* weights, int F, const SlotSrc& src,
+                                           int64_t b, int64_t v0, int32_t vper, int64_t& bs) {
     bs = vper > 0 ? (v0 + b) / vper : b;
-    return src.src == S_INPUT ? ((const Real*)inputs)[bs * F + src.index] : ((const Real*)weights)[src.index];
+    if (src.src == S_WEIGHT) return src.scale * (double)((const Real*)weights)[src.index];
+    const double v = (double)((const Real*)inputs)[bs * F + src.index];
+    if (src.src == S_INPUT) return src.scale * v;
+    const int which = v < src.c1 ? 1 : v < src.c2 ? 2 : v < src.c3 ? 3 : 0;
+    return which == src.axis ? 3.141592653589793238463 : 0.0;
 }
 
 // Parameter-shift offset of slot s in circuit b: v % vper = 2s+1 adds pi/2,
@@ -126,7 +133,7 @@ __global__ void k_bind(const BindArgs a) {
     const int s = (int)(t - b * a.n_slots);
     const SlotSrc src = a.slots[s];
     int64_t bs = b;
-    const double th = (double)angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, s, bs) +
+    const double th = angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, bs) +
                       shift_of(b, a.v0, a.vper, s);
     double sn, cs;
     sincos(0.5 * th, &sn, &cs);
@@ -228,7 +235,10 @@ __global__ void __launch_bounds__(256) k_whole(const WholeArgs a) {
     double* red = (double*)(lam + dim);  // [n][NW]
     const T2* coef = (const T2*)a.coef + b * a.n_slots;
 
-    for (int j = tid; j < dim; j += nt) psi[j] = mk<T2>((Real)(j == 0), (Real)0);
+    if (a.psi_in)
+        for (int j = tid; j < dim; j += nt) psi[j] = ((const T2*)a.psi_in)[b * dim + j];
+    else
+        for (int j = tid; j < dim; j += nt) psi[j] = mk<T2>((Real)(j == 0), (Real)0);
     __syncthreads();
     for (int gi = 0; gi < a.n_gates; ++gi) {
         const DevGate g = a.gates[gi];
@@ -287,6 +297,8 @@ __global__ void __launch_bounds__(256) k_whole(const WholeArgs a) {
         lds_gate(lam, g, c, -s, n, tid, nt);
         __syncthreads();
     }
+    if (a.lam_out)
+        for (int j = tid; j < dim; j += nt) ((T2*)a.lam_out)[b * dim + j] = lam[j];
 }
 
 // ---------------------------------------------------------------------------
@@ -1123,7 +1135,7 @@ __global__ void k_bind_tile(const BindTileArgs a) {
     if (op.slot >= 0) {
         const SlotSrc src = a.slots[op.slot];
         int64_t bs;
-        double th = (double)angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, op.slot, bs) +
+        double th = angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, bs) +
                     shift_of(b, a.v0, a.vper, op.slot);
         const double two_pi = 6.283185307179586476925;
         th -= two_pi * rint(th / two_pi);  // [-pi, pi]; the dropped sign is common to psi and lambda
@@ -1170,7 +1182,8 @@ __global__ void __launch_bounds__(256) k_reduce(const ReduceArgs a) {
         const int f = (int)(u - b * a.F);
         for (int i = a.x_ptr[f]; i < a.x_ptr[f + 1]; ++i) {
             const int s = a.x_slot[i];
-            for (int w = lane; w < a.n_wg; w += 64) acc += a.gpart[((size_t)s * a.B + b) * a.n_wg + w];
+            const double sc = a.slots[s].scale;
+            for (int w = lane; w < a.n_wg; w += 64) acc += sc * a.gpart[((size_t)s * a.B + b) * a.n_wg + w];
         }
         acc = wave_sum(acc);
         if (lane == 0) ((Real*)a.grad_inputs)[u] = (Real)acc;
@@ -1179,7 +1192,8 @@ __global__ void __launch_bounds__(256) k_reduce(const ReduceArgs a) {
         const int64_t per = a.B * a.n_wg;
         for (int i = a.w_ptr[p]; i < a.w_ptr[p + 1]; ++i) {
             const double* src = a.gpart + (size_t)a.w_slot[i] * per;
-            for (int64_t j = lane; j < per; j += 64) acc += src[j];
+            const double sc = a.slots[a.w_slot[i]].scale;
+            for (int64_t j = lane; j < per; j += 64) acc += sc * src[j];
         }
         acc = wave_sum(acc);
         if (lane == 0) ((Real*)a.grad_weights)[p] = (Real)acc;
@@ -1219,7 +1233,7 @@ __global__ void __launch_bounds__(256) k_shift_grad(const ShiftGradArgs a) {
         for (int i = lane; i < cnt; i += 64) {
             const int s = a.x_slot[a.x_ptr[f] + i];
             const double* d = a.dv + b * a.vper;
-            acc += 0.5 * (d[2 * s + 1] - d[2 * s + 2]);
+            acc += a.slots[s].scale * 0.5 * (d[2 * s + 1] - d[2 * s + 2]);
         }
         acc = wave_sum(acc);
         if (lane == 0) ((Real*)a.grad_inputs)[e] = (Real)acc;
@@ -1231,7 +1245,7 @@ __global__ void __launch_bounds__(256) k_shift_grad(const ShiftGradArgs a) {
             const int64_t b = j / cnt;
             const int s = a.w_slot[a.w_ptr[p] + (int)(j - b * cnt)];
             const double* d = a.dv + b * a.vper;
-            acc += 0.5 * (d[2 * s + 1] - d[2 * s + 2]);
+            acc += a.slots[s].scale * 0.5 * (d[2 * s + 1] - d[2 * s + 2]);
         }
         acc = wave_sum(acc);
         if (lane == 0) ((Real*)a.grad_weights)[p] = (Real)acc;
@@ -1249,20 +1263,31 @@ __global__ void __launch_bounds__(256) k_shift_grad(const ShiftGradArgs a) {
 // state by the inverse phase.
 
 template <typename Real>
-__global__ void k_state_phase(const BindTileArgs a, double* phase) {
+__global__ void k_state_phase(const BindTileArgs a, int whole, int n_slots, double* phase) {
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= a.B) return;
     const double pi = 3.141592653589793238463, two_pi = 2.0 * pi;
     double ph = 0.0;
+    int64_t bs;
+    if (whole) {
+        // exact rotations; a Pauli outcome P was applied as R(pi) = -i P
+        for (int s = 0; s < n_slots; ++s) {
+            const SlotSrc src = a.slots[s];
+            if (src.src == S_PAULI && angle_of<Real>(a.inputs, a.weights, a.F, src, b, 0, 0, bs) != 0.0)
+                ph -= 0.5 * pi;
+        }
+        phase[b] = ph;
+        return;
+    }
     for (int o = 0; o < a.bwd_first; ++o) {
         const DevOp op = a.ops[o];
         if (op.slot < 0) continue;
         const SlotSrc src = a.slots[op.slot];
-        int64_t bs;
-        const double th = (double)angle_of<Real>(a.inputs, a.weights, a.F, src, b, 0, 0, op.slot, bs);
+        const double th = angle_of<Real>(a.inputs, a.weights, a.F, src, b, 0, 0, bs);
         const double k = rint(th / two_pi);
         ph += pi * k;
         if (op.h >= H_G1 + 15 && op.h < H_G1 + 20) ph += 0.5 * (th - two_pi * k);
+        if (src.src == S_PAULI && th != 0.0) ph -= 0.5 * pi;
     }
     phase[b] = ph;
 }
@@ -1279,6 +1304,100 @@ __global__ void k_phase_fix(void* psi, const double* phase, int64_t B, int n) {
         v.x = (decltype(v.x))(x * cs - y * sn);
         v.y = (decltype(v.y))(x * sn + y * cs);
         ((T2*)psi)[i] = v;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// initial-state embeddings
+
+// Sum of 256 per-thread fp64 values in a fixed tree order (thread 0 returns it).
+__device__ __forceinline__ double block_sum256(double v, double* red) {
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    return red[0];
+}
+
+// Per circuit (one 256-thread workgroup each): amplitude embedding |x| of the
+// 2^n features, basis embedding the basis index (exact in fp64).
+template <typename Real>
+__global__ void __launch_bounds__(256) k_embed_norm(const EmbedArgs a) {
+    __shared__ double red[256];
+    const int64_t i = blockIdx.x;
+    const int64_t bs = a.vper > 0 ? (a.v0 + i) / a.vper : i;
+    const Real* x = (const Real*)a.inputs + bs * a.F + a.first;
+    if (a.kind == E_BASIS) {
+        if (threadIdx.x == 0) {
+            int64_t idx = 0;
+            for (int q = 0; q < a.n; ++q)
+                if ((double)x[q] >= 0.5) idx |= (int64_t)1 << q;
+            a.norm[i] = (double)idx;
+        }
+        return;
+    }
+    const int64_t dim = (int64_t)1 << a.n;
+    double acc = 0.0;
+    for (int64_t j = threadIdx.x; j < dim; j += 256) {
+        const double v = (double)x[j];
+        acc = fma(v, v, acc);
+    }
+    const double t = block_sum256(acc, red);
+    if (threadIdx.x == 0) a.norm[i] = sqrt(t);
+}
+
+// psi_0 of every circuit, grid-stride over count * 2^n amplitudes.
+template <typename Real>
+__global__ void __launch_bounds__(256) k_embed_write(const EmbedArgs a) {
+    using T2 = typename Cx<Real>::T;
+    const int64_t dim = (int64_t)1 << a.n, total = a.count << a.n;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = t >> a.n, j = t & (dim - 1);
+        const double r = a.norm[i];
+        Real re;
+        if (a.kind == E_BASIS) {
+            re = (Real)(j == (int64_t)r);
+        } else {
+            const int64_t bs = a.vper > 0 ? (a.v0 + i) / a.vper : i;
+            const Real v = ((const Real*)a.inputs)[bs * a.F + a.first + j];
+            re = r > 0 ? (Real)((double)v / r) : (Real)0;
+        }
+        ((T2*)a.psi)[t] = mk<T2>(re, (Real)0);
+    }
+}
+
+// L_b = sum_j x_j Re lam_j / |x| (one 256-thread workgroup per sample).
+template <typename Real>
+__global__ void __launch_bounds__(256) k_embed_dot(const EmbedGradArgs a) {
+    using T2 = typename Cx<Real>::T;
+    __shared__ double red[256];
+    const int64_t b = blockIdx.x;
+    const int64_t dim = (int64_t)1 << a.n;
+    const Real* x = (const Real*)a.inputs + b * a.F + a.first;
+    const T2* lam = (const T2*)a.lam + b * dim;
+    double acc = 0.0;
+    for (int64_t j = threadIdx.x; j < dim; j += 256) acc = fma((double)x[j], (double)lam[j].x, acc);
+    const double t = block_sum256(acc, red);
+    if (threadIdx.x == 0) a.dot[b] = a.norm[b] > 0 ? t / a.norm[b] : 0.0;
+}
+
+// grad_inputs[b][first + j] += (2 / |x|) (Re lam_j - (x_j / |x|) L_b).
+template <typename Real>
+__global__ void __launch_bounds__(256) k_embed_grad(const EmbedGradArgs a) {
+    using T2 = typename Cx<Real>::T;
+    const int64_t dim = (int64_t)1 << a.n, total = a.B << a.n;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t b = t >> a.n, j = t & (dim - 1);
+        const double r = a.norm[b];
+        if (!(r > 0)) continue;
+        const double x = (double)((const Real*)a.inputs)[b * a.F + a.first + j];
+        const double g = 2.0 / r * ((double)((const T2*)a.lam)[t].x - x / r * a.dot[b]);
+        Real* out = (Real*)a.grad_inputs + b * a.F + a.first + j;
+        *out = (Real)((double)*out + g);
     }
 }
 
@@ -1521,6 +1640,34 @@ hipError_t launch_shift_dot(int dtype, const ShiftDotArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+hipError_t launch_embed(int dtype, const EmbedArgs& a, hipStream_t s) {
+    if (a.count <= 0) return hipSuccess;
+    const int64_t total = a.count << a.n;
+    const int grid = (int)std::min<int64_t>((total + 255) / 256, 65536);
+    if (dtype == 0) {
+        hipLaunchKernelGGL(k_embed_norm<float>, dim3((unsigned)a.count), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_embed_write<float>, dim3(grid), dim3(256), 0, s, a);
+    } else {
+        hipLaunchKernelGGL(k_embed_norm<double>, dim3((unsigned)a.count), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_embed_write<double>, dim3(grid), dim3(256), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_embed_grad(int dtype, const EmbedGradArgs& a, hipStream_t s) {
+    if (a.B <= 0) return hipSuccess;
+    const int64_t total = a.B << a.n;
+    const int grid = (int)std::min<int64_t>((total + 255) / 256, 65536);
+    if (dtype == 0) {
+        hipLaunchKernelGGL(k_embed_dot<float>, dim3((unsigned)a.B), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_embed_grad<float>, dim3(grid), dim3(256), 0, s, a);
+    } else {
+        hipLaunchKernelGGL(k_embed_dot<double>, dim3((unsigned)a.B), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_embed_grad<double>, dim3(grid), dim3(256), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s) {
     const int64_t waves = (a.grad_inputs ? a.B * a.F : 0) + (a.grad_weights ? a.P : 0);
     if (waves == 0) return hipSuccess;
@@ -1530,16 +1677,17 @@ hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, void* psi, int n,
-                              hipStream_t s) {
+hipError_t launch_state_phase(int dtype, const BindTileArgs& a, bool whole, int n_slots, double* phase,
+                              void* psi, int n, hipStream_t s) {
     const unsigned g1 = (unsigned)((a.B + 255) / 256);
     const int64_t total = a.B << n;
     const unsigned g2 = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
+    const int w = whole ? 1 : 0;
     if (dtype == 0) {
-        hipLaunchKernelGGL(k_state_phase<float>, dim3(g1), dim3(256), 0, s, a, phase);
+        hipLaunchKernelGGL(k_state_phase<float>, dim3(g1), dim3(256), 0, s, a, w, n_slots, phase);
         hipLaunchKernelGGL(k_phase_fix<float2>, dim3(g2), dim3(256), 0, s, psi, (const double*)phase, a.B, n);
     } else {
-        hipLaunchKernelGGL(k_state_phase<double>, dim3(g1), dim3(256), 0, s, a, phase);
+        hipLaunchKernelGGL(k_state_phase<double>, dim3(g1), dim3(256), 0, s, a, w, n_slots, phase);
         hipLaunchKernelGGL(k_phase_fix<double2>, dim3(g2), dim3(256), 0, s, psi, (const double*)phase, a.B, n);
     }
     return hipGetLastError();

@@ -9,9 +9,15 @@
 
 namespace qlayer {
 
-// Rotation slot -> (src, index); one row per slot.
+// Angle source of a rotation slot; one row per slot. Input/weight slots:
+// angle = scale * value. Pauli-channel slots (src S_PAULI): angle pi when the
+// uniform input feature `index` selects `axis` (1 X if u < c1, 2 Y if u < c2,
+// 3 Z if u < c3), else 0.
 struct SlotSrc {
     int32_t src, index;
+    int32_t axis, pad;
+    double scale;
+    double c1, c2, c3;
 };
 
 // Whole-state (one workgroup per sample, state in LDS) gate entry.
@@ -67,6 +73,7 @@ struct ShiftGradArgs {
     const int32_t* x_slot;
     const int32_t* w_ptr;
     const int32_t* w_slot;
+    const SlotSrc* slots;  // scales of the rotation slots
     int64_t B;
     int32_t vper, F, P;
 };
@@ -81,6 +88,34 @@ struct WholeArgs {
     double* zpart;        // [B][n]           (one workgroup per sample)
     double* gpart;        // [n_slots][B]
     void* psi_out;        // [B][2^n] complex: the final state, or null
+    const void* psi_in;   // [B][2^n] complex: the initial state, or null for |0...0>
+    void* lam_out;        // [B][2^n] complex: lambda after the backward sweep, or null
+};
+
+// Initial-state embeddings: circuit i of a call (sample i, or sample
+// (v0 + i) / vper of a parameter-shift chunk) starts from the basis state of
+// features first..first+n-1 (>= 0.5 is a 1) or from x / |x| over the 2^n
+// features from `first` on.
+struct EmbedArgs {
+    const void* inputs;   // [B][F] Real
+    void* psi;            // [count][2^n] complex
+    double* norm;         // [count]: |x| (amplitude embedding)
+    int64_t count;        // circuits
+    int64_t v0;
+    int32_t vper;         // 0: circuit i is sample i
+    int32_t kind, first, F, n;
+};
+
+// Amplitude-embedding VJP: grad_inputs[b][first + j] += (2 / |x|) (Re lam_j -
+// psi0_j L_b) with L_b = sum_j psi0_j Re lam_j (dot: [B] fp64 scratch).
+struct EmbedGradArgs {
+    const void* inputs;   // [B][F] Real
+    const void* lam;      // [B][2^n] complex: lambda_0
+    const double* norm;   // [B]
+    double* dot;          // [B]
+    void* grad_inputs;    // [B][F] Real
+    int64_t B;
+    int32_t first, F, n;
 };
 
 // Shot sampling from states psi[B][2^n]: blocks of 2^bb amplitudes, each
@@ -122,6 +157,7 @@ struct ReduceArgs {
     const int32_t* x_slot;
     const int32_t* w_ptr;  // [P+1] CSR: rotation slots bound to weight p
     const int32_t* w_slot;
+    const SlotSrc* slots;  // scales of the rotation slots
     int64_t B;
     int32_t n, n_wg, F, P, n_slots;
     int32_t grads;         // 1: reduce gradients too
@@ -144,10 +180,14 @@ hipError_t launch_tile(int dtype, int log_r, bool bwd, const TileArgs& a, int th
 hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_shift_dot(int dtype, const ShiftDotArgs& a, hipStream_t s);
 hipError_t launch_sample(int dtype, const SampleArgs& a, hipStream_t s);
-// Undo the per-sample global phase the tile kernel leaves on final states
-// (phase: [B] fp64 scratch).
-hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, void* psi, int n,
-                              hipStream_t s);
+// Undo the per-sample global phase the kernels leave on final states
+// (phase: [B] fp64 scratch). Tile path: the ops' phases; whole-state path
+// (whole = true, a.ops unused): only the Pauli-channel rotations' -i each,
+// over the n_slots slots.
+hipError_t launch_state_phase(int dtype, const BindTileArgs& a, bool whole, int n_slots, double* phase,
+                              void* psi, int n, hipStream_t s);
+hipError_t launch_embed(int dtype, const EmbedArgs& a, hipStream_t s);
+hipError_t launch_embed_grad(int dtype, const EmbedGradArgs& a, hipStream_t s);
 hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s);
 
 // Raise the dynamic-LDS limit of every kernel on the current device.

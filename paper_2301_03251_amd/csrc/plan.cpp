@@ -399,44 +399,112 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
 int whole_state_max_qubits(int dtype) { return dtype == 0 ? 12 : 11; }
 
 std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, int n_weights,
-                          const Options& opts, Circuit& out) {
+                          const Extras& ext, const Options& opts, Circuit& out) {
     if (n < 1 || n > 32) return fmt("n_qubits=%ld out of range [1, 32]", n);
     if (n_gates < 0) return "n_gates < 0";
     if (n_gates > 0 && !g5) return "gates is NULL";
     if (n_inputs < 0 || n_weights < 0) return "negative n_inputs or n_weights";
-    if (n_gates > (1 << 24)) return "too many gates";
+    if (n_gates > (1 << 22)) return "too many gates";
     out = Circuit{};
     out.n = n;
     out.n_inputs = n_inputs;
     out.n_weights = n_weights;
+    out.n_user_gates = n_gates;
     out.opts = opts;
-    for (int i = 0; i < n_gates; i++) {
-        Gate g{g5[5 * i], g5[5 * i + 1], g5[5 * i + 2], g5[5 * i + 3], g5[5 * i + 4], -1};
-        if (g.kind < K_H || g.kind > K_CZ) return fmt("gate %ld: unknown kind %ld", i, g.kind);
-        if (g.q0 < 0 || g.q0 >= n) return fmt("gate %ld: qubit %ld out of range", i, g.q0);
-        if (g.kind == K_CNOT || g.kind == K_CZ) {
-            if (g.q1 < 0 || g.q1 >= n) return fmt("gate %ld: qubit %ld out of range", i, g.q1);
-            if (g.q1 == g.q0) return fmt("gate %ld: q0 == q1 == %ld", i, g.q0);
-        } else if (g.q1 != -1) {
-            return fmt("gate %ld: one-qubit gate needs q1 = -1 (got %ld)", i, g.q1);
-        }
-        if (is_rotation(g.kind)) {
-            if (g.src == S_INPUT) {
-                if (g.index < 0 || g.index >= n_inputs)
-                    return fmt("gate %ld: input index %ld out of range [0, %ld)", i, g.index, n_inputs);
-            } else if (g.src == S_WEIGHT) {
-                if (g.index < 0 || g.index >= n_weights)
-                    return fmt("gate %ld: weight index %ld out of range [0, %ld)", i, g.index, n_weights);
-            } else {
-                return fmt("gate %ld: rotation needs src INPUT or WEIGHT (got %ld)", i, g.src);
-            }
-            g.slot = (int)out.slot_gate.size();
-            out.slot_gate.push_back(i);
-        } else if (g.src != S_NONE) {
-            return fmt("gate %ld: H/CNOT/CZ take no angle source (got %ld)", i, g.src);
-        }
-        out.gates.push_back(g);
+    out.embed = ext.embed;
+    out.embed_first = ext.embed_first;
+    if (ext.embed == E_BASIS) {
+        if (ext.embed_first < 0 || (int64_t)ext.embed_first + n > n_inputs)
+            return fmt("basis embedding needs features [%ld, %ld + n) within n_inputs = %ld", ext.embed_first,
+                       ext.embed_first, n_inputs);
+    } else if (ext.embed == E_AMPLITUDE) {
+        if (n > AMPLITUDE_MAX_QUBITS) return fmt("amplitude embedding supports at most %ld qubits", AMPLITUDE_MAX_QUBITS);
+        if (ext.embed_first < 0 || (int64_t)ext.embed_first + ((int64_t)1 << n) > n_inputs)
+            return fmt("amplitude embedding needs features [%ld, %ld + 2^n) within n_inputs = %ld",
+                       ext.embed_first, ext.embed_first, n_inputs);
+    } else if (ext.embed != E_NONE) {
+        return fmt("unknown embedding %ld", ext.embed);
     }
+    // rotation occurrences in gate order; numbered below (trainable first)
+    std::vector<Slot> pending_slots;
+    std::vector<int> slot_of_gate;  // per internal gate: pending slot or -1
+    int user = 0;                   // gate as given being rewritten
+    auto emit = [&](int kind, int q0, int q1, const Slot* sl) {
+        out.gates.push_back(Gate{kind, q0, q1, sl ? sl->src : (int)S_NONE, sl ? sl->index : 0, -1, user});
+        slot_of_gate.push_back(sl ? (int)pending_slots.size() : -1);
+        if (sl) pending_slots.push_back(*sl);
+    };
+    int n_channels = 0;
+    for (int i = 0; i < n_gates; i++) {
+        user = i;
+        const int kind = g5[5 * i], q0 = g5[5 * i + 1], q1 = g5[5 * i + 2], src = g5[5 * i + 3],
+                  index = g5[5 * i + 4];
+        if (kind < K_H || kind > P_PAULI) return fmt("gate %ld: unknown kind %ld", i, kind);
+        if (q0 < 0 || q0 >= n) return fmt("gate %ld: qubit %ld out of range", i, q0);
+        const bool two = kind == K_CNOT || kind == K_CZ || kind == P_CRX || kind == P_CRY || kind == P_CRZ;
+        if (two) {
+            if (q1 < 0 || q1 >= n) return fmt("gate %ld: qubit %ld out of range", i, q1);
+            if (q1 == q0) return fmt("gate %ld: q0 == q1 == %ld", i, q0);
+        } else if (q1 != -1) {
+            return fmt("gate %ld: one-qubit gate needs q1 = -1 (got %ld)", i, q1);
+        }
+        const bool angled = is_rotation(kind) || kind == P_CRX || kind == P_CRY || kind == P_CRZ;
+        if (angled) {
+            if (src == S_INPUT) {
+                if (index < 0 || index >= n_inputs)
+                    return fmt("gate %ld: input index %ld out of range [0, %ld)", i, index, n_inputs);
+            } else if (src == S_WEIGHT) {
+                if (index < 0 || index >= n_weights)
+                    return fmt("gate %ld: weight index %ld out of range [0, %ld)", i, index, n_weights);
+            } else {
+                return fmt("gate %ld: rotation needs src INPUT or WEIGHT (got %ld)", i, src);
+            }
+        } else if (kind == P_PAULI) {
+            if (src != S_INPUT || index < 0 || index >= n_inputs)
+                return fmt("gate %ld: Pauli channel needs src INPUT and an input index in [0, %ld)", i, n_inputs);
+        } else if (src != S_NONE) {
+            return fmt("gate %ld: H/CNOT/CZ take no angle source (got %ld)", i, src);
+        }
+        if (kind <= K_CZ) {
+            Slot sl{src, index, 1.0, 0, 0, 0, 0};
+            emit(kind, q0, q1, is_rotation(kind) ? &sl : nullptr);
+        } else if (kind == P_PAULI) {
+            if (!ext.pauli_p) return fmt("gate %ld: Pauli channel without probabilities", i);
+            const double* p = ext.pauli_p + 3 * n_channels++;
+            if (!(p[0] >= 0 && p[1] >= 0 && p[2] >= 0 && p[0] + p[1] + p[2] <= 1.0))
+                return fmt("gate %ld: Pauli probabilities must be >= 0 with sum <= 1", i);
+            Slot sl{S_PAULI, index, 1.0, 0, p[0], p[0] + p[1], p[0] + p[1] + p[2]};
+            // one rotation by pi per axis that can occur: RX(pi), RY(pi), RZ(pi)
+            // are -i X, -i Y, -i Z
+            for (int ax = 1; ax <= 3; ax++)
+                if (p[ax - 1] > 0) {
+                    sl.axis = ax;
+                    emit(ax == 1 ? K_RX : ax == 2 ? K_RY : K_RZ, q0, -1, &sl);
+                }
+        } else {
+            // controlled rotation CR(t) on (control q0, target q1) as
+            // R(t/2) E R(-t/2) E with E = CNOT(q0, q1) for RY and RZ (X R(a) X =
+            // R(-a)) and E = CZ(q0, q1) for RX (Z RX(a) Z = RX(-a))
+            const int rot = kind == P_CRX ? K_RX : kind == P_CRY ? K_RY : K_RZ;
+            const int ent = kind == P_CRX ? K_CZ : K_CNOT;
+            Slot hp{src, index, 0.5, 0, 0, 0, 0}, hm{src, index, -0.5, 0, 0, 0, 0};
+            emit(rot, q1, -1, &hp);
+            emit(ent, q0, q1, nullptr);
+            emit(rot, q1, -1, &hm);
+            emit(ent, q0, q1, nullptr);
+        }
+    }
+    // slot numbers: input/weight slots in gate order, then Pauli slots
+    std::vector<int> num(pending_slots.size(), -1);
+    for (int pass = 0; pass < 2; pass++)
+        for (size_t s = 0; s < pending_slots.size(); s++)
+            if ((pending_slots[s].src == S_PAULI) == (pass == 1)) {
+                num[s] = (int)out.slots.size();
+                out.slots.push_back(pending_slots[s]);
+                if (pass == 0) out.n_param_slots++;
+            }
+    for (size_t i = 0; i < out.gates.size(); i++)
+        if (slot_of_gate[i] >= 0) out.gates[i].slot = num[slot_of_gate[i]];
     const Options& o = opts;
     if (o.log_regs && (o.log_regs < 2 || o.log_regs > MAX_LOG_R)) return "option: log_regs out of range [2, 5]";
     if (o.log_threads && (o.log_threads < 6 || o.log_threads > 9)) return "option: log_threads out of range [6, 9]";
@@ -453,7 +521,7 @@ std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, i
 std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
     pl = Plan{};
     pl.n = c.n;
-    pl.n_slots = (int)c.slot_gate.size();
+    pl.n_slots = (int)c.slots.size();
     const Options& o = c.opts;
     // The register-tile kernel needs at least 2^8 amplitudes per tile; below
     // that, or when asked (force_tiled < 0) and the state fits in LDS, the

@@ -23,12 +23,30 @@
 
 namespace qlayer {
 
+// Gate kinds the planner and kernels run. The public kinds 6..9 (controlled
+// rotations, Pauli-channel trajectories) are rewritten into these at intake.
 enum GateKind { K_H = 0, K_RX = 1, K_RY = 2, K_RZ = 3, K_CNOT = 4, K_CZ = 5 };
-enum Src { S_NONE = 0, S_INPUT = 1, S_WEIGHT = 2 };
+enum PublicKind { P_CRX = 6, P_CRY = 7, P_CRZ = 8, P_PAULI = 9 };
+// Angle sources of rotation slots; S_PAULI marks a trajectory slot (angle pi
+// or 0 from a uniform input feature).
+enum Src { S_NONE = 0, S_INPUT = 1, S_WEIGHT = 2, S_PAULI = 3 };
+enum Embed { E_NONE = 0, E_BASIS = 1, E_AMPLITUDE = 2 };
+
+// One rotation occurrence after intake. Input and weight slots have angle
+// scale * value; a Pauli-channel slot has angle pi when the uniform u (input
+// feature `index`) selects its axis (X if u < c1, Y if u < c2, Z if u < c3)
+// and 0 otherwise.
+struct Slot {
+    int32_t src, index;
+    double scale;
+    int32_t axis;        // Pauli slots: 1 X, 2 Y, 3 Z
+    double c1, c2, c3;   // Pauli slots: cumulative probabilities
+};
 
 struct Gate {
     int32_t kind, q0, q1, src, index;
     int32_t slot;  // rotation slot (coefficient + gradient), -1 otherwise
+    int32_t user;  // index of the gate as given that this gate came from
 };
 
 // Operand location relative to the current tile phase.
@@ -160,17 +178,31 @@ struct Plan {
     int n_slots = 0;           // rotation slots
 };
 
+// Intake extras: the initial-state embedding and the Pauli-channel
+// probabilities ([channels][3], in gate order).
+struct Extras {
+    int embed = E_NONE, embed_first = 0;
+    const double* pauli_p = nullptr;
+};
+
 struct Circuit {
     int n = 0, n_inputs = 0, n_weights = 0;
-    std::vector<Gate> gates;
-    std::vector<int> slot_gate;  // rotation slot -> gate index
+    int embed = E_NONE, embed_first = 0;
+    std::vector<Gate> gates;     // after intake: kinds H..CZ only
+    std::vector<Slot> slots;     // rotation slots: trainable ones first, then Pauli ones
+    int n_param_slots = 0;       // slots bound to inputs or weights
+    int n_user_gates = 0;        // gates as given
     Options opts;
     Plan plan[2];                // per dtype (0 = c64, 1 = c128)
 };
 
-// Validate and copy gates, assign rotation slots. Returns "" or an error.
+// Validate and copy gates, rewrite controlled rotations and Pauli channels
+// into rotations and CNOT/CZ, assign rotation slots. Returns "" or an error.
 std::string build_circuit(int n, const int32_t* gates5, int n_gates, int n_inputs,
-                          int n_weights, const Options& opts, Circuit& out);
+                          int n_weights, const Extras& ext, const Options& opts, Circuit& out);
+
+// Largest qubit count for amplitude embedding (2^n features per sample).
+constexpr int AMPLITUDE_MAX_QUBITS = 30;
 
 // Build the plan for one dtype. Returns "" or an error message.
 std::string build_plan(const Circuit& c, int dtype, Plan& out);

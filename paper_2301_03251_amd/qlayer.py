@@ -18,6 +18,9 @@ LIB_PATH = os.path.join(_HERE, "libqlayer.so")
 
 C64, C128 = 0, 1
 MODE_FWD, MODE_FWD_BWD = 0, 1
+H, RX, RY, RZ, CNOT, CZ, CRX, CRY, CRZ, PAULI = range(10)
+SRC_NONE, SRC_INPUT, SRC_WEIGHT = 0, 1, 2
+EMBED_NONE, EMBED_BASIS, EMBED_AMPLITUDE = 0, 1, 2
 DTYPES = {"c64": C64, "c128": C128}
 ERRORS = {-1: "QL_EINVAL", -2: "QL_ENOMEM", -3: "QL_EUNSUPPORTED", -4: "QL_EHIP"}
 
@@ -34,6 +37,11 @@ class _Options(ctypes.Structure):
                                               "wg_per_sample")]
 
 
+class _Desc(ctypes.Structure):
+    _fields_ = [("embedding", ctypes.c_int32), ("embed_first", ctypes.c_int32),
+                ("pauli_p", ctypes.c_void_p)]
+
+
 class _PlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "n_passes", "tile_qubits", "log_regs",
                                               "log_threads", "low_qubits", "n_transposes",
@@ -41,7 +49,7 @@ class _PlanInfo(ctypes.Structure):
 
 
 _lib = None
-EXPORTS = ("ql_circuit_create", "ql_circuit_create_ex", "ql_circuit_destroy",
+EXPORTS = ("ql_circuit_create", "ql_circuit_create_ex", "ql_circuit_create_desc", "ql_circuit_destroy",
            "ql_workspace_bytes", "ql_forward", "ql_forward_backward", "ql_last_error",
            "ql_param_shift_workspace_bytes", "ql_param_shift", "ql_state_workspace_bytes",
            "ql_state", "ql_sample_workspace_bytes", "ql_sample",
@@ -62,6 +70,8 @@ def load():
     lib.ql_circuit_create.argtypes = [I32, P, I32, I32, I32, ctypes.POINTER(P)]
     lib.ql_circuit_create_ex.argtypes = [I32, P, I32, I32, I32, ctypes.POINTER(_Options),
                                          ctypes.POINTER(P)]
+    lib.ql_circuit_create_desc.argtypes = [I32, P, I32, I32, I32, ctypes.POINTER(_Desc),
+                                           ctypes.POINTER(_Options), ctypes.POINTER(P)]
     lib.ql_circuit_destroy.argtypes = [P]
     lib.ql_circuit_destroy.restype = None
     lib.ql_workspace_bytes.argtypes = [P, ctypes.c_int, I64, ctypes.c_int, ctypes.POINTER(SZ)]
@@ -81,7 +91,8 @@ def load():
                                         ctypes.POINTER(ctypes.c_double)]
     lib.ql_timing_enable.argtypes = [P, ctypes.c_int]
     lib.ql_timing_read.argtypes = [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I32)]
-    for name in ("ql_circuit_create", "ql_circuit_create_ex", "ql_workspace_bytes", "ql_forward",
+    for name in ("ql_circuit_create", "ql_circuit_create_ex", "ql_circuit_create_desc",
+                 "ql_workspace_bytes", "ql_forward",
                  "ql_forward_backward", "ql_param_shift_workspace_bytes", "ql_param_shift",
                  "ql_state_workspace_bytes", "ql_state", "ql_sample_workspace_bytes", "ql_sample",
                  "ql_plan_info_get", "ql_plan_schedule",
@@ -101,19 +112,31 @@ def _dt(dtype):
 
 
 class Circuit:
-    """A validated gate list with its pass plans (``ql_circuit_create_ex``)."""
+    """A validated gate list with its pass plans (``ql_circuit_create_desc``).
 
-    def __init__(self, n_qubits, gates, n_inputs, n_weights, **options):
+    ``embed = (kind, first)`` selects an initial-state embedding (``EMBED_*``)
+    reading features from ``first`` on; ``pauli_p[c] = (p_x, p_y, p_z)`` are
+    the probabilities of the c-th ``PAULI`` gate. Other keyword arguments are
+    planning options (``ql_options`` fields).
+    """
+
+    def __init__(self, n_qubits, gates, n_inputs, n_weights, embed=None, pauli_p=None, **options):
         lib = load()
         g = np.ascontiguousarray(np.asarray(gates, dtype=np.int32).reshape(-1, 5))
         self.n = int(n_qubits)
         self.gates = g
         self.n_inputs, self.n_weights = int(n_inputs), int(n_weights)
         opts = _Options(**{k: int(v) for k, v in options.items()})
+        pp = None
+        if pauli_p is not None:
+            pp = np.ascontiguousarray(np.asarray(pauli_p, dtype=np.float64).reshape(-1, 3))
+        kind, first = (EMBED_NONE, 0) if embed is None else (int(embed[0]), int(embed[1]))
+        self.embed = (kind, first)
+        desc = _Desc(kind, first, None if pp is None else pp.ctypes.data_as(ctypes.c_void_p))
         h = ctypes.c_void_p()
-        _check(lib.ql_circuit_create_ex(self.n, g.ctypes.data_as(ctypes.c_void_p), g.shape[0],
-                                        self.n_inputs, self.n_weights, ctypes.byref(opts),
-                                        ctypes.byref(h)))
+        _check(lib.ql_circuit_create_desc(self.n, g.ctypes.data_as(ctypes.c_void_p), g.shape[0],
+                                          self.n_inputs, self.n_weights, ctypes.byref(desc),
+                                          ctypes.byref(opts), ctypes.byref(h)))
         self._h = h
 
     def close(self):

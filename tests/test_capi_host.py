@@ -57,7 +57,11 @@ G1 = [[W.RY, 0, -1, W.SRC_WEIGHT, 0]]
     ([[W.RX, 0, -1, W.SRC_NONE, 0]], 3, 0, 1, -1),       # rotation without source
     ([[W.RZ, 0, -1, W.SRC_INPUT, 2]], 3, 2, 0, -1),      # input index out of range
     ([[W.RZ, 0, -1, W.SRC_WEIGHT, -1]], 3, 0, 1, -1),    # negative weight index
-    ([[9, 0, -1, 0, 0]], 3, 0, 0, -1),                   # unknown kind
+    ([[10, 0, -1, 0, 0]], 3, 0, 0, -1),                  # unknown kind
+    ([[W.CRY, 1, 1, W.SRC_WEIGHT, 0]], 3, 0, 1, -1),     # controlled rotation with q0 == q1
+    ([[W.CRX, 0, 1, W.SRC_NONE, 0]], 3, 0, 1, -1),       # controlled rotation without source
+    ([[W.CRZ, 0, -1, W.SRC_WEIGHT, 0]], 3, 0, 1, -1),    # controlled rotation without target
+    ([[W.PAULI, 0, -1, W.SRC_WEIGHT, 0]], 3, 0, 1, -1),  # channel uniform must be an input
     ([[W.RY, 0, 1, W.SRC_WEIGHT, 0]], 3, 0, 1, -1),      # one-qubit gate with q1
     (G1, 0, 0, 1, -1),                                   # n = 0
     (G1, 33, 0, 1, -1),                                  # n = 33
@@ -173,7 +177,7 @@ def _check_schedule(c, gates, dtype):
     # gates that share a qubit keep their relative order
     last = {}
     for i, g in enumerate(gates):
-        qs = [int(g[1])] + ([int(g[2])] if g[0] in (W.CNOT, W.CZ) else [])
+        qs = [int(g[1])] + ([int(g[2])] if g[0] in (W.CNOT, W.CZ) + W.CONTROLLED else [])
         for q in qs:
             if q in last:
                 assert pos[last[q]] < pos[i], f"gate {i} overtakes gate {last[q]} on qubit {q}"
@@ -218,3 +222,63 @@ def test_pass_counts_are_small(lib):
         wl = W.get(name)
         c = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
         assert c.plan_info("c64")["n_passes"] <= limit, name
+
+
+# ---------------------------------------------------------------------------
+# controlled rotations, embeddings, Pauli channels (host side)
+
+def _desc_err(n, gates, F, P, **kw):
+    return _err(lambda: Q.Circuit(n, np.asarray(gates, np.int32), F, P, **kw))
+
+
+def test_extension_validation(lib):
+    pauli = [[W.PAULI, 0, -1, W.SRC_INPUT, 0]]
+    assert _desc_err(2, pauli, 1, 0) == -1                                  # no probabilities
+    assert _desc_err(2, pauli, 1, 0, pauli_p=[[-0.1, 0, 0]]) == -1          # negative
+    assert _desc_err(2, pauli, 1, 0, pauli_p=[[0.5, 0.4, 0.2]]) == -1       # sum above 1
+    Q.Circuit(2, np.asarray(pauli, np.int32), 1, 0, pauli_p=[[0.5, 0.25, 0.25]])
+    assert _desc_err(3, G1, 2, 1, embed=(W.EMBED_BASIS, 0)) == -1           # 3 features needed
+    assert _desc_err(3, G1, 5, 1, embed=(W.EMBED_BASIS, 3)) == -1
+    Q.Circuit(3, np.asarray(G1, np.int32), 5, 1, embed=(W.EMBED_BASIS, 2))
+    assert _desc_err(3, G1, 8, 1, embed=(W.EMBED_AMPLITUDE, 1)) == -1       # 2^3 from feature 1
+    assert _desc_err(3, G1, 9, 1, embed=(W.EMBED_AMPLITUDE, -1)) == -1
+    Q.Circuit(3, np.asarray(G1, np.int32), 9, 1, embed=(W.EMBED_AMPLITUDE, 1))
+    assert _desc_err(3, G1, 9, 1, embed=(7, 0)) == -1                       # unknown embedding
+
+
+def test_extension_slot_counts(lib):
+    """A controlled rotation is two trainable half-angle rotations; Pauli
+    channels add no trainable slot."""
+    gates = np.asarray([[W.CRX, 0, 1, W.SRC_WEIGHT, 0], [W.CRY, 1, 2, W.SRC_INPUT, 0],
+                        [W.CRZ, 2, 0, W.SRC_WEIGHT, 1], [W.RX, 1, -1, W.SRC_WEIGHT, 1],
+                        [W.PAULI, 2, -1, W.SRC_INPUT, 1], [W.PAULI, 0, -1, W.SRC_INPUT, 2]], np.int32)
+    c = Q.Circuit(3, gates, 3, 2, pauli_p=[[0.1, 0.0, 0.2], [0.0, 0.0, 0.0]])
+    for dt in ("c64", "c128"):
+        assert c.plan_info(dt)["n_param_gates"] == 7
+        pog, order = c.schedule(dt)
+        assert pog[5] == -1 and order[0] == 5          # a channel with all p = 0 applies nothing
+        assert sorted(order.tolist()) == list(range(6))
+    qae = W.get("qae")
+    cq = Q.Circuit(qae.n, qae.gates(), qae.n_inputs, qae.n_weights, embed=qae.embed)
+    assert qae.n_weights == 60 and cq.plan_info("c64")["n_param_gates"] == 24 + 2 * 36
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_extension_schedules(lib, seed):
+    n = 9 + seed
+    kinds = (W.H, W.RX, W.RY, W.RZ, W.CNOT, W.CZ, W.CRX, W.CRY, W.CRZ)
+    gates = W.random_circuit(n, 120, 4, 6, seed=300 + seed, kinds=kinds)
+    gates, pp, nch = W.with_depolarizing(gates, n, 4, 0.05, every=17)
+    for opts in (dict(), dict(force_tiled=1, log_regs=3, log_threads=6)):
+        c = Q.Circuit(n, gates, 4 + nch, 6, pauli_p=pp, **opts)
+        for dt in ("c64", "c128"):
+            _check_schedule(c, gates, dt)
+
+
+def test_param_shift_rejects_amplitude_input_grads(lib):
+    n, F = 3, 8
+    c = Q.Circuit(n, np.asarray(G1, np.int32), F, 1, embed=(W.EMBED_AMPLITUDE, 0))
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    need = c.param_shift_workspace_bytes("c64", 2, 0)
+    assert _err(lambda: c.param_shift_raw("c64", 2, fake, fake, fake, fake, fake, None, 0, fake,
+                                          need, None)) == -3

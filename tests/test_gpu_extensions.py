@@ -1,0 +1,218 @@
+"""Controlled rotations, initial-state embeddings and Pauli-channel trajectories:
+HIP path vs the CPU oracle through the C ABI (needs an MI355X).
+
+Same tolerances as the core parity tests: 1e-5 absolute for complex64, 1e-12
+for complex128, on <Z_i>, input gradients and weight gradients (and on exact
+final states). The oracle applies controlled rotations, embeddings and Pauli
+outcomes directly; the library rewrites them into its own gate set.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+torch = pytest.importorskip("torch")
+import paper_2301_03251_amd as Q  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"c64": 1e-5, "c128": 1e-12}
+CR_KINDS = (W.H, W.RX, W.RY, W.RZ, W.CNOT, W.CZ, W.CRX, W.CRY, W.CRZ)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    Q.load()
+
+
+def _dev(a, dtype):
+    real = torch.float32 if dtype == "c64" else torch.float64
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=real)
+
+
+def _host(a, dtype):
+    """The values the GPU receives, as the oracle's fp64 inputs."""
+    return np.asarray(a, np.float32 if dtype == "c64" else np.float64).astype(np.float64)
+
+
+def gpu_fb(circ, dtype, x, w, g):
+    e, gx, gw = Q.Runner(circ, dtype).forward_backward(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype))
+    torch.cuda.synchronize()
+    return {"expz": e.cpu().double().numpy(), "grad_inputs": gx.cpu().double().numpy(),
+            "grad_weights": gw.cpu().double().numpy()}
+
+
+def check(got, want, tol, what, keys=("expz", "grad_inputs", "grad_weights")):
+    for k in keys:
+        a, b = np.asarray(got[k], np.float64), np.asarray(want[k], np.float64)
+        assert a.shape == b.shape, f"{what} {k}: shape {a.shape} vs {b.shape}"
+        err = float(np.max(np.abs(a - b))) if a.size else 0.0
+        assert err <= tol, f"{what} {k}: max abs err {err:.3e} > {tol:.0e}"
+
+
+# (n, dtype, options): whole state, small register tiles, default tiles
+CASES = [
+    (3, "c128", dict()),
+    (6, "c64", dict()),
+    (10, "c64", dict(force_tiled=-1)),
+    (9, "c64", dict(force_tiled=1, log_regs=3, log_threads=6)),
+    (11, "c128", dict(force_tiled=1, log_regs=3, log_threads=7, low_qubits=3)),
+    (13, "c64", dict()),
+    (14, "c128", dict()),
+    (15, "c64", dict(log_regs=5, log_threads=7, wg_per_sample=3)),
+]
+IDS = [f"n{c[0]}-{c[1]}-{'-'.join(f'{k}{v}' for k, v in c[2].items()) or 'default'}" for c in CASES]
+
+
+@pytest.mark.parametrize("n,dtype,opts", CASES, ids=IDS)
+def test_controlled_rotations_vs_oracle(n, dtype, opts):
+    F, P, B = 4, 6, 3
+    gates = W.random_circuit(n, 10 * n, F, P, seed=1100 + n, kinds=CR_KINDS)
+    x, w, g = W.random_inputs(B, F, P, n, seed=1200 + n, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P, **opts)
+    want = oracle.run(n, gates, _host(x, dtype), _host(w, dtype), grad_out=_host(g, dtype))
+    check(gpu_fb(circ, dtype, x, w, g), want, TOL[dtype], f"crot n={n} {dtype} {opts}")
+
+
+@pytest.mark.parametrize("n,dtype", [(5, "c128"), (9, "c64"), (13, "c128")])
+def test_controlled_rotations_param_shift(n, dtype):
+    """GPU parameter shift (two half-angle occurrences per controlled rotation)
+    against the oracle's four-term rule."""
+    F, P, B = 3, 4, 2
+    gates = W.random_circuit(n, 6 * n, F, P, seed=1300 + n, kinds=CR_KINDS)
+    x, w, g = W.random_inputs(B, F, P, n, seed=1400 + n, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P)
+    e, gx, gw = Q.Runner(circ, dtype).param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), max_chunk=64)
+    torch.cuda.synchronize()
+    xh, wh, gh = _host(x, dtype), _host(w, dtype), _host(g, dtype)
+    ox, ow = oracle.param_shift(n, gates, xh, wh, gh)
+    want = {"expz": oracle.run(n, gates, xh, wh)["expz"], "grad_inputs": ox, "grad_weights": ow}
+    got = {"expz": e.cpu().double().numpy(), "grad_inputs": gx.cpu().double().numpy(),
+           "grad_weights": gw.cpu().double().numpy()}
+    check(got, want, TOL[dtype], f"crot shift n={n} {dtype}")
+
+
+def _embedded_case(n, kind, dtype, seed, B=3, F0=3, P=5):
+    """Random circuit plus F0 angle features and the embedding's features."""
+    rng = np.random.default_rng(seed)
+    gates = W.random_circuit(n, 8 * n, F0, P, seed=seed, kinds=CR_KINDS)
+    x, w, g = W.random_inputs(B, F0, P, n, seed=seed + 1, dtype=dtype)
+    if kind == W.EMBED_BASIS:
+        feats = rng.integers(0, 2, size=(B, n)).astype(np.float64)
+        feats[0, :2] = [0.5, 0.49]      # the threshold itself, and just below it
+    else:
+        feats = rng.standard_normal((B, 1 << n))
+    rdt = x.dtype
+    return gates, np.concatenate([x, feats.astype(rdt)], axis=1), w, g, (kind, F0)
+
+
+@pytest.mark.parametrize("kind", [W.EMBED_BASIS, W.EMBED_AMPLITUDE], ids=["basis", "amplitude"])
+@pytest.mark.parametrize("n,dtype,opts", CASES, ids=IDS)
+def test_embeddings_vs_oracle(kind, n, dtype, opts):
+    gates, x, w, g, emb = _embedded_case(n, kind, dtype, seed=1500 + 3 * n + kind)
+    circ = Q.Circuit(n, gates, x.shape[1], w.size, embed=emb, **opts)
+    want = oracle.run(n, gates, _host(x, dtype), _host(w, dtype), grad_out=_host(g, dtype), embed=emb)
+    check(gpu_fb(circ, dtype, x, w, g), want, TOL[dtype], f"embed {kind} n={n} {dtype} {opts}")
+
+
+def test_amplitude_embedding_zero_vector():
+    n, dtype = 9, "c64"
+    gates, x, w, g, emb = _embedded_case(n, W.EMBED_AMPLITUDE, dtype, seed=1600)
+    x[1, emb[1]:] = 0
+    got = gpu_fb(Q.Circuit(n, gates, x.shape[1], w.size, embed=emb), dtype, x, w, g)
+    assert np.all(got["expz"][1] == 0) and np.all(got["grad_inputs"][1] == 0)
+    want = oracle.run(n, gates, _host(x, dtype), _host(w, dtype), grad_out=_host(g, dtype), embed=emb)
+    check(got, want, TOL[dtype], "zero vector")
+
+
+def _noisy_case(n, dtype, seed, B=4, p=0.3):
+    F, P = 3, 5
+    base = W.random_circuit(n, 6 * n, F, P, seed=seed, kinds=CR_KINDS)
+    gates, pp, nch = W.with_depolarizing(base, n, F, p, every=max(1, (6 * n) // 3))
+    rng = np.random.default_rng(seed + 2)
+    pp[:, 0] *= rng.uniform(0.2, 1.5, nch)       # unequal X, Y, Z probabilities
+    x, w, g = W.random_inputs(B, F, P, n, seed=seed + 1, dtype=dtype)
+    u = rng.random((B, nch)).astype(x.dtype)
+    return gates, pp, np.concatenate([x, u], axis=1), w, g
+
+
+@pytest.mark.parametrize("n,dtype,opts", CASES, ids=IDS)
+def test_pauli_trajectories_vs_oracle(n, dtype, opts):
+    """Each sample is one trajectory: the same uniforms give the same Paulis on
+    both sides, so <Z> and gradients agree element by element."""
+    gates, pp, x, w, g = _noisy_case(n, dtype, seed=1700 + n)
+    circ = Q.Circuit(n, gates, x.shape[1], w.size, pauli_p=pp, **opts)
+    want = oracle.run(n, gates, _host(x, dtype), _host(w, dtype), grad_out=_host(g, dtype), pauli_p=pp)
+    check(gpu_fb(circ, dtype, x, w, g), want, TOL[dtype], f"pauli n={n} {dtype} {opts}")
+
+
+def test_depolarizing_average():
+    """RY(t) then a depolarizing channel of strength p on one qubit: the mean of
+    <Z> over many trajectories approaches (1 - 4p/3) cos t (X and Y flip Z,
+    Z keeps it); 2^16 trajectories, five standard errors."""
+    p, t, B = 0.3, 0.8, 1 << 16
+    gates = np.asarray([[W.RY, 0, -1, W.SRC_WEIGHT, 0], [W.PAULI, 0, -1, W.SRC_INPUT, 0]], np.int32)
+    u = np.random.default_rng(5).random((B, 1))
+    circ = Q.Circuit(1, gates, 1, 1, pauli_p=[[p / 3, p / 3, p / 3]])
+    e = Q.Runner(circ, "c128").forward(_dev(u, "c128"), _dev([t], "c128"))
+    torch.cuda.synchronize()
+    z = e.cpu().numpy()[:, 0]
+    assert set(np.round(np.abs(z), 12)) == {round(abs(np.cos(t)), 12)}
+    se = np.abs(np.cos(t)) / np.sqrt(B)
+    assert abs(z.mean() - (1 - 4 * p / 3) * np.cos(t)) <= 5 * se
+
+
+@pytest.mark.parametrize("n,dtype,opts", [(4, "c128", dict()), (9, "c64", dict()),
+                                          (13, "c64", dict()), (14, "c128", dict())])
+def test_state_with_extensions(n, dtype, opts):
+    """Exact final states (global phase included) with an amplitude embedding,
+    controlled rotations and Pauli trajectories."""
+    gates, pp, x, w, _ = _noisy_case(n, dtype, seed=1800 + n, B=3)
+    feats = np.random.default_rng(n).standard_normal((3, 1 << n)).astype(x.dtype)
+    xe = np.concatenate([x, feats], axis=1)
+    emb = (W.EMBED_AMPLITUDE, x.shape[1])
+    r = Q.Runner(Q.Circuit(n, gates, xe.shape[1], w.size, embed=emb, pauli_p=pp, **opts), dtype)
+    psi = r.state(_dev(xe, dtype), _dev(w, dtype))
+    torch.cuda.synchronize()
+    want = oracle.run(n, gates, _host(xe, dtype), _host(w, dtype), want_state=True, embed=emb,
+                      pauli_p=pp)["state"]
+    err = float(np.max(np.abs(psi.cpu().numpy().astype(np.complex128) - want)))
+    assert err <= TOL[dtype], f"state n={n} {dtype}: {err:.3e}"
+
+
+def test_param_shift_with_embeddings():
+    """Basis embedding: shift gradients equal the oracle's adjoint; amplitude
+    embedding: weight gradients by shift, input gradients refused."""
+    n, dtype = 10, "c128"
+    gates, x, w, g, emb = _embedded_case(n, W.EMBED_BASIS, dtype, seed=1900)
+    r = Q.Runner(Q.Circuit(n, gates, x.shape[1], w.size, embed=emb), dtype)
+    e, gx, gw = r.param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), max_chunk=128)
+    torch.cuda.synchronize()
+    want = oracle.run(n, gates, x, w, grad_out=g, embed=emb)
+    check({"expz": e.cpu().numpy(), "grad_inputs": gx.cpu().numpy(), "grad_weights": gw.cpu().numpy()},
+          want, 1e-11, "basis shift")
+    gates, x, w, g, emb = _embedded_case(n, W.EMBED_AMPLITUDE, dtype, seed=1901)
+    r = Q.Runner(Q.Circuit(n, gates, x.shape[1], w.size, embed=emb), dtype)
+    e, _, gw = r.param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), want_inputs=False)
+    torch.cuda.synchronize()
+    want = oracle.run(n, gates, x, w, grad_out=g, embed=emb)
+    check({"expz": e.cpu().numpy(), "grad_weights": gw.cpu().numpy()}, want, 1e-11, "amplitude shift",
+          keys=("expz", "grad_weights"))
+    with pytest.raises(Q.QLError):
+        r.param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype))
+
+
+def test_qae_workload():
+    """The 7-qubit autoencoder workload at full batch against the oracle."""
+    wl = W.get("qae")
+    x, w, g = wl.inputs()
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, embed=wl.embed)
+    want = oracle.run(wl.n, wl.gates(), _host(x, wl.dtype), _host(w, wl.dtype), grad_out=_host(g, wl.dtype),
+                      embed=wl.embed)
+    check(gpu_fb(circ, wl.dtype, x, w, g), want, TOL[wl.dtype], "qae")

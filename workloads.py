@@ -178,7 +178,101 @@ WORKLOADS = {
 }
 
 
-def get(name: str) -> Workload:
+@dataclasses.dataclass(frozen=True)
+class QAEWorkload:
+    """The quantum-autoencoder layer of the paper's appendix ("Quantum
+    Autoencoder"): 7 qubits = 4 training qubits (0..3), of which 2 are trash
+    (2, 3), plus 1 auxiliary (4) and 2 reference (5, 6) qubits; 60 weights =
+    a Rot on each training qubit (12), a controlled Rot on every ordered pair
+    of training qubits (12 pairs, 36), and a Rot on each training qubit (12).
+    Rot(a, b, c) is RZ(a), RY(b), RZ(c) in that order; the controlled Rot is
+    CRZ, CRY, CRZ with the pair's first qubit as control.
+
+    Input states: the paper compresses ground states of Hubbard and molecular
+    Hamiltonians, which are not available; seeded random real 16-dimensional
+    states on the training qubits stand in for them, given as an amplitude
+    embedding of 2^7 features (zero off the training subspace). Output: <Z>
+    of every qubit; the trash qubits' <Z> give the compression cost
+    sum_t (1 - <Z_t>) / 2 (the swap test against |0> references measures the
+    same populations)."""
+    name: str = "qae7_b256_c64"
+    n: int = 7
+    batch: int = 256
+    dtype: str = "c64"
+    seed: int = 107
+    n_train: int = 4
+
+    @property
+    def n_inputs(self) -> int:
+        return 1 << self.n
+
+    @property
+    def n_weights(self) -> int:
+        t = self.n_train
+        return 3 * t + 3 * t * (t - 1) + 3 * t
+
+    @property
+    def embed(self):
+        return (EMBED_AMPLITUDE, 0)
+
+    def gates(self) -> np.ndarray:
+        t = self.n_train
+        gates, w = [], 0
+        for rng_ in ("begin", "pairs", "end"):
+            if rng_ == "pairs":
+                for c in range(t):
+                    for q in range(t):
+                        if c == q:
+                            continue
+                        for kind in (CRZ, CRY, CRZ):
+                            gates.append(_g(kind, c, q, SRC_WEIGHT, w))
+                            w += 1
+            else:
+                for q in range(t):
+                    for kind in (RZ, RY, RZ):
+                        gates.append(_g(kind, q, -1, SRC_WEIGHT, w))
+                        w += 1
+        return np.asarray(gates, dtype=np.int32).reshape(-1, 5)
+
+    @property
+    def n_gates(self) -> int:
+        return int(self.gates().shape[0])
+
+    def updates(self) -> int:
+        """3 * G * B * 2^n with G the gates as listed (a controlled rotation is one)."""
+        return 3 * self.n_gates * self.batch * (1 << self.n)
+
+    def inputs(self):
+        """Seeded ``(inputs[B, 2^n], weights[60], grad_out[B, n])``: a standard
+        normal 16-vector per sample in features 0..15 (normalised by the
+        embedding), weights U[-pi, pi], grad_out = u / B with u ~ U[-1, 1]."""
+        rng = np.random.default_rng(self.seed)
+        B, n = self.batch, self.n
+        x = np.zeros((B, 1 << n))
+        x[:, :1 << self.n_train] = rng.standard_normal((B, 1 << self.n_train))
+        w = rng.uniform(-math.pi, math.pi, size=self.n_weights)
+        g = rng.uniform(-1.0, 1.0, size=(B, n)) / B
+        rdt = np.float32 if self.dtype == "c64" else np.float64
+        return x.astype(rdt), w.astype(rdt), g.astype(rdt)
+
+
+def with_depolarizing(gates, n_qubits: int, n_inputs: int, p: float, every: int = 1):
+    """Insert a depolarizing-channel trajectory (X, Y, Z with p/3 each) on every
+    qubit after every ``every``-th gate. Channel c reads its uniform from input
+    feature ``n_inputs + c``. Returns ``(gates, pauli_p, n_channels)``."""
+    out, pp = [], []
+    for i, g in enumerate(np.asarray(gates).tolist()):
+        out.append(g)
+        if (i + 1) % every == 0:
+            for q in range(n_qubits):
+                out.append(_g(PAULI, q, -1, SRC_INPUT, n_inputs + len(pp)))
+                pp.append([p / 3, p / 3, p / 3])
+    return np.asarray(out, dtype=np.int32).reshape(-1, 5), np.asarray(pp, dtype=np.float64).reshape(-1, 3), len(pp)
+
+
+def get(name: str):
+    if name == "qae":
+        return QAEWorkload()
     return WORKLOADS[name]
 
 
