@@ -35,33 +35,37 @@ ALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 # Algorithmic flops per amplitude, each gate in its cheapest exact form: RX/RY
 # rotate a real plane per pair of components, 6 flops per amplitude; RZ is, up
 # to a global phase, a complex multiply of the bit-1 half of the amplitudes,
-# 3 flops per amplitude; H is 4; CNOT/CZ are permutations/signs (0). One step
-# applies every gate once (forward) and un-applies it on psi and lambda
-# (backward); each rotation also takes a gradient term Im<lambda|P|psi>
-# (4 flops per amplitude).
-FLOPS_FWD = {W.H: 4, W.RX: 6, W.RY: 6, W.RZ: 3, W.CNOT: 0, W.CZ: 0}
-FLOPS_GRAD = 4
+# 3 flops per amplitude; H is 4; CNOT/CZ are permutations/signs (0); a
+# controlled rotation is its rotation on the control-1 half; a Pauli-channel
+# outcome is a permutation/sign (0). One step applies every gate once
+# (forward) and un-applies it on psi and lambda (backward); each rotation also
+# takes a gradient term Im<lambda|P|psi> (4 flops per amplitude, 2 for a
+# controlled one).
+FLOPS_FWD = {W.H: 4, W.RX: 6, W.RY: 6, W.RZ: 3, W.CNOT: 0, W.CZ: 0, W.CRX: 3, W.CRY: 3, W.CRZ: 1.5,
+             W.PAULI: 0}
+FLOPS_GRAD = {W.RX: 4, W.RY: 4, W.RZ: 4, W.CRX: 2, W.CRY: 2, W.CRZ: 2}
 
 
-def algorithmic_flops(wl) -> float:
+def algorithmic_flops(gates, batch, n) -> float:
     per_amp = 0
-    for g in wl.gates():
+    for g in gates:
         k = int(g[0])
-        per_amp += 3 * FLOPS_FWD[k] + (FLOPS_GRAD if k in W.ROTATIONS else 0)
-    return float(per_amp) * wl.batch * (1 << wl.n)
+        per_amp += 3 * FLOPS_FWD[k] + FLOPS_GRAD.get(k, 0)
+    return float(per_amp) * batch * (1 << n)
 
 
-def shift_circuits(wl) -> int:
+def shift_circuits(gates, batch) -> int:
     """Circuits one parameter-shift VJP runs: per sample the unshifted circuit
-    and two shifted copies per rotation gate."""
-    rot = sum(1 for g in wl.gates() if int(g[0]) in W.ROTATIONS)
-    return wl.batch * (2 * rot + 1)
+    and two shifted copies per rotation occurrence (a controlled rotation is
+    two half-angle rotations)."""
+    rot = sum(1 if int(g[0]) in W.ROTATIONS else 2 if int(g[0]) in W.CONTROLLED else 0 for g in gates)
+    return batch * (2 * rot + 1)
 
 
-def shift_flops(wl) -> float:
+def shift_flops(gates, batch, n) -> float:
     """Algorithmic flops of one parameter-shift VJP: forward passes only."""
-    per_amp = sum(FLOPS_FWD[int(g[0])] for g in wl.gates())
-    return float(per_amp) * shift_circuits(wl) * (1 << wl.n)
+    per_amp = sum(FLOPS_FWD[int(g[0])] for g in gates)
+    return float(per_amp) * shift_circuits(gates, batch) * (1 << n)
 
 
 def profiled_traffic(wl):
@@ -77,21 +81,22 @@ def profiled_traffic(wl):
     return float(fields["traffic_bytes_per_step"])
 
 
-def cpu_baseline(wl, n_gates: int):
+def cpu_baseline(wl, gates, x, w, g, pauli_p, n_gates: int):
     """The CPU oracle (complex128, all host threads) on a bounded sample of the
     same workload: the first `n_gates` gates of the circuit at full size, one
     sample, forward + adjoint."""
     import oracle
-    x, w, g = wl.inputs()
-    gates = wl.gates()[:n_gates]
+    sub = gates[:n_gates]
+    n_ch = int(sum(1 for gg in sub if int(gg[0]) == W.PAULI))
+    pp = None if pauli_p is None else pauli_p[:max(n_ch, 1)]
     oracle.build()
     t0 = time.perf_counter()
-    oracle.run(wl.n, gates, x[:1], w, grad_out=g[:1])
+    oracle.run(wl.n, sub, x[:1], w, grad_out=g[:1], embed=getattr(wl, "embed", None), pauli_p=pp)
     dt = time.perf_counter() - t0
     upd = 3.0 * n_gates * (1 << wl.n)
     return {"value": upd / dt, "unit": "amplitude-gate updates/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"first {n_gates} of {wl.n_gates} gates of {wl.name}, batch row 0 of "
+            "sample": f"first {n_gates} of {len(gates)} gates of {wl.name}, batch row 0 of "
                       f"{wl.batch}, n={wl.n}, complex128, forward + adjoint; {dt:.2f} s"}
 
 
@@ -100,7 +105,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="30q", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--workload", default="30q", choices=sorted(W.WORKLOADS) + ["qae"])
+    ap.add_argument("--noise", type=float, default=0.0,
+                    help="depolarizing probability p: a Pauli-channel trajectory on every qubit "
+                         "after every --noise-every gates, one trajectory per sample")
+    ap.add_argument("--noise-every", type=int, default=1)
     ap.add_argument("--cpu-gates", type=int, default=8,
                     help="gates in the CPU-oracle sample (0 disables it)")
     ap.add_argument("--no-timing", action="store_true",
@@ -131,8 +140,15 @@ def main():
 
     wl = W.get(args.workload)
     x, w, g = wl.inputs()
+    gates, pauli_p, n_in = wl.gates(), None, wl.n_inputs
+    if args.noise > 0:
+        gates, pauli_p, n_ch = W.with_depolarizing(gates, wl.n, wl.n_inputs, args.noise, args.noise_every)
+        u = np.random.default_rng(wl.seed + 1000).random((wl.batch, n_ch)).astype(x.dtype)
+        x = np.concatenate([x, u], axis=1)
+        n_in = x.shape[1]
     opts = {kv.split("=")[0]: int(kv.split("=")[1]) for kv in args.opt}
-    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, **opts)
+    circ = Q.Circuit(wl.n, gates, n_in, wl.n_weights, embed=getattr(wl, "embed", None), pauli_p=pauli_p,
+                     **opts)
     runner = Q.Runner(circ, wl.dtype)
     real = torch.float32 if wl.dtype == "c64" else torch.float64
     dev = torch.device("cuda")
@@ -140,11 +156,14 @@ def main():
     wt = torch.from_numpy(w).to(dev, real)
     gt = torch.from_numpy(g).to(dev, real)
     outs = (torch.empty((wl.batch, wl.n), dtype=real, device=dev),
-            torch.empty((wl.batch, wl.n_inputs), dtype=real, device=dev),
+            torch.empty((wl.batch, n_in), dtype=real, device=dev),
             torch.empty(wl.n_weights, dtype=real, device=dev))
     shift = args.grad == "shift"
+    if shift and getattr(wl, "embed", (W.EMBED_NONE, 0))[0] == W.EMBED_AMPLITUDE:
+        outs = (outs[0], None, outs[2])  # the shift rule gives no amplitude gradient
     amp = 8 if wl.dtype == "c64" else 16
-    chunk = args.shift_chunk or max(1, min(shift_circuits(wl), (8 << 30) // ((1 << wl.n) * amp)))
+    n_shift = shift_circuits(gates, wl.batch)
+    chunk = args.shift_chunk or max(1, min(n_shift, (8 << 30) // ((1 << wl.n) * amp)))
     if args.shots > 0:
         uni = torch.from_numpy(np.random.default_rng(7).random((wl.batch, args.shots))).to(dev)
         step = lambda: Q.sample(runner.state(xt, wt), uni)  # noqa: E731
@@ -179,12 +198,13 @@ def main():
     circ.timing(False)
 
     info = circ.plan_info(wl.dtype)
-    U = wl.updates()
+    G = int(gates.shape[0])
+    U = 3 * G * wl.batch * (1 << wl.n)
     if shift:
         # amplitude-gate updates the parameter-shift VJP performs
-        U = shift_circuits(wl) * wl.n_gates * (1 << wl.n)
+        U = n_shift * G * (1 << wl.n)
     if args.shots > 0:
-        U = wl.n_gates * wl.batch * (1 << wl.n)  # forward only
+        U = G * wl.batch * (1 << wl.n)  # forward only
     line = {
         "metric": ("amplitude-gate updates/s (final states + shot sampling)" if args.shots > 0 else
                    "amplitude-gate updates/s (batched parameter-shift grad)" if shift else METRIC),
@@ -200,31 +220,36 @@ def main():
         "dtype": wl.dtype,
         "data": "synthetic",
         "config": {"workload": wl.name, "n_qubits": wl.n, "batch": wl.batch,
-                   "gates": wl.n_gates, "weights": wl.n_weights,
+                   "gates": G, "weights": wl.n_weights,
                    "updates_per_step": U, "tile_passes": info["n_passes"],
                    "tile_qubits": info["tile_qubits"], "planner_options": opts},
     }
+    if getattr(wl, "embed", None):
+        line["config"]["embedding"] = {W.EMBED_BASIS: "basis", W.EMBED_AMPLITUDE: "amplitude"}[wl.embed[0]]
+    if args.noise > 0:
+        line["config"]["noise"] = {"model": "depolarizing trajectories", "p": args.noise,
+                                   "every": args.noise_every, "channels": int(pauli_p.shape[0])}
     if args.shots > 0:
         line["config"].update({"measurement": "shots", "shots": args.shots})
         line["shots_per_s"] = args.shots * wl.batch * 1e3 / ms_step
     elif shift:
-        line["config"].update({"grad": "parameter shift", "circuits_per_step": shift_circuits(wl),
+        line["config"].update({"grad": "parameter shift", "circuits_per_step": n_shift,
                                "chunk": chunk})
         line["vjp_per_s"] = 1e3 / ms_step
     if timing and kcnt[0] > 0:
         tile_ms = kms[0] / args.steps
         if args.shots > 0:
             state_bytes = circ.state_bytes(wl.dtype, wl.batch, Q.MODE_FWD) + (1 << wl.n) * wl.batch * amp
-            flops = sum(FLOPS_FWD[int(g_[0])] for g_ in wl.gates()) * wl.batch * float(1 << wl.n)
+            flops = sum(FLOPS_FWD[int(g_[0])] for g_ in gates) * wl.batch * float(1 << wl.n)
             traffic = None
         elif shift:
-            state_bytes = circ.state_bytes(wl.dtype, shift_circuits(wl), Q.MODE_FWD)
-            flops = shift_flops(wl)
+            state_bytes = circ.state_bytes(wl.dtype, n_shift, Q.MODE_FWD)
+            flops = shift_flops(gates, wl.batch, wl.n)
             traffic = None
         else:
             state_bytes = circ.state_bytes(wl.dtype, wl.batch)
-            flops = algorithmic_flops(wl)
-            traffic = profiled_traffic(wl)
+            flops = algorithmic_flops(gates, wl.batch, wl.n)
+            traffic = profiled_traffic(wl) if args.noise == 0 else None
         hbm = state_bytes / (tile_ms / 1e3) / 1e9
         alu = flops / (tile_ms / 1e3) / 1e12
         launches = kcnt[0] / args.steps
@@ -242,12 +267,13 @@ def main():
                                       "k_bind": kms[2] / args.steps, "k_reduce": kms[3] / args.steps}
     elif timing and kcnt[1] > 0:
         whole_ms = kms[1] / args.steps
-        alu = (shift_flops(wl) if shift else algorithmic_flops(wl)) / (whole_ms / 1e3) / 1e12
+        alu = (shift_flops(gates, wl.batch, wl.n) if shift else
+               algorithmic_flops(gates, wl.batch, wl.n)) / (whole_ms / 1e3) / 1e12
         line["roofline"] = {"bound": "alu", "kernel": "k_whole", "achieved": alu,
                             "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": alu / ALU_PEAK_TFLOPS,
                             "traffic": None, "kernel_ms_per_step": whole_ms}
     if args.cpu_gates > 0:
-        line["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_gates, wl.n_gates))
+        line["cpu_baseline"] = cpu_baseline(wl, gates, x, w, g, pauli_p, min(args.cpu_gates, G))
     print(json.dumps(line), flush=True)
 
 
