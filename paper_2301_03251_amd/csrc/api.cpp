@@ -91,7 +91,7 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
         }
     }
     std::vector<SlotSrc> slots;
-    for (const Slot& sl : c.slots) slots.push_back({sl.src, sl.index, sl.axis, 0, sl.scale, sl.c1, sl.c2, sl.c3});
+    for (const Slot& sl : c.slots) slots.push_back({sl.src, sl.index, sl.scale, sl.c1, sl.c2, sl.c3});
     std::vector<int32_t> xptr(c.n_inputs + 1, 0), wptr(c.n_weights + 1, 0), xs, ws;
     for (int f = 0; f < c.n_inputs; f++) {
         for (int s = 0; s < (int)slots.size(); s++)
@@ -631,10 +631,7 @@ int state(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs, c
     if ((rc = bind(x, B, inputs, weights, 0, 0))) return rc;
     if ((rc = embed(x, B, inputs, psi, 0, 0))) return rc;
     if ((rc = state_passes(x, B, false, nullptr, psi))) return rc;
-    const int n_slots = (int)h->c.slots.size();
-    // the whole-state kernel applies exact rotations: only Pauli outcomes
-    // (applied as -i P) leave a phase
-    if (x.pl.whole_state && n_slots == h->c.n_param_slots) return QL_OK;
+    if (x.pl.whole_state) return QL_OK;  // exact gates: no phase to undo
     BindTileArgs ba{};
     ba.inputs = inputs;
     ba.weights = weights;
@@ -644,8 +641,7 @@ int state(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs, c
     ba.n_ops = x.T.n_ops;
     ba.bwd_first = x.T.bwd_first;
     ba.F = h->c.n_inputs;
-    hipError_t e = launch_state_phase(dt, ba, x.pl.whole_state, n_slots, (double*)(x.W + x.L.zpart), psi,
-                                      h->c.n, stream);
+    hipError_t e = launch_state_phase(dt, ba, (double*)(x.W + x.L.zpart), psi, h->c.n, stream);
     return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("state phase: ") + hipGetErrorString(e));
 }
 

@@ -92,21 +92,27 @@ __device__ __forceinline__ double wave_total(double v) {
 // ---------------------------------------------------------------------------
 // angle sources (shared by the binding kernels)
 
-// The angle (fp64) of a rotation slot for circuit b. In a parameter-shift
-// chunk (vper > 0) circuit b is virtual circuit v = v0 + b of sample v / vper.
-// Input and weight slots: scale * bound value (scale 1, or +-1/2 for the
-// halves of a controlled rotation). Pauli-channel slots: pi when the
-// trajectory uniform selects the slot's axis, else 0 (the comparisons are in
-// fp64 against cumulative sums formed on the host).
+// The angle (fp64) of a rotation slot for circuit b: scale * the bound input
+// or weight (scale 1, or +-1/2 for the halves of a controlled rotation). In a
+// parameter-shift chunk (vper > 0) circuit b is virtual circuit v = v0 + b of
+// sample v / vper.
 template <typename Real>
 __device__ __forceinline__ double angle_of(const void* inputs, const void* weights, int F, const SlotSrc& src,
                                            int64_t b, int64_t v0, int32_t vper, int64_t& bs) {
     bs = vper > 0 ? (v0 + b) / vper : b;
     if (src.src == S_WEIGHT) return src.scale * (double)((const Real*)weights)[src.index];
-    const double v = (double)((const Real*)inputs)[bs * F + src.index];
-    if (src.src == S_INPUT) return src.scale * v;
-    const int which = v < src.c1 ? 1 : v < src.c2 ? 2 : v < src.c3 ? 3 : 0;
-    return which == src.axis ? 3.141592653589793238463 : 0.0;
+    return src.scale * (double)((const Real*)inputs)[bs * F + src.index];
+}
+
+// The Pauli a channel slot applies in circuit b: 1 X, 2 Y, 3 Z, 0 none, from
+// fp64 comparisons of the trajectory uniform with the cumulative
+// probabilities formed on the host.
+template <typename Real>
+__device__ __forceinline__ int pauli_of(const void* inputs, int F, const SlotSrc& src, int64_t b, int64_t v0,
+                                        int32_t vper) {
+    const int64_t bs = vper > 0 ? (v0 + b) / vper : b;
+    const double u = (double)((const Real*)inputs)[bs * F + src.index];
+    return u < src.c1 ? 1 : u < src.c2 ? 2 : u < src.c3 ? 3 : 0;
 }
 
 // Parameter-shift offset of slot s in circuit b: v % vper = 2s+1 adds pi/2,
@@ -132,6 +138,10 @@ __global__ void k_bind(const BindArgs a) {
     const int64_t b = t / a.n_slots;
     const int s = (int)(t - b * a.n_slots);
     const SlotSrc src = a.slots[s];
+    if (src.src == S_PAULI) {
+        ((T2*)a.coef)[t] = mk<T2>((Real)pauli_of<Real>(a.inputs, a.F, src, b, a.v0, a.vper), (Real)0);
+        return;
+    }
     int64_t bs = b;
     const double th = angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, bs) +
                       shift_of(b, a.v0, a.vper, s);
@@ -199,6 +209,26 @@ __device__ __forceinline__ void lds_gate(T2* st, const DevGate g, Real c, Real s
     }
 }
 
+// Pauli X (1), Y (2) or Z (3) on qubit q of a state in LDS; 0 leaves it.
+template <typename T2>
+__device__ __forceinline__ void lds_pauli(T2* st, int q, int which, int n, int tid, int nt) {
+    if (which == 0) return;
+    const int half = 1 << (n - 1), M = 1 << q;
+    for (int p = tid; p < half; p += nt) {
+        const int i = insert0(p, q);
+        const T2 u = st[i], v = st[i | M];
+        if (which == 1) {
+            st[i] = v;
+            st[i | M] = u;
+        } else if (which == 2) {
+            st[i] = mk<T2>(v.y, -v.x);
+            st[i | M] = mk<T2>(-u.y, u.x);
+        } else {
+            st[i | M] = mk<T2>(-v.x, -v.y);
+        }
+    }
+}
+
 template <typename T2, typename Real>
 __device__ __forceinline__ Real lds_grad(const T2* p, const T2* l, const DevGate g, int n, int tid,
                                          int nt) {
@@ -242,6 +272,11 @@ __global__ void __launch_bounds__(256) k_whole(const WholeArgs a) {
     __syncthreads();
     for (int gi = 0; gi < a.n_gates; ++gi) {
         const DevGate g = a.gates[gi];
+        if (g.kind == K_PAULI) {
+            lds_pauli(psi, g.q0, (int)coef[g.slot].x, n, tid, nt);
+            __syncthreads();
+            continue;
+        }
         Real c = 1, s = 0;
         if (g.slot >= 0) {
             const T2 cs = coef[g.slot];
@@ -279,6 +314,13 @@ __global__ void __launch_bounds__(256) k_whole(const WholeArgs a) {
     __syncthreads();
     for (int gi = a.n_gates - 1; gi >= 0; --gi) {
         const DevGate g = a.gates[gi];
+        if (g.kind == K_PAULI) {  // its own inverse, no gradient
+            const int which = (int)coef[g.slot].x;
+            lds_pauli(psi, g.q0, which, n, tid, nt);
+            lds_pauli(lam, g.q0, which, n, tid, nt);
+            __syncthreads();
+            continue;
+        }
         Real c = 1, s = 0;
         if (g.slot >= 0) {
             const T2 cs = coef[g.slot];
@@ -526,6 +568,30 @@ __device__ __forceinline__ void swap_all(T2* a) {
 #pragma unroll
     for (int i = 0; i < R; ++i)
         if (!(i & M)) xswap2(a[i], a[i | M]);
+}
+
+// Pauli P (0 X, 1 Y, 2 Z) on register bit J, exactly. Y maps (u, v) to
+// (-i v, i u): swap u.x with v.y and u.y with v.x, then negate u.y and v.x.
+template <int LOG_R, int P, int J, typename T2>
+__device__ __forceinline__ void pauli(T2* a) {
+    constexpr int R = 1 << LOG_R, M = 1 << J;
+    if constexpr (P == 0) {
+        swap_all<LOG_R, J>(a);
+    } else {
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+            if (!(i & M)) {
+                if constexpr (P == 1) {
+                    xswap(a[i].x, a[i | M].y);
+                    xswap(a[i].y, a[i | M].x);
+                    a[i].y = -a[i].y;
+                    a[i | M].x = -a[i | M].x;
+                } else {
+                    a[i | M].x = -a[i | M].x;
+                    a[i | M].y = -a[i | M].y;
+                }
+            }
+    }
 }
 
 // swap_all in the lanes where `on` holds
@@ -778,6 +844,17 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         }                                                                                   \
         break;
 #define QL_LSWAP_M(M) QL_LSWAP(M, 4) QL_LSWAP(M, 5)
+// A Pauli is its own inverse and maps each thread's register set onto itself,
+// so the backward sweep applies it as is and the per-thread Im<lambda|psi>
+// stays valid.
+#define QL_PAULI_CASE(P, J)                                                                 \
+    case H_PX + P * 5 + J:                                                                  \
+        if constexpr (J < LOG_R) {                                                          \
+            pauli<LOG_R, P, J>(ps);                                                         \
+            if constexpr (OPM != OP_ONE) pauli<LOG_R, P, J>(lm);                            \
+        }                                                                                   \
+        break;
+#define QL_PAULI_J(J) QL_PAULI_CASE(0, J) QL_PAULI_CASE(1, J) QL_PAULI_CASE(2, J)
 #define QL_CZ_RX(A)                                                                         \
     case H_CZ_RX + A:                                                                       \
         if constexpr (A < LOG_R) {                                                          \
@@ -793,6 +870,9 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         QL_CZ_RX(0) QL_CZ_RX(1) QL_CZ_RX(2) QL_CZ_RX(3) QL_CZ_RX(4)
         QL_RZN_CASE(0) QL_RZN_CASE(1) QL_RZN_CASE(2) QL_RZN_CASE(3) QL_RZN_CASE(4)
         QL_LSWAP_M(0) QL_LSWAP_M(1) QL_LSWAP_M(2) QL_LSWAP_M(3) QL_LSWAP_M(4)
+        QL_PAULI_J(0) QL_PAULI_J(1) QL_PAULI_J(2) QL_PAULI_J(3) QL_PAULI_J(4)
+        case H_NOP:
+            break;
         case H_RZU: {
             const bool bit = loc_bit(arg, cx.tb, cx.gb);
             if constexpr (OPM == OP_BWD) {
@@ -834,6 +914,8 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
 #undef QL_CZ_RX
 #undef QL_LSWAP
 #undef QL_LSWAP_M
+#undef QL_PAULI_CASE
+#undef QL_PAULI_J
 }
 
 // <Z_q> partials of one tile held in registers t: register bits from the
@@ -1132,7 +1214,11 @@ __global__ void k_bind_tile(const BindTileArgs a) {
     const DevOp op = a.ops[o];
     e.h = op.h;
     e.arg = op.arg;
-    if (op.slot >= 0) {
+    if (op.kind == K_PAULI) {
+        // the Pauli this sample's trajectory draws, on the op's register bit
+        const int which = pauli_of<Real>(a.inputs, a.F, a.slots[op.slot], b, a.v0, a.vper);
+        e.h = which == 0 ? (uint32_t)H_NOP : op.h + 5u * (uint32_t)(which - 1);
+    } else if (op.slot >= 0) {
         const SlotSrc src = a.slots[op.slot];
         int64_t bs;
         double th = angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, bs) +
@@ -1263,31 +1349,19 @@ __global__ void __launch_bounds__(256) k_shift_grad(const ShiftGradArgs a) {
 // state by the inverse phase.
 
 template <typename Real>
-__global__ void k_state_phase(const BindTileArgs a, int whole, int n_slots, double* phase) {
+__global__ void k_state_phase(const BindTileArgs a, double* phase) {
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= a.B) return;
     const double pi = 3.141592653589793238463, two_pi = 2.0 * pi;
     double ph = 0.0;
     int64_t bs;
-    if (whole) {
-        // exact rotations; a Pauli outcome P was applied as R(pi) = -i P
-        for (int s = 0; s < n_slots; ++s) {
-            const SlotSrc src = a.slots[s];
-            if (src.src == S_PAULI && angle_of<Real>(a.inputs, a.weights, a.F, src, b, 0, 0, bs) != 0.0)
-                ph -= 0.5 * pi;
-        }
-        phase[b] = ph;
-        return;
-    }
     for (int o = 0; o < a.bwd_first; ++o) {
         const DevOp op = a.ops[o];
-        if (op.slot < 0) continue;
-        const SlotSrc src = a.slots[op.slot];
-        const double th = angle_of<Real>(a.inputs, a.weights, a.F, src, b, 0, 0, bs);
+        if (op.slot < 0 || op.kind == K_PAULI) continue;  // Paulis are applied exactly
+        const double th = angle_of<Real>(a.inputs, a.weights, a.F, a.slots[op.slot], b, 0, 0, bs);
         const double k = rint(th / two_pi);
         ph += pi * k;
         if (op.h >= H_G1 + 15 && op.h < H_G1 + 20) ph += 0.5 * (th - two_pi * k);
-        if (src.src == S_PAULI && th != 0.0) ph -= 0.5 * pi;
     }
     phase[b] = ph;
 }
@@ -1677,17 +1751,16 @@ hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_state_phase(int dtype, const BindTileArgs& a, bool whole, int n_slots, double* phase,
-                              void* psi, int n, hipStream_t s) {
+hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, void* psi, int n,
+                              hipStream_t s) {
     const unsigned g1 = (unsigned)((a.B + 255) / 256);
     const int64_t total = a.B << n;
     const unsigned g2 = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
-    const int w = whole ? 1 : 0;
     if (dtype == 0) {
-        hipLaunchKernelGGL(k_state_phase<float>, dim3(g1), dim3(256), 0, s, a, w, n_slots, phase);
+        hipLaunchKernelGGL(k_state_phase<float>, dim3(g1), dim3(256), 0, s, a, phase);
         hipLaunchKernelGGL(k_phase_fix<float2>, dim3(g2), dim3(256), 0, s, psi, (const double*)phase, a.B, n);
     } else {
-        hipLaunchKernelGGL(k_state_phase<double>, dim3(g1), dim3(256), 0, s, a, w, n_slots, phase);
+        hipLaunchKernelGGL(k_state_phase<double>, dim3(g1), dim3(256), 0, s, a, phase);
         hipLaunchKernelGGL(k_phase_fix<double2>, dim3(g2), dim3(256), 0, s, psi, (const double*)phase, a.B, n);
     }
     return hipGetLastError();

@@ -9,13 +9,11 @@
 
 namespace qlayer {
 
-// Angle source of a rotation slot; one row per slot. Input/weight slots:
-// angle = scale * value. Pauli-channel slots (src S_PAULI): angle pi when the
-// uniform input feature `index` selects `axis` (1 X if u < c1, 2 Y if u < c2,
-// 3 Z if u < c3), else 0.
+// Source of a slot; one row per slot. Rotation slots: angle = scale * the
+// bound input or weight. Pauli-channel slots (src S_PAULI): the uniform input
+// feature `index` selects X if u < c1, Y if u < c2, Z if u < c3, else none.
 struct SlotSrc {
     int32_t src, index;
-    int32_t axis, pad;
     double scale;
     double c1, c2, c3;
 };
@@ -29,7 +27,7 @@ struct BindArgs {
     const void* inputs;   // [B][F] Real
     const void* weights;  // [P] Real
     const SlotSrc* slots; // [n_slots]
-    void* coef;           // [B][n_slots] complex (cos, sin) of theta/2
+    void* coef;           // [B][n_slots] complex (cos, sin) of theta/2; a Pauli slot: (which, 0)
     int64_t B;
     int32_t n_slots, F;
     int64_t v0;           // parameter-shift chunks: first virtual circuit
@@ -180,12 +178,10 @@ hipError_t launch_tile(int dtype, int log_r, bool bwd, const TileArgs& a, int th
 hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_shift_dot(int dtype, const ShiftDotArgs& a, hipStream_t s);
 hipError_t launch_sample(int dtype, const SampleArgs& a, hipStream_t s);
-// Undo the per-sample global phase the kernels leave on final states
-// (phase: [B] fp64 scratch). Tile path: the ops' phases; whole-state path
-// (whole = true, a.ops unused): only the Pauli-channel rotations' -i each,
-// over the n_slots slots.
-hipError_t launch_state_phase(int dtype, const BindTileArgs& a, bool whole, int n_slots, double* phase,
-                              void* psi, int n, hipStream_t s);
+// Undo the per-sample global phase the tile kernel leaves on final states
+// (phase: [B] fp64 scratch).
+hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, void* psi, int n,
+                              hipStream_t s);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, hipStream_t s);
 hipError_t launch_embed_grad(int dtype, const EmbedGradArgs& a, hipStream_t s);
 hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s);

@@ -20,7 +20,7 @@ bool is_rotation(int kind) { return kind == K_RX || kind == K_RY || kind == K_RZ
 // controls can be fixed bits of the tile).
 int needed_tile_qubit(const Gate& g) {
     switch (g.kind) {
-        case K_H: case K_RX: case K_RY: return g.q0;
+        case K_H: case K_RX: case K_RY: case K_PAULI: return g.q0;
         case K_CNOT: return g.q1;
         default: return -1;
     }
@@ -341,6 +341,10 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
             uint32_t ta, pa, tb, pb;
             DevOp op{};
             switch (g.kind) {
+                case K_PAULI:  // planned on a register bit, like RX
+                    loc(g.q0, ta, pa);
+                    op = make_op(H_PX + pa, 0, g.slot, K_PAULI);
+                    break;
                 case K_H: case K_RX: case K_RY: case K_RZ:
                     loc(g.q0, ta, pa);
                     if (ta == LOC_REG)
@@ -466,28 +470,22 @@ std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, i
             return fmt("gate %ld: H/CNOT/CZ take no angle source (got %ld)", i, src);
         }
         if (kind <= K_CZ) {
-            Slot sl{src, index, 1.0, 0, 0, 0, 0};
+            Slot sl{src, index, 1.0, 0, 0, 0};
             emit(kind, q0, q1, is_rotation(kind) ? &sl : nullptr);
         } else if (kind == P_PAULI) {
             if (!ext.pauli_p) return fmt("gate %ld: Pauli channel without probabilities", i);
             const double* p = ext.pauli_p + 3 * n_channels++;
             if (!(p[0] >= 0 && p[1] >= 0 && p[2] >= 0 && p[0] + p[1] + p[2] <= 1.0))
                 return fmt("gate %ld: Pauli probabilities must be >= 0 with sum <= 1", i);
-            Slot sl{S_PAULI, index, 1.0, 0, p[0], p[0] + p[1], p[0] + p[1] + p[2]};
-            // one rotation by pi per axis that can occur: RX(pi), RY(pi), RZ(pi)
-            // are -i X, -i Y, -i Z
-            for (int ax = 1; ax <= 3; ax++)
-                if (p[ax - 1] > 0) {
-                    sl.axis = ax;
-                    emit(ax == 1 ? K_RX : ax == 2 ? K_RY : K_RZ, q0, -1, &sl);
-                }
+            const Slot sl{S_PAULI, index, 1.0, p[0], p[0] + p[1], p[0] + p[1] + p[2]};
+            if (p[0] > 0 || p[1] > 0 || p[2] > 0) emit(K_PAULI, q0, -1, &sl);
         } else {
             // controlled rotation CR(t) on (control q0, target q1) as
             // R(t/2) E R(-t/2) E with E = CNOT(q0, q1) for RY and RZ (X R(a) X =
             // R(-a)) and E = CZ(q0, q1) for RX (Z RX(a) Z = RX(-a))
             const int rot = kind == P_CRX ? K_RX : kind == P_CRY ? K_RY : K_RZ;
             const int ent = kind == P_CRX ? K_CZ : K_CNOT;
-            Slot hp{src, index, 0.5, 0, 0, 0, 0}, hm{src, index, -0.5, 0, 0, 0, 0};
+            Slot hp{src, index, 0.5, 0, 0, 0}, hm{src, index, -0.5, 0, 0, 0};
             emit(rot, q1, -1, &hp);
             emit(ent, q0, q1, nullptr);
             emit(rot, q1, -1, &hm);

@@ -24,22 +24,22 @@
 namespace qlayer {
 
 // Gate kinds the planner and kernels run. The public kinds 6..9 (controlled
-// rotations, Pauli-channel trajectories) are rewritten into these at intake.
-enum GateKind { K_H = 0, K_RX = 1, K_RY = 2, K_RZ = 3, K_CNOT = 4, K_CZ = 5 };
+// rotations, Pauli-channel trajectories) are rewritten into these at intake;
+// K_PAULI is one channel trajectory on q0 whose Pauli (or none) each sample
+// draws from its uniform (slot of kind S_PAULI).
+enum GateKind { K_H = 0, K_RX = 1, K_RY = 2, K_RZ = 3, K_CNOT = 4, K_CZ = 5, K_PAULI = 16 };
 enum PublicKind { P_CRX = 6, P_CRY = 7, P_CRZ = 8, P_PAULI = 9 };
-// Angle sources of rotation slots; S_PAULI marks a trajectory slot (angle pi
-// or 0 from a uniform input feature).
+// Sources of slots: rotation angles from inputs or weights; S_PAULI marks a
+// channel slot (the Pauli a uniform input feature selects).
 enum Src { S_NONE = 0, S_INPUT = 1, S_WEIGHT = 2, S_PAULI = 3 };
 enum Embed { E_NONE = 0, E_BASIS = 1, E_AMPLITUDE = 2 };
 
-// One rotation occurrence after intake. Input and weight slots have angle
-// scale * value; a Pauli-channel slot has angle pi when the uniform u (input
-// feature `index`) selects its axis (X if u < c1, Y if u < c2, Z if u < c3)
-// and 0 otherwise.
+// One rotation occurrence or Pauli channel after intake. Input and weight
+// slots have angle scale * value; a Pauli-channel slot selects X if its
+// uniform u (input feature `index`) is < c1, Y if < c2, Z if < c3, else none.
 struct Slot {
     int32_t src, index;
     double scale;
-    int32_t axis;        // Pauli slots: 1 X, 2 Y, 3 Z
     double c1, c2, c3;   // Pauli slots: cumulative probabilities
 };
 
@@ -70,7 +70,11 @@ enum HandlerId : uint32_t {
     H_LSWAP = 93,      // + m * 6 + b: exchange register bit m with lane bit b (4 or 5) by
                        //      permlane swaps; arg = lswap_arg(new phase, tile bit lane b
                        //      leaves, tile bit it takes)
-    H_END = 123,
+    H_PX = 123,        // + P * 5 + J: Pauli X (P = 0), Y (1) or Z (2) on register bit J; a
+                       //      channel op is planned as H_PX + J and set per sample by the
+                       //      binding kernel to the Pauli its uniform selects, or to H_NOP
+    H_NOP = 138,
+    H_END = 139,
 };
 // Argument of a lane swap: the new phase (< 2^20) and the tile bits x (leaving
 // the lane bit for the registers) and y (taking its place).
@@ -189,7 +193,7 @@ struct Circuit {
     int n = 0, n_inputs = 0, n_weights = 0;
     int embed = E_NONE, embed_first = 0;
     std::vector<Gate> gates;     // after intake: kinds H..CZ only
-    std::vector<Slot> slots;     // rotation slots: trainable ones first, then Pauli ones
+    std::vector<Slot> slots;     // slots: trainable rotations first, then Pauli channels
     int n_param_slots = 0;       // slots bound to inputs or weights
     int n_user_gates = 0;        // gates as given
     Options opts;
