@@ -736,6 +736,19 @@ struct TileCtx {
     int ph;        // current phase
 };
 
+// An empty asm that uses an op record in scalar registers: the first record
+// of an op loop is waited for before the loop, so the loop header (reached
+// from the preheader and from the back edge) has no pending scalar load and
+// each iteration's load of the next record overlaps the current op. (Without
+// it the header waits on every iteration, since scalar loads return out of
+// order and the wait must cover the record just issued.)
+__device__ __forceinline__ void op_ready(const XOp<float>& o) {
+    asm volatile("" ::"s"(o.h), "s"(o.arg), "s"(o.a), "s"(o.b));
+}
+__device__ __forceinline__ void op_ready(const XOp<double>& o) {
+    asm volatile("" ::"s"(o.h), "s"(o.arg), "s"(o.a), "s"(o.b));
+}
+
 // An empty asm that reads every amplitude of a register tile: the compiler
 // waits for the tile's pending loads here, once, instead of before the first
 // use of each register inside every op handler.
@@ -1072,7 +1085,18 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     // highest fixed qubit
     const int64_t tiles = PAIR ? a.tiles >> 1 : a.tiles;
     const uint32_t top_fixed = (PAIR && n_fixed > 0) ? 1u << P.fixed_qubit[n_fixed - 1] : 0u;
+    // fixed-qubit bits of tile t (the same in every lane)
+    auto fixed_bits = [&](int64_t t) {
+        const uint32_t tb = lane < n_fixed ? (((uint32_t)t >> lane) & 1u) : 0u;
+        return wave_or(tb << fq_lane);
+    };
     T2 ps[R], lm[R];
+    // one-tile forward mode: the next tile's loads are issued before this
+    // tile's ops run (nothing in the ops reads nx, so they stay in flight
+    // through the exchanges)
+    constexpr bool PREF = KM == KM_FWD1;
+    T2 nx[PREF ? R : 1];
+    if (PREF && load && w < tiles) load_tile(nx, psi_s, fixed_bits(w));
     Real ival = 0;  // see run_op
     for (int64_t tile = w; tile < tiles; tile += a.n_wg) {
         const uint32_t tbit = lane < n_fixed ? (((uint32_t)tile >> lane) & 1u) : 0u;
@@ -1091,6 +1115,10 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
 #pragma unroll
                 for (int i = 0; i < R; ++i) lm[i] = mk<T2>((Real)0, (Real)0);
             }
+        } else if constexpr (PREF) {
+#pragma unroll
+            for (int i = 0; i < R; ++i) ps[i] = nx[i];
+            if (tile + a.n_wg < tiles) load_tile(nx, psi_s, fixed_bits(tile + a.n_wg));
         } else {
             load_tile(ps, psi_s, cx.gb);
             if (PAIR) load_tile(lm, psi_s, cx.gb2);
@@ -1102,6 +1130,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
         // ---- forward ops
         if (flags & PF_FWD) {
             XOp<Real> cur = xops[fwd_begin];
+            op_ready(cur);
             for (int o = fwd_begin; o < fwd_end; ++o) {
                 const XOp<Real> nxt = xops[o + 1];
                 run_op<LOG_R, LOG_T, PAIR ? OP_PAIR : OP_ONE>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx,
@@ -1141,6 +1170,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
             if (flags & PF_BWD) {
                 ival = im_sum<LOG_R, -1, T2, Real>(ps, lm);
                 XOp<Real> cur = xops[bwd_begin];
+                op_ready(cur);
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
                     run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, ival, lds,
