@@ -537,6 +537,11 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
     // tile, four wavefronts per SIMD); complex128: 16 per thread, 256 threads
     int log_r = o.log_regs ? o.log_regs : 4;
     int log_t = o.log_threads ? o.log_threads : (dtype == 0 ? 9 : 8);
+    // A circuit smaller than the default tile runs one tile per sample; such
+    // passes are latency-bound, so unless asked otherwise the tile keeps its
+    // threads (more wavefronts per sample) and gives up registers first.
+    if (!o.log_regs)
+        while (log_r + log_t > c.n && log_r > 2) log_r--;
     while (log_r + log_t > c.n && log_t > 6) log_t--;
     while (log_r + log_t > c.n && log_r > 2) log_r--;
     if (log_r + log_t > c.n) return "circuit too small for the tile kernel";
