@@ -194,16 +194,34 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         return 1 << 30;
     };
     // thread bits for register set R after an LDS exchange: the low tile bits
-    // on their own thread bits; the bits needed soonest on the swap lanes
-    // (4, 5), the rest in order of use
+    // on their own thread bits; lanes 0-3 free of them take bits of distinct
+    // classes j mod 4 (the LDS slot map folds tile bit j onto slot bit j mod
+    // 4, so 16 consecutive lanes then hit 16 distinct bank pairs), taken from
+    // the bits needed last; the bits needed soonest on the swap lanes (4, 5);
+    // the rest in order of use
     auto fresh_thr = [&](const std::vector<int>& R) {
         std::vector<int> thr(log_t, -1), rest;
+        unsigned used = 0;  // classes j mod 4 on lanes 0-3
         for (int j = 0; j < k; j++) {
             if (std::find(R.begin(), R.end(), j) != R.end()) continue;
-            if (j < home) thr[j] = j;
-            else rest.push_back(j);
+            if (j < home) {
+                thr[j] = j;
+                if (j < 4) used |= 1u << (j & 3);
+            } else {
+                rest.push_back(j);
+            }
         }
         std::stable_sort(rest.begin(), rest.end(), [&](int x, int y) { return next_use(x) < next_use(y); });
+        for (int sl = 0; sl < std::min(4, log_t); sl++) {
+            if (thr[sl] >= 0) continue;
+            for (int i = (int)rest.size() - 1; i >= 0; i--)
+                if (!(used >> (rest[i] & 3) & 1)) {
+                    thr[sl] = rest[i];
+                    used |= 1u << (rest[i] & 3);
+                    rest.erase(rest.begin() + i);
+                    break;
+                }
+        }
         size_t ri = 0;
         for (int sl : {4, 5})
             if (swap_lane(sl) && thr[sl] < 0 && ri < rest.size()) thr[sl] = rest[ri++];
