@@ -216,3 +216,22 @@ def test_qae_workload():
     want = oracle.run(wl.n, wl.gates(), _host(x, wl.dtype), _host(w, wl.dtype), grad_out=_host(g, wl.dtype),
                       embed=wl.embed)
     check(gpu_fb(circ, wl.dtype, x, w, g), want, TOL[wl.dtype], "qae")
+
+
+@pytest.mark.parametrize("n,dtype", [(6, "c128"), (12, "c64")])
+def test_param_shift_with_pauli_channels(n, dtype):
+    """Parameter shift over a noisy circuit: only the trainable rotations are
+    shifted (2S + 1 circuits per sample), each shifted circuit keeps the
+    sample's trajectory; against the oracle's shift on the same uniforms."""
+    gates, pp, x, w, g = _noisy_case(n, dtype, seed=2000 + n, B=3)
+    circ = Q.Circuit(n, gates, x.shape[1], w.size, pauli_p=pp)
+    e, gx, gw = Q.Runner(circ, dtype).param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), max_chunk=50)
+    torch.cuda.synchronize()
+    xh, wh, gh = _host(x, dtype), _host(w, dtype), _host(g, dtype)
+    ox, ow = oracle.param_shift(n, gates, xh, wh, gh, pauli_p=pp)
+    want = {"expz": oracle.run(n, gates, xh, wh, pauli_p=pp)["expz"], "grad_inputs": ox, "grad_weights": ow}
+    got = {"expz": e.cpu().double().numpy(), "grad_inputs": gx.cpu().double().numpy(),
+           "grad_weights": gw.cpu().double().numpy()}
+    check(got, want, TOL[dtype], f"pauli shift n={n} {dtype}")
+    adj = oracle.run(n, gates, xh, wh, grad_out=gh, pauli_p=pp)
+    check(got, adj, TOL[dtype], f"pauli shift vs adjoint n={n} {dtype}", keys=("grad_weights",))
