@@ -235,3 +235,26 @@ def test_param_shift_with_pauli_channels(n, dtype):
     check(got, want, TOL[dtype], f"pauli shift n={n} {dtype}")
     adj = oracle.run(n, gates, xh, wh, grad_out=gh, pauli_p=pp)
     check(got, adj, TOL[dtype], f"pauli shift vs adjoint n={n} {dtype}", keys=("grad_weights",))
+
+
+def test_noisy_16q_full_batch_sampled_rows():
+    """The noisy 16-qubit line as bench.py times it (full batch of 1024, a
+    depolarizing channel on every qubit after every 48 gates, p = 0.01, the
+    bench's seeded uniforms): sampled rows against the oracle's trajectories."""
+    wl = W.get("16q")
+    x, w, g = wl.inputs()
+    gates, pp, n_ch = W.with_depolarizing(wl.gates(), wl.n, wl.n_inputs, 0.01, 48)
+    u = np.random.default_rng(wl.seed + 1000).random((wl.batch, n_ch)).astype(x.dtype)
+    xe = np.concatenate([x, u], axis=1)
+    circ = Q.Circuit(wl.n, gates, xe.shape[1], wl.n_weights, pauli_p=pp)
+    got = gpu_fb(circ, wl.dtype, xe, w, g)
+    rows = [0, 511, 1023]
+    want = oracle.run(wl.n, gates, _host(xe[rows], wl.dtype), _host(w, wl.dtype), grad_out=_host(g[rows], wl.dtype),
+                      pauli_p=pp)
+    sub = {"expz": got["expz"][rows], "grad_inputs": got["grad_inputs"][rows]}
+    check(sub, want, TOL[wl.dtype], "noisy 16q rows", keys=("expz", "grad_inputs"))
+    # weight gradients sum over the whole batch: check them through linearity
+    # on a batch restricted to the sampled rows
+    circ_r = Q.Circuit(wl.n, gates, xe.shape[1], wl.n_weights, pauli_p=pp)
+    got_r = gpu_fb(circ_r, wl.dtype, xe[rows], w, g[rows])
+    check(got_r, want, TOL[wl.dtype], "noisy 16q rows as a batch")
