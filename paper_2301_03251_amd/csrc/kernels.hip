@@ -1224,6 +1224,254 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
 }
 
 // ---------------------------------------------------------------------------
+// k_wave: the whole state of one sample in one wavefront's registers (n <= 8)
+//
+// Amplitude j = lane + 64 i sits in register i of lane j mod 64: 2^(n-6)
+// registers per lane, one for n <= 6 (lanes >= 2^n then hold zeros and never
+// mix with the others). A gate on qubit q < 6 pairs each lane with lane ^ 2^q
+// through a cross-lane shuffle; on qubit q >= 6, register i with register
+// i ^ 2^(q-6) of the same lane. Every lane computes its own new amplitude from
+// its old one and its partner's, so there is no LDS traffic and no barrier:
+// each gate is wavefront-synchronous. Same arguments, coefficient table and
+// partial layouts as k_whole.
+
+// bit q of amplitude lane + 64 r
+__device__ __forceinline__ int amp_bit(int q, int lane, int r) {
+    return q < 6 ? (lane >> q) & 1 : (r >> (q - 6)) & 1;
+}
+
+// The value of lane ^ 2^B, without the LDS pipe: quad permutes (B = 0, 1),
+// two row shifts under bank masks (B = 2, 3: lanes with bit B clear read from
+// +2^B, the others from -2^B), a permlane swap of two copies and a select
+// (B = 4, 5).
+template <int B>
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t v, int lane) {
+    if constexpr (B == 0) {
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+    } else if constexpr (B == 1) {
+        return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+    } else if constexpr (B <= 3) {
+        constexpr int SHL = 0x100 + (1 << B), SHR = 0x110 + (1 << B);
+        constexpr int LOW = B == 2 ? 0x5 : 0x3, HIGH = B == 2 ? 0xA : 0xC;  // banks by lane bit B
+        const int lo = __builtin_amdgcn_update_dpp(0, (int)v, SHL, 0xF, LOW, false);
+        return (uint32_t)__builtin_amdgcn_update_dpp(lo, (int)v, SHR, 0xF, HIGH, false);
+    } else {
+        const auto r = B == 4 ? __builtin_amdgcn_permlane16_swap(v, v, false, false)
+                              : __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return ((lane >> B) & 1) ? r[0] : r[1];
+    }
+}
+template <int B>
+__device__ __forceinline__ float xor_lane(float v, int lane) {
+    return __builtin_bit_cast(float, xor_lane_u32<B>(__builtin_bit_cast(uint32_t, v), lane));
+}
+template <int B>
+__device__ __forceinline__ double xor_lane(double v, int lane) {
+    uint2 u = __builtin_bit_cast(uint2, v);
+    u.x = xor_lane_u32<B>(u.x, lane);
+    u.y = xor_lane_u32<B>(u.y, lane);
+    return __builtin_bit_cast(double, u);
+}
+template <typename T2>
+__device__ __forceinline__ T2 xlane(T2 v, int q, int lane) {
+    switch (q) {
+        case 0: return mk<T2>(xor_lane<0>(v.x, lane), xor_lane<0>(v.y, lane));
+        case 1: return mk<T2>(xor_lane<1>(v.x, lane), xor_lane<1>(v.y, lane));
+        case 2: return mk<T2>(xor_lane<2>(v.x, lane), xor_lane<2>(v.y, lane));
+        case 3: return mk<T2>(xor_lane<3>(v.x, lane), xor_lane<3>(v.y, lane));
+        case 4: return mk<T2>(xor_lane<4>(v.x, lane), xor_lane<4>(v.y, lane));
+        default: return mk<T2>(xor_lane<5>(v.x, lane), xor_lane<5>(v.y, lane));
+    }
+}
+
+// New value of one amplitude (bit `bit` of the gate's qubit) from its old value
+// and its partner's: H, RX (both bits alike), RY; Pauli X (1), Y (2), Z (3) by
+// `which` for K_PAULI. (c, s) = (cos t/2, sin t/2); the inverse passes -s.
+template <typename T2, typename Real>
+__device__ __forceinline__ T2 mix_el(int kind, T2 own, T2 par, int bit, Real c, Real s, int which) {
+    const Real sg = bit ? (Real)1 : (Real)-1;
+    switch (kind) {
+        case K_H: {
+            const Real r = (Real)0.70710678118654752440;
+            return mk<T2>((par.x - sg * own.x) * r, (par.y - sg * own.y) * r);
+        }
+        case K_RX:
+            return mk<T2>(c * own.x + s * par.y, c * own.y - s * par.x);
+        case K_RY:
+            return mk<T2>(c * own.x + sg * s * par.x, c * own.y + sg * s * par.y);
+        default:  // K_PAULI
+            if (which == 1) return par;
+            if (which == 2) return mk<T2>(-sg * par.y, sg * par.x);
+            return bit ? mk<T2>(-own.x, -own.y) : own;
+    }
+}
+
+// This element's term of Im<l | P | p> for the rotation's generator P.
+template <typename T2, typename Real>
+__device__ __forceinline__ Real grad_el(int kind, T2 l, T2 own, T2 par, int bit) {
+    if (kind == K_RX) return l.x * par.y - l.y * par.x;
+    if (kind == K_RY) return (bit ? (Real)1 : (Real)-1) * (l.x * par.x + l.y * par.y);
+    const Real t = l.x * own.y - l.y * own.x;  // K_RZ
+    return bit ? -t : t;
+}
+
+// Apply gate g to st (and, when GRAD, return this lane's gradient term taken
+// before the gate with l = lambda). Uniform branches only.
+template <int R, typename T2, typename Real>
+__device__ __forceinline__ void wave_gate(T2* st, const DevGate g, Real c, Real s, int which, int lane) {
+    const int q = g.kind == K_CNOT ? g.q1 : g.q0;
+    if (g.kind == K_RZ) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const Real sg = amp_bit(q, lane, r) ? (Real)1 : (Real)-1;
+            const T2 u = st[r];
+            st[r] = mk<T2>(c * u.x - sg * s * u.y, c * u.y + sg * s * u.x);
+        }
+        return;
+    }
+    if (g.kind == K_CZ) {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            if (amp_bit(g.q0, lane, r) & amp_bit(g.q1, lane, r)) st[r] = mk<T2>(-st[r].x, -st[r].y);
+        return;
+    }
+    if (g.kind == K_PAULI && which == 0) return;
+    T2 old[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) old[r] = st[r];
+    if (q < 6) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const T2 par = xlane(old[r], q, lane);
+            if (g.kind == K_CNOT) st[r] = amp_bit(g.q0, lane, r) ? par : old[r];
+            else st[r] = mix_el<T2, Real>(g.kind, old[r], par, amp_bit(q, lane, r), c, s, which);
+        }
+    } else {
+        const int m = 1 << (q - 6);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            T2 par = old[r];
+            // registers are compile-time indices: pick the partner by a
+            // uniform comparison instead of a runtime array index
+#pragma unroll
+            for (int u = 0; u < R; ++u)
+                if (u == (r ^ m)) par = old[u];
+            if (g.kind == K_CNOT) st[r] = amp_bit(g.q0, lane, r) ? par : old[r];
+            else st[r] = mix_el<T2, Real>(g.kind, old[r], par, (r & m) ? 1 : 0, c, s, which);
+        }
+    }
+}
+
+template <int R, typename T2, typename Real>
+__device__ __forceinline__ Real wave_grad(const T2* p, const T2* l, const DevGate g, int lane) {
+    const int q = g.q0;
+    Real acc = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        T2 par = p[r];
+        if (g.kind != K_RZ) {
+            if (q < 6) {
+                par = xlane(p[r], q, lane);
+            } else {
+#pragma unroll
+                for (int u = 0; u < R; ++u)
+                    if (u == (r ^ (1 << (q - 6)))) par = p[u];
+            }
+        }
+        acc += grad_el<T2, Real>(g.kind, l[r], p[r], par, amp_bit(q, lane, r));
+    }
+    return acc;
+}
+
+// Coefficients of gate g for this sample: (c, s) = (cos t/2, sin t/2), or the
+// Pauli index of a channel in c.
+template <typename T2>
+__device__ __forceinline__ T2 gate_coef(const DevGate& g, const T2* coef) {
+    return g.slot >= 0 ? coef[g.slot] : mk<T2>((decltype(T2::x))1, (decltype(T2::x))0);
+}
+
+// One wavefront (one sample) per workgroup: the sample index is uniform, so
+// the gate table and the sample's coefficients are scalar loads, issued one
+// gate ahead of their use.
+// The gate table and coefficients come in as restrict parameters: the kernel
+// writes only outputs, so they stay scalar loads even next to those stores.
+template <typename Real, int R>
+__global__ void __launch_bounds__(64) k_wave(const WholeArgs a, const DevGate* __restrict__ gates,
+                                             const typename Cx<Real>::T* __restrict__ coef_all) {
+    using T2 = typename Cx<Real>::T;
+    const int lane = threadIdx.x;
+    const int64_t b = blockIdx.x;
+    const int n = a.n, dim = 1 << n, G = a.n_gates;
+    const T2* coef = coef_all + b * a.n_slots;
+    T2 ps[R], lm[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int j = lane + 64 * r;
+        if (j >= dim) ps[r] = mk<T2>((Real)0, (Real)0);
+        else if (a.psi_in) ps[r] = ((const T2*)a.psi_in)[b * dim + j];
+        else ps[r] = mk<T2>((Real)(j == 0), (Real)0);
+    }
+    // gate records two gates ahead, coefficients one ahead: each iteration
+    // waits only for loads issued during the previous gate
+    auto gate_at = [&](int i) { return gates[__builtin_amdgcn_readfirstlane(i < 0 ? 0 : i < G ? i : G - 1)]; };
+    if (G > 0) {
+        DevGate g0 = gate_at(0), g1 = gate_at(1);
+        T2 c0 = gate_coef(g0, coef);
+        for (int gi = 0; gi < G; ++gi) {
+            const T2 c1 = gate_coef(g1, coef);
+            const DevGate g2 = gate_at(gi + 2);
+            wave_gate<R, T2, Real>(ps, g0, c0.x, c0.y, (int)c0.x, lane);
+            g0 = g1;
+            g1 = g2;
+            c0 = c1;
+        }
+    }
+    if (a.psi_out)
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            if (lane + 64 * r < dim) ((T2*)a.psi_out)[b * dim + lane + 64 * r] = ps[r];
+    for (int q = 0; q < n; ++q) {
+        Real acc = 0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const Real p = ps[r].x * ps[r].x + ps[r].y * ps[r].y;
+            acc += amp_bit(q, lane, r) ? -p : p;
+        }
+        const Real t = wave_to_last(acc);
+        if (lane == 63) a.zpart[b * n + q] = (double)t;
+    }
+    if (!a.bwd) return;
+    const Real* go = (const Real*)a.grad_out + b * n;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        Real d = 0;
+        for (int q = 0; q < n; ++q) d += amp_bit(q, lane, r) ? -go[q] : go[q];
+        lm[r] = mk<T2>(d * ps[r].x, d * ps[r].y);
+    }
+    if (G > 0) {
+        DevGate g0 = gate_at(G - 1), g1 = gate_at(G - 2);
+        T2 c0 = gate_coef(g0, coef);
+        for (int gi = G - 1; gi >= 0; --gi) {
+            const T2 c1 = gate_coef(g1, coef);
+            const DevGate g2 = gate_at(gi - 2);
+            if (g0.slot >= 0 && g0.kind != K_PAULI) {
+                const Real t = wave_to_last(wave_grad<R, T2, Real>(ps, lm, g0, lane));
+                if (lane == 63) a.gpart[(size_t)g0.slot * a.B + b] = (double)t;
+            }
+            wave_gate<R, T2, Real>(ps, g0, c0.x, -c0.y, (int)c0.x, lane);
+            wave_gate<R, T2, Real>(lm, g0, c0.x, -c0.y, (int)c0.x, lane);
+            g0 = g1;
+            g1 = g2;
+            c0 = c1;
+        }
+    }
+    if (a.lam_out)
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            if (lane + 64 * r < dim) ((T2*)a.lam_out)[b * dim + lane + 64 * r] = lm[r];
+}
+
+// ---------------------------------------------------------------------------
 // k_bind_tile: per-sample op records of every tile op (one thread per
 // (sample, op)); shear coefficients in fp64, rounded once. The inverse of a
 // rotation (backward ops) negates both coefficients.
@@ -1665,6 +1913,23 @@ hipError_t launch_bind(int dtype, const BindArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_whole(int dtype, const WholeArgs& a, int threads, size_t lds, hipStream_t s) {
+    if (a.n <= 8) {  // one wavefront per sample
+        const dim3 grid((unsigned)a.B), block(64);
+#define QL_WAVE(REAL)                                                                     \
+    {                                                                                     \
+        const auto* cf = (const typename Cx<REAL>::T*)a.coef;                             \
+        if (a.n <= 6) hipLaunchKernelGGL((k_wave<REAL, 1>), grid, block, 0, s, a, a.gates, cf);      \
+        else if (a.n == 7) hipLaunchKernelGGL((k_wave<REAL, 2>), grid, block, 0, s, a, a.gates, cf); \
+        else hipLaunchKernelGGL((k_wave<REAL, 4>), grid, block, 0, s, a, a.gates, cf);               \
+    }
+        if (dtype == 0) {
+            QL_WAVE(float)
+        } else {
+            QL_WAVE(double)
+        }
+#undef QL_WAVE
+        return hipGetLastError();
+    }
     if (dtype == 0) hipLaunchKernelGGL(k_whole<float>, dim3((unsigned)a.B), dim3(threads), lds, s, a);
     else hipLaunchKernelGGL(k_whole<double>, dim3((unsigned)a.B), dim3(threads), lds, s, a);
     return hipGetLastError();
