@@ -16,6 +16,15 @@
 //               psi and lambda and accumulates Im<lambda|P|psi> per rotation
 //   k_reduce -- deterministic fp64 sums of the per-workgroup partials into
 //               <Z_q>, input gradients and (batch-summed) weight gradients
+//   k_wave   -- states of n <= 8 qubits: one wavefront per sample holds psi and
+//               lambda in registers (same job as k_whole, no LDS, no barriers)
+//   k_bind_tile -- per-sample op records of the tile ops (handler, argument,
+//               shear coefficients; the Pauli of a channel trajectory)
+//   k_embed_* -- basis / amplitude embedding of the initial state, and the
+//               amplitude embedding's VJP from lambda_0
+//   k_shift_dot, k_shift_grad -- parameter-shift VJP from batched shifted circuits
+//   k_state_phase, k_phase_fix -- the global phase of the tile path's final states
+//   k_block_sums, k_block_scan, k_shots, k_shot_z -- shot sampling by inverse CDF
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
