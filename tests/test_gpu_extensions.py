@@ -258,3 +258,19 @@ def test_noisy_16q_full_batch_sampled_rows():
     circ_r = Q.Circuit(wl.n, gates, xe.shape[1], wl.n_weights, pauli_p=pp)
     got_r = gpu_fb(circ_r, wl.dtype, xe[rows], w, g[rows])
     check(got_r, want, TOL[wl.dtype], "noisy 16q rows as a batch")
+
+
+def test_qae_param_shift_full_batch():
+    """The QAE parameter-shift line as bench.py times it (full batch, no input
+    gradients under amplitude embedding): <Z> and weight gradients equal the
+    oracle's adjoint ones (the shift rule is exact)."""
+    wl = W.get("qae")
+    x, w, g = wl.inputs()
+    circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, embed=wl.embed)
+    e, _, gw = Q.Runner(circ, wl.dtype).param_shift(_dev(x, wl.dtype), _dev(w, wl.dtype), _dev(g, wl.dtype),
+                                                     want_inputs=False)
+    torch.cuda.synchronize()
+    want = oracle.run(wl.n, wl.gates(), _host(x, wl.dtype), _host(w, wl.dtype), grad_out=_host(g, wl.dtype),
+                      embed=wl.embed)
+    check({"expz": e.cpu().double().numpy(), "grad_weights": gw.cpu().double().numpy()}, want, TOL[wl.dtype],
+          "qae shift", keys=("expz", "grad_weights"))
