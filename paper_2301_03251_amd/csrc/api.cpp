@@ -405,9 +405,11 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         ta.n_wg = x.L.n_wg;
         ta.flags = flags;
         ta.n_gslots = (flags & PF_BWD) ? d.n_gslots : 0;
-        // dynamic LDS: <Z> and gradient scratch (the exchange buffer is static)
-        const size_t lds = (size_t)(c.n + ta.n_gslots) * NW * 8;
-        if (lds + tile_static_lds(x.dt, pl.log_r, threads) > g_lds_limit)
+        // dynamic LDS: <Z> scratch and gradient accumulators (the exchange
+        // buffer is static)
+        const size_t st = tile_static_lds(x.dt, pl.log_r, threads), real = x.dt == 0 ? 4 : 8;
+        const size_t lds = (size_t)c.n * NW * 8 + (size_t)ta.n_gslots * NW * TILE_GRAD_WORDS * real;
+        if (lds + st > g_lds_limit)
             return fail(QL_EUNSUPPORTED, "tile pass needs more LDS than available");
         x.tm.start(0);
         hipError_t le = launch_tile(x.dt, pl.log_r, (flags & PF_BWD) != 0, ta, threads, lds, x.stream);

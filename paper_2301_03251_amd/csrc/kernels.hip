@@ -533,15 +533,37 @@ __device__ __forceinline__ double wave_to_last(double v) {
     return v;
 }
 
-// Add the wavefront's gradient partial to its LDS accumulator gacc[g][wave].
-// Only lane 63 of this wavefront ever touches that word, so the sum is in
-// program order (deterministic); the add has no return value.
+// Sum over each 16-lane row, left in every lane of the row (the first four
+// steps of wave_to_last).
+__device__ __forceinline__ float row_sum(float v) {
+    v += dpp_f32<0xB1>(v);
+    v += dpp_f32<0x4E>(v);
+    v += dpp_f32<0x141>(v);
+    v += dpp_f32<0x140>(v);
+    return v;
+}
+__device__ __forceinline__ double row_sum(double v) {
+    v += dpp_f64<0xB1>(v);
+    v += dpp_f64<0x4E>(v);
+    v += dpp_f64<0x141>(v);
+    v += dpp_f64<0x140>(v);
+    return v;
+}
+
+// Add the wavefront's gradient partial to its LDS accumulators gacc[g][wave]
+// [2]: a row butterfly and one row broadcast leave each half-wavefront's sum
+// in lanes 31 and 63, which add it to their own word (two words instead of
+// one save the last broadcast step). Every word has one writer lane, so its
+// sum is in program order (deterministic); the add has no return value.
+constexpr int GRAD_WORDS = TILE_GRAD_WORDS;
 template <typename Real>
 __device__ __forceinline__ void grad_add(Real* gacc, uint32_t g, Real part, int lane, int wave, int nw) {
-    const Real w = wave_to_last(part);
-    if (lane == 63)
-        __hip_atomic_fetch_add(gacc + g * (uint32_t)nw + (uint32_t)wave, w, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_WORKGROUP);
+    Real v = row_sum(part);
+    if constexpr (sizeof(Real) == 4) v += bcast_f32<0x142, 0xA>(v);
+    else v += bcast_f64<0x142, 0xA>(v);
+    if ((lane & 31) == 31)
+        __hip_atomic_fetch_add(gacc + (g * (uint32_t)nw + (uint32_t)wave) * GRAD_WORDS + (lane >> 5), v,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Exchange two values in place (their registers keep their roles, so the
@@ -1016,7 +1038,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     const int bwd_begin = P.bwd_begin, bwd_end = P.bwd_end;
     unsigned char* lds = tile_lds;
     double* red = (double*)smem;                       // [n][NW]
-    Real* gacc = (Real*)(red + (size_t)n * NW);        // [n_gslots][NW]
+    constexpr int GW = GRAD_WORDS;
+    Real* gacc = (Real*)(red + (size_t)n * NW);        // [n_gslots][NW][GW]
 
     const size_t dim = (size_t)1 << n;
     T2* psi_s = (T2*)a.psi + b * dim;
@@ -1025,7 +1048,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     const Real* gout = gout_all + b * n;
 
     if (BWD && (flags & PF_BWD)) {
-        for (int i = tid; i < a.n_gslots * NW; i += nt) gacc[i] = (Real)0;
+        for (int i = tid; i < a.n_gslots * NW * GW; i += nt) gacc[i] = (Real)0;
         __syncthreads();
     }
 
@@ -1227,7 +1250,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     if (BWD && (flags & PF_BWD))
         for (int g = tid; g < a.n_gslots; g += nt) {
             double t = 0;
-            for (int v = 0; v < NW; ++v) t += (double)gacc[g * NW + v];
+            for (int v = 0; v < NW * GW; ++v) t += (double)gacc[g * NW * GW + v];
             a.gpart[((size_t)gslots[g] * a.B + b) * a.n_wg + w] = t;
         }
 }

@@ -144,6 +144,8 @@ struct TileArgs {
     int32_t n, n_ops, n_wg, flags;
     int32_t n_gslots;          // gradient accumulators of this pass
 };
+// LDS words per (gradient accumulator, wavefront) of the tile kernel
+constexpr int TILE_GRAD_WORDS = 2;
 
 struct ReduceArgs {
     const double* zpart;   // [B][n_wg][n]
