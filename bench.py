@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -70,15 +71,20 @@ def shift_flops(gates, batch, n) -> float:
 
 def profiled_traffic(wl):
     """Calibrated HBM bytes per step of the tile kernel from the committed
-    rocprofv3 summary, if it was taken with the current kernel source."""
+    rocprofv3 summary (None unless it was taken with the current kernel
+    source), and the bandwidth of the plain 1 GiB copy kernel measured in the
+    same runs (the achievable line), in GB/s."""
     path = os.path.join(ROOT, "profiles", f"k_tile_{wl.name}.txt")
     if not os.path.exists(path):
-        return None
-    fields = dict(l.split(": ", 1) for l in open(path).read().splitlines() if ": " in l and not l.startswith("#"))
+        return None, None
+    text = open(path).read()
+    fields = dict(l.split(": ", 1) for l in text.splitlines() if ": " in l and not l.startswith("#"))
+    m = re.search(r"copy duration ([0-9.]+) ms", text)
+    copy_gbs = 2 * 2 ** 30 / (float(m.group(1)) * 1e-3) / 1e9 if m else None
     src = os.path.join(ROOT, "paper_2301_03251_amd", "csrc", "kernels.hip")
     if fields.get("kernels_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
-        return None
-    return float(fields["traffic_bytes_per_step"])
+        return None, copy_gbs
+    return float(fields["traffic_bytes_per_step"]), copy_gbs
 
 
 def cpu_baseline(wl, gates, x, w, g, pauli_p, n_gates: int):
@@ -249,7 +255,8 @@ def main():
         else:
             state_bytes = circ.state_bytes(wl.dtype, wl.batch)
             flops = algorithmic_flops(gates, wl.batch, wl.n)
-            traffic = profiled_traffic(wl) if args.noise == 0 else None
+            traffic = profiled_traffic(wl)[0] if args.noise == 0 else None
+        copy_gbs = profiled_traffic(wl)[1]
         hbm = state_bytes / (tile_ms / 1e3) / 1e9
         alu = flops / (tile_ms / 1e3) / 1e12
         launches = kcnt[0] / args.steps
@@ -262,7 +269,7 @@ def main():
                             "algorithmic_flops_per_step": flops,
                             "algorithmic_bytes_per_step": state_bytes,
                             "hbm": {"achieved": hbm, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                                    "frac": hbm / HBM_PEAK_GBS}}
+                                    "frac": hbm / HBM_PEAK_GBS, "copy_kernel": copy_gbs}}
         line["kernel_ms_per_step"] = {"k_tile": kms[0] / args.steps, "k_whole": kms[1] / args.steps,
                                       "k_bind": kms[2] / args.steps, "k_reduce": kms[3] / args.steps}
     elif timing and kcnt[1] > 0:
