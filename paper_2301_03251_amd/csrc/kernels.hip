@@ -997,15 +997,17 @@ __device__ __forceinline__ void zpart_tile(const T2* t, uint32_t tbit, const uin
     accf += tbit ? -wp : wp;
 }
 
-// OR over the 64 lanes (every lane gets the result): row butterfly by DPP,
-// then the four row results from readlanes.
-__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
-    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
-    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
-    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);
-    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);
-    return (uint32_t)(__builtin_amdgcn_readlane((int)v, 0) | __builtin_amdgcn_readlane((int)v, 16) |
-                      __builtin_amdgcn_readlane((int)v, 32) | __builtin_amdgcn_readlane((int)v, 48));
+// Bits of t deposited, lowest first, on the set bits of mask (both uniform:
+// scalar arithmetic).
+__device__ __forceinline__ uint32_t deposit_bits(uint32_t t, uint32_t mask) {
+    uint32_t r = 0;
+    while (mask) {
+        const uint32_t low = mask & (0u - mask);
+        if (t & 1u) r |= low;
+        t >>= 1;
+        mask ^= low;
+    }
+    return r;
 }
 
 // Kernel modes: one forward tile per iteration, two forward tiles per
@@ -1067,9 +1069,14 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     thread_layout<LOG_T>((uint32_t)tid, phases[ph0], tb0, ts0);
     thread_layout<LOG_T>((uint32_t)tid, phases[ph_st], tb_st, ts_st);
     const uint32_t toff0 = amp_offset(tb0), toff_st = amp_offset(tb_st);
-    // lane i < n_fixed holds fixed qubit i: a tile's fixed bits are the OR
-    // over lanes of (bit i of the tile index) << qubit
+    // lane i < n_fixed holds fixed qubit i (for the per-qubit sums)
     const uint32_t fq_lane = lane < n_fixed ? (uint32_t)P.fixed_qubit[lane] : 0u;
+    // a tile's fixed (out-of-tile) amplitude-index bits: the bits of the tile
+    // index deposited on the fixed qubits, lowest first. Uniform arithmetic:
+    // no lane-dependent value is needed where the tile loop begins, so its
+    // first wait is not a wait for every memory operation in flight.
+    uint32_t fixed_mask = 0;
+    for (int j = 0; j < n_fixed; ++j) fixed_mask |= 1u << P.fixed_qubit[j];
 
     // <Z> and seed constants of the last forward layout: the qubit of each
     // register bit and of each thread-index bit
@@ -1117,11 +1124,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     // highest fixed qubit
     const int64_t tiles = PAIR ? a.tiles >> 1 : a.tiles;
     const uint32_t top_fixed = (PAIR && n_fixed > 0) ? 1u << P.fixed_qubit[n_fixed - 1] : 0u;
-    // fixed-qubit bits of tile t (the same in every lane)
-    auto fixed_bits = [&](int64_t t) {
-        const uint32_t tb = lane < n_fixed ? (((uint32_t)t >> lane) & 1u) : 0u;
-        return wave_or(tb << fq_lane);
-    };
+    auto fixed_bits = [&](int64_t t) { return deposit_bits((uint32_t)t, fixed_mask); };
     T2 ps[R], lm[R];
     // one-tile forward mode: the next tile's loads are issued before this
     // tile's ops run (nothing in the ops reads nx, so they stay in flight
@@ -1133,7 +1136,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     for (int64_t tile = w; tile < tiles; tile += a.n_wg) {
         const uint32_t tbit = lane < n_fixed ? (((uint32_t)tile >> lane) & 1u) : 0u;
         TileCtx cx;
-        cx.gb = wave_or(tbit << fq_lane);
+        cx.gb = fixed_bits(tile);
         cx.gb2 = cx.gb | top_fixed;
         cx.ph = ph0;
         cx.tb = tb0;
