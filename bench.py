@@ -176,7 +176,7 @@ def main():
     elif shift:
         step = lambda: runner.param_shift(xt, wt, gt, max_chunk=chunk, outs=outs)  # noqa: E731
     else:
-        runner.workspace(wl.batch, Q.MODE_FWD_BWD)
+        runner.workspace(wl.batch, runner.backward_mode(wl.batch))
         step = lambda: runner.forward_backward(xt, wt, gt, outs=outs)  # noqa: E731
     if args.calibrate:
         src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
@@ -241,6 +241,8 @@ def main():
     elif shift:
         line["config"].update({"grad": "parameter shift", "circuits_per_step": n_shift,
                                "chunk": chunk})
+    else:
+        line["config"]["kept_states"] = runner.backward_mode(wl.batch) == Q.MODE_FWD_BWD_KEEP
         line["vjp_per_s"] = 1e3 / ms_step
     if timing and kcnt[0] > 0:
         tile_ms = kms[0] / args.steps
@@ -253,7 +255,7 @@ def main():
             flops = shift_flops(gates, wl.batch, wl.n)
             traffic = None
         else:
-            state_bytes = circ.state_bytes(wl.dtype, wl.batch)
+            state_bytes = circ.state_bytes(wl.dtype, wl.batch, runner.backward_mode(wl.batch))
             flops = algorithmic_flops(gates, wl.batch, wl.n)
             traffic = profiled_traffic(wl)[0] if args.noise == 0 else None
         copy_gbs = profiled_traffic(wl)[1]

@@ -113,7 +113,20 @@ typedef struct {
 
 typedef enum { QL_C64 = 0, QL_C128 = 1 } ql_dtype;
 
-enum { QL_MODE_FWD = 0, QL_MODE_FWD_BWD = 1 };
+/* Workspace modes. QL_MODE_FWD_BWD_KEEP is ql_forward_backward with the
+ * state after every tile pass but the last kept in the workspace: the
+ * backward pass over tile pass p+1 then leaves its un-computed state unstored
+ * and the one over pass p loads the kept state after pass p instead (one
+ * state write fewer per backward pass: 5m - 5 instead of 6m - 6 state
+ * transfers for m tile passes), at the cost of m - 2 more states of
+ * workspace (m - 1 with an embedding, whose initial state keeps its
+ * buffer). ql_forward_backward takes this path whenever its workspace holds
+ * ql_workspace_bytes(..., QL_MODE_FWD_BWD_KEEP) bytes; results agree with the
+ * other path up to rounding (the backward reads the forward's states rather
+ * than re-derived ones). With one tile pass (or the whole-state kernel) there
+ * is nothing to keep; with two the kept state takes the place of the psi
+ * buffer, the two sizes are equal and the states are always kept. */
+enum { QL_MODE_FWD = 0, QL_MODE_FWD_BWD = 1, QL_MODE_FWD_BWD_KEEP = 2 };
 
 enum {
     QL_OK = 0,
@@ -168,7 +181,8 @@ int ql_circuit_create_desc(int32_t n_qubits, const ql_gate* gates, int32_t n_gat
 
 void ql_circuit_destroy(ql_circuit* c);
 
-/* Bytes of device workspace a call with this dtype, batch and mode needs. */
+/* Bytes of device workspace a call with this dtype, batch and mode
+ * (QL_MODE_*) needs. */
 int ql_workspace_bytes(const ql_circuit* c, ql_dtype dtype, int64_t batch, int mode,
                        size_t* out);
 
@@ -282,8 +296,9 @@ int ql_plan_info_get(const ql_circuit* c, ql_dtype dtype, ql_plan_info* out);
 int ql_plan_schedule(const ql_circuit* c, ql_dtype dtype, int32_t* pass_of_gate,
                      int32_t* order);
 
-/* Algorithmic HBM bytes of the state passes of one call (reads + writes of
- * psi and lambda by the tile kernel; 0 for the whole-state kernel). */
+/* Algorithmic HBM bytes of the state passes of one call in a mode (QL_MODE_*:
+ * reads + writes of psi and lambda by the tile kernel; 0 for the whole-state
+ * kernel). */
 int ql_plan_state_bytes(const ql_circuit* c, ql_dtype dtype, int64_t batch, int mode,
                         double* out);
 

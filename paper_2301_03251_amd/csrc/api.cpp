@@ -125,6 +125,9 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
 struct Layout {
     size_t tables = 0, coef = 0, opc = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
     size_t enorm = 0, edot = 0;  // embedding: per-circuit |x| or basis index; L_b
+    size_t keep = 0;             // kept forward states: n_keep buffers of state_bytes each
+    size_t state_bytes = 0;
+    int n_keep = 0;
     int n_wg = 1;
 };
 
@@ -171,7 +174,7 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
         if (nwg * B > (int64_t)INT32_MAX) return fail(QL_ENOMEM, "grid too large");
         L.n_wg = (int)nwg;
     }
-    const bool bwd = mode == QL_MODE_FWD_BWD;
+    const bool bwd = mode == QL_MODE_FWD_BWD || mode == QL_MODE_FWD_BWD_KEEP;
     size_t off = 0, sz = 0;
     L.tables = off;
     off = align256(off + h->t[dt].blob.size());
@@ -196,19 +199,32 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
     }
     // state buffers: psi between tile passes or for an embedded initial state
     // (the caller's buffer when own_psi is false); lambda between backward
-    // passes or for the amplitude-embedding gradient (lambda_0)
+    // passes or for the amplitude-embedding gradient (lambda_0). Keep mode
+    // gives each forward pass but the last its own output buffer, which the
+    // backward pass over the next pass reads instead of a stored
+    // un-computed state.
     const bool multi = !pl.whole_state && pl.passes.size() > 1;
     const bool emb = c.embed != E_NONE, amp_bwd = bwd && c.embed == E_AMPLITUDE;
+    const bool keep = multi && mode == QL_MODE_FWD_BWD_KEEP;
+    const bool need_psi = own_psi && (emb || (multi && !keep)), need_lam = (bwd && multi) || amp_bwd;
     size_t st = 0;
-    if ((own_psi && (multi || emb)) || (bwd && multi) || amp_bwd)
+    if (need_psi || need_lam || keep)
         if (!mul_ok((size_t)B, ((size_t)1 << c.n) * amp, st)) return fail(QL_ENOMEM, "size overflow");
-    if (own_psi && (multi || emb)) {
+    L.state_bytes = st;
+    if (need_psi) {
         L.psi = off;
         off = align256(off + st);
     }
-    if ((bwd && multi) || amp_bwd) {
+    if (need_lam) {
         L.lam = off;
         off = align256(off + st);
+    }
+    if (keep) {
+        L.keep = off;
+        L.n_keep = (int)pl.passes.size() - 1;
+        if (!mul_ok(st, (size_t)L.n_keep, sz) || sz > SIZE_MAX - off - 256)
+            return fail(QL_ENOMEM, "size overflow");
+        off = align256(off + sz);
     }
     if (emb) {
         L.enorm = off;
@@ -358,6 +374,9 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
     // an embedded initial state is in the state buffer (written by embed())
     const bool emb = c.embed != E_NONE, amp_bwd = bwd && c.embed == E_AMPLITUDE;
     void* psi_buf = psi_ext ? psi_ext : (x.L.psi ? (void*)(x.W + x.L.psi) : nullptr);
+    // keep mode: kept[p] is the state after forward pass p
+    const bool keep = bwd && x.L.n_keep > 0;
+    auto kept = [&](int p) -> void* { return x.W + x.L.keep + (size_t)p * x.L.state_bytes; };
     if (pl.whole_state) {
         WholeArgs wa{};
         wa.gates = (const DevGate*)(x.W + x.L.tables + x.T.off_gates);
@@ -385,10 +404,12 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
     const int m = (int)pl.passes.size();
     const int threads = 1 << pl.log_t;
     const int NW = threads / 64;
-    auto launch_pass = [&](int p, int flags) -> int {
+    // psi_in: the state the pass loads; psi_out: where it stores its state
+    auto launch_pass = [&](int p, int flags, void* psi_in, void* psi_out) -> int {
         const DevPass& d = x.T.passes[p];
         TileArgs ta{};
-        ta.psi = psi_buf;
+        ta.psi = psi_in;
+        ta.psi_out = psi_out;
         ta.lam = x.L.lam ? (void*)(x.W + x.L.lam) : nullptr;
         ta.pass = (const DevPass*)(x.W + x.L.tables + x.T.off_pass) + p;
         ta.phases = (const DevPhase*)(x.W + x.L.tables + x.T.off_phase);
@@ -424,16 +445,23 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
     const int init = emb ? 0 : PF_INIT;
     const int lam0 = amp_bwd ? PF_STORE_LAM : 0;
     for (int p = 0; p + 1 < m; p++) {
-        rc = launch_pass(p, (p == 0 ? init : 0) | PF_FWD | PF_STORE_PSI);
+        void* out = keep ? kept(p) : psi_buf;
+        void* in = keep && p > 0 ? kept(p - 1) : (p == 0 && !emb ? out : psi_buf);
+        rc = launch_pass(p, (p == 0 ? init : 0) | PF_FWD | PF_STORE_PSI, in, out);
         if (rc) return rc;
     }
+    // with kept states no backward pass stores psi: the next one loads the
+    // forward state instead
+    const int bwd_psi = keep ? 0 : PF_STORE_PSI;
     int last = (m == 1 ? init : 0) | PF_FWD | (psi_ext ? PF_STORE_PSI : PF_ZPART);
-    if (bwd) last |= PF_SEED | PF_BWD | (m > 1 ? (PF_STORE_PSI | PF_STORE_LAM) : lam0);
-    rc = launch_pass(m - 1, last);
+    if (bwd) last |= PF_SEED | PF_BWD | (m > 1 ? (bwd_psi | PF_STORE_LAM) : lam0);
+    void* last_in = keep ? kept(m - 2) : psi_buf;
+    rc = launch_pass(m - 1, last, last_in, keep ? last_in : psi_buf);
     if (rc) return rc;
     if (bwd)
         for (int p = m - 2; p >= 0; p--) {
-            rc = launch_pass(p, PF_LOAD_LAM | PF_BWD | (p > 0 ? (PF_STORE_PSI | PF_STORE_LAM) : lam0));
+            void* in = keep ? kept(p) : psi_buf;
+            rc = launch_pass(p, PF_LOAD_LAM | PF_BWD | (p > 0 ? (bwd_psi | PF_STORE_LAM) : lam0), in, in);
             if (rc) return rc;
         }
     return QL_OK;
@@ -486,6 +514,11 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
     Layout L;
     int rc = compute_layout(h, dt, B, mode, L);
     if (rc) return rc;
+    if (bwd) {  // keep the forward states when the workspace holds them
+        Layout K;
+        if (compute_layout(h, dt, B, QL_MODE_FWD_BWD_KEEP, K) == QL_OK && K.n_keep > 0 && ws_bytes >= K.total)
+            L = K;
+    }
     rc = check_args(h->c, inputs, weights, expz, bwd, grad_out, ws);
     if (rc) return rc;
     if (ws_bytes < L.total)
@@ -740,7 +773,8 @@ void ql_circuit_destroy(ql_circuit* h) {
 int ql_workspace_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, int mode, size_t* out) {
     if (!h || !out) return fail(QL_EINVAL, "NULL argument");
     if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
-    if (mode != QL_MODE_FWD && mode != QL_MODE_FWD_BWD) return fail(QL_EINVAL, "unknown mode");
+    if (mode != QL_MODE_FWD && mode != QL_MODE_FWD_BWD && mode != QL_MODE_FWD_BWD_KEEP)
+        return fail(QL_EINVAL, "unknown mode");
     Layout L;
     int rc = compute_layout(h, (int)dtype, batch, mode, L);
     if (rc) return rc;
@@ -900,7 +934,8 @@ int ql_plan_state_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, int 
     const double S = (double)batch * (double)((size_t)1 << h->c.n) * (dtype == QL_C64 ? 8.0 : 16.0);
     const int m = (int)pl.passes.size();
     double units = 0;
-    if (!pl.whole_state && m > 1) units = mode == QL_MODE_FWD_BWD ? 6.0 * m - 6.0 : 2.0 * m - 2.0;
+    if (!pl.whole_state && m > 1)
+        units = mode == QL_MODE_FWD_BWD ? 6.0 * m - 6.0 : mode == QL_MODE_FWD_BWD_KEEP ? 5.0 * m - 5.0 : 2.0 * m - 2.0;
     *out = units * S;
     return QL_OK;
 }

@@ -1044,7 +1044,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     Real* gacc = (Real*)(red + (size_t)n * NW);        // [n_gslots][NW][GW]
 
     const size_t dim = (size_t)1 << n;
-    T2* psi_s = (T2*)a.psi + b * dim;
+    const T2* psi_s = (const T2*)a.psi + b * dim;
+    T2* psi_o = (T2*)a.psi_out + b * dim;
     T2* lam_s = (T2*)a.lam + b * dim;
     const XOp<Real>* xops = xops_all + b * (a.n_ops + 1);
     const Real* gout = gout_all + b * n;
@@ -1219,11 +1220,11 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
             const DevPhase& F = phases[ph_st];
             const uint32_t base = cx.gb | toff_st;
             if (flags & PF_STORE_PSI) {
-                T2* dst = psi_s + base;
+                T2* dst = psi_o + base;
 #pragma unroll
                 for (int i = 0; i < R; ++i) dst[F.reg_qoff[i]] = ps[i];
                 if constexpr (PAIR) {
-                    T2* dst2 = psi_s + (cx.gb2 | toff_st);
+                    T2* dst2 = psi_o + (cx.gb2 | toff_st);
 #pragma unroll
                     for (int i = 0; i < R; ++i) dst2[F.reg_qoff[i]] = lm[i];
                 }

@@ -129,7 +129,8 @@ struct SampleArgs {
 };
 
 struct TileArgs {
-    void* psi;                 // [B][2^n] complex
+    const void* psi;           // [B][2^n] complex: loaded state
+    void* psi_out;             // [B][2^n] complex: stored state (psi itself, or another buffer)
     void* lam;                 // [B][2^n] complex
     const DevPass* pass;
     const DevPhase* phases;

@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libqlayer.so")
 
 C64, C128 = 0, 1
-MODE_FWD, MODE_FWD_BWD = 0, 1
+MODE_FWD, MODE_FWD_BWD, MODE_FWD_BWD_KEEP = 0, 1, 2
 H, RX, RY, RZ, CNOT, CZ, CRX, CRY, CRZ, PAULI = range(10)
 SRC_NONE, SRC_INPUT, SRC_WEIGHT = 0, 1, 2
 EMBED_NONE, EMBED_BASIS, EMBED_AMPLITUDE = 0, 1, 2
@@ -232,15 +232,40 @@ def _ptr(t):
 
 
 class Runner:
-    """Holds a circuit, a dtype and a reusable device workspace."""
+    """Holds a circuit, a dtype and a reusable device workspace.
 
-    def __init__(self, circuit: Circuit, dtype="c64", device="cuda"):
+    keep_states: forward_backward keeps the state after every tile pass in the
+    workspace (QL_MODE_FWD_BWD_KEEP: fewer HBM bytes, m - 2 more states of
+    memory for m passes) when True, never when False, and when None whenever
+    the larger workspace fits in 80 % of the device's free memory. With two
+    passes the sizes are equal and the library always keeps the state."""
+
+    def __init__(self, circuit: Circuit, dtype="c64", device="cuda", keep_states=None):
         torch = _torch()
         self.c = circuit
         self.dtype = dtype
         self.real = torch.float32 if _dt(dtype) == C64 else torch.float64
         self.device = torch.device(device)
+        self.keep_states = keep_states
         self._ws = None
+
+    def backward_mode(self, batch) -> int:
+        """MODE_FWD_BWD_KEEP or MODE_FWD_BWD, as forward_backward will run."""
+        info = self.c.plan_info(self.dtype)
+        if info["kernel"] == 0 or info["n_passes"] < 2:
+            return MODE_FWD_BWD  # whole state, or one tile pass: nothing to keep
+        need = self.c.workspace_bytes(self.dtype, batch, MODE_FWD_BWD_KEEP)
+        if need == self.c.workspace_bytes(self.dtype, batch, MODE_FWD_BWD):
+            return MODE_FWD_BWD_KEEP  # two passes: the kept state replaces the psi buffer
+        if self.keep_states is False:
+            return MODE_FWD_BWD
+        if self.keep_states:
+            return MODE_FWD_BWD_KEEP
+        have = self._ws.numel() if self._ws is not None else 0
+        if need <= have:
+            return MODE_FWD_BWD_KEEP
+        free, _ = _torch().cuda.mem_get_info(self.device)
+        return MODE_FWD_BWD_KEEP if need - have <= 0.8 * free else MODE_FWD_BWD
 
     def workspace(self, batch, mode):
         torch = _torch()
@@ -282,11 +307,15 @@ class Runner:
             gw = torch.empty(self.c.n_weights, dtype=self.real, device=self.device) if want_weights else None
         else:
             expz, gx, gw = outs
-        ws = self.workspace(B, MODE_FWD_BWD)
+        mode = self.backward_mode(B)
+        ws = self.workspace(B, mode)
+        # the library keeps the states whenever the workspace it is given holds
+        # them, so the plain path is handed exactly its own size
+        ws_bytes = ws.numel() if mode == MODE_FWD_BWD_KEEP else self.c.workspace_bytes(self.dtype, B, mode)
         self.c.forward_backward_raw(
             self.dtype, B, _ptr(x) if self.c.n_inputs else None, _ptr(w) if self.c.n_weights else None,
             _ptr(grad_out), _ptr(expz), _ptr(gx) if (gx is not None and self.c.n_inputs) else None,
-            _ptr(gw) if (gw is not None and self.c.n_weights) else None, _ptr(ws), ws.numel(),
+            _ptr(gw) if (gw is not None and self.c.n_weights) else None, _ptr(ws), ws_bytes,
             ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
         return expz, gx, gw
 

@@ -163,6 +163,30 @@ def test_workspace_arithmetic(lib):
     assert c.state_bytes("c64", 1, Q.MODE_FWD) == (2 * m - 2) * S
     small = Q.Circuit(4, W.get("4q").gates(), 4, 16)
     assert small.state_bytes("c128", 8) == 0.0   # whole state in LDS: no HBM state traffic
+    # kept forward states: lambda plus one state per pass but the last (no
+    # separate psi buffer), one state write fewer per backward pass
+    keep = c.workspace_bytes("c64", 1, Q.MODE_FWD_BWD_KEEP)
+    assert m * S <= keep < m * S + (64 << 20)
+    assert keep - fb == (m - 2) * S
+    assert c.state_bytes("c64", 1, Q.MODE_FWD_BWD_KEEP) == (5 * m - 5) * S
+    assert small.workspace_bytes("c64", 8, Q.MODE_FWD_BWD_KEEP) == small.workspace_bytes("c64", 8)
+    assert _err(lambda: c.workspace_bytes("c64", 1, 3)) == -1
+
+
+def test_keep_mode_embeddings_and_single_pass(lib):
+    # an embedded initial state keeps its own buffer; a one-pass tiled circuit
+    # has nothing to keep
+    n = 12
+    gates = W.random_circuit(n, 40, 2 ** n, 6, seed=3)
+    emb = Q.Circuit(n, gates, 2 ** n, 6, embed=(W.EMBED_AMPLITUDE, 0), log_regs=2, log_threads=6,
+                    max_gates_per_pass=8)
+    m = emb.plan_info("c64")["n_passes"]
+    assert m > 2
+    S = (1 << n) * 8 * 3
+    assert emb.workspace_bytes("c64", 3, Q.MODE_FWD_BWD_KEEP) - emb.workspace_bytes("c64", 3) == (m - 1) * S
+    one = Q.Circuit(n, gates[:1], 2 ** n, 6, force_tiled=1)
+    assert one.plan_info("c64")["n_passes"] == 1
+    assert one.workspace_bytes("c64", 3, Q.MODE_FWD_BWD_KEEP) == one.workspace_bytes("c64", 3)
 
 
 def _check_schedule(c, gates, dtype):

@@ -41,8 +41,9 @@ def _host(a, dtype):
     return np.asarray(a, np.float32 if dtype == "c64" else np.float64).astype(np.float64)
 
 
-def gpu_fb(circ, dtype, x, w, g):
-    e, gx, gw = Q.Runner(circ, dtype).forward_backward(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype))
+def gpu_fb(circ, dtype, x, w, g, keep_states=None):
+    r = Q.Runner(circ, dtype, keep_states=keep_states)
+    e, gx, gw = r.forward_backward(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype))
     torch.cuda.synchronize()
     return {"expz": e.cpu().double().numpy(), "grad_inputs": gx.cpu().double().numpy(),
             "grad_weights": gw.cpu().double().numpy()}
@@ -119,6 +120,21 @@ def test_embeddings_vs_oracle(kind, n, dtype, opts):
     circ = Q.Circuit(n, gates, x.shape[1], w.size, embed=emb, **opts)
     want = oracle.run(n, gates, _host(x, dtype), _host(w, dtype), grad_out=_host(g, dtype), embed=emb)
     check(gpu_fb(circ, dtype, x, w, g), want, TOL[dtype], f"embed {kind} n={n} {dtype} {opts}")
+
+
+@pytest.mark.parametrize("keep", [False, True], ids=["plain", "kept"])
+@pytest.mark.parametrize("kind", [W.EMBED_BASIS, W.EMBED_AMPLITUDE], ids=["basis", "amplitude"])
+def test_embeddings_kept_states(kind, keep):
+    """Multi-pass tiled circuits with an embedding, with and without the kept
+    forward states (the embedded state has its own buffer; lambda_0 is stored
+    by the last backward pass in both)."""
+    n, dtype = 12, "c64"
+    gates, x, w, g, emb = _embedded_case(n, kind, dtype, seed=1700 + kind)
+    circ = Q.Circuit(n, gates, x.shape[1], w.size, embed=emb, log_regs=3, log_threads=6,
+                     max_gates_per_pass=9)
+    assert circ.plan_info(dtype)["n_passes"] > 2
+    want = oracle.run(n, gates, _host(x, dtype), _host(w, dtype), grad_out=_host(g, dtype), embed=emb)
+    check(gpu_fb(circ, dtype, x, w, g, keep_states=keep), want, TOL[dtype], f"embed {kind} keep={keep}")
 
 
 def test_amplitude_embedding_zero_vector():

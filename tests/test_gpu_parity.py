@@ -92,6 +92,30 @@ def test_random_tiled(n, G, B, dtype, opts):
     check(got, want, TOL[dtype], f"tiled n={n} {dtype} {opts} passes={info['n_passes']}")
 
 
+@pytest.mark.parametrize("case", [1, 2, 5, 7, 9, 11])
+def test_kept_states_and_plain(case):
+    """forward_backward with the forward states kept in the workspace (the
+    backward passes load them) and without (each backward pass stores its
+    un-computed state): both against the oracle, and against each other."""
+    n, G, B, dtype, opts = TILED[case]
+    F, P = 5, 7
+    gates = W.random_circuit(n, G, F, P, seed=n * 100 + G)
+    x, w, g = W.random_inputs(B, F, P, n, seed=n + G, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P, **opts)
+    m = circ.plan_info(dtype)["n_passes"]
+    assert m > 1
+    want = oracle.run(n, gates, x, w, grad_out=g)
+    got = {}
+    # two passes: the kept state has the plain path's size and is always used
+    plain = Q.MODE_FWD_BWD if m > 2 else Q.MODE_FWD_BWD_KEEP
+    for keep, mode in ((False, plain), (True, Q.MODE_FWD_BWD_KEEP)):
+        r = Q.Runner(circ, dtype, keep_states=keep)
+        assert r.backward_mode(B) == mode
+        got[keep] = gpu_fb(circ, dtype, x, w, g, runner=r)
+        check(got[keep], want, TOL[dtype], f"tiled n={n} {dtype} keep={keep}")
+    check(got[True], got[False], TOL[dtype], f"kept vs plain n={n} {dtype}")
+
+
 @pytest.mark.parametrize("dtype", ["c64", "c128"])
 @pytest.mark.parametrize("n", [1, 2, 3, 5, 7, 8, 11, 12])
 def test_random_whole_state(n, dtype):
@@ -172,9 +196,11 @@ def test_workload_16q_sampled():
     assert np.all(np.abs(got["expz"]) <= 1 + 1e-5)
 
 
+@pytest.mark.parametrize("keep", [True, False], ids=["kept", "plain"])
 @pytest.mark.parametrize("name", ["24q", "30q"])
-def test_workload_golden(name):
-    """Full workload on the GPU vs oracle values stored by tests/golden/make_golden.py."""
+def test_workload_golden(name, keep):
+    """Full workload on the GPU vs oracle values stored by tests/golden/make_golden.py,
+    with and without the kept forward states."""
     path = os.path.join(GOLDEN, f"{name}.npz")
     if not os.path.exists(path):
         pytest.skip(f"{path} not generated")
@@ -187,7 +213,7 @@ def test_workload_golden(name):
     assert str(gold["digest"]) == make_golden.digest(x, w, g), "golden file is stale"
     rows = [int(v) for v in gold["rows"]]
     circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
-    r = Q.Runner(circ, wl.dtype)
+    r = Q.Runner(circ, wl.dtype, keep_states=keep)
     got = gpu_fb(circ, wl.dtype, x, w, g, r)
     if len(rows) < wl.batch:
         gm = np.zeros_like(g)
