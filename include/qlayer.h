@@ -152,6 +152,10 @@ typedef struct {
                                    -1 whole state in LDS whenever it fits (n <= 12 for
                                    QL_C64, n <= 11 for QL_C128) */
     int32_t wg_per_sample;      /* workgroups per sample in a tile pass */
+    int32_t rz_groups;          /* 0: RZs on the register bits of one tile layout that
+                                   commute into one place (at least three, on distinct
+                                   bits) run as one per-register phase op; -1: every
+                                   RZ runs on its own */
 } ql_options;
 
 typedef struct ql_circuit ql_circuit; /* opaque */
@@ -284,6 +288,7 @@ typedef struct {
                               parameter-shift count; a controlled rotation counts 2) */
     int32_t n_lane_swaps;  /* in-register layout changes (register bit <-> lane bit) summed
                               over the forward passes */
+    int32_t n_rz_groups;   /* RZ groups (several RZs run as one phase op), all passes */
 } ql_plan_info;
 
 int ql_plan_info_get(const ql_circuit* c, ql_dtype dtype, ql_plan_info* out);

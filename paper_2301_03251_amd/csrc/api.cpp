@@ -38,8 +38,9 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 struct Tables {
     std::vector<uint8_t> blob;
     size_t off_pass = 0, off_phase = 0, off_ops = 0, off_gslot = 0, off_slots = 0;
-    size_t off_xptr = 0, off_xslot = 0, off_wptr = 0, off_wslot = 0, off_gates = 0;
+    size_t off_xptr = 0, off_xslot = 0, off_wptr = 0, off_wslot = 0, off_gates = 0, off_diag = 0;
     std::vector<DevPass> passes;
+    int n_diags = 0;
     int n_ops = 0;
     int bwd_first = 0;
 };
@@ -117,13 +118,15 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
     T.off_wptr = put(T.blob, wptr);
     T.off_wslot = put(T.blob, ws);
     T.off_gates = put(T.blob, gates);
+    T.off_diag = put(T.blob, pl.diags);
+    T.n_diags = (int)pl.diags.size();
     T.blob.resize(align256(T.blob.size()), 0);
     T.passes = passes;
     T.n_ops = (int)ops.size();
 }
 
 struct Layout {
-    size_t tables = 0, coef = 0, opc = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
+    size_t tables = 0, coef = 0, opc = 0, dzc = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
     size_t enorm = 0, edot = 0;  // embedding: per-circuit |x| or basis index; L_b
     size_t keep = 0;             // kept forward states: n_keep buffers of state_bytes each
     size_t state_bytes = 0;
@@ -185,6 +188,11 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
         // per-sample op records (16 bytes fp32 / 32 bytes fp64) plus an end record
         L.opc = off;
         if (!mul_ok((size_t)B * (size_t)(h->t[dt].n_ops + 1), dt == 0 ? 16 : 32, sz))
+            return fail(QL_ENOMEM, "size overflow");
+        off = align256(off + sz);
+        // per-sample phase tables of the RZ groups
+        L.dzc = off;
+        if (!mul_ok((size_t)B * (size_t)h->t[dt].n_diags, (size_t)DZ_REGS * amp, sz))
             return fail(QL_ENOMEM, "size overflow");
         off = align256(off + sz);
     }
@@ -327,6 +335,9 @@ int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0,
         ba.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
         ba.ops = (const DevOp*)(x.W + x.L.tables + x.T.off_ops);
         ba.opc = x.W + x.L.opc;
+        ba.diags = (const DevDiag*)(x.W + x.L.tables + x.T.off_diag);
+        ba.dzc = x.W + x.L.dzc;
+        ba.n_diags = x.T.n_diags;
         ba.B = B;
         ba.n_ops = x.T.n_ops;
         ba.bwd_first = x.T.bwd_first;
@@ -416,6 +427,8 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         ta.ops = (const DevOp*)(x.W + x.L.tables + x.T.off_ops);
         ta.gslots = (const int32_t*)(x.W + x.L.tables + x.T.off_gslot) + d.gslot_base;
         ta.opc = x.W + x.L.opc;
+        ta.dzc = x.W + x.L.dzc;
+        ta.n_diags = x.T.n_diags;
         ta.grad_out = grad_out;
         ta.zpart = zpart;
         ta.gpart = gpart;
@@ -672,6 +685,8 @@ int state(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs, c
     ba.weights = weights;
     ba.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
     ba.ops = (const DevOp*)(x.W + x.L.tables + x.T.off_ops);
+    ba.diags = (const DevDiag*)(x.W + x.L.tables + x.T.off_diag);
+    ba.n_diags = x.T.n_diags;
     ba.B = B;
     ba.n_ops = x.T.n_ops;
     ba.bwd_first = x.T.bwd_first;
@@ -708,6 +723,7 @@ Options to_options(const ql_options* o) {
         r.max_gates_per_pass = o->max_gates_per_pass;
         r.force_tiled = o->force_tiled;
         r.wg_per_sample = o->wg_per_sample;
+        r.rz_groups = o->rz_groups;
     }
     return r;
 }
@@ -898,6 +914,7 @@ int ql_plan_info_get(const ql_circuit* h, ql_dtype dtype, ql_plan_info* out) {
         r.n_transposes += pp.n_transposes;
         r.n_lane_swaps += pp.n_lane_swaps;
     }
+    r.n_rz_groups = (int)pl.diags.size();
     r.n_param_gates = h->c.n_param_slots;
     *out = r;
     return QL_OK;

@@ -798,6 +798,52 @@ __device__ __forceinline__ void tile_ready(const double2* t) {
                      "v"(t[i + 2].y), "v"(t[i + 3].x), "v"(t[i + 3].y));
 }
 
+// RZ group (H_DZ): register i of the tile gets the phase exp(i phi_i), phi_i
+// the sum of the group's angles over the set bits of i (each RZ as
+// diag(1, exp(i theta)), as on a single register bit); tab[i] = (cos phi_i,
+// sin phi_i) from the binding kernel, INV: the inverse phase. A phase of any
+// size is exact this way (four operations per register).
+template <int LOG_R, bool INV, bool BOTH, typename T2>
+__device__ __forceinline__ void dz_apply(T2* a, T2* b, const T2* __restrict__ tab) {
+#pragma unroll
+    for (int i = 1; i < (1 << LOG_R); ++i) {
+        const T2 cs = tab[i];
+        const auto c = cs.x, sn = INV ? -cs.y : cs.y;
+        const auto x = a[i].x, y = a[i].y;
+        a[i].x = fma(c, x, -sn * y);
+        a[i].y = fma(c, y, sn * x);
+        if constexpr (BOTH) {
+            const auto u = b[i].x, v = b[i].y;
+            b[i].x = fma(c, u, -sn * v);
+            b[i].y = fma(c, v, sn * u);
+        }
+    }
+}
+
+// Gradient slot of the group's RZ on register bit J (NO_GSLOT: none), from
+// the record's two coefficient words.
+__device__ __forceinline__ uint32_t dz_gslot(float a, float b, int j) {
+    const uint32_t w = __builtin_bit_cast(uint32_t, j < 2 ? a : b);
+    return (w >> ((j & 1) * 16)) & 0xffffu;
+}
+__device__ __forceinline__ uint32_t dz_gslot(double a, double, int j) {
+    return (uint32_t)(__builtin_bit_cast(uint64_t, a) >> (j * 16)) & 0xffffu;
+}
+
+// Z-generator terms of the group's RZs (each as for a single RZ on its bit;
+// a diagonal op leaves every register's Im(conj(lambda) psi) unchanged, so
+// the terms are the same before and after the group's phase).
+template <int LOG_R, int J, typename T2, typename Real>
+__device__ __forceinline__ void dz_grads(const T2* ps, const T2* lm, Real ca, Real cb, Real ival, Real* gacc,
+                                         int lane, int wave, int nw) {
+    if constexpr (J < LOG_R) {
+        const uint32_t g = dz_gslot(ca, cb, J);
+        if (g != NO_GSLOT)
+            grad_add(gacc, g, fma((Real)-2, im_sum<LOG_R, J, T2, Real>(ps, lm), ival), lane, wave, nw);
+        dz_grads<LOG_R, J + 1>(ps, lm, ca, cb, ival, gacc, lane, wave, nw);
+    }
+}
+
 // Apply one op. OPM selects the register arrays it acts on:
 //   OP_ONE  -- ps only (one forward tile);
 //   OP_PAIR -- ps and lm, two forward tiles that differ in their fixed bits
@@ -815,7 +861,7 @@ template <int LOG_R, int LOG_T, int OPM, typename T2, typename Real>
 __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
                                        TileCtx& cx, Real& ival, unsigned char* lds,
                                        const DevPhase* phases, Real* gacc, int lane, int wave, int nw,
-                                       int tid) {
+                                       int tid, const T2* __restrict__ dz) {
 #define QL_G1_CASE(KIND, J)                                                                 \
     case H_G1 + KIND * 5 + J:                                                               \
         if constexpr (J < LOG_R) {                                                          \
@@ -916,6 +962,12 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         QL_LSWAP_M(0) QL_LSWAP_M(1) QL_LSWAP_M(2) QL_LSWAP_M(3) QL_LSWAP_M(4)
         QL_PAULI_J(0) QL_PAULI_J(1) QL_PAULI_J(2) QL_PAULI_J(3) QL_PAULI_J(4)
         case H_NOP:
+            break;
+        case H_DZ:
+            if constexpr (LOG_R <= MAX_DZ_BITS) {
+                if constexpr (OPM == OP_BWD) dz_grads<LOG_R, 0>(ps, lm, ca, cb, ival, gacc, lane, wave, nw);
+                dz_apply<LOG_R, OPM == OP_BWD, OPM != OP_ONE>(ps, lm, dz + (size_t)arg * DZ_REGS);
+            }
             break;
         case H_RZU: {
             const bool bit = loc_bit(arg, cx.tb, cx.gb);
@@ -1019,7 +1071,7 @@ template <typename Real, int LOG_R, int KM, int MAXT>
 __global__ void __launch_bounds__(MAXT) __attribute__((amdgpu_waves_per_eu(2)))
 k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __restrict__ phases,
        const XOp<Real>* __restrict__ xops_all, const Real* __restrict__ gout_all,
-       const int32_t* __restrict__ gslots) {
+       const int32_t* __restrict__ gslots, const typename Cx<Real>::T* __restrict__ dz_all) {
     using T2 = typename Cx<Real>::T;
     constexpr bool BWD = KM == KM_BWD, PAIR = KM == KM_FWD2;
     constexpr int R = 1 << LOG_R;
@@ -1048,6 +1100,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     T2* psi_o = (T2*)a.psi_out + b * dim;
     T2* lam_s = (T2*)a.lam + b * dim;
     const XOp<Real>* xops = xops_all + b * (a.n_ops + 1);
+    const T2* dz = dz_all + b * a.n_diags * DZ_REGS;
     const Real* gout = gout_all + b * n;
 
     if (BWD && (flags & PF_BWD)) {
@@ -1171,7 +1224,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 const XOp<Real> nxt = xops[o + 1];
                 run_op<LOG_R, LOG_T, PAIR ? OP_PAIR : OP_ONE>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx,
                                                               ival, lds, phases, gacc, lane, wave, NW,
-                                                              tid);
+                                                              tid, dz);
                 cur = nxt;
             }
         }
@@ -1210,7 +1263,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
                     run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, ival, lds,
-                                                 phases, gacc, lane, wave, NW, tid);
+                                                 phases, gacc, lane, wave, NW, tid, dz);
                     cur = nxt;
                 }
             }
@@ -1514,6 +1567,7 @@ __global__ void __launch_bounds__(64) k_wave(const WholeArgs a, const DevGate* _
 
 template <typename Real>
 __global__ void k_bind_tile(const BindTileArgs a) {
+    using T2 = typename Cx<Real>::T;
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t per = (int64_t)a.n_ops + 1;
     if (t >= a.B * per) return;
@@ -1528,7 +1582,39 @@ __global__ void k_bind_tile(const BindTileArgs a) {
     const DevOp op = a.ops[o];
     e.h = op.h;
     e.arg = op.arg;
-    if (op.kind == K_PAULI) {
+    if (op.h == H_DZ) {
+        // RZ group: the members' gradient slots in the two coefficient words;
+        // the forward record also writes the sample's phase table (the
+        // backward record reads the same table and applies its inverse)
+        const DevDiag d = a.diags[op.arg];
+        uint64_t w = 0;
+        for (int j = 0; j < MAX_DZ_BITS; ++j) w |= (uint64_t)(d.gslot[j] & 0xffffu) << (16 * j);
+        if constexpr (sizeof(Real) == 4) {
+            e.a = __builtin_bit_cast(float, (uint32_t)w);
+            e.b = __builtin_bit_cast(float, (uint32_t)(w >> 32));
+        } else {
+            e.a = __builtin_bit_cast(double, w);
+        }
+        if (o < a.bwd_first) {
+            double th[MAX_DZ_BITS];
+            for (int j = 0; j < MAX_DZ_BITS; ++j) {
+                th[j] = 0.0;
+                if (d.slot[j] < 0) continue;
+                int64_t bs;
+                th[j] = angle_of<Real>(a.inputs, a.weights, a.F, a.slots[d.slot[j]], b, a.v0, a.vper, bs) +
+                        shift_of(b, a.v0, a.vper, d.slot[j]);
+            }
+            T2* tab = (T2*)a.dzc + ((size_t)b * a.n_diags + op.arg) * DZ_REGS;
+            for (int i = 0; i < DZ_REGS; ++i) {
+                double phi = 0.0;
+                for (int j = 0; j < MAX_DZ_BITS; ++j)
+                    if (i >> j & 1) phi += th[j];
+                double sn, cs;
+                sincos(phi, &sn, &cs);
+                tab[i] = mk<T2>((Real)cs, (Real)sn);
+            }
+        }
+    } else if (op.kind == K_PAULI) {
         // the Pauli this sample's trajectory draws, on the op's register bit
         const int which = pauli_of<Real>(a.inputs, a.F, a.slots[op.slot], b, a.v0, a.vper);
         e.h = which == 0 ? (uint32_t)H_NOP : op.h + 5u * (uint32_t)(which - 1);
@@ -1671,6 +1757,13 @@ __global__ void k_state_phase(const BindTileArgs a, double* phase) {
     int64_t bs;
     for (int o = 0; o < a.bwd_first; ++o) {
         const DevOp op = a.ops[o];
+        if (op.h == H_DZ) {  // an RZ group drops exp(-i theta / 2) per member, unreduced
+            const DevDiag d = a.diags[op.arg];
+            for (int j = 0; j < MAX_DZ_BITS; ++j)
+                if (d.slot[j] >= 0)
+                    ph += 0.5 * angle_of<Real>(a.inputs, a.weights, a.F, a.slots[d.slot[j]], b, 0, 0, bs);
+            continue;
+        }
         if (op.slot < 0 || op.kind == K_PAULI) continue;  // Paulis are applied exactly
         const double th = angle_of<Real>(a.inputs, a.weights, a.F, a.slots[op.slot], b, 0, 0, bs);
         const double k = rint(th / two_pi);
@@ -1976,15 +2069,16 @@ static hipError_t launch_tile_t(bool bwd, const TileArgs& a, int threads, size_t
     const dim3 grid((unsigned)(a.B * a.n_wg));
     const XOp<Real>* xo = (const XOp<Real>*)a.opc;
     const Real* gout = (const Real*)a.grad_out;
+    const typename Cx<Real>::T* dzt = (const typename Cx<Real>::T*)a.dzc;
     if (bwd)
         hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_BWD, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
-                           a.phases, xo, gout, a.gslots);
+                           a.phases, xo, gout, a.gslots, dzt);
     else if (a.tiles >= 2)  // forward passes carry two tiles per iteration when there are two
         hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_FWD2, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
-                           a.phases, xo, gout, a.gslots);
+                           a.phases, xo, gout, a.gslots, dzt);
     else
         hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_FWD1, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
-                           a.phases, xo, gout, a.gslots);
+                           a.phases, xo, gout, a.gslots, dzt);
     return hipGetLastError();
 }
 

@@ -43,6 +43,9 @@ struct BindTileArgs {
     const SlotSrc* slots;  // [n_slots]
     const DevOp* ops;      // [n_ops]
     void* opc;             // [B][n_ops + 1] records
+    const DevDiag* diags;  // [n_diags] RZ groups
+    void* dzc;             // [B][n_diags][DZ_REGS] complex: (cos, sin) of each register's phase
+    int32_t n_diags;
     int64_t B;
     int32_t n_ops, bwd_first, F;
     int64_t v0;            // parameter-shift chunks: first virtual circuit
@@ -128,6 +131,9 @@ struct SampleArgs {
     int32_t n, bb;
 };
 
+// Registers of an RZ group's phase table (one entry per register index).
+constexpr int DZ_REGS = 1 << MAX_DZ_BITS;
+
 struct TileArgs {
     const void* psi;           // [B][2^n] complex: loaded state
     void* psi_out;             // [B][2^n] complex: stored state (psi itself, or another buffer)
@@ -137,6 +143,8 @@ struct TileArgs {
     const DevOp* ops;
     const int32_t* gslots;     // pass-local gradient index -> rotation slot
     const void* opc;           // [B][n_ops + 1] per-sample op records
+    const void* dzc;           // [B][n_diags][DZ_REGS] RZ-group phase tables
+    int32_t n_diags;
     const void* grad_out;      // [B][n] Real
     double* zpart;             // [B][n_wg][n]
     double* gpart;             // [n_slots][B][n_wg]

@@ -95,8 +95,22 @@ DevPhase make_phase(const std::vector<int>& tq, const std::vector<int>& reg_bits
 }
 
 // Schedule the gates of one pass onto register phases.
+// Whether op h (a gate op within one layout) commutes with Z on each register
+// bit of `bits`: diagonal ops do, CNOTs whose target is not in `bits` do (a Z
+// on the control commutes), other one-qubit ops do unless they act on a bit
+// of `bits`.
+bool commutes_with_z(uint32_t h, uint32_t bits) {
+    auto off = [&](uint32_t j) { return !(bits >> j & 1u); };
+    if (h < H_G1 + 20) return (h - H_G1) / 5 == 3 || off((h - H_G1) % 5);
+    if (h == H_RZU || (h >= H_CZ_RR && h <= H_CZ_XX)) return true;
+    if (h >= H_CNOT_RR && h < H_CNOT_T) return off((h - H_CNOT_RR) / 5);
+    if (h >= H_CNOT_T && h < H_CZ_RR) return off((h - H_CNOT_T) % 5);
+    if (h >= H_PX && h < H_PX + 15) return (h - H_PX) / 5 == 2 || off((h - H_PX) % 5);
+    return false;
+}
+
 void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_r, int low,
-                   uint32_t amp, std::vector<DevPhase>& phases) {
+                   uint32_t amp, std::vector<DevPhase>& phases, std::vector<DevDiag>* diags) {
     const int r = log_r;
     std::vector<int> bit_of(64, -1);  // qubit -> tile bit
     for (int j = 0; j < k; j++) bit_of[pp.qubits[j]] = j;
@@ -341,9 +355,57 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         for (size_t i = 0; i < in.size(); i++) lane_swap(slot_of(regs, out[i]), slot_of(thr, in[i]));
     };
 
+    // RZ groups: within the ops of one layout, each RZ on a register bit is
+    // moved later, past ops that commute with it (an RZ and its gradient term
+    // are unchanged by that), and collected. An op that does not commute with
+    // a collected RZ, or a second RZ on its bit, ends the collection there:
+    // as one H_DZ op if MIN_DZ_SIZE or more RZs are collected, else by putting
+    // out only the RZs in the way, on their own (the others move on).
+    auto group_rz = [&](size_t seg0) {
+        if (!diags || r > MAX_DZ_BITS) return;
+        std::vector<Rec> out(recs.begin(), recs.begin() + (long)seg0);
+        Rec grp[MAX_DZ_BITS];
+        uint32_t bits = 0;
+        auto put_out = [&](uint32_t which) {
+            if (__builtin_popcount(bits) >= MIN_DZ_SIZE) {
+                DevDiag d;
+                for (int j = 0; j < MAX_DZ_BITS; j++) {
+                    d.slot[j] = (bits >> j & 1u) ? grp[j].op.slot : -1;
+                    d.gslot[j] = (bits >> j & 1u) ? grp[j].op.arg : NO_GSLOT;
+                }
+                const uint32_t idx = (uint32_t)diags->size();
+                diags->push_back(d);
+                out.push_back({make_op(H_DZ, idx, -1, K_RZ), idx});
+                bits = 0;
+                return;
+            }
+            for (int j = 0; j < MAX_DZ_BITS; j++)
+                if ((which & bits) >> j & 1u) out.push_back(grp[j]);
+            bits &= ~which;
+        };
+        for (size_t i = seg0; i < recs.size(); i++) {
+            const uint32_t h = recs[i].op.h;
+            if (h >= H_G1 + 15 && h < H_G1 + 15 + (uint32_t)r) {
+                const uint32_t j = h - (H_G1 + 15);
+                if (bits >> j & 1u) put_out(1u << j);
+                grp[j] = recs[i];
+                bits |= 1u << j;
+                continue;
+            }
+            uint32_t clash = 0;
+            for (int j = 0; j < MAX_DZ_BITS; j++)
+                if ((bits >> j & 1u) && !commutes_with_z(h, 1u << j)) clash |= 1u << j;
+            if (clash) put_out(clash);
+            out.push_back(recs[i]);
+        }
+        put_out(bits);
+        recs.swap(out);
+    };
+
     while (!pending.empty()) {
         uint64_t blocked = 0;
         std::vector<int> rest;
+        const size_t seg0 = recs.size();
         for (int gi : pending) {
             const Gate& g = gates[gi];
             uint64_t qs = (1ull << g.q0) | (n_qubits_of(g) == 2 ? (1ull << g.q1) : 0);
@@ -391,6 +453,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
             }
             recs.push_back({op, op.arg});
         }
+        group_rz(seg0);
         pending.swap(rest);
         if (pending.empty()) break;
         change_to(choose_next());
@@ -527,6 +590,7 @@ std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, i
     if (o.low_qubits && (o.low_qubits < 1 || o.low_qubits > 8)) return "option: low_qubits out of range [1, 8]";
     if (o.max_gates_per_pass < 0) return "option: max_gates_per_pass < 0";
     if (o.wg_per_sample < 0) return "option: wg_per_sample < 0";
+    if (o.rz_groups != 0 && o.rz_groups != -1) return "option: rz_groups must be 0 or -1";
     for (int dt = 0; dt < 2; dt++) {
         std::string e = build_plan(out, dt, out.plan[dt]);
         if (!e.empty()) return e;
@@ -600,7 +664,8 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         pp.gates = best;
         for (int gi : best) done[gi] = 1;
         remaining -= (int)best.size();
-        schedule_pass(c.gates, pp, k, log_r, low, dtype == 0 ? 8u : 16u, pl.phases);
+        schedule_pass(c.gates, pp, k, log_r, low, dtype == 0 ? 8u : 16u, pl.phases,
+                      o.rz_groups == 0 ? &pl.diags : nullptr);
         pl.passes.push_back(std::move(pp));
         if (G == 0) break;
     }

@@ -73,9 +73,25 @@ enum HandlerId : uint32_t {
     H_PX = 123,        // + P * 5 + J: Pauli X (P = 0), Y (1) or Z (2) on register bit J; a
                        //      channel op is planned as H_PX + J and set per sample by the
                        //      binding kernel to the Pauli its uniform selects, or to H_NOP
-    H_NOP = 138,
-    H_END = 139,
+    H_DZ = 138,        // RZ group: the RZs of up to MAX_DZ_BITS register bits in one diagonal
+                       //      op (a per-register phase); arg = group index (DevDiag)
+    H_NOP = 139,
+    H_END = 140,
 };
+// Register bits an RZ group can span (its gradient slots travel in the op
+// record's two coefficient words, 16 bits each).
+constexpr int MAX_DZ_BITS = 4;
+// An RZ group is formed from at least this many RZs: below it the separate
+// ops cost less than a phase on every register.
+constexpr int MIN_DZ_SIZE = 3;
+
+// Members of an RZ group, by register bit J: the rotation slot and the
+// gradient slot of the RZ on bit J (-1 / NO_GSLOT: no RZ on that bit).
+struct DevDiag {
+    int32_t slot[MAX_DZ_BITS];
+    uint32_t gslot[MAX_DZ_BITS];
+};
+static_assert(sizeof(DevDiag) == 32, "DevDiag layout");
 // Argument of a lane swap: the new phase (< 2^20) and the tile bits x (leaving
 // the lane bit for the registers) and y (taking its place).
 constexpr uint32_t lswap_arg(uint32_t phase, uint32_t x, uint32_t y) {
@@ -159,6 +175,7 @@ struct DevPass {
 struct Options {
     int log_regs = 0, log_threads = 0, low_qubits = 0, max_gates_per_pass = 0;
     int force_tiled = 0, wg_per_sample = 0;
+    int rz_groups = 0;  // 0: RZs on register bits are grouped into H_DZ ops; -1: never
 };
 
 // One forward tile pass as planned (host form).
@@ -179,6 +196,7 @@ struct Plan {
     int n = 0, k = 0, log_r = 0, log_t = 0, low = 0;
     std::vector<PassPlan> passes;
     std::vector<DevPhase> phases;
+    std::vector<DevDiag> diags;  // RZ groups (H_DZ ops), all passes
     int n_slots = 0;           // rotation slots
 };
 

@@ -34,7 +34,7 @@ class QLError(RuntimeError):
 class _Options(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("log_regs", "log_threads", "low_qubits",
                                               "max_gates_per_pass", "force_tiled",
-                                              "wg_per_sample")]
+                                              "wg_per_sample", "rz_groups")]
 
 
 class _Desc(ctypes.Structure):
@@ -45,7 +45,7 @@ class _Desc(ctypes.Structure):
 class _PlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "n_passes", "tile_qubits", "log_regs",
                                               "log_threads", "low_qubits", "n_transposes",
-                                              "n_param_gates", "n_lane_swaps")]
+                                              "n_param_gates", "n_lane_swaps", "n_rz_groups")]
 
 
 _lib = None

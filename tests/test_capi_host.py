@@ -71,7 +71,8 @@ def test_create_rejects(lib, gates, n, F, P, code):
 
 
 @pytest.mark.parametrize("opts", [dict(log_regs=1), dict(log_regs=6), dict(log_threads=5),
-                                  dict(log_threads=10), dict(low_qubits=9), dict(wg_per_sample=-1)])
+                                  dict(log_threads=10), dict(low_qubits=9), dict(wg_per_sample=-1),
+                                  dict(rz_groups=2)])
 def test_create_rejects_options(lib, opts):
     assert _err(lambda: Q.Circuit(14, np.array(G1, np.int32), 0, 1, **opts)) == -3
 
@@ -171,6 +172,21 @@ def test_workspace_arithmetic(lib):
     assert c.state_bytes("c64", 1, Q.MODE_FWD_BWD_KEEP) == (5 * m - 5) * S
     assert small.workspace_bytes("c64", 8, Q.MODE_FWD_BWD_KEEP) == small.workspace_bytes("c64", 8)
     assert _err(lambda: c.workspace_bytes("c64", 1, 3)) == -1
+
+
+@pytest.mark.parametrize("name", ["16q", "24q", "30q"])
+def test_rz_groups_in_workload_plans(lib, name):
+    """The workloads' RZs on register bits form groups; the option turns them off."""
+    wl = W.get(name)
+    on = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    off = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, rz_groups=-1)
+    for dt in ("c64", "c128"):
+        assert on.plan_info(dt)["n_rz_groups"] > 0
+        assert off.plan_info(dt)["n_rz_groups"] == 0
+        assert on.plan_info(dt)["n_passes"] == off.plan_info(dt)["n_passes"]
+        # grouping moves ops within a pass, never between passes
+        assert np.array_equal(on.schedule(dt)[0], off.schedule(dt)[0])
+    assert _err(lambda: Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, rz_groups=1)) == -3
 
 
 def test_keep_mode_embeddings_and_single_pass(lib):
