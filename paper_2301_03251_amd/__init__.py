@@ -4,7 +4,7 @@ C ABI (``include/qlayer.h``). See ``qlayer.py`` for the Python binding."""
 
 from .qlayer import (C64, C128, MODE_FWD, MODE_FWD_BWD, MODE_FWD_BWD_KEEP, Circuit, QLError, Runner,  # noqa: F401
                      sample, sample_workspace_bytes,
-                     load, quantum_layer_function)
+                     load, quantum_layer_function, QuantumLayer)
 
 __all__ = ["C64", "C128", "MODE_FWD", "MODE_FWD_BWD", "MODE_FWD_BWD_KEEP", "Circuit", "QLError", "Runner", "load", "sample", "sample_workspace_bytes",
-           "quantum_layer_function"]
+           "quantum_layer_function", "QuantumLayer"]

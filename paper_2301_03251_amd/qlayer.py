@@ -417,3 +417,47 @@ def quantum_layer_function():
             return None, gx, gw
 
     return QuantumLayerFn
+
+
+_QL_MODULE = None
+
+
+def _ql_module_class():
+    global _QL_MODULE
+    if _QL_MODULE is None:
+        torch = _torch()
+
+        class QuantumLayerModule(torch.nn.Module):
+            def __init__(self, circuit, dtype, device, weights, keep_states):
+                super().__init__()
+                self.circuit = circuit
+                self.runner = Runner(circuit, dtype, device, keep_states=keep_states)
+                real = self.runner.real
+                if weights is None:
+                    w = (torch.rand(circuit.n_weights, dtype=torch.float64) * 2.0 - 1.0) * np.pi
+                else:
+                    w = torch.as_tensor(weights, dtype=torch.float64).reshape(circuit.n_weights)
+                self.weights = torch.nn.Parameter(w.to(device=self.runner.device, dtype=real))
+                self._fn = quantum_layer_function()
+
+            def forward(self, inputs):
+                return self._fn.apply(self.runner, inputs, self.weights)
+
+        _QL_MODULE = QuantumLayerModule
+    return _QL_MODULE
+
+
+def QuantumLayer(gates, n_qubits, n_inputs, n_weights, dtype="c64", device="cuda", weights=None,
+                 keep_states=None, embed=None, pauli_p=None, **options):
+    """A quantum node as a ``torch.nn.Module`` (the paper's quantum layer:
+    section "Pipeline of VQNet 2.0", quantum node, and the simulator choice in
+    "Unification of Classical and Quantum Machine"): the circuit's trainable
+    angles are the module's ``weights`` parameter (initialised uniformly in
+    [-pi, pi) from torch's generator unless given), ``forward(inputs)`` returns
+    <Z_i> per sample and autograd's backward runs the library's fused forward +
+    adjoint call. With ``pauli_p`` the circuit holds Pauli channels (the
+    noise-inclusive simulator's trajectories: each channel reads its uniform
+    from an input feature)."""
+    circ = Circuit(n_qubits, gates, n_inputs, n_weights, embed=embed, pauli_p=pauli_p, **options)
+    return _ql_module_class()(circ, dtype, device, weights, keep_states)
+

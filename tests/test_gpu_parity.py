@@ -329,6 +329,26 @@ def test_autograd_function():
     assert np.max(np.abs(wt.grad.cpu().double().numpy() - want["grad_weights"])) <= 1e-5
 
 
+def test_quantum_layer_module():
+    """The nn.Module form: weights are its parameter, autograd gives the
+    library's VJP, and an optimizer step moves them."""
+    wl = W.get("10q")
+    x, w, g = wl.inputs()
+    layer = Q.QuantumLayer(wl.gates(), wl.n, wl.n_inputs, wl.n_weights, dtype="c64", weights=w)
+    assert [p.shape for p in layer.parameters()] == [torch.Size([wl.n_weights])]
+    xt = _dev(x, "c64").requires_grad_(True)
+    out = layer(xt)
+    (out * _dev(g, "c64")).sum().backward()
+    torch.cuda.synchronize()
+    want = oracle.run(wl.n, wl.gates(), x, w, grad_out=g)
+    check({"expz": out.detach().cpu().numpy(), "grad_inputs": xt.grad.cpu().numpy(),
+           "grad_weights": layer.weights.grad.cpu().numpy()}, want, 1e-5, "QuantumLayer")
+    opt = torch.optim.SGD(layer.parameters(), lr=0.1)
+    w0 = layer.weights.detach().clone()
+    opt.step()
+    assert torch.allclose(layer.weights.detach(), w0 - 0.1 * layer.weights.grad)
+
+
 def test_shared_parameter_closed_form():
     """The paper's compatibility example at 14 qubits (tiled path): H on every
     qubit, RY with one shared weight; d/dt sum_i <Z_i> = -n cos t."""
