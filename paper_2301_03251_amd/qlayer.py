@@ -248,9 +248,18 @@ class Runner:
         self.device = torch.device(device)
         self.keep_states = keep_states
         self._ws = None
+        self._modes = {}
+        self._sizes = {}
 
     def backward_mode(self, batch) -> int:
-        """MODE_FWD_BWD_KEEP or MODE_FWD_BWD, as forward_backward will run."""
+        """MODE_FWD_BWD_KEEP or MODE_FWD_BWD, as forward_backward will run (the
+        first answer for a batch size is kept)."""
+        mode = self._modes.get(batch)
+        if mode is None:
+            mode = self._modes[batch] = self._choose_mode(batch)
+        return mode
+
+    def _choose_mode(self, batch) -> int:
         info = self.c.plan_info(self.dtype)
         if info["kernel"] == 0 or info["n_passes"] < 2:
             return MODE_FWD_BWD  # whole state, or one tile pass: nothing to keep
@@ -267,9 +276,15 @@ class Runner:
         free, _ = _torch().cuda.mem_get_info(self.device)
         return MODE_FWD_BWD_KEEP if need - have <= 0.8 * free else MODE_FWD_BWD
 
+    def _need(self, batch, mode) -> int:
+        key = (batch, mode)
+        if key not in self._sizes:
+            self._sizes[key] = self.c.workspace_bytes(self.dtype, batch, mode)
+        return self._sizes[key]
+
     def workspace(self, batch, mode):
         torch = _torch()
-        need = self.c.workspace_bytes(self.dtype, batch, mode)
+        need = self._need(batch, mode)
         if self._ws is None or self._ws.numel() < need:
             self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
         return self._ws
@@ -311,7 +326,7 @@ class Runner:
         ws = self.workspace(B, mode)
         # the library keeps the states whenever the workspace it is given holds
         # them, so the plain path is handed exactly its own size
-        ws_bytes = ws.numel() if mode == MODE_FWD_BWD_KEEP else self.c.workspace_bytes(self.dtype, B, mode)
+        ws_bytes = ws.numel() if mode == MODE_FWD_BWD_KEEP else self._need(B, mode)
         self.c.forward_backward_raw(
             self.dtype, B, _ptr(x) if self.c.n_inputs else None, _ptr(w) if self.c.n_weights else None,
             _ptr(grad_out), _ptr(expz), _ptr(gx) if (gx is not None and self.c.n_inputs) else None,
