@@ -2041,8 +2041,15 @@ hipError_t launch_bind(int dtype, const BindArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Circuits per launch from which a forward-only whole-state launch of n <= 8
+// qubits takes the LDS kernel: with that many wavefronts in flight its LDS
+// partner exchanges outrun k_wave's DPP and permlane ones (parameter-shift
+// chunks of the 7-qubit autoencoder: 0.53 against 0.72 ms at 49408 circuits,
+// 1.56 against 1.78 ms at 2048, even at 512).
+constexpr int64_t WAVE_MAX_FWD_CIRCUITS = 2048;
+
 hipError_t launch_whole(int dtype, const WholeArgs& a, int threads, size_t lds, hipStream_t s) {
-    if (a.n <= 8) {  // one wavefront per sample
+    if (a.n <= 8 && (a.bwd || a.B < WAVE_MAX_FWD_CIRCUITS)) {  // one wavefront per sample
         const dim3 grid((unsigned)a.B), block(64);
 #define QL_WAVE(REAL)                                                                     \
     {                                                                                     \

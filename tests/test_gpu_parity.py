@@ -130,6 +130,24 @@ def test_random_whole_state(n, dtype):
           f"whole n={n} {dtype}")
 
 
+@pytest.mark.parametrize("n,dtype", [(6, "c64"), (8, "c128")])
+def test_whole_state_forward_large_batch(n, dtype):
+    """Forward-only launches of many small circuits (the LDS whole-state
+    kernel takes them over from the one-wavefront kernel): <Z> and final
+    states against the oracle."""
+    F, P, B = 3, 4, 2100
+    gates = W.random_circuit(n, 40 + 5 * n, F, P, seed=500 + n)
+    x, w, _ = W.random_inputs(B, F, P, n, seed=501 + n, dtype=dtype)
+    r = Q.Runner(Q.Circuit(n, gates, F, P), dtype)
+    e = r.forward(_dev(x, dtype), _dev(w, dtype))
+    psi = r.state(_dev(x, dtype), _dev(w, dtype))
+    torch.cuda.synchronize()
+    want = oracle.run(n, gates, x, w, want_state=True)
+    assert np.max(np.abs(e.cpu().double().numpy() - want["expz"])) <= TOL[dtype]
+    err = float(np.max(np.abs(psi.cpu().numpy().astype(np.complex128) - want["state"])))
+    assert err <= TOL[dtype], f"state n={n} {dtype}: {err:.3e}"
+
+
 @pytest.mark.parametrize("dtype", ["c64", "c128"])
 def test_degenerate_circuits(dtype):
     """No gates, no rotations, inputs only, weights only."""
