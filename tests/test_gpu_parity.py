@@ -318,6 +318,33 @@ def test_product_state_full_size(name):
     assert np.max(np.abs(got["grad_weights"] - gw)) <= 1e-5
 
 
+@pytest.mark.parametrize("n,dtype,keep", [(32, "c64", False), (31, "c128", True)],
+                         ids=["n32-c64-plain", "n31-c128-kept"])
+def test_maximum_qubits(n, dtype, keep):
+    """The largest state each dtype allows (32 GiB), one sample: rotation layers
+    around CNOT and CZ pairs that cancel (on qubits 0, 3, n-2 and n-1, so the
+    top amplitude-index bits take part), against the SO(3) closed form of the
+    product state."""
+    torch.cuda.empty_cache()
+    P = 2 * n
+    ry = [(W.RY, q, -1, W.SRC_WEIGHT, q) for q in range(n)]
+    rest = [(W.RZ, q, -1, W.SRC_WEIGHT, n + q) for q in range(n)] + \
+        [(W.RX, q, -1, W.SRC_INPUT, 0) for q in (0, n - 1)]
+    pairs = [(W.CNOT, n - 1, 0, 0, 0), (W.CZ, 3, n - 2, 0, 0)]
+    gates = np.array(ry + pairs + pairs + rest, np.int32)
+    x, w, g = W.random_inputs(1, 1, P, n, seed=n, dtype=dtype)
+    circ = Q.Circuit(n, gates, 1, P)
+    assert circ.plan_info(dtype)["n_passes"] > 1
+    r = Q.Runner(circ, dtype, keep_states=keep)
+    got = gpu_fb(circ, dtype, x, w, g, r)
+    del r
+    torch.cuda.empty_cache()
+    one_qubit = np.array(ry + rest, np.int32)
+    e, gx, gw = oracle_pins.product_state_reference(n, one_qubit, x[0].astype(np.float64), w.astype(np.float64),
+                                                    g[0].astype(np.float64))
+    check(got, {"expz": e[None], "grad_inputs": gx[None], "grad_weights": gw}, TOL[dtype], f"n={n} {dtype}")
+
+
 def test_hybrid_node_closed_form():
     """The paper's one-qubit hybrid node (H, then RY(input)): <Z> = -sin t and
     d<Z>/dt = -cos t, on a batch of angles."""
