@@ -154,8 +154,9 @@ typedef struct {
     int32_t wg_per_sample;      /* workgroups per sample in a tile pass */
     int32_t rz_groups;          /* 0: RZs on the register bits of one tile layout that
                                    commute into one place (at least three, on distinct
-                                   bits) run as one per-register phase op; -1: every
-                                   RZ runs on its own */
+                                   bits) run as one per-register phase op, and an RZ
+                                   that commutes back to an RY on its bit runs in one
+                                   op with it; -1: every RZ runs on its own */
 } ql_options;
 
 typedef struct ql_circuit ql_circuit; /* opaque */
@@ -289,6 +290,7 @@ typedef struct {
     int32_t n_lane_swaps;  /* in-register layout changes (register bit <-> lane bit) summed
                               over the forward passes */
     int32_t n_rz_groups;   /* RZ groups (several RZs run as one phase op), all passes */
+    int32_t n_ryz_pairs;   /* RZs run together with their bit's RY in one op, all passes */
 } ql_plan_info;
 
 int ql_plan_info_get(const ql_circuit* c, ql_dtype dtype, ql_plan_info* out);

@@ -39,8 +39,9 @@ struct Tables {
     std::vector<uint8_t> blob;
     size_t off_pass = 0, off_phase = 0, off_ops = 0, off_gslot = 0, off_slots = 0;
     size_t off_xptr = 0, off_xslot = 0, off_wptr = 0, off_wslot = 0, off_gates = 0, off_diag = 0;
+    size_t off_fuse = 0;
     std::vector<DevPass> passes;
-    int n_diags = 0;
+    int n_diags = 0, n_fuses = 0;
     int n_ops = 0;
     int bwd_first = 0;
 };
@@ -120,13 +121,15 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
     T.off_gates = put(T.blob, gates);
     T.off_diag = put(T.blob, pl.diags);
     T.n_diags = (int)pl.diags.size();
+    T.off_fuse = put(T.blob, pl.fuses);
+    T.n_fuses = (int)pl.fuses.size();
     T.blob.resize(align256(T.blob.size()), 0);
     T.passes = passes;
     T.n_ops = (int)ops.size();
 }
 
 struct Layout {
-    size_t tables = 0, coef = 0, opc = 0, dzc = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
+    size_t tables = 0, coef = 0, opc = 0, dzc = 0, fzc = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
     size_t enorm = 0, edot = 0;  // embedding: per-circuit |x| or basis index; L_b
     size_t keep = 0;             // kept forward states: n_keep buffers of state_bytes each
     size_t state_bytes = 0;
@@ -194,6 +197,10 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
         L.dzc = off;
         if (!mul_ok((size_t)B * (size_t)h->t[dt].n_diags, (size_t)DZ_REGS * amp, sz))
             return fail(QL_ENOMEM, "size overflow");
+        off = align256(off + sz);
+        // per-sample RZ coefficients of the RY-RZ pair ops
+        L.fzc = off;
+        if (!mul_ok((size_t)B * (size_t)h->t[dt].n_fuses, amp, sz)) return fail(QL_ENOMEM, "size overflow");
         off = align256(off + sz);
     }
     L.zpart = off;
@@ -338,6 +345,9 @@ int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0,
         ba.diags = (const DevDiag*)(x.W + x.L.tables + x.T.off_diag);
         ba.dzc = x.W + x.L.dzc;
         ba.n_diags = x.T.n_diags;
+        ba.fuses = (const DevFuse*)(x.W + x.L.tables + x.T.off_fuse);
+        ba.fzc = x.W + x.L.fzc;
+        ba.n_fuses = x.T.n_fuses;
         ba.B = B;
         ba.n_ops = x.T.n_ops;
         ba.bwd_first = x.T.bwd_first;
@@ -429,6 +439,8 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         ta.opc = x.W + x.L.opc;
         ta.dzc = x.W + x.L.dzc;
         ta.n_diags = x.T.n_diags;
+        ta.fzc = x.W + x.L.fzc;
+        ta.n_fuses = x.T.n_fuses;
         ta.grad_out = grad_out;
         ta.zpart = zpart;
         ta.gpart = gpart;
@@ -687,6 +699,8 @@ int state(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs, c
     ba.ops = (const DevOp*)(x.W + x.L.tables + x.T.off_ops);
     ba.diags = (const DevDiag*)(x.W + x.L.tables + x.T.off_diag);
     ba.n_diags = x.T.n_diags;
+    ba.fuses = (const DevFuse*)(x.W + x.L.tables + x.T.off_fuse);
+    ba.n_fuses = x.T.n_fuses;
     ba.B = B;
     ba.n_ops = x.T.n_ops;
     ba.bwd_first = x.T.bwd_first;
@@ -915,6 +929,7 @@ int ql_plan_info_get(const ql_circuit* h, ql_dtype dtype, ql_plan_info* out) {
         r.n_lane_swaps += pp.n_lane_swaps;
     }
     r.n_rz_groups = (int)pl.diags.size();
+    r.n_ryz_pairs = (int)pl.fuses.size();
     r.n_param_gates = h->c.n_param_slots;
     *out = r;
     return QL_OK;

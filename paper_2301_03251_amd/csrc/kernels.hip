@@ -861,7 +861,7 @@ template <int LOG_R, int LOG_T, int OPM, typename T2, typename Real>
 __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
                                        TileCtx& cx, Real& ival, unsigned char* lds,
                                        const DevPhase* phases, Real* gacc, int lane, int wave, int nw,
-                                       int tid, const T2* __restrict__ dz) {
+                                       int tid, const T2* __restrict__ dz, const T2* __restrict__ fz) {
 #define QL_G1_CASE(KIND, J)                                                                 \
     case H_G1 + KIND * 5 + J:                                                               \
         if constexpr (J < LOG_R) {                                                          \
@@ -945,6 +945,30 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         }                                                                                   \
         break;
 #define QL_PAULI_J(J) QL_PAULI_CASE(0, J) QL_PAULI_CASE(1, J) QL_PAULI_CASE(2, J)
+// RY then RZ on register bit J (the RZ's shear coefficients, forward, from
+// the pair table; the backward form inverts both and runs them in reverse
+// order, each with its gradient term first, as the two separate ops would).
+#define QL_RYZ_CASE(J, NEG)                                                                 \
+    case (NEG ? H_RYZN : H_RYZ) + J:                                                        \
+        if constexpr (J < LOG_R) {                                                          \
+            const T2 zc = fz[arg >> 16];                                                    \
+            if constexpr (OPM == OP_BWD) {                                                  \
+                grad_add(gacc, (arg >> 8) & 0xffu,                                          \
+                         fma((Real)-2, im_sum<LOG_R, J, T2, Real>(ps, lm), ival), lane, wave, nw); \
+                g1<LOG_R, 3, J, T2, Real, NEG>(lm, -zc.x, -zc.y);                           \
+                g1<LOG_R, 3, J, T2, Real, NEG>(ps, -zc.x, -zc.y);                           \
+                grad_add(gacc, arg & 0xffu, gpart<LOG_R, 2, J, T2, Real>(ps, lm), lane, wave, nw); \
+                g1<LOG_R, 2, J, T2, Real>(lm, ca, cb);                                      \
+                g1<LOG_R, 2, J, T2, Real>(ps, ca, cb);                                      \
+            } else {                                                                        \
+                g1<LOG_R, 2, J, T2, Real>(ps, ca, cb);                                      \
+                if constexpr (OPM == OP_PAIR) g1<LOG_R, 2, J, T2, Real>(lm, ca, cb);        \
+                g1<LOG_R, 3, J, T2, Real, NEG>(ps, zc.x, zc.y);                             \
+                if constexpr (OPM == OP_PAIR) g1<LOG_R, 3, J, T2, Real, NEG>(lm, zc.x, zc.y); \
+            }                                                                               \
+        }                                                                                   \
+        break;
+#define QL_RYZ_J(J) QL_RYZ_CASE(J, false) QL_RYZ_CASE(J, true)
 #define QL_CZ_RX(A)                                                                         \
     case H_CZ_RX + A:                                                                       \
         if constexpr (A < LOG_R) {                                                          \
@@ -961,6 +985,7 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         QL_RZN_CASE(0) QL_RZN_CASE(1) QL_RZN_CASE(2) QL_RZN_CASE(3) QL_RZN_CASE(4)
         QL_LSWAP_M(0) QL_LSWAP_M(1) QL_LSWAP_M(2) QL_LSWAP_M(3) QL_LSWAP_M(4)
         QL_PAULI_J(0) QL_PAULI_J(1) QL_PAULI_J(2) QL_PAULI_J(3) QL_PAULI_J(4)
+        QL_RYZ_J(0) QL_RYZ_J(1) QL_RYZ_J(2) QL_RYZ_J(3) QL_RYZ_J(4)
         case H_NOP:
             break;
         case H_DZ:
@@ -1012,6 +1037,8 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
 #undef QL_LSWAP_M
 #undef QL_PAULI_CASE
 #undef QL_PAULI_J
+#undef QL_RYZ_CASE
+#undef QL_RYZ_J
 }
 
 // <Z_q> partials of one tile held in registers t: register bits from the
@@ -1071,7 +1098,8 @@ template <typename Real, int LOG_R, int KM, int MAXT>
 __global__ void __launch_bounds__(MAXT) __attribute__((amdgpu_waves_per_eu(2)))
 k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __restrict__ phases,
        const XOp<Real>* __restrict__ xops_all, const Real* __restrict__ gout_all,
-       const int32_t* __restrict__ gslots, const typename Cx<Real>::T* __restrict__ dz_all) {
+       const int32_t* __restrict__ gslots, const typename Cx<Real>::T* __restrict__ dz_all,
+       const typename Cx<Real>::T* __restrict__ fz_all) {
     using T2 = typename Cx<Real>::T;
     constexpr bool BWD = KM == KM_BWD, PAIR = KM == KM_FWD2;
     constexpr int R = 1 << LOG_R;
@@ -1101,6 +1129,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     T2* lam_s = (T2*)a.lam + b * dim;
     const XOp<Real>* xops = xops_all + b * (a.n_ops + 1);
     const T2* dz = dz_all + b * a.n_diags * DZ_REGS;
+    const T2* fz = fz_all + b * a.n_fuses;
     const Real* gout = gout_all + b * n;
 
     if (BWD && (flags & PF_BWD)) {
@@ -1224,7 +1253,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 const XOp<Real> nxt = xops[o + 1];
                 run_op<LOG_R, LOG_T, PAIR ? OP_PAIR : OP_ONE>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx,
                                                               ival, lds, phases, gacc, lane, wave, NW,
-                                                              tid, dz);
+                                                              tid, dz, fz);
                 cur = nxt;
             }
         }
@@ -1263,7 +1292,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
                     run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, ival, lds,
-                                                 phases, gacc, lane, wave, NW, tid, dz);
+                                                 phases, gacc, lane, wave, NW, tid, dz, fz);
                     cur = nxt;
                 }
             }
@@ -1641,6 +1670,23 @@ __global__ void k_bind_tile(const BindTileArgs a) {
             e.a = (Real)tan(0.25 * th);
             e.b = (Real)sin(0.5 * th);
         }
+        if (op.h >= H_RYZ && op.h < H_RYZ + 5) {
+            // RY-RZ pair: the RZ's phase, reduced as for a single RZ, from the
+            // forward angle in both records (the backward form inverts it);
+            // the forward record writes the sample's coefficients
+            const uint32_t fi = op.arg >> 16;
+            int64_t bz;
+            double tz = angle_of<Real>(a.inputs, a.weights, a.F, a.slots[a.fuses[fi].slot], b, a.v0, a.vper, bz) +
+                        shift_of(b, a.v0, a.vper, a.fuses[fi].slot);
+            tz -= two_pi * rint(tz / two_pi);
+            const double half_pi = 1.570796326794896619231;
+            double phi = tz;
+            if (phi > half_pi) phi -= 2.0 * half_pi;
+            else if (phi < -half_pi) phi += 2.0 * half_pi;
+            if (phi != tz) e.h = H_RYZN + (op.h - H_RYZ);
+            if (o < a.bwd_first)
+                ((T2*)a.fzc)[(size_t)b * a.n_fuses + fi] = mk<T2>((Real)tan(0.5 * phi), (Real)sin(phi));
+        }
     }
     ((XOp<Real>*)a.opc)[t] = e;
 }
@@ -1769,6 +1815,8 @@ __global__ void k_state_phase(const BindTileArgs a, double* phase) {
         const double k = rint(th / two_pi);
         ph += pi * k;
         if (op.h >= H_G1 + 15 && op.h < H_G1 + 20) ph += 0.5 * (th - two_pi * k);
+        if (op.h >= H_RYZ && op.h < H_RYZ + 5)  // the pair's RZ, as a single RZ on a register bit
+            ph += 0.5 * angle_of<Real>(a.inputs, a.weights, a.F, a.slots[a.fuses[op.arg >> 16].slot], b, 0, 0, bs);
     }
     phase[b] = ph;
 }
@@ -2077,15 +2125,16 @@ static hipError_t launch_tile_t(bool bwd, const TileArgs& a, int threads, size_t
     const XOp<Real>* xo = (const XOp<Real>*)a.opc;
     const Real* gout = (const Real*)a.grad_out;
     const typename Cx<Real>::T* dzt = (const typename Cx<Real>::T*)a.dzc;
+    const typename Cx<Real>::T* fzt = (const typename Cx<Real>::T*)a.fzc;
     if (bwd)
         hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_BWD, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
-                           a.phases, xo, gout, a.gslots, dzt);
+                           a.phases, xo, gout, a.gslots, dzt, fzt);
     else if (a.tiles >= 2)  // forward passes carry two tiles per iteration when there are two
         hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_FWD2, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
-                           a.phases, xo, gout, a.gslots, dzt);
+                           a.phases, xo, gout, a.gslots, dzt, fzt);
     else
         hipLaunchKernelGGL((k_tile<Real, LOG_R, KM_FWD1, MAXT>), grid, dim3(threads), lds, s, a, a.pass,
-                           a.phases, xo, gout, a.gslots, dzt);
+                           a.phases, xo, gout, a.gslots, dzt, fzt);
     return hipGetLastError();
 }
 

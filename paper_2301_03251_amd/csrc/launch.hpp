@@ -46,6 +46,9 @@ struct BindTileArgs {
     const DevDiag* diags;  // [n_diags] RZ groups
     void* dzc;             // [B][n_diags][DZ_REGS] complex: (cos, sin) of each register's phase
     int32_t n_diags;
+    const DevFuse* fuses;  // [n_fuses] RZs of RY-RZ pair ops
+    void* fzc;             // [B][n_fuses] (a, b) shear coefficients of each pair's RZ (forward)
+    int32_t n_fuses;
     int64_t B;
     int32_t n_ops, bwd_first, F;
     int64_t v0;            // parameter-shift chunks: first virtual circuit
@@ -145,6 +148,8 @@ struct TileArgs {
     const void* opc;           // [B][n_ops + 1] per-sample op records
     const void* dzc;           // [B][n_diags][DZ_REGS] RZ-group phase tables
     int32_t n_diags;
+    const void* fzc;           // [B][n_fuses] RZ coefficients of the RY-RZ pair ops
+    int32_t n_fuses;
     const void* grad_out;      // [B][n] Real
     double* zpart;             // [B][n_wg][n]
     double* gpart;             // [n_slots][B][n_wg]

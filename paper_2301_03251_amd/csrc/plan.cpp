@@ -110,7 +110,8 @@ bool commutes_with_z(uint32_t h, uint32_t bits) {
 }
 
 void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_r, int low,
-                   uint32_t amp, std::vector<DevPhase>& phases, std::vector<DevDiag>* diags) {
+                   uint32_t amp, std::vector<DevPhase>& phases, std::vector<DevDiag>* diags,
+                   std::vector<DevFuse>* fuses) {
     const int r = log_r;
     std::vector<int> bit_of(64, -1);  // qubit -> tile bit
     for (int j = 0; j < k; j++) bit_of[pp.qubits[j]] = j;
@@ -401,6 +402,39 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         put_out(bits);
         recs.swap(out);
     };
+    // RY-RZ pairs: an RZ left on its own after grouping joins the nearest
+    // earlier RY on its register bit in the same layout when every op between
+    // them commutes with Z on that bit (the RZ moves back to the RY); the pair
+    // runs as one H_RYZ op.
+    auto pair_ryz = [&](size_t seg0) {
+        if (!fuses) return;
+        std::vector<bool> gone(recs.size(), false);
+        for (size_t i = seg0; i < recs.size(); i++) {
+            const uint32_t h = recs[i].op.h;
+            if (!(h >= H_G1 + 15 && h < H_G1 + 15 + (uint32_t)r)) continue;
+            const uint32_t j = h - (H_G1 + 15);
+            for (size_t k = i; k-- > seg0;) {
+                if (gone[k]) continue;
+                const uint32_t hk = recs[k].op.h;
+                if (hk == H_G1 + 10 + j) {
+                    if (fuses->size() >= 65536) break;
+                    const uint32_t idx = (uint32_t)fuses->size();
+                    fuses->push_back({recs[i].op.slot, recs[i].op.arg});
+                    const uint32_t arg = recs[k].op.arg | recs[i].op.arg << 8 | idx << 16;
+                    recs[k].op.h = H_RYZ + j;
+                    recs[k].op.arg = arg;
+                    recs[k].bwd_arg = arg;
+                    gone[i] = true;
+                    break;
+                }
+                if (!commutes_with_z(hk, 1u << j)) break;
+            }
+        }
+        std::vector<Rec> out;
+        for (size_t i = 0; i < recs.size(); i++)
+            if (!gone[i]) out.push_back(recs[i]);
+        recs.swap(out);
+    };
 
     while (!pending.empty()) {
         uint64_t blocked = 0;
@@ -454,6 +488,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
             recs.push_back({op, op.arg});
         }
         group_rz(seg0);
+        pair_ryz(seg0);
         pending.swap(rest);
         if (pending.empty()) break;
         change_to(choose_next());
@@ -665,7 +700,7 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         for (int gi : best) done[gi] = 1;
         remaining -= (int)best.size();
         schedule_pass(c.gates, pp, k, log_r, low, dtype == 0 ? 8u : 16u, pl.phases,
-                      o.rz_groups == 0 ? &pl.diags : nullptr);
+                      o.rz_groups == 0 ? &pl.diags : nullptr, o.rz_groups == 0 ? &pl.fuses : nullptr);
         pl.passes.push_back(std::move(pp));
         if (G == 0) break;
     }

@@ -75,8 +75,17 @@ enum HandlerId : uint32_t {
                        //      binding kernel to the Pauli its uniform selects, or to H_NOP
     H_DZ = 138,        // RZ group: the RZs of up to MAX_DZ_BITS register bits in one diagonal
                        //      op (a per-register phase); arg = group index (DevDiag)
-    H_NOP = 139,
-    H_END = 140,
+    H_RYZ = 139,       // + J: RY then RZ on register bit J in one op; arg = RY gradient slot |
+                       //      RZ gradient slot << 8 | pair index (DevFuse) << 16
+    H_RYZN = 144,      // + J: the same with the RZ's phase negated (chosen per sample by the
+                       //      binding kernel, as H_RZN for a single RZ)
+    H_NOP = 149,
+    H_END = 150,
+};
+// The RZ of an RY-RZ pair op (H_RYZ): its rotation slot and gradient slot.
+struct DevFuse {
+    int32_t slot;
+    uint32_t gslot;
 };
 // Register bits an RZ group can span (its gradient slots travel in the op
 // record's two coefficient words, 16 bits each).
@@ -175,7 +184,8 @@ struct DevPass {
 struct Options {
     int log_regs = 0, log_threads = 0, low_qubits = 0, max_gates_per_pass = 0;
     int force_tiled = 0, wg_per_sample = 0;
-    int rz_groups = 0;  // 0: RZs on register bits are grouped into H_DZ ops; -1: never
+    int rz_groups = 0;  // 0: RZs on register bits are grouped into H_DZ ops or joined to their
+                        // bit's RY (H_RYZ); -1: every RZ runs on its own
 };
 
 // One forward tile pass as planned (host form).
@@ -197,6 +207,7 @@ struct Plan {
     std::vector<PassPlan> passes;
     std::vector<DevPhase> phases;
     std::vector<DevDiag> diags;  // RZ groups (H_DZ ops), all passes
+    std::vector<DevFuse> fuses;  // RZs of RY-RZ pair ops (H_RYZ), all passes
     int n_slots = 0;           // rotation slots
 };
 

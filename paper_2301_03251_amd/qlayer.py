@@ -45,7 +45,8 @@ class _Desc(ctypes.Structure):
 class _PlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "n_passes", "tile_qubits", "log_regs",
                                               "log_threads", "low_qubits", "n_transposes",
-                                              "n_param_gates", "n_lane_swaps", "n_rz_groups")]
+                                              "n_param_gates", "n_lane_swaps", "n_rz_groups",
+                                              "n_ryz_pairs")]
 
 
 _lib = None

@@ -181,8 +181,8 @@ def test_rz_groups_in_workload_plans(lib, name):
     on = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
     off = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, rz_groups=-1)
     for dt in ("c64", "c128"):
-        assert on.plan_info(dt)["n_rz_groups"] > 0
-        assert off.plan_info(dt)["n_rz_groups"] == 0
+        assert on.plan_info(dt)["n_rz_groups"] > 0 and on.plan_info(dt)["n_ryz_pairs"] > 0
+        assert off.plan_info(dt)["n_rz_groups"] == 0 and off.plan_info(dt)["n_ryz_pairs"] == 0
         assert on.plan_info(dt)["n_passes"] == off.plan_info(dt)["n_passes"]
         # grouping moves ops within a pass, never between passes
         assert np.array_equal(on.schedule(dt)[0], off.schedule(dt)[0])

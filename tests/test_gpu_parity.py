@@ -516,25 +516,48 @@ def rz_layer_circuit(n, layers, F, P, seed):
     return np.array(g, np.int32)
 
 
+def staircase_circuit(n, layers, F, P, seed):
+    """RY then RZ on each qubit, then a CNOT chain, per layer (the workloads'
+    shape): most RZs commute back to their qubit's RY and run in one op with
+    it, the rest form groups."""
+    rng = np.random.default_rng(seed)
+    g = []
+    for _ in range(layers):
+        for q in range(n):
+            for kind in (W.RY, W.RZ):
+                if rng.random() < 0.3:
+                    g.append((kind, q, -1, W.SRC_INPUT, int(rng.integers(F))))
+                else:
+                    g.append((kind, q, -1, W.SRC_WEIGHT, int(rng.integers(P))))
+        for q in range(n - 1):
+            g.append((W.CNOT, q, q + 1, 0, 0))
+    return np.array(g, np.int32)
+
+
 RZ_GROUP_CASES = [(13, "c64", dict()), (14, "c128", dict()), (12, "c64", dict(log_regs=3, log_threads=6)),
                   (11, "c128", dict(force_tiled=1, log_regs=4, log_threads=6, max_gates_per_pass=20))]
 
 
+@pytest.mark.parametrize("shape", ["layers", "staircase"])
 @pytest.mark.parametrize("n,dtype,opts", RZ_GROUP_CASES,
                          ids=[f"n{c[0]}-{c[1]}-{'-'.join(f'{k}{v}' for k, v in c[2].items()) or 'default'}"
                               for c in RZ_GROUP_CASES])
-def test_rz_groups(n, dtype, opts):
-    """RZ groups (one phase op for several RZs) against the oracle and against
-    the plan without them: forward + adjoint VJP, and exact final states."""
+def test_rz_groups(n, dtype, opts, shape):
+    """RZ groups (one phase op for several RZs) and RY-RZ pair ops against the
+    oracle and against the plan without them: forward + adjoint VJP, and exact
+    final states."""
     F, P, B = 4, 6, 3
-    gates = rz_layer_circuit(n, 3, F, P, seed=70 + n)
+    build = rz_layer_circuit if shape == "layers" else staircase_circuit
+    gates = build(n, 3, F, P, seed=70 + n)
     x, w, g = W.random_inputs(B, F, P, n, seed=71 + n, dtype=dtype)
     x[0, 0] = 9.0      # angles well outside [-pi, pi]
     w[1] = -7.5
     grouped = Q.Circuit(n, gates, F, P, **opts)
     single = Q.Circuit(n, gates, F, P, rz_groups=-1, **opts)
     assert grouped.plan_info(dtype)["n_rz_groups"] > 0
-    assert single.plan_info(dtype)["n_rz_groups"] == 0
+    if shape == "staircase":
+        assert grouped.plan_info(dtype)["n_ryz_pairs"] > 0
+    assert single.plan_info(dtype)["n_rz_groups"] == 0 and single.plan_info(dtype)["n_ryz_pairs"] == 0
     want = oracle.run(n, gates, x, w, grad_out=g)
     got = gpu_fb(grouped, dtype, x, w, g)
     check(got, want, TOL[dtype], f"rz groups n={n} {dtype}")
@@ -550,10 +573,10 @@ def test_rz_groups_param_shift():
     """The shifted circuits of a parameter-shift chunk shift one member of an
     RZ group's phase table at a time."""
     n, dtype, F, P, B = 13, "c128", 3, 5, 2
-    gates = rz_layer_circuit(n, 2, F, P, seed=90)
+    gates = np.concatenate([rz_layer_circuit(n, 1, F, P, seed=90), staircase_circuit(n, 1, F, P, seed=92)])
     x, w, g = W.random_inputs(B, F, P, n, seed=91, dtype=dtype)
     circ = Q.Circuit(n, gates, F, P)
-    assert circ.plan_info(dtype)["n_rz_groups"] > 0
+    assert circ.plan_info(dtype)["n_rz_groups"] > 0 and circ.plan_info(dtype)["n_ryz_pairs"] > 0
     e, gx, gw = Q.Runner(circ, dtype).param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), max_chunk=37)
     torch.cuda.synchronize()
     got = {"expz": e.cpu().numpy(), "grad_inputs": gx.cpu().numpy(), "grad_weights": gw.cpu().numpy()}
