@@ -148,9 +148,13 @@ typedef struct {
     int32_t low_qubits;         /* qubits 0..low_qubits-1 are in every tile (1..8) */
     int32_t max_gates_per_pass; /* cap on gates per tile pass (>= 1) */
     int32_t force_tiled;        /* kernel choice: 0 library default (register tiles for
-                                   n >= 8, whole state in LDS below), 1 register tiles,
-                                   -1 whole state in LDS whenever it fits (n <= 12 for
-                                   QL_C64, n <= 11 for QL_C128) */
+                                   n >= 8, a whole-state kernel below), 1 register
+                                   tiles, -1 a whole-state kernel whenever it fits
+                                   (n <= 12 for QL_C64, n <= 11 for QL_C128). The
+                                   whole-state kernels hold a sample in one
+                                   wavefront's registers for n <= 8 (in LDS for
+                                   forward-only launches of 2048 or more circuits)
+                                   and in LDS above */
     int32_t wg_per_sample;      /* workgroups per sample in a tile pass */
     int32_t rz_groups;          /* 0: RZs on the register bits of one tile layout that
                                    commute into one place (at least three, on distinct
