@@ -269,8 +269,9 @@ int ql_state(const ql_circuit* c, ql_dtype dtype, int64_t batch, const void* inp
  * QL_C64, fp64 for QL_C128; may be NULL) receives the shot estimate of <Z_q>:
  * (shots with bit q = 0 minus shots with bit q = 1) / shots. The states need
  * not be normalised. shots = 0 writes nothing. Workspace:
- * ql_sample_workspace_bytes(n_qubits, batch) bytes (one fp64 per 4096
- * amplitudes). n_qubits in [1, 32] (QL_C128: [1, 31]). */
+ * ql_sample_workspace_bytes(n_qubits, batch) bytes (per block of up to 4096
+ * amplitudes, the prefix of block totals and the block's 64 chunk sums:
+ * 65 fp64). n_qubits in [1, 32] (QL_C128: [1, 31]). */
 int ql_sample_workspace_bytes(int32_t n_qubits, int64_t batch, size_t* out);
 int ql_sample(ql_dtype dtype, int32_t n_qubits, int64_t batch, const void* psi, int64_t shots,
               const double* uniforms, int64_t* samples, void* zhat, void* workspace,

@@ -723,8 +723,11 @@ int sample_bytes(int n, int64_t B, size_t& out) {
     int rc = sample_blocks(n, bb, nblk);
     if (rc) return rc;
     if (B < 1) return fail(QL_EINVAL, "batch must be >= 1");
-    if (!mul_ok((size_t)B, (size_t)nblk * 8, out)) return fail(QL_ENOMEM, "size overflow");
-    out = align256(out);
+    // block prefix, then the 64 lane-chunk sums of every block
+    size_t chunks = 0;
+    if (!mul_ok((size_t)B, (size_t)nblk * 8, out) || !mul_ok(out, 64, chunks))
+        return fail(QL_ENOMEM, "size overflow");
+    out = align256(out) + chunks;
     return QL_OK;
 }
 
@@ -905,6 +908,7 @@ int ql_sample(ql_dtype dtype, int32_t n_qubits, int64_t batch, const void* psi, 
     a.n = n_qubits;
     rc = sample_blocks(n_qubits, a.bb, a.nblk);
     if (rc) return rc;
+    a.csum = (double*)((char*)ws + align256((size_t)batch * (size_t)a.nblk * 8));
     hipError_t e = launch_sample((int)dtype, a, stream);
     if (e != hipSuccess) return fail(QL_EHIP, std::string("sampling: ") + hipGetErrorString(e));
     g_err.clear();

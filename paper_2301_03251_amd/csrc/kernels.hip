@@ -1974,7 +1974,9 @@ __global__ void __launch_bounds__(256) k_block_sums(const SampleArgs a) {
     int64_t lo, cnt;
     chunk_of(a.bb, lane, lo, cnt);
     const int64_t base = (b << a.n) + (blk << a.bb);
-    const double s = lane_scan(chunk_sum((const T2*)a.psi, base, lo, cnt), lane);
+    const double c = chunk_sum((const T2*)a.psi, base, lo, cnt);
+    a.csum[wv * 64 + lane] = c;
+    const double s = lane_scan(c, lane);
     if (lane == 63) a.bsum[wv] = s;
 }
 
@@ -2008,17 +2010,22 @@ __global__ void __launch_bounds__(256) k_block_scan(const SampleArgs a) {
 }
 
 // One wavefront per shot: the block (binary search over the prefix), the lane
-// chunk (ballot over the lane scan), then the amplitude (running sum in the
-// chunk). The index is the first one whose running total exceeds u * total.
+// chunk (the block's stored chunk sums, the same lane scan, a ballot), then
+// the amplitude (a lane scan of the chunk's probabilities, a ballot). The
+// index is the first one whose running total exceeds u * total.
 template <typename T2>
-__global__ void __launch_bounds__(256) k_shots(const SampleArgs a) {
-    const int64_t wv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+__global__ void __launch_bounds__(256) k_shots(const SampleArgs a, const double* __restrict__ pre_all,
+                                               const double* __restrict__ cs_all,
+                                               const double* __restrict__ uni) {
+    // the wavefront's shot, uniform by construction (scalar loads below)
+    const int64_t wv = (int64_t)blockIdx.x * (blockDim.x >> 6) +
+                       __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = threadIdx.x & 63;
     if (wv >= a.B * a.shots) return;
     const int64_t b = wv / a.shots;
-    const double* pre = a.bsum + b * a.nblk;
+    const double* pre = pre_all + b * a.nblk;
     const double total = pre[a.nblk - 1];
-    const double r = a.uniforms[wv] * total;
+    const double r = uni[wv] * total;
     int64_t lo = 0, hi = a.nblk - 1;  // first block with pre > r (pre[nblk-1] = total > r)
     while (lo < hi) {
         const int64_t mid = lo + (hi - lo) / 2;
@@ -2031,7 +2038,7 @@ __global__ void __launch_bounds__(256) k_shots(const SampleArgs a) {
     chunk_of(a.bb, lane, clo, ccnt);
     const int64_t base = (b << a.n) + (blk << a.bb);
     const T2* p = (const T2*)a.psi;
-    const double incl = lane_scan(chunk_sum(p, base, clo, ccnt), lane);
+    const double incl = lane_scan(cs_all[(b * a.nblk + blk) * 64 + lane], lane);
     // shuffle with every lane active, then select (a shuffle inside the
     // conditional would read lane 0 while it is switched off)
     const double up = __shfl_up(incl, 1, 64);
@@ -2044,23 +2051,22 @@ __global__ void __launch_bounds__(256) k_shots(const SampleArgs a) {
     }
     const double start = before + __shfl(prev, L, 64);
     int64_t lL, cL;
-    chunk_of(a.bb, L, lL, cL);
-    int64_t idx = -1, last_nz = lL;
-    if (lane == 0) {
-        double run = start;
-        for (int64_t j = lL; j < lL + cL; ++j) {
-            const T2 v = p[base + j];
-            const double q = (double)v.x * (double)v.x + (double)v.y * (double)v.y;
-            if (q > 0.0) last_nz = j;
-            run += q;
-            if (run > r && q > 0.0) {
-                idx = j;
-                break;
-            }
-        }
-        if (idx < 0) idx = last_nz;  // rounding: the chunk's last amplitude of nonzero probability
-        a.samples[wv] = (blk << a.bb) + idx;
+    chunk_of(a.bb, L, lL, cL);  // cL <= 64: one amplitude per lane
+    double q = 0.0;
+    if (lane < cL) {
+        const T2 v = p[base + lL + lane];
+        q = (double)v.x * (double)v.x + (double)v.y * (double)v.y;
     }
+    const double run = start + lane_scan(q, lane);
+    const uint64_t in = __ballot(lane < cL && run > r && q > 0.0);
+    int64_t idx;
+    if (in) {
+        idx = lL + (int64_t)__builtin_ctzll(in);
+    } else {  // rounding: the chunk's last amplitude of nonzero probability
+        const uint64_t nz = __ballot(lane < cL && q > 0.0);
+        idx = nz ? lL + 63 - (int64_t)__builtin_clzll(nz) : lL;
+    }
+    if (lane == 0) a.samples[wv] = (blk << a.bb) + idx;
 }
 
 // <Z_q> from the shots: one thread per (sample, qubit), exact integer counts.
@@ -2253,8 +2259,12 @@ hipError_t launch_sample(int dtype, const SampleArgs& a, hipStream_t s) {
     else hipLaunchKernelGGL(k_block_sums<double2>, dim3((unsigned)((wb + 3) / 4)), dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_block_scan, dim3((unsigned)a.B), dim3(256), 0, s, a);
     if (ws > 0) {
-        if (dtype == 0) hipLaunchKernelGGL(k_shots<float2>, dim3((unsigned)((ws + 3) / 4)), dim3(256), 0, s, a);
-        else hipLaunchKernelGGL(k_shots<double2>, dim3((unsigned)((ws + 3) / 4)), dim3(256), 0, s, a);
+        if (dtype == 0)
+            hipLaunchKernelGGL(k_shots<float2>, dim3((unsigned)((ws + 3) / 4)), dim3(256), 0, s, a, a.bsum,
+                               a.csum, a.uniforms);
+        else
+            hipLaunchKernelGGL(k_shots<double2>, dim3((unsigned)((ws + 3) / 4)), dim3(256), 0, s, a, a.bsum,
+                               a.csum, a.uniforms);
     }
     if (a.zhat) {
         const int64_t t = a.B * a.n;

@@ -130,6 +130,7 @@ struct SampleArgs {
     int64_t* samples;       // [B][shots]
     void* zhat;             // [B][n] Real or null: <Z_q> estimated from the shots
     double* bsum;           // [B][nblk]: block sums, then their inclusive prefix
+    double* csum;           // [B][nblk][64]: each block's 64 lane-chunk sums
     int64_t B, shots, nblk;
     int32_t n, bb;
 };

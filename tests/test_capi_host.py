@@ -137,8 +137,9 @@ def test_state_and_sample_validation(lib):
     assert need + 2 * (1 << 14) * 8 == c.workspace_bytes("c64", 2, Q.MODE_FWD)
     assert _err(lambda: c.state_raw("c64", 2, None, fake, None, fake, need, None)) == -1
     assert _err(lambda: c.state_raw("c64", 2, None, fake, fake, fake, need - 1, None)) == -2
-    assert Q.sample_workspace_bytes(30, 3) == 3 * (1 << 18) * 8   # one fp64 per 4096 amplitudes
-    assert Q.sample_workspace_bytes(5, 1) == 256
+    # per block of 4096 amplitudes: the prefix of block totals and 64 chunk sums
+    assert Q.sample_workspace_bytes(30, 3) == 3 * (1 << 18) * 8 * 65
+    assert Q.sample_workspace_bytes(5, 1) == 256 + 64 * 8
     assert _err(lambda: Q.sample_workspace_bytes(0, 1)) == -1
     assert _err(lambda: Q.sample_workspace_bytes(33, 1)) == -1
     ws = Q.sample_workspace_bytes(10, 2)
