@@ -148,6 +148,10 @@ bool mul_ok(size_t a, size_t b, size_t& out) {
 struct ql_circuit {
     Circuit c;
     Tables t[2];
+    // pinned host copies of the table blobs (made on the first call of each
+    // dtype), so the per-call upload is an asynchronous DMA
+    void* pinned[2] = {nullptr, nullptr};
+    std::once_flag pin_once[2];
     // timing
     int timing = 0;
     struct Ev {
@@ -310,8 +314,17 @@ struct Ctx {
 };
 
 int upload_tables(Ctx& x) {
-    hipError_t e = hipMemcpyAsync(x.W + x.L.tables, x.T.blob.data(), x.T.blob.size(), hipMemcpyHostToDevice,
-                                  x.stream);
+    std::call_once(x.h->pin_once[x.dt], [&] {
+        void* p = nullptr;
+        if (hipHostMalloc(&p, x.T.blob.size(), hipHostMallocDefault) == hipSuccess) {
+            std::memcpy(p, x.T.blob.data(), x.T.blob.size());
+            x.h->pinned[x.dt] = p;
+        } else {
+            (void)hipGetLastError();  // keep the pageable copy
+        }
+    });
+    const void* src = x.h->pinned[x.dt] ? x.h->pinned[x.dt] : (const void*)x.T.blob.data();
+    hipError_t e = hipMemcpyAsync(x.W + x.L.tables, src, x.T.blob.size(), hipMemcpyHostToDevice, x.stream);
     return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("table upload: ") + hipGetErrorString(e));
 }
 
@@ -796,6 +809,12 @@ int ql_circuit_create(int32_t n_qubits, const ql_gate* gates, int32_t n_gates, i
 
 void ql_circuit_destroy(ql_circuit* h) {
     if (!h) return;
+    if (h->pinned[0] || h->pinned[1]) {
+        // table uploads of calls still queued read the pinned copies
+        (void)hipDeviceSynchronize();
+        for (void* p : h->pinned)
+            if (p) (void)hipHostFree(p);
+    }
     for (auto& e : h->ev) {
         (void)hipEventDestroy(e.a);
         (void)hipEventDestroy(e.b);
