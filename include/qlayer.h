@@ -35,7 +35,10 @@
  * pointers on the current HIP device, row-major and contiguous, owned by the
  * caller. The caller also provides the device workspace (size from
  * ql_workspace_bytes). The library never allocates device memory in these
- * calls; it only writes the workspace and the outputs. Outputs are
+ * calls; it only writes the workspace and the outputs. (The first call of
+ * each dtype on a handle makes a pinned host copy of the handle's plan tables,
+ * which later calls upload by DMA; ql_circuit_destroy synchronises the
+ * current device before freeing it.) Outputs are
  * overwritten (not accumulated). Buffers must not alias each other or the
  * workspace.
  *
