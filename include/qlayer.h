@@ -319,12 +319,15 @@ int ql_plan_state_bytes(const ql_circuit* c, ql_dtype dtype, int64_t batch, int 
 
 /* ---- timing (for benchmarks) --------------------------------------------- */
 
-/* When enabled on a handle, every kernel launch of a call is bracketed by HIP
- * events on the call's stream; ql_timing_read synchronises on the last event
- * and returns the summed milliseconds per kernel class:
- * ms[0] tile passes, ms[1] whole-state kernel, ms[2] angle binding,
- * ms[3] reductions; launches[0..3] the launch counts. Reading resets them.
- * Not thread-safe: one timed call in flight per handle. */
+/* Kernel classes: 0 tile passes, 1 whole-state kernel, 2 angle binding and
+ * embedding, 3 reductions. enable = 0 turns timing off; otherwise bit c of
+ * enable selects class c (15: all). Every launch of a selected class is then
+ * bracketed by HIP events on the call's stream (each pair costs host time,
+ * which shows on launch-bound workloads: time only the classes needed).
+ * ql_timing_read synchronises on the last event and returns the summed
+ * milliseconds per class in ms[0..3] and the launch counts in
+ * launches[0..3]. Reading resets them. Not thread-safe: one timed call in
+ * flight per handle. */
 int ql_timing_enable(ql_circuit* c, int enable);
 int ql_timing_read(ql_circuit* c, double ms[4], int32_t launches[4]);
 

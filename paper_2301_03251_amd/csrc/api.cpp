@@ -281,9 +281,11 @@ struct Timer {
     ql_circuit* h;
     hipStream_t s;
     int cls = 0;
+    bool on = false;
     void start(int c) {
         cls = c;
-        if (!h->timing) return;
+        on = (h->timing >> c & 1) != 0;
+        if (!on) return;
         if (h->ev_used == h->ev.size()) {
             ql_circuit::Ev e{};
             if (hipEventCreate(&e.a) != hipSuccess || hipEventCreate(&e.b) != hipSuccess) return;
@@ -293,7 +295,7 @@ struct Timer {
         (void)hipEventRecord(h->ev[h->ev_used].a, s);
     }
     void stop() {
-        if (!h->timing || h->ev_used >= h->ev.size()) return;
+        if (!on || h->ev_used >= h->ev.size()) return;
         (void)hipEventRecord(h->ev[h->ev_used].b, s);
         h->ev_used++;
     }
@@ -997,7 +999,8 @@ int ql_plan_state_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, int 
 
 int ql_timing_enable(ql_circuit* h, int enable) {
     if (!h) return fail(QL_EINVAL, "NULL argument");
-    h->timing = enable ? 1 : 0;
+    if (enable < 0 || enable > 15) return fail(QL_EINVAL, "timing mask out of range [0, 15]");
+    h->timing = enable;
     h->ev_used = 0;
     return QL_OK;
 }

@@ -178,8 +178,10 @@ class Circuit:
         _check(load().ql_plan_state_bytes(self._h, _dt(dtype), int(batch), int(mode), ctypes.byref(out)))
         return out.value
 
-    def timing(self, enable: bool):
-        _check(load().ql_timing_enable(self._h, 1 if enable else 0))
+    def timing(self, enable: bool, classes: int = 0xF):
+        """Bracket the launches of the kernel classes in the mask `classes`
+        (bit 0 tile passes, 1 whole-state kernel, 2 binding, 3 reductions)."""
+        _check(load().ql_timing_enable(self._h, int(classes) & 0xF if enable else 0))
 
     def timing_read(self):
         ms = (ctypes.c_double * 4)()

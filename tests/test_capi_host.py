@@ -190,6 +190,17 @@ def test_rz_groups_in_workload_plans(lib, name):
     assert _err(lambda: Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, rz_groups=1)) == -3
 
 
+def test_timing_mask(lib):
+    """ql_timing_enable takes a mask of kernel classes (0..15)."""
+    c = Q.Circuit(14, np.array(G1, np.int32), 0, 1)
+    for m in (0, 1, 2, 15):
+        assert lib.ql_timing_enable(c.handle, m) == 0
+    for m in (-1, 16):
+        assert lib.ql_timing_enable(c.handle, m) == -1
+    c.timing(True, 1)
+    c.timing(False)
+
+
 def test_keep_mode_embeddings_and_single_pass(lib):
     # an embedded initial state keeps its own buffer; a one-pass tiled circuit
     # has nothing to keep
