@@ -272,6 +272,43 @@ def test_forward_only_and_null_grads():
     assert np.max(np.abs(gw.cpu().double().numpy() - want["grad_weights"])) <= 1e-5
 
 
+def test_destroy_right_after_a_call():
+    """A handle destroyed while its call may still be queued: the outputs are
+    still right (the table upload reads the handle's pinned copy, and
+    destruction waits for the device first)."""
+    import gc
+    n, F, P, B = 14, 3, 5, 2
+    gates = W.random_circuit(n, 120, F, P, seed=33)
+    x, w, g = W.random_inputs(B, F, P, n, seed=34, dtype="c64")
+    circ = Q.Circuit(n, gates, F, P)
+    r = Q.Runner(circ, "c64")
+    e, gx, gw = r.forward_backward(_dev(x, "c64"), _dev(w, "c64"), _dev(g, "c64"))
+    r.c = None
+    del r, circ
+    gc.collect()
+    torch.cuda.synchronize()
+    got = {"expz": e.cpu().double().numpy(), "grad_inputs": gx.cpu().double().numpy(),
+           "grad_weights": gw.cpu().double().numpy()}
+    check(got, oracle.run(n, gates, x, w, grad_out=g), 1e-5, "destroyed handle")
+
+
+def test_timing_classes():
+    """Only the selected kernel classes are bracketed by events."""
+    n, F, P, B = 14, 3, 5, 2
+    gates = W.random_circuit(n, 120, F, P, seed=35)
+    x, w, g = W.random_inputs(B, F, P, n, seed=36, dtype="c64")
+    circ = Q.Circuit(n, gates, F, P)
+    r = Q.Runner(circ, "c64")
+    for mask, want in ((1, (True, False, False, False)), (12, (False, False, True, True)),
+                       (15, (True, False, True, True))):
+        circ.timing(True, mask)
+        r.forward_backward(_dev(x, "c64"), _dev(w, "c64"), _dev(g, "c64"))
+        ms, cnt = circ.timing_read()
+        circ.timing(False)
+        assert tuple(c > 0 for c in cnt) == want, (mask, cnt)
+        assert all((m > 0) == (c > 0) for m, c in zip(ms, cnt))
+
+
 def test_deterministic():
     """Two calls give bit-identical outputs (fixed-order fp64 reductions, no atomics)."""
     wl = W.get("16q")
