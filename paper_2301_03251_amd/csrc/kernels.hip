@@ -1932,19 +1932,9 @@ __global__ void __launch_bounds__(256) k_embed_grad(const EmbedGradArgs a) {
 
 // ---------------------------------------------------------------------------
 // shot sampling (inverse CDF). A block of 2^bb amplitudes is 64 lane chunks
-// of consecutive amplitudes; every block quantity below comes from one
-// function (chunk sums, then a fixed-order lane scan), so the block totals and
-// the in-block search see bitwise the same numbers.
-
-template <typename T2>
-__device__ __forceinline__ double chunk_sum(const T2* p, int64_t base, int64_t lo, int64_t cnt) {
-    double acc = 0.0;
-    for (int64_t j = lo; j < lo + cnt; ++j) {
-        const T2 v = p[base + j];
-        acc += (double)v.x * (double)v.x + (double)v.y * (double)v.y;
-    }
-    return acc;
-}
+// of consecutive amplitudes. The chunk sums are computed once and stored; the
+// block totals and the in-block search both lane-scan those stored sums, so
+// they see bitwise the same numbers.
 
 // Inclusive scan over the 64 lanes, Hillis-Steele, fixed order.
 __device__ __forceinline__ double lane_scan(double v, int lane) {
@@ -1964,19 +1954,34 @@ __device__ __forceinline__ void chunk_of(int bb, int lane, int64_t& lo, int64_t&
     cnt = lo < bs ? csz : 0;
 }
 
-// One wavefront per (sample, block): block total into bsum.
+// One wavefront per (sample, block): the 64 chunk sums into csum and the
+// block total into bsum. The block is read in coalesced rows of 64
+// amplitudes; a row holds 64 / csz whole chunks, summed by a butterfly over
+// each group of csz lanes (fixed order), and lane c keeps chunk c's sum.
 template <typename T2>
 __global__ void __launch_bounds__(256) k_block_sums(const SampleArgs a) {
     const int64_t wv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int lane = threadIdx.x & 63;
     if (wv >= a.B * a.nblk) return;
     const int64_t b = wv / a.nblk, blk = wv - b * a.nblk;
-    int64_t lo, cnt;
-    chunk_of(a.bb, lane, lo, cnt);
-    const int64_t base = (b << a.n) + (blk << a.bb);
-    const double c = chunk_sum((const T2*)a.psi, base, lo, cnt);
-    a.csum[wv * 64 + lane] = c;
-    const double s = lane_scan(c, lane);
+    const int64_t bs = (int64_t)1 << a.bb;
+    const int csz = bs >= 64 ? (int)(bs / 64) : 1, per = 64 / csz;
+    const int rows = bs >= 64 ? 64 / per : 1;
+    const T2* p = (const T2*)a.psi + (b << a.n) + (blk << a.bb);
+    double mine = 0.0;
+    for (int k = 0; k < rows; ++k) {
+        const int64_t i = lane + 64 * (int64_t)k;
+        double q = 0.0;
+        if (i < bs) {
+            const T2 v = p[i];
+            q = (double)v.x * (double)v.x + (double)v.y * (double)v.y;
+        }
+        for (int off = 1; off < csz; off <<= 1) q += __shfl_xor(q, off, 64);
+        const double g = __shfl(q, (lane % per) * csz, 64);
+        if (lane / per == k) mine = g;
+    }
+    a.csum[wv * 64 + lane] = mine;
+    const double s = lane_scan(mine, lane);
     if (lane == 63) a.bsum[wv] = s;
 }
 
