@@ -1791,8 +1791,8 @@ __global__ void __launch_bounds__(256) k_shift_grad(const ShiftGradArgs a) {
 // (a factor (-1)^k per rotation whose angle moved by 2 pi k) and an RZ on a
 // register bit as diag(1, exp(i t)) (dropping exp(-i t / 2)); both are global
 // phases per sample. k_state_phase sums them over the forward ops, from the
-// same angle sources and reduction as k_bind_tile; k_phase_fix multiplies the
-// state by the inverse phase.
+// same angle sources and reduction as k_bind_tile and stores the inverse
+// phase factor (cos, sin) per sample; k_phase_fix multiplies the state by it.
 
 template <typename Real>
 __global__ void k_state_phase(const BindTileArgs a, double* phase) {
@@ -1818,7 +1818,10 @@ __global__ void k_state_phase(const BindTileArgs a, double* phase) {
         if (op.h >= H_RYZ && op.h < H_RYZ + 5)  // the pair's RZ, as a single RZ on a register bit
             ph += 0.5 * angle_of<Real>(a.inputs, a.weights, a.F, a.slots[a.fuses[op.arg >> 16].slot], b, 0, 0, bs);
     }
-    phase[b] = ph;
+    double sn, cs;  // the inverse phase factor, once per sample
+    sincos(-ph, &sn, &cs);
+    phase[2 * b] = cs;
+    phase[2 * b + 1] = sn;
 }
 
 template <typename T2>
@@ -1826,8 +1829,7 @@ __global__ void k_phase_fix(void* psi, const double* phase, int64_t B, int n) {
     const int64_t total = B << n;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (int64_t)gridDim.x * blockDim.x) {
-        double sn, cs;
-        sincos(-phase[i >> n], &sn, &cs);
+        const double cs = phase[2 * (i >> n)], sn = phase[2 * (i >> n) + 1];
         T2 v = ((T2*)psi)[i];
         const double x = (double)v.x, y = (double)v.y;
         v.x = (decltype(v.x))(x * cs - y * sn);

@@ -196,7 +196,7 @@ hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_shift_dot(int dtype, const ShiftDotArgs& a, hipStream_t s);
 hipError_t launch_sample(int dtype, const SampleArgs& a, hipStream_t s);
 // Undo the per-sample global phase the tile kernel leaves on final states
-// (phase: [B] fp64 scratch).
+// (phase: [2B] fp64 scratch: the inverse phase factor per sample).
 hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, void* psi, int n,
                               hipStream_t s);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, hipStream_t s);
