@@ -31,8 +31,13 @@ import workloads as W  # noqa: E402
 
 METRIC = "amplitude-gate updates/s (batched fwd+adjoint grad); % of HBM peak BW"
 HBM_PEAK_GBS = 8000.0
-# fp32 FMA without packed-FP32 instructions: 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz
-ALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+# MI355X published vector peaks (TFLOP/s): fp32 157.3 (reached only with packed
+# two-wide fp32 instructions), fp64 78.6.
+ALU_PEAK_TFLOPS = {"c64": 157.3, "c128": 78.6}
+# The issue ceiling of the arithmetic this library emits: one fp32 (or fp64)
+# FMA per lane per cycle, no packed fp32: 256 CUs x 4 SIMDs x 16 lanes x 2 flop
+# x 2.4 GHz.
+ISSUE_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 # Algorithmic flops per amplitude, each gate in its cheapest exact form: RX/RY
 # rotate a real plane per pair of components, 6 flops per amplitude; RZ is, up
 # to a global phase, a complex multiply of the bit-1 half of the amplitudes,
@@ -87,23 +92,56 @@ def profiled_traffic(wl):
     return float(fields["traffic_bytes_per_step"]), copy_gbs
 
 
-def cpu_baseline(wl, gates, x, w, g, pauli_p, n_gates: int):
+def host_info():
+    """CPU model, CPUs this process may run on, and installed RAM."""
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    ram = None
+    try:
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal:"):
+                ram = round(int(line.split()[1]) / 2 ** 20, 1)
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "affinity_cpus": len(os.sched_getaffinity(0)), "ram_gib": ram}
+
+
+def cpu_baseline(wl, gates, x, w, g, pauli_p, prefixes):
     """The CPU oracle (complex128, all host threads) on a bounded sample of the
-    same workload: the first `n_gates` gates of the circuit at full size, one
-    sample, forward + adjoint."""
+    same workload: one sample at full size, forward + adjoint, over two
+    prefixes of the gate list (k1 < k2 gates). The rate is the slope: the
+    amplitude-gate updates of the k2 - k1 extra gates over the extra time, so
+    that the costs that do not depend on the gate count (allocating and
+    clearing the states, the <Z> sums, the lambda seed) are reported apart
+    (``fixed_s``) instead of diluting the per-gate rate."""
     import oracle
-    sub = gates[:n_gates]
-    n_ch = int(sum(1 for gg in sub if int(gg[0]) == W.PAULI))
-    pp = None if pauli_p is None else pauli_p[:max(n_ch, 1)]
     oracle.build()
-    t0 = time.perf_counter()
-    oracle.run(wl.n, sub, x[:1], w, grad_out=g[:1], embed=getattr(wl, "embed", None), pauli_p=pp)
-    dt = time.perf_counter() - t0
-    upd = 3.0 * n_gates * (1 << wl.n)
+    times = []
+    for k in prefixes:
+        sub = gates[:k]
+        n_ch = int(sum(1 for gg in sub if int(gg[0]) == W.PAULI))
+        pp = None if pauli_p is None else pauli_p[:max(n_ch, 1)]
+        t0 = time.perf_counter()
+        oracle.run(wl.n, sub, x[:1], w, grad_out=g[:1], embed=getattr(wl, "embed", None), pauli_p=pp)
+        times.append(time.perf_counter() - t0)
+    (k1, k2), (t1, t2) = prefixes, times
+    upd = 3.0 * (k2 - k1) * (1 << wl.n)
+    dt = max(t2 - t1, 1e-9)
+    fixed = max(t1 - k1 * dt / (k2 - k1), 0.0)
     return {"value": upd / dt, "unit": "amplitude-gate updates/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"first {n_gates} of {len(gates)} gates of {wl.name}, batch row 0 of "
-                      f"{wl.batch}, n={wl.n}, complex128, forward + adjoint; {dt:.2f} s"}
+            "sample": f"{wl.name} batch row 0 of {wl.batch}, n={wl.n}, complex128, forward + adjoint "
+                      f"over the first {k1} and the first {k2} of {len(gates)} gates: {t1:.2f} s and "
+                      f"{t2:.2f} s; value = 3*({k2}-{k1})*2^{wl.n} updates / {dt:.2f} s",
+            "fixed_s": fixed, "prefix_gates": [k1, k2], "prefix_s": [t1, t2],
+            "whole_prefix_rate": 3.0 * k2 * (1 << wl.n) / t2, **host_info()}
 
 
 def main():
@@ -116,8 +154,8 @@ def main():
                     help="depolarizing probability p: a Pauli-channel trajectory on every qubit "
                          "after every --noise-every gates, one trajectory per sample")
     ap.add_argument("--noise-every", type=int, default=1)
-    ap.add_argument("--cpu-gates", type=int, default=8,
-                    help="gates in the CPU-oracle sample (0 disables it)")
+    ap.add_argument("--cpu-gates", default="8,32",
+                    help="the two gate-list prefixes the CPU oracle times, k1,k2 (0 disables it)")
     ap.add_argument("--no-timing", action="store_true",
                     help="time only the whole step (no per-kernel events)")
     ap.add_argument("--calibrate", action="store_true",
@@ -265,26 +303,38 @@ def main():
         hbm = state_bytes / (tile_ms / 1e3) / 1e9
         alu = flops / (tile_ms / 1e3) / 1e12
         launches = kcnt[0] / args.steps
+        peak = ALU_PEAK_TFLOPS[wl.dtype]
         line["roofline"] = {"bound": "alu", "kernel": "k_tile", "achieved": alu,
-                            "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": alu / ALU_PEAK_TFLOPS,
+                            "peak": peak, "unit": "TFLOP/s", "frac": alu / peak,
                             "traffic": None if traffic is None else traffic / launches,
                             "traffic_unit": "bytes per launch",
                             "launches_per_step": launches,
                             "kernel_ms_per_step": tile_ms,
                             "algorithmic_flops_per_step": flops,
                             "algorithmic_bytes_per_step": state_bytes,
+                            "issue_peak": ISSUE_PEAK_TFLOPS,
+                            "frac_of_issue_peak": alu / ISSUE_PEAK_TFLOPS,
                             "hbm": {"achieved": hbm, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                     "frac": hbm / HBM_PEAK_GBS, "copy_kernel": copy_gbs}}
+        line["alu_frac"] = alu / peak
+        line["hbm_frac"] = hbm / HBM_PEAK_GBS
         line["kernel_ms_per_step"] = {"k_tile": kms[0] / args.steps}
     elif timing and kcnt[1] > 0:
         whole_ms = kms[1] / args.steps
         alu = (shift_flops(gates, wl.batch, wl.n) if shift else
                algorithmic_flops(gates, wl.batch, wl.n)) / (whole_ms / 1e3) / 1e12
+        peak = ALU_PEAK_TFLOPS[wl.dtype]
         line["roofline"] = {"bound": "alu", "kernel": "k_whole", "achieved": alu,
-                            "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": alu / ALU_PEAK_TFLOPS,
-                            "traffic": None, "kernel_ms_per_step": whole_ms}
-    if args.cpu_gates > 0:
-        line["cpu_baseline"] = cpu_baseline(wl, gates, x, w, g, pauli_p, min(args.cpu_gates, G))
+                            "peak": peak, "unit": "TFLOP/s", "frac": alu / peak,
+                            "traffic": None, "kernel_ms_per_step": whole_ms,
+                            "issue_peak": ISSUE_PEAK_TFLOPS, "frac_of_issue_peak": alu / ISSUE_PEAK_TFLOPS}
+        line["alu_frac"] = alu / peak
+    pre = [int(v) for v in str(args.cpu_gates).split(",") if v.strip()]
+    if pre and pre[0] > 0:
+        k2 = min(pre[-1], G)
+        k1 = min(pre[0], k2 - 1) if len(pre) > 1 else max(1, k2 // 4)
+        if k1 >= 1:
+            line["cpu_baseline"] = cpu_baseline(wl, gates, x, w, g, pauli_p, (k1, k2))
     print(json.dumps(line), flush=True)
 
 

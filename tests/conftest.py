@@ -22,3 +22,19 @@ def _announce_gpu_case(request):
         sys.__stderr__.write(f"\n[gpu-case] {request.node.nodeid}\n")
         sys.__stderr__.flush()
     yield
+
+
+@pytest.fixture(autouse=True)
+def _parity_case(request):
+    """Tell the parity recorder which test its comparisons belong to."""
+    import parity
+    parity.CURRENT["test"] = request.node.nodeid
+    yield
+
+
+def pytest_sessionfinish(session, exitstatus):
+    path = os.environ.get("QL_PARITY_JSON")
+    if path:
+        import parity
+        if parity.RECORD:
+            parity.write(path)

@@ -676,6 +676,50 @@ def pin_pauli_channel_average(orc):
     _close(avg, _density_reference(n, gates, xb, w, pp), what="trajectory average vs density matrix")
 
 
+def pin_large_states(orc):
+    """States of 2^16 and 2^18 amplitudes, where the oracle's amplitude loops run
+    in parallel and its pairwise sums split into 4 and 16 chunks combined as a
+    tree: workload-shaped circuits without entanglers against the per-qubit
+    SO(3) closed form (expectations and gradients); a CNOT chain over a basis
+    state gives prefix parities; H CZ H on qubits far apart acts as a CNOT;
+    Pauli channels with probability 1 flip <Z> (X and Y on |0>, Z on |+>);
+    un-applying a random entangled circuit returns |0...0> and lambda_0[0]
+    equals sum_i g_i <Z_i>."""
+    for name, n in (("24q", 16), ("30q", 18)):
+        wl = W.scaled(W.get(name), n=n, batch=1, layers=1, entangler=None, dtype="c128")
+        x, w, g = wl.inputs()
+        gates = wl.gates()
+        r = orc.run(n, gates, x, w, grad_out=g)
+        e, gx, gw = product_state_reference(n, gates, x[0], w, g[0])
+        _close(r["expz"][0], e, tol=1e-12, what=f"n={n} product expz")
+        _close(r["grad_inputs"][0], gx, tol=1e-12, what=f"n={n} product grad_x")
+        _close(r["grad_weights"], gw, tol=1e-12, what=f"n={n} product grad_w")
+    n = 16
+    rng = np.random.default_rng(16)
+    bits = [int(v) for v in rng.integers(0, 2, n)]
+    bits[0] = bits[n - 1] = 1
+    r = orc.run(n, _arr(_basis_prep(bits) + [_g(W.CNOT, q, q + 1) for q in range(n - 1)]), [[math.pi]], [])
+    _close(r["expz"][0], 1 - 2 * (np.cumsum(bits) % 2), what="n=16 chain parity")
+    for c, t, a_, b_ in ((0, 15, 15, 0), (14, 1, 1, 14)):
+        gates = _arr(_basis_prep(bits) + [_g(W.H, t), _g(W.CZ, a_, b_), _g(W.H, t)])
+        out = list(bits)
+        out[t] ^= bits[c]
+        _close(orc.run(n, gates, [[math.pi]], [])["expz"][0], [1 - 2 * v for v in out], what="n=16 CZ kickback")
+    pp = [[1.0, 0.0, 0.0], [0.0, 1.0, 0.0], [0.0, 0.0, 1.0]]
+    gates = _arr([_g(W.PAULI, 15, -1, W.SRC_INPUT, 0), _g(W.PAULI, 3, -1, W.SRC_INPUT, 0),
+                  _g(W.H, 9), _g(W.PAULI, 9, -1, W.SRC_INPUT, 0), _g(W.H, 9)])
+    want = np.ones(n)
+    want[[15, 3, 9]] = -1
+    _close(orc.run(n, gates, [[0.5]], [], pauli_p=pp)["expz"][0], want, what="n=16 Pauli channels")
+    gates, x, w, g = _random_case(n, 40, 1616, B=1)
+    r = orc.run(n, gates, x, w, grad_out=g, want_state=True, want_back=True)
+    _close(np.sum(np.abs(r["state"]) ** 2), 1.0, what="n=16 norm")
+    e0 = np.zeros(1 << n)
+    e0[0] = 1
+    _close(r["back_psi"][0], e0, what="n=16 inverse sweep")
+    _close(r["back_lam0"][0], np.sum(g[0] * r["expz"][0]), what="n=16 lambda_0[0]")
+
+
 ALL_PINS = [
     pin_rotations_on_zero, pin_rotation_axes, pin_h_rz_h, pin_hybrid_node,
     pin_shared_parameter, pin_cnot_truth_table, pin_cnot_chain_parity, pin_cz_kickback,
@@ -684,5 +728,5 @@ ALL_PINS = [
     pin_controlled_rotation_closed_forms, pin_controlled_rotation_brute_force,
     pin_controlled_rotation_decomposition, pin_controlled_rotation_shift_and_fd,
     pin_basis_embedding, pin_amplitude_embedding, pin_amplitude_embedding_gradient,
-    pin_pauli_trajectory_choices, pin_pauli_channel_average,
+    pin_pauli_trajectory_choices, pin_pauli_channel_average, pin_large_states,
 ]

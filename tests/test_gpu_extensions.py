@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
+from parity import check, close
 import workloads as W
 
 torch = pytest.importorskip("torch")
@@ -49,12 +50,6 @@ def gpu_fb(circ, dtype, x, w, g, keep_states=None):
             "grad_weights": gw.cpu().double().numpy()}
 
 
-def check(got, want, tol, what, keys=("expz", "grad_inputs", "grad_weights")):
-    for k in keys:
-        a, b = np.asarray(got[k], np.float64), np.asarray(want[k], np.float64)
-        assert a.shape == b.shape, f"{what} {k}: shape {a.shape} vs {b.shape}"
-        err = float(np.max(np.abs(a - b))) if a.size else 0.0
-        assert err <= tol, f"{what} {k}: max abs err {err:.3e} > {tol:.0e}"
 
 
 # (n, dtype, options): whole state, small register tiles, default tiles
@@ -198,8 +193,7 @@ def test_state_with_extensions(n, dtype, opts):
     torch.cuda.synchronize()
     want = oracle.run(n, gates, _host(xe, dtype), _host(w, dtype), want_state=True, embed=emb,
                       pauli_p=pp)["state"]
-    err = float(np.max(np.abs(psi.cpu().numpy().astype(np.complex128) - want)))
-    assert err <= TOL[dtype], f"state n={n} {dtype}: {err:.3e}"
+    close(psi.cpu().numpy(), want, TOL[dtype], f"state n={n} {dtype}", "state")
 
 
 def test_param_shift_with_embeddings():
@@ -212,13 +206,13 @@ def test_param_shift_with_embeddings():
     torch.cuda.synchronize()
     want = oracle.run(n, gates, x, w, grad_out=g, embed=emb)
     check({"expz": e.cpu().numpy(), "grad_inputs": gx.cpu().numpy(), "grad_weights": gw.cpu().numpy()},
-          want, 1e-11, "basis shift")
+          want, 1e-12, "basis shift")
     gates, x, w, g, emb = _embedded_case(n, W.EMBED_AMPLITUDE, dtype, seed=1901)
     r = Q.Runner(Q.Circuit(n, gates, x.shape[1], w.size, embed=emb), dtype)
     e, _, gw = r.param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), want_inputs=False)
     torch.cuda.synchronize()
     want = oracle.run(n, gates, x, w, grad_out=g, embed=emb)
-    check({"expz": e.cpu().numpy(), "grad_weights": gw.cpu().numpy()}, want, 1e-11, "amplitude shift",
+    check({"expz": e.cpu().numpy(), "grad_weights": gw.cpu().numpy()}, want, 1e-12, "amplitude shift",
           keys=("expz", "grad_weights"))
     with pytest.raises(Q.QLError):
         r.param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype))
