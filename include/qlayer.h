@@ -164,6 +164,11 @@ typedef struct {
                                    bits) run as one per-register phase op, and an RZ
                                    that commutes back to an RY on its bit runs in one
                                    op with it; -1: every RZ runs on its own */
+    int32_t pass_search;        /* 0: the tile of each pass is the candidate whose pass
+                                   plus a greedy completion of the rest is cheapest
+                                   under a memory/arithmetic cost model (no nearly
+                                   empty passes at the end of long CNOT chains);
+                                   -1: the candidate that runs the most gates */
 } ql_options;
 
 typedef struct ql_circuit ql_circuit; /* opaque */

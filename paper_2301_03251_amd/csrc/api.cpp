@@ -756,6 +756,7 @@ Options to_options(const ql_options* o) {
         r.force_tiled = o->force_tiled;
         r.wg_per_sample = o->wg_per_sample;
         r.rz_groups = o->rz_groups;
+        r.pass_search = o->pass_search;
     }
     return r;
 }

@@ -626,6 +626,7 @@ std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, i
     if (o.max_gates_per_pass < 0) return "option: max_gates_per_pass < 0";
     if (o.wg_per_sample < 0) return "option: wg_per_sample < 0";
     if (o.rz_groups != 0 && o.rz_groups != -1) return "option: rz_groups must be 0 or -1";
+    if (o.pass_search != 0 && o.pass_search != -1) return "option: pass_search must be 0 or -1";
     for (int dt = 0; dt < 2; dt++) {
         std::string e = build_plan(out, dt, out.plan[dt]);
         if (!e.empty()) return e;
@@ -675,22 +676,97 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
     std::vector<char> done(G, 0);
     int remaining = G;
     const uint64_t low_tile = (low >= 64) ? ~0ull : ((1ull << low) - 1);
-    while (remaining > 0 || pl.passes.empty()) {
-        // candidates: first-need greedy growth, and contiguous windows of the
-        // high qubits; keep the one that executes the most gates
-        std::vector<int> best;
-        uint64_t best_tile = 0;
-        {
-            uint64_t t = low_tile;
-            best = scan(c.gates, done, t, k, true, o.max_gates_per_pass);
-            best_tile = t;
-        }
+    // Candidate tiles of the next pass: first-need greedy growth, and
+    // contiguous windows of the high qubits.
+    struct Cand {
+        std::vector<int> gates;
+        uint64_t tile;
+    };
+    auto candidates = [&](const std::vector<char>& dn) {
+        std::vector<Cand> out;
+        uint64_t t = low_tile;
+        std::vector<int> e = scan(c.gates, dn, t, k, true, o.max_gates_per_pass);
+        out.push_back({std::move(e), t});
         const int h = k - low;
         for (int s = low; s + h <= c.n; s++) {
-            uint64_t t = low_tile | (((1ull << h) - 1) << s);
-            std::vector<int> e = scan(c.gates, done, t, k, false, o.max_gates_per_pass);
-            if (e.size() > best.size()) { best = e; best_tile = t; }
+            uint64_t w = low_tile | (((1ull << h) - 1) << s);
+            std::vector<int> ew = scan(c.gates, dn, w, k, false, o.max_gates_per_pass);
+            out.push_back({std::move(ew), w});
         }
+        return out;
+    };
+    // the candidate that executes the most gates (the first of equals)
+    auto widest = [](const std::vector<Cand>& cs) {
+        size_t b = 0;
+        for (size_t i = 1; i < cs.size(); i++)
+            if (cs[i].gates.size() > cs[b].gates.size()) b = i;
+        return b;
+    };
+    // Cost model of the look-ahead, in FMAs per amplitude. A pass is bound by
+    // its memory traffic or by its arithmetic, whichever takes longer: a
+    // forward pass moves 2 amplitudes (16 B in complex64) per amplitude and
+    // does 3 FMAs per rotation (RX, RY); a backward pass moves 3 (psi and
+    // lambda in, lambda out) and does 8 per rotation (psi and lambda
+    // un-applied, the gradient term). At about 5 TB/s of streaming bandwidth
+    // against about 3.8e13 fp32 FMA/s (MI355X), one byte costs as long as 7.6
+    // FMAs. Other gates count by their arithmetic relative to a rotation.
+    const double amp_bytes = dtype == 0 ? 8.0 : 16.0;
+    const double mem_fwd = 7.6 * 2 * amp_bytes, mem_bwd = 7.6 * 3 * amp_bytes;
+    auto weight = [&](const std::vector<int>& ex) {
+        double w = 0;
+        for (int i : ex) {
+            const int kd = c.gates[i].kind;
+            w += (kd == K_RX || kd == K_RY) ? 1.0 : kd == K_RZ ? 0.5 : kd == K_H ? 0.7 : 0.25;
+        }
+        return w;
+    };
+    auto pass_cost = [&](double w) { return std::max(mem_fwd, 3 * w) + std::max(mem_bwd, 8 * w); };
+    // Greedy completion from `dn` for at most `horizon` passes; the gates
+    // left after it are priced at their arithmetic alone.
+    auto rollout = [&](std::vector<char> dn, int rem, int horizon) {
+        double cost = 0;
+        for (int p = 0; p < horizon && rem > 0; p++) {
+            std::vector<Cand> cs = candidates(dn);
+            const Cand& b = cs[widest(cs)];
+            if (b.gates.empty()) return 1e300;
+            for (int i : b.gates) dn[i] = 1;
+            rem -= (int)b.gates.size();
+            cost += pass_cost(weight(b.gates));
+        }
+        if (rem > 0) {
+            std::vector<int> left;
+            for (int i = 0; i < G; i++)
+                if (!dn[i]) left.push_back(i);
+            cost += 11 * weight(left);
+        }
+        return cost;
+    };
+    const int horizon = G > 4096 ? 4 : 16;
+    while (remaining > 0 || pl.passes.empty()) {
+        // The greedy choice is the candidate that executes the most gates.
+        // By default each candidate is instead priced by the cost of its pass
+        // plus a greedy completion of the rest of the circuit, which avoids
+        // leaving a tail of nearly empty, memory-bound passes (such as the
+        // ends of long CNOT chains).
+        std::vector<Cand> cs = candidates(done);
+        size_t pick = widest(cs);
+        if (o.pass_search == 0 && remaining > 0) {
+            double best_cost = 1e300;
+            for (size_t i = 0; i < cs.size(); i++) {
+                if (cs[i].gates.empty()) continue;
+                std::vector<char> d2 = done;
+                for (int g : cs[i].gates) d2[g] = 1;
+                const double cst = pass_cost(weight(cs[i].gates)) +
+                                   rollout(std::move(d2), remaining - (int)cs[i].gates.size(), horizon);
+                if (cst < best_cost * (1 - 1e-12) ||
+                    (cst <= best_cost * (1 + 1e-12) && cs[i].gates.size() > cs[pick].gates.size())) {
+                    best_cost = cst;
+                    pick = i;
+                }
+            }
+        }
+        std::vector<int> best = std::move(cs[pick].gates);
+        uint64_t best_tile = cs[pick].tile;
         if (best.empty() && remaining > 0) return "planner made no progress";
         // fill the tile up to k qubits with the lowest unused qubits
         for (int q = 0; q < c.n && __builtin_popcountll(best_tile) < k; q++) best_tile |= 1ull << q;

@@ -186,6 +186,7 @@ struct Options {
     int force_tiled = 0, wg_per_sample = 0;
     int rz_groups = 0;  // 0: RZs on register bits are grouped into H_DZ ops or joined to their
                         // bit's RY (H_RYZ); -1: every RZ runs on its own
+    int pass_search = 0;  // 0: each pass's tile priced by a look-ahead; -1: the widest pass
 };
 
 // One forward tile pass as planned (host form).

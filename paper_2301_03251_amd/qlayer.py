@@ -34,7 +34,7 @@ class QLError(RuntimeError):
 class _Options(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("log_regs", "log_threads", "low_qubits",
                                               "max_gates_per_pass", "force_tiled",
-                                              "wg_per_sample", "rz_groups")]
+                                              "wg_per_sample", "rz_groups", "pass_search")]
 
 
 class _Desc(ctypes.Structure):

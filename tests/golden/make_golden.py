@@ -10,7 +10,11 @@ as ``<workload>.npz`` (plain arrays, no pickle):
   grad_weights  VJP w.r.t. the weights with grad_out zeroed outside `rows`  [P]
   digest        sha256 of the workload's inputs, weights and grad_out
 
-Usage: python tests/golden/make_golden.py 24q 30q
+``16q`` holds the whole batch (all 1024 rows, so ``grad_weights`` is the
+batch sum of the workload itself). ``24q_c128`` is the 24-qubit workload in
+complex128: the same circuit with its inputs drawn and kept in fp64.
+
+Usage: python tests/golden/make_golden.py 24q 30q 16q 24q_c128
 """
 
 from __future__ import annotations
@@ -29,7 +33,14 @@ sys.path.insert(0, ROOT)
 import oracle  # noqa: E402
 import workloads as W  # noqa: E402
 
-ROWS = {"24q": [0, 7, 15], "30q": [0], "16q": [0, 1, 511, 1023]}
+ROWS = {"24q": [0, 7, 15], "30q": [0], "16q": list(range(1024)), "24q_c128": [0, 7, 15]}
+
+
+def workload(name: str):
+    """The workload a golden file is for: ``<name>`` or ``<name>_c128``."""
+    if name.endswith("_c128"):
+        return W.scaled(W.get(name[:-5]), dtype="c128")
+    return W.get(name)
 
 
 def digest(x, w, g) -> str:
@@ -40,12 +51,13 @@ def digest(x, w, g) -> str:
 
 
 def make(name: str):
-    wl = W.get(name)
+    wl = workload(name)
     x, w, g = wl.inputs()
     rows = ROWS[name]
     t0 = time.time()
     r = oracle.run(wl.n, wl.gates(), x[rows], w, grad_out=g[rows])
-    print(f"{name}: oracle on rows {rows} took {time.time() - t0:.1f}s", flush=True)
+    shown = rows if len(rows) <= 8 else f"0..{rows[-1]}"
+    print(f"{name}: oracle on rows {shown} took {time.time() - t0:.1f}s", flush=True)
     out = os.path.join(HERE, f"{name}.npz")
     np.savez(out, rows=np.asarray(rows, dtype=np.int64), expz=r["expz"],
              grad_inputs=r["grad_inputs"], grad_weights=r["grad_weights"],

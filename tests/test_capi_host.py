@@ -276,6 +276,25 @@ def test_pass_counts_are_small(lib):
         assert c.plan_info("c64")["n_passes"] <= limit, name
 
 
+def test_pass_search(lib):
+    """The look-ahead tile choice against the widest-pass greedy on the
+    30-qubit CNOT staircase: fewer passes, no nearly empty pass at the end of
+    the chains, and both plans valid. The option takes 0 or -1 only."""
+    wl = W.get("30q")
+    gates = wl.gates()
+    look = Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights)
+    greedy = Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights, pass_search=-1)
+    for dt in ("c64", "c128"):
+        _check_schedule(look, gates, dt)
+        _check_schedule(greedy, gates, dt)
+        assert look.plan_info(dt)["n_passes"] < greedy.plan_info(dt)["n_passes"], dt
+        sizes = np.bincount(look.schedule(dt)[0])
+        assert sizes.min() >= 30, (dt, sizes)
+        assert np.bincount(greedy.schedule(dt)[0]).min() < 30
+    for bad in (1, -2):
+        assert _err(lambda: Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights, pass_search=bad)) == -3
+
+
 # ---------------------------------------------------------------------------
 # controlled rotations, embeddings, Pauli channels (host side)
 

@@ -209,19 +209,21 @@ def test_workload_16q_sampled():
 
 
 @pytest.mark.parametrize("keep", [True, False], ids=["kept", "plain"])
-@pytest.mark.parametrize("name", ["24q", "30q"])
+@pytest.mark.parametrize("name", ["16q", "24q", "24q_c128", "30q"])
 def test_workload_golden(name, keep):
     """Full workload on the GPU vs oracle values stored by tests/golden/make_golden.py,
-    with and without the kept forward states."""
+    with and without the kept forward states: 16q over its whole batch (so the
+    weight gradients are the batch sums of the workload itself), 24q and 30q on
+    sampled rows, and 24q in complex128 (inputs drawn in fp64) at 1e-12."""
     path = os.path.join(GOLDEN, f"{name}.npz")
     if not os.path.exists(path):
         pytest.skip(f"{path} not generated")
     gold = np.load(path, allow_pickle=False)
-    wl = W.get(name)
-    x, w, g = wl.inputs()
     import sys
     sys.path.insert(0, GOLDEN)
-    import make_golden  # noqa: E402  (digest only)
+    import make_golden  # noqa: E402  (digest and workload only)
+    wl = make_golden.workload(name)
+    x, w, g = wl.inputs()
     assert str(gold["digest"]) == make_golden.digest(x, w, g), "golden file is stale"
     rows = [int(v) for v in gold["rows"]]
     circ = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
@@ -237,6 +239,60 @@ def test_workload_golden(name, keep):
           {"expz": gold["expz"], "grad_inputs": gold["grad_inputs"],
            "grad_weights": gold["grad_weights"]}, TOL[wl.dtype], name)
     assert np.all(np.abs(got["expz"]) <= 1 + 1e-5)
+
+
+def sweep_circuit(n, kind, F, P, seed):
+    """A generic state (RY then RZ on every qubit), then `kind` on every qubit
+    (one-qubit kinds) or on pairs that put the operands low/high, high/low,
+    high/high, at the ends of the register and at qubit n-1 (two-qubit
+    kinds), then a closing RX layer."""
+    rng = np.random.default_rng(seed)
+
+    def rot(k, q):
+        if rng.random() < 0.4:
+            return (k, q, -1, W.SRC_INPUT, int(rng.integers(F)))
+        return (k, q, -1, W.SRC_WEIGHT, int(rng.integers(P)))
+    g = [rot(W.RY, q) for q in range(n)] + [rot(W.RZ, q) for q in range(n)]
+    if kind in (W.CNOT, W.CZ):
+        pairs = [(0, n - 1), (n - 1, 0), (1, 12), (12, 1), (11, 12), (12, 11), (12, 13), (13, n - 1),
+                 (n - 1, 13), (n - 2, n - 1), (2, 3), (3, 2), (5, 16), (16, 5), (9, 17), (17, 9)]
+        for a, b in pairs:
+            g.append((kind, a, b, 0, 0))
+            g.append(rot(W.RY, b))
+    elif kind == W.H:
+        g += [(W.H, q, -1, 0, 0) for q in range(n)]
+    else:
+        g += [rot(kind, q) for q in range(n)]
+    g += [rot(W.RX, q) for q in range(n)]
+    return np.array(g, np.int32)
+
+
+SWEEP_OPTS = [dict(), dict(max_gates_per_pass=5), dict(log_regs=3, log_threads=7, low_qubits=2)]
+
+
+@pytest.mark.parametrize("opts", SWEEP_OPTS, ids=["default", "five-per-pass", "r3-t7-low2"])
+@pytest.mark.parametrize("kind", [W.H, W.RX, W.RY, W.RZ, W.CNOT, W.CZ], ids=["H", "RX", "RY", "RZ", "CNOT", "CZ"])
+def test_gate_sweep_n20(kind, opts):
+    """Every gate kind on every qubit of a 20-qubit state (two-qubit kinds on
+    pairs across the tile edges and the top qubit), in complex128 against the
+    oracle at 1e-12, under three plans that put the operands on different
+    register, lane, wavefront and fixed bits."""
+    n, F, P, B = 20, 4, 9, 2
+    gates = sweep_circuit(n, kind, F, P, seed=2000 + kind)
+    x, w, g = W.random_inputs(B, F, P, n, seed=2100 + kind, dtype="c128")
+    circ = Q.Circuit(n, gates, F, P, **opts)
+    assert circ.plan_info("c128")["kernel"] == 1
+    want = _sweep_oracle(n, kind, gates, x, w, g)
+    check(gpu_fb(circ, "c128", x, w, g), want, 1e-12, f"sweep n={n} kind={kind} {opts}")
+
+
+_SWEEP_CACHE = {}
+
+
+def _sweep_oracle(n, kind, gates, x, w, g):
+    if kind not in _SWEEP_CACHE:
+        _SWEEP_CACHE[kind] = oracle.run(n, gates, x, w, grad_out=g)
+    return _SWEEP_CACHE[kind]
 
 
 def test_batch_edges():
