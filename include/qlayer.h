@@ -37,8 +37,9 @@
  * ql_workspace_bytes). The library never allocates device memory in these
  * calls; it only writes the workspace and the outputs. (The first call of
  * each dtype on a handle makes a pinned host copy of the handle's plan tables,
- * which later calls upload by DMA; ql_circuit_destroy synchronises the
- * current device before freeing it.) Outputs are
+ * which later calls upload by DMA; ql_circuit_destroy waits, through an event
+ * per stream that uploaded from it, for the last such upload on each of those
+ * streams before freeing it.) Outputs are
  * overwritten (not accumulated). Buffers must not alias each other or the
  * workspace.
  *
@@ -196,6 +197,9 @@ int ql_circuit_create_desc(int32_t n_qubits, const ql_gate* gates, int32_t n_gat
                            int32_t n_inputs, int32_t n_weights, const ql_circuit_desc* desc,
                            const ql_options* opts, ql_circuit** out);
 
+/* Free a handle (NULL is a no-op). Waits only for the queued table uploads
+ * of calls made with it (an event per stream that made any), not for other
+ * work on the device. The handle must not be used afterwards. */
 void ql_circuit_destroy(ql_circuit* c);
 
 /* Bytes of device workspace a call with this dtype, batch and mode

@@ -152,6 +152,10 @@ struct ql_circuit {
     // dtype), so the per-call upload is an asynchronous DMA
     void* pinned[2] = {nullptr, nullptr};
     std::once_flag pin_once[2];
+    // an event per stream that copied from a pinned blob, recorded after each
+    // such copy: destruction waits for these copies only
+    std::mutex up_mu;
+    std::vector<std::pair<hipStream_t, hipEvent_t>> uploads;
     // timing
     int timing = 0;
     struct Ev {
@@ -327,7 +331,20 @@ int upload_tables(Ctx& x) {
     });
     const void* src = x.h->pinned[x.dt] ? x.h->pinned[x.dt] : (const void*)x.T.blob.data();
     hipError_t e = hipMemcpyAsync(x.W + x.L.tables, src, x.T.blob.size(), hipMemcpyHostToDevice, x.stream);
-    return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("table upload: ") + hipGetErrorString(e));
+    if (e != hipSuccess) return fail(QL_EHIP, std::string("table upload: ") + hipGetErrorString(e));
+    if (!x.h->pinned[x.dt]) return QL_OK;
+    // mark the copy's completion on this stream for ql_circuit_destroy
+    std::lock_guard<std::mutex> lk(x.h->up_mu);
+    hipEvent_t ev = nullptr;
+    for (auto& u : x.h->uploads)
+        if (u.first == x.stream) ev = u.second;
+    if (!ev) {
+        e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e != hipSuccess) return fail(QL_EHIP, std::string("hipEventCreate: ") + hipGetErrorString(e));
+        x.h->uploads.push_back({x.stream, ev});
+    }
+    e = hipEventRecord(ev, x.stream);
+    return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("hipEventRecord: ") + hipGetErrorString(e));
 }
 
 // Angle binding for B circuits. With vper > 0 the circuits are the shifted
@@ -812,12 +829,14 @@ int ql_circuit_create(int32_t n_qubits, const ql_gate* gates, int32_t n_gates, i
 
 void ql_circuit_destroy(ql_circuit* h) {
     if (!h) return;
-    if (h->pinned[0] || h->pinned[1]) {
-        // table uploads of calls still queued read the pinned copies
-        (void)hipDeviceSynchronize();
-        for (void* p : h->pinned)
-            if (p) (void)hipHostFree(p);
+    // table uploads of calls still queued read the pinned copies: wait for
+    // the last one on each stream that made any (not for the whole device)
+    for (auto& u : h->uploads) {
+        (void)hipEventSynchronize(u.second);
+        (void)hipEventDestroy(u.second);
     }
+    for (void* p : h->pinned)
+        if (p) (void)hipHostFree(p);
     for (auto& e : h->ev) {
         (void)hipEventDestroy(e.a);
         (void)hipEventDestroy(e.b);

@@ -1962,29 +1962,30 @@ __device__ __forceinline__ void chunk_of(int bb, int lane, int64_t& lo, int64_t&
 // each group of csz lanes (fixed order), and lane c keeps chunk c's sum.
 template <typename T2>
 __global__ void __launch_bounds__(256) k_block_sums(const SampleArgs a) {
-    const int64_t wv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int lane = threadIdx.x & 63;
-    if (wv >= a.B * a.nblk) return;
-    const int64_t b = wv / a.nblk, blk = wv - b * a.nblk;
-    const int64_t bs = (int64_t)1 << a.bb;
-    const int csz = bs >= 64 ? (int)(bs / 64) : 1, per = 64 / csz;
-    const int rows = bs >= 64 ? 64 / per : 1;
-    const T2* p = (const T2*)a.psi + (b << a.n) + (blk << a.bb);
-    double mine = 0.0;
-    for (int k = 0; k < rows; ++k) {
-        const int64_t i = lane + 64 * (int64_t)k;
-        double q = 0.0;
-        if (i < bs) {
-            const T2 v = p[i];
-            q = (double)v.x * (double)v.x + (double)v.y * (double)v.y;
+    const int64_t stride = (int64_t)gridDim.x * (blockDim.x >> 6);
+    for (int64_t wv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6; wv < a.B * a.nblk; wv += stride) {
+        const int64_t b = wv / a.nblk, blk = wv - b * a.nblk;
+        const int64_t bs = (int64_t)1 << a.bb;
+        const int csz = bs >= 64 ? (int)(bs / 64) : 1, per = 64 / csz;
+        const int rows = bs >= 64 ? 64 / per : 1;
+        const T2* p = (const T2*)a.psi + (b << a.n) + (blk << a.bb);
+        double mine = 0.0;
+        for (int k = 0; k < rows; ++k) {
+            const int64_t i = lane + 64 * (int64_t)k;
+            double q = 0.0;
+            if (i < bs) {
+                const T2 v = p[i];
+                q = (double)v.x * (double)v.x + (double)v.y * (double)v.y;
+            }
+            for (int off = 1; off < csz; off <<= 1) q += __shfl_xor(q, off, 64);
+            const double g = __shfl(q, (lane % per) * csz, 64);
+            if (lane / per == k) mine = g;
         }
-        for (int off = 1; off < csz; off <<= 1) q += __shfl_xor(q, off, 64);
-        const double g = __shfl(q, (lane % per) * csz, 64);
-        if (lane / per == k) mine = g;
+        a.csum[wv * 64 + lane] = mine;
+        const double s = lane_scan(mine, lane);
+        if (lane == 63) a.bsum[wv] = s;
     }
-    a.csum[wv * 64 + lane] = mine;
-    const double s = lane_scan(mine, lane);
-    if (lane == 63) a.bsum[wv] = s;
 }
 
 // One workgroup per sample: inclusive prefix of the block totals, in place,
@@ -2024,68 +2025,72 @@ template <typename T2>
 __global__ void __launch_bounds__(256) k_shots(const SampleArgs a, const double* __restrict__ pre_all,
                                                const double* __restrict__ cs_all,
                                                const double* __restrict__ uni) {
-    // the wavefront's shot, uniform by construction (scalar loads below)
-    const int64_t wv = (int64_t)blockIdx.x * (blockDim.x >> 6) +
-                       __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    // the wavefront's shots, uniform by construction (scalar loads below)
     const int lane = threadIdx.x & 63;
-    if (wv >= a.B * a.shots) return;
-    const int64_t b = wv / a.shots;
-    const double* pre = pre_all + b * a.nblk;
-    const double total = pre[a.nblk - 1];
-    const double r = uni[wv] * total;
-    int64_t lo = 0, hi = a.nblk - 1;  // first block with pre > r (pre[nblk-1] = total > r)
-    while (lo < hi) {
-        const int64_t mid = lo + (hi - lo) / 2;
-        if (pre[mid] > r) hi = mid;
-        else lo = mid + 1;
+    const int64_t stride = (int64_t)gridDim.x * (blockDim.x >> 6);
+    for (int64_t wv = (int64_t)blockIdx.x * (blockDim.x >> 6) +
+                      __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+         wv < a.B * a.shots; wv += stride) {
+        const int64_t b = wv / a.shots;
+        const double* pre = pre_all + b * a.nblk;
+        const double total = pre[a.nblk - 1];
+        const double r = uni[wv] * total;
+        int64_t lo = 0, hi = a.nblk - 1;  // first block with pre > r (pre[nblk-1] = total > r)
+        while (lo < hi) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            if (pre[mid] > r) hi = mid;
+            else lo = mid + 1;
+        }
+        const int64_t blk = lo;
+        const double before = blk > 0 ? pre[blk - 1] : 0.0;
+        int64_t clo, ccnt;
+        chunk_of(a.bb, lane, clo, ccnt);
+        const int64_t base = (b << a.n) + (blk << a.bb);
+        const T2* p = (const T2*)a.psi;
+        const double mine = cs_all[(b * a.nblk + blk) * 64 + lane];  // this lane's chunk sum
+        const double incl = lane_scan(mine, lane);
+        // shuffle with every lane active, then select (a shuffle inside the
+        // conditional would read lane 0 while it is switched off)
+        const double up = __shfl_up(incl, 1, 64);
+        const double prev = lane > 0 ? up : 0.0;
+        const uint64_t hit = __ballot(before + incl > r && ccnt > 0 && mine > 0.0);
+        int L = hit ? (int)__builtin_ctzll(hit) : -1;
+        if (L < 0) {  // rounding left r above the block: the last chunk of nonzero probability
+            const uint64_t has = __ballot(ccnt > 0 && mine > 0.0);
+            L = has ? 63 - (int)__builtin_clzll(has) : 63 - (int)__builtin_clzll(__ballot(ccnt > 0));
+        }
+        const double start = before + __shfl(prev, L, 64);
+        int64_t lL, cL;
+        chunk_of(a.bb, L, lL, cL);  // cL <= 64: one amplitude per lane
+        double q = 0.0;
+        if (lane < cL) {
+            const T2 v = p[base + lL + lane];
+            q = (double)v.x * (double)v.x + (double)v.y * (double)v.y;
+        }
+        const double run = start + lane_scan(q, lane);
+        const uint64_t in = __ballot(lane < cL && run > r && q > 0.0);
+        int64_t idx;
+        if (in) {
+            idx = lL + (int64_t)__builtin_ctzll(in);
+        } else {  // rounding: the chunk's last amplitude of nonzero probability
+            const uint64_t nz = __ballot(lane < cL && q > 0.0);
+            idx = nz ? lL + 63 - (int64_t)__builtin_clzll(nz) : lL;
+        }
+        if (lane == 0) a.samples[wv] = (blk << a.bb) + idx;
     }
-    const int64_t blk = lo;
-    const double before = blk > 0 ? pre[blk - 1] : 0.0;
-    int64_t clo, ccnt;
-    chunk_of(a.bb, lane, clo, ccnt);
-    const int64_t base = (b << a.n) + (blk << a.bb);
-    const T2* p = (const T2*)a.psi;
-    const double incl = lane_scan(cs_all[(b * a.nblk + blk) * 64 + lane], lane);
-    // shuffle with every lane active, then select (a shuffle inside the
-    // conditional would read lane 0 while it is switched off)
-    const double up = __shfl_up(incl, 1, 64);
-    const double prev = lane > 0 ? up : 0.0;
-    const uint64_t hit = __ballot(before + incl > r && ccnt > 0);
-    int L = hit ? (int)__builtin_ctzll(hit) : -1;
-    if (L < 0) {  // rounding left r above the block: last lane with amplitudes
-        const uint64_t has = __ballot(ccnt > 0);
-        L = 63 - (int)__builtin_clzll(has);
-    }
-    const double start = before + __shfl(prev, L, 64);
-    int64_t lL, cL;
-    chunk_of(a.bb, L, lL, cL);  // cL <= 64: one amplitude per lane
-    double q = 0.0;
-    if (lane < cL) {
-        const T2 v = p[base + lL + lane];
-        q = (double)v.x * (double)v.x + (double)v.y * (double)v.y;
-    }
-    const double run = start + lane_scan(q, lane);
-    const uint64_t in = __ballot(lane < cL && run > r && q > 0.0);
-    int64_t idx;
-    if (in) {
-        idx = lL + (int64_t)__builtin_ctzll(in);
-    } else {  // rounding: the chunk's last amplitude of nonzero probability
-        const uint64_t nz = __ballot(lane < cL && q > 0.0);
-        idx = nz ? lL + 63 - (int64_t)__builtin_clzll(nz) : lL;
-    }
-    if (lane == 0) a.samples[wv] = (blk << a.bb) + idx;
 }
 
 // <Z_q> from the shots: one thread per (sample, qubit), exact integer counts.
 template <typename Real>
 __global__ void __launch_bounds__(256) k_shot_z(const SampleArgs a) {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= a.B * a.n) return;
-    const int64_t b = t / a.n;
-    const int q = (int)(t - b * a.n);
-    int64_t ones = 0;
-    for (int64_t s = 0; s < a.shots; ++s) ones += (a.samples[b * a.shots + s] >> q) & 1;
-    ((Real*)a.zhat)[t] = a.shots > 0 ? (Real)((double)(a.shots - 2 * ones) / (double)a.shots) : (Real)0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < a.B * a.n; t += stride) {
+        const int64_t b = t / a.n;
+        const int q = (int)(t - b * a.n);
+        int64_t ones = 0;
+        for (int64_t s = 0; s < a.shots; ++s) ones += (a.samples[b * a.shots + s] >> q) & 1;
+        ((Real*)a.zhat)[t] = a.shots > 0 ? (Real)((double)(a.shots - 2 * ones) / (double)a.shots) : (Real)0;
+    }
 }
 
 }  // namespace
@@ -2260,25 +2265,37 @@ hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, v
     return hipGetLastError();
 }
 
+// Workgroups of 256 threads for `items` work items of `per_block` per
+// workgroup, capped (the sampling kernels stride over the rest).
+static unsigned sample_grid(int64_t items, int64_t per_block) {
+    const int64_t g = (items + per_block - 1) / per_block;
+    return (unsigned)std::max<int64_t>(1, std::min<int64_t>(g, (int64_t)1 << 20));
+}
+
 hipError_t launch_sample(int dtype, const SampleArgs& a, hipStream_t s) {
     const int64_t wb = a.B * a.nblk, ws = a.B * a.shots;
-    if (dtype == 0) hipLaunchKernelGGL(k_block_sums<float2>, dim3((unsigned)((wb + 3) / 4)), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(k_block_sums<double2>, dim3((unsigned)((wb + 3) / 4)), dim3(256), 0, s, a);
+    hipError_t e;
+    if (dtype == 0) hipLaunchKernelGGL(k_block_sums<float2>, dim3(sample_grid(wb, 4)), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_block_sums<double2>, dim3(sample_grid(wb, 4)), dim3(256), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_block_scan, dim3((unsigned)a.B), dim3(256), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ws > 0) {
         if (dtype == 0)
-            hipLaunchKernelGGL(k_shots<float2>, dim3((unsigned)((ws + 3) / 4)), dim3(256), 0, s, a, a.bsum,
-                               a.csum, a.uniforms);
+            hipLaunchKernelGGL(k_shots<float2>, dim3(sample_grid(ws, 4)), dim3(256), 0, s, a, a.bsum, a.csum,
+                               a.uniforms);
         else
-            hipLaunchKernelGGL(k_shots<double2>, dim3((unsigned)((ws + 3) / 4)), dim3(256), 0, s, a, a.bsum,
-                               a.csum, a.uniforms);
+            hipLaunchKernelGGL(k_shots<double2>, dim3(sample_grid(ws, 4)), dim3(256), 0, s, a, a.bsum, a.csum,
+                               a.uniforms);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (a.zhat) {
         const int64_t t = a.B * a.n;
-        if (dtype == 0) hipLaunchKernelGGL(k_shot_z<float>, dim3((unsigned)((t + 255) / 256)), dim3(256), 0, s, a);
-        else hipLaunchKernelGGL(k_shot_z<double>, dim3((unsigned)((t + 255) / 256)), dim3(256), 0, s, a);
+        if (dtype == 0) hipLaunchKernelGGL(k_shot_z<float>, dim3(sample_grid(t, 256)), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL(k_shot_z<double>, dim3(sample_grid(t, 256)), dim3(256), 0, s, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 hipError_t configure_kernels(size_t max_lds) {
