@@ -221,6 +221,28 @@ int ql_forward_backward(const ql_circuit* c, ql_dtype dtype, int64_t batch,
                         void* expz, void* grad_inputs, void* grad_weights,
                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Allocation-free forward + backward, for callers that cannot allocate
+ * device memory or pass a workspace (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation).
+ *
+ * Same arguments, results and errors as ql_forward_backward without the
+ * workspace: the call runs in a static device buffer of
+ * QL_STATIC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends, and returns QL_ENOMEM (before launching anything)
+ * when the circuit, dtype and batch need more than that
+ * (ql_workspace_bytes(..., QL_MODE_FWD_BWD) tells). It calls no device or
+ * host allocator: the plan tables are copied from the handle's own host copy.
+ * The caller still provides inputs and outputs. All calls on one GPU share
+ * that GPU's buffer: calls that overlap in time on one GPU (other streams,
+ * other threads) race and give wrong results; serialise them. Nothing in the
+ * buffer needs to start at zero, so its contents from an earlier call do not
+ * matter. */
+#define QL_STATIC_SCRATCH_BYTES (64u << 20)
+int ql_forward_backward_static(const ql_circuit* c, ql_dtype dtype, int64_t batch,
+                               const void* inputs, const void* weights, const void* grad_out,
+                               void* expz, void* grad_inputs, void* grad_weights,
+                               hipStream_t stream);
 /* ---- parameter-shift gradients -------------------------------------------
  *
  * The same VJP as ql_forward_backward, computed with the two-term

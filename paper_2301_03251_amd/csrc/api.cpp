@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <new>
 #include <set>
@@ -261,6 +262,32 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
     return QL_OK;
 }
 
+// Scratch of ql_forward_backward_static: one copy on every GPU the library
+// runs on, held until the process ends. In host code `scratch` names a
+// host-side stand-in, not device memory: only the address hipGetSymbolAddress
+// returns (per device, with that device current) is passed to kernels.
+__device__ __align__(256) unsigned char scratch[QL_STATIC_SCRATCH_BYTES];
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch;
+
+// The current device's scratch address (looked up once per device).
+int static_scratch(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(QL_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    auto it = g_scratch.find(dev);
+    if (it == g_scratch.end()) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(QL_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+        it = g_scratch.emplace(dev, p).first;
+    }
+    *out = it->second;
+    return QL_OK;
+}
+
 std::mutex g_dev_mu;
 std::set<int> g_dev_ready;
 size_t g_lds_limit = 65536;
@@ -288,7 +315,7 @@ struct Timer {
     bool on = false;
     void start(int c) {
         cls = c;
-        on = (h->timing >> c & 1) != 0;
+        on = h && (h->timing >> c & 1) != 0;
         if (!on) return;
         if (h->ev_used == h->ev.size()) {
             ql_circuit::Ev e{};
@@ -317,9 +344,15 @@ struct Ctx {
     Layout L;
     hipStream_t stream;
     Timer tm;
+    bool no_alloc = false;  // make no host or device allocation (no pinned copy, no event)
 };
 
 int upload_tables(Ctx& x) {
+    if (x.no_alloc) {  // from the handle's own (pageable) copy
+        hipError_t e = hipMemcpyAsync(x.W + x.L.tables, x.T.blob.data(), x.T.blob.size(), hipMemcpyHostToDevice,
+                                      x.stream);
+        return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("table upload: ") + hipGetErrorString(e));
+    }
     std::call_once(x.h->pin_once[x.dt], [&] {
         void* p = nullptr;
         if (hipHostMalloc(&p, x.T.blob.size(), hipHostMallocDefault) == hipSuccess) {
@@ -562,7 +595,7 @@ int check_args(const Circuit& c, const void* inputs, const void* weights, const 
 
 int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* inputs,
         const void* weights, const void* grad_out, void* expz, void* grad_inputs,
-        void* grad_weights, void* ws, size_t ws_bytes, hipStream_t stream) {
+        void* grad_weights, void* ws, size_t ws_bytes, hipStream_t stream, bool no_alloc = false) {
     if (!hc) return fail(QL_EINVAL, "circuit is NULL");
     ql_circuit* h = const_cast<ql_circuit*>(hc);  // only the timing state is touched
     if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
@@ -584,6 +617,8 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
     rc = ensure_device();
     if (rc) return rc;
     Ctx x{h, dt, h->c, h->c.plan[dt], h->t[dt], (uint8_t*)ws, L, stream, Timer{h, stream}};
+    x.no_alloc = no_alloc;
+    if (no_alloc) x.tm.h = nullptr;  // no timing events either
     if ((rc = upload_tables(x))) return rc;
     if ((rc = bind(x, B, inputs, weights, 0, 0))) return rc;
     if ((rc = embed(x, B, inputs, x.L.psi ? (void*)(x.W + x.L.psi) : nullptr, 0, 0))) return rc;
@@ -869,6 +904,27 @@ int ql_forward_backward(const ql_circuit* h, ql_dtype dtype, int64_t batch, cons
                         void* grad_weights, void* ws, size_t ws_bytes, hipStream_t stream) {
     int rc = run(h, dtype, batch, QL_MODE_FWD_BWD, inputs, weights, grad_out, expz, grad_inputs,
                  grad_weights, ws, ws_bytes, stream);
+    if (rc == QL_OK) g_err.clear();
+    return rc;
+}
+
+int ql_forward_backward_static(const ql_circuit* h, ql_dtype dtype, int64_t batch, const void* inputs,
+                               const void* weights, const void* grad_out, void* expz, void* grad_inputs,
+                               void* grad_weights, hipStream_t stream) {
+    if (!h) return fail(QL_EINVAL, "circuit is NULL");
+    if (dtype != QL_C64 && dtype != QL_C128) return fail(QL_EINVAL, "unknown dtype");
+    Layout L;
+    int rc = compute_layout(h, (int)dtype, batch, QL_MODE_FWD_BWD, L);
+    if (rc) return rc;
+    if (L.total > QL_STATIC_SCRATCH_BYTES)
+        return fail(QL_ENOMEM, "ql_forward_backward_static needs " + std::to_string(L.total) +
+                                   " bytes of scratch, above its static maximum of " +
+                                   std::to_string((size_t)QL_STATIC_SCRATCH_BYTES) +
+                                   " (use ql_forward_backward with a workspace)");
+    void* ws = nullptr;
+    if ((rc = static_scratch(&ws))) return rc;
+    rc = run(h, dtype, batch, QL_MODE_FWD_BWD, inputs, weights, grad_out, expz, grad_inputs, grad_weights, ws,
+             QL_STATIC_SCRATCH_BYTES, stream, true);
     if (rc == QL_OK) g_err.clear();
     return rc;
 }

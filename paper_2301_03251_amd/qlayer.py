@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libqlayer.so")
 
 C64, C128 = 0, 1
 MODE_FWD, MODE_FWD_BWD, MODE_FWD_BWD_KEEP = 0, 1, 2
+STATIC_SCRATCH_BYTES = 64 << 20  # QL_STATIC_SCRATCH_BYTES of qlayer.h
 H, RX, RY, RZ, CNOT, CZ, CRX, CRY, CRZ, PAULI = range(10)
 SRC_NONE, SRC_INPUT, SRC_WEIGHT = 0, 1, 2
 EMBED_NONE, EMBED_BASIS, EMBED_AMPLITUDE = 0, 1, 2
@@ -78,6 +79,7 @@ def load():
     lib.ql_workspace_bytes.argtypes = [P, ctypes.c_int, I64, ctypes.c_int, ctypes.POINTER(SZ)]
     lib.ql_forward.argtypes = [P, ctypes.c_int, I64, P, P, P, P, SZ, P]
     lib.ql_forward_backward.argtypes = [P, ctypes.c_int, I64, P, P, P, P, P, P, P, SZ, P]
+    lib.ql_forward_backward_static.argtypes = [P, ctypes.c_int, I64, P, P, P, P, P, P, P]
     lib.ql_param_shift_workspace_bytes.argtypes = [P, ctypes.c_int, I64, I64, ctypes.POINTER(SZ)]
     lib.ql_param_shift.argtypes = [P, ctypes.c_int, I64, P, P, P, P, P, P, I64, P, SZ, P]
     lib.ql_state_workspace_bytes.argtypes = [P, ctypes.c_int, I64, ctypes.POINTER(SZ)]
@@ -215,6 +217,11 @@ class Circuit:
                                           grad_out, expz, grad_inputs, grad_weights, ws,
                                           int(ws_bytes), stream))
 
+    def forward_backward_static_raw(self, dtype, batch, inputs, weights, grad_out, expz, grad_inputs,
+                                    grad_weights, stream):
+        _check(load().ql_forward_backward_static(self._h, _dt(dtype), int(batch), inputs, weights,
+                                                 grad_out, expz, grad_inputs, grad_weights, stream))
+
     def param_shift_raw(self, dtype, batch, inputs, weights, grad_out, expz, grad_inputs,
                         grad_weights, max_chunk, ws, ws_bytes, stream):
         _check(load().ql_param_shift(self._h, _dt(dtype), int(batch), inputs, weights, grad_out,
@@ -337,6 +344,25 @@ class Runner:
             ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
         return expz, gx, gw
 
+
+    def forward_backward_static(self, inputs, weights, grad_out, outs=None):
+        """forward_backward through the allocation-free entry point: the
+        library's static per-GPU scratch instead of this runner's workspace
+        (small circuits and batches only; calls on one GPU must not overlap)."""
+        torch = _torch()
+        B = int(inputs.shape[0])
+        x, w = self._args(inputs, weights, B)
+        if outs is None:
+            outs = (torch.empty((B, self.c.n), dtype=self.real, device=self.device),
+                    torch.empty((B, self.c.n_inputs), dtype=self.real, device=self.device),
+                    torch.empty(self.c.n_weights, dtype=self.real, device=self.device))
+        expz, gx, gw = outs
+        self.c.forward_backward_static_raw(
+            self.dtype, B, _ptr(x) if self.c.n_inputs else None, _ptr(w) if self.c.n_weights else None,
+            _ptr(grad_out), _ptr(expz), _ptr(gx) if (gx is not None and self.c.n_inputs) else None,
+            _ptr(gw) if (gw is not None and self.c.n_weights) else None,
+            ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream))
+        return expz, gx, gw
 
     def param_shift(self, inputs, weights, grad_out, max_chunk=0, want_inputs=True, want_weights=True,
                     outs=None):

@@ -31,6 +31,12 @@ def test_exports_every_declared_symbol(lib):
         assert hasattr(lib, name), f"{name} declared in qlayer.h but not exported"
 
 
+def test_static_scratch_size_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define QL_STATIC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == Q.STATIC_SCRATCH_BYTES
+
+
 def test_product_package_never_uses_the_oracle():
     pkg = os.path.join(ROOT, "paper_2301_03251_amd")
     for dirpath, _, files in os.walk(pkg):
