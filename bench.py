@@ -86,13 +86,25 @@ def profiled_traffic(wl):
     fields = dict(l.split(": ", 1) for l in text.splitlines() if ": " in l and not l.startswith("#"))
     m = re.search(r"copy duration ([0-9.]+) ms", text)
     copy_gbs = 2 * 2 ** 30 / (float(m.group(1)) * 1e-3) / 1e9 if m else None
-    # the counters hold only for the kernel source and the planner that made
-    # the passes they were taken on
-    for key, name in (("kernels_sha256", "kernels.hip"), ("plan_sha256", "plan.cpp")):
-        src = os.path.join(ROOT, "paper_2301_03251_amd", "csrc", name)
-        if fields.get(key) != hashlib.sha256(open(src, "rb").read()).hexdigest():
+    # the counters hold only for the tile kernel's source and the planner that
+    # made the passes they were taken on
+    digests = source_digests()
+    for key in ("tile_sha256", "plan_sha256"):
+        if fields.get(key) != digests[key]:
             return None, copy_gbs
     return float(fields["traffic_bytes_per_step"]), copy_gbs
+
+
+def source_digests():
+    """sha256 of the tile kernel's sources (tile.hip, kcommon.hpp, launch.hpp,
+    plan.hpp) and of the planner (plan.cpp), which key the committed rocprofv3
+    summaries."""
+    csrc = os.path.join(ROOT, "paper_2301_03251_amd", "csrc")
+    h = hashlib.sha256()
+    for name in ("tile.hip", "kcommon.hpp", "launch.hpp", "plan.hpp"):
+        h.update(open(os.path.join(csrc, name), "rb").read())
+    return {"tile_sha256": h.hexdigest(),
+            "plan_sha256": hashlib.sha256(open(os.path.join(csrc, "plan.cpp"), "rb").read()).hexdigest()}
 
 
 def host_info():

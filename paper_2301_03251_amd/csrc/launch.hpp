@@ -1,4 +1,4 @@
-// launch.hpp -- host-side launchers of the HIP kernels (kernels.hip).
+// launch.hpp -- host-side launchers of the HIP kernels (kernels.hip, tile.hip).
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -205,5 +205,7 @@ hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s);
 
 // Raise the dynamic-LDS limit of every kernel on the current device.
 hipError_t configure_kernels(size_t max_lds);
+// The same for the tile kernels only (tile.hip).
+hipError_t configure_tile_kernels(size_t max_lds);
 
 }  // namespace qlayer
