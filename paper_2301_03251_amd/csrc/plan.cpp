@@ -512,6 +512,22 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         op.arg = recs[i].bwd_arg;
         pp.bwd_ops.push_back(op);
     }
+    // A backward layout change refreshes the thread's Im<lambda|psi> sum only
+    // when an RZ-type gradient term (RZ on a register, thread or fixed bit,
+    // an RZ group, an RY-RZ pair) reads it before the next layout change.
+    auto layout_change = [](uint32_t h) { return h == H_TRANSPOSE || (h >= H_LSWAP && h < H_PX); };
+    auto reads_ival = [](uint32_t h) {
+        return (h >= H_G1 + 15 && h < H_G1 + 20) || h == H_RZU || (h >= H_RZN && h < H_RZN + 5) || h == H_DZ ||
+               (h >= H_RYZ && h < H_RYZN + 5);
+    };
+    for (size_t i = 0; i < pp.bwd_ops.size(); i++) {
+        if (!layout_change(pp.bwd_ops[i].h)) continue;
+        for (size_t j = i + 1; j < pp.bwd_ops.size() && !layout_change(pp.bwd_ops[j].h); j++)
+            if (reads_ival(pp.bwd_ops[j].h)) {
+                pp.bwd_ops[i].arg |= ARG_IVAL;
+                break;
+            }
+    }
 }
 
 }  // namespace

@@ -109,6 +109,10 @@ constexpr uint32_t lswap_arg(uint32_t phase, uint32_t x, uint32_t y) {
 // A loc in an op argument: tile bit or qubit in bits 0..7, LocType in bits 8..9.
 constexpr uint32_t loc_word(uint32_t type, uint32_t pos) { return pos | (type << 8); }
 constexpr uint32_t NO_GSLOT = 0xffffu;
+// Flag in the argument of a backward layout change (H_TRANSPOSE, H_LSWAP):
+// refresh the thread's Im<lambda|psi> sum after it, because an RZ-type
+// gradient term uses that sum before the next layout change.
+constexpr uint32_t ARG_IVAL = 1u << 30;
 
 // Static op of a tile pass (the binding kernel turns it into a per-sample record).
 struct DevOp {

@@ -147,15 +147,18 @@ __device__ __forceinline__ Real im_sum(const T2* p, const T2* l) {
 // in lanes 31 and 63, which add it to their own word (two words instead of
 // one save the last broadcast step). Every word has one writer lane, so its
 // sum is in program order (deterministic); the add has no return value.
+// `gthr` is this thread's word of accumulator 0, gacc + wave * GRAD_WORDS +
+// (lane >> 5), and `stride` the uniform distance between accumulators: the
+// address then costs one vector add.
 constexpr int GRAD_WORDS = TILE_GRAD_WORDS;
 template <typename Real>
-__device__ __forceinline__ void grad_add(Real* gacc, uint32_t g, Real part, int lane, int wave, int nw) {
+__device__ __forceinline__ void grad_add(Real* gthr, uint32_t g, Real part, int lane, int /*wave*/,
+                                         int stride) {
     Real v = row_sum(part);
     if constexpr (sizeof(Real) == 4) v += bcast_f32<0x142, 0xA>(v);
     else v += bcast_f64<0x142, 0xA>(v);
     if ((lane & 31) == 31)
-        __hip_atomic_fetch_add(gacc + (g * (uint32_t)nw + (uint32_t)wave) * GRAD_WORDS + (lane >> 5), v,
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __hip_atomic_fetch_add(gthr + g * (uint32_t)stride, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Exchange two values in place (their registers keep their roles, so the
@@ -446,9 +449,11 @@ __device__ __forceinline__ void dz_grads(const T2* ps, const T2* lm, Real ca, Re
 enum { OP_ONE = 0, OP_PAIR = 1, OP_BWD = 2 };
 //
 // In OP_BWD, `ival` holds the thread's full Im(conj(lambda) psi) sum of the
-// current layout (refreshed after each exchange), so the Z-generator term of
-// an RZ is ival - 2 * (the bit-1 half), and of an RZ on a thread or fixed bit
-// +-ival.
+// current layout (refreshed after a layout change whose argument carries
+// ARG_IVAL: one that an RZ-type term follows), so the Z-generator term of an
+// RZ is ival - 2 * (the bit-1 half), and of an RZ on a thread or fixed bit
+// +-ival. `gacc` is the thread's word of gradient accumulator 0 and `nw` the
+// stride between accumulators (see grad_add).
 template <int LOG_R, int LOG_T, int OPM, typename T2, typename Real>
 __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
                                        TileCtx& cx, Real& ival, unsigned char* lds,
@@ -517,12 +522,13 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
             lane_swap<LOG_R, M, B>(ps);                                                     \
             if constexpr (OPM != OP_ONE) lane_swap<LOG_R, M, B>(lm);                        \
             cx.ph = (int)(arg & 0xfffff);                                                   \
-            const uint32_t dtb = (1u << ((arg >> 20) & 31)) | (1u << (arg >> 25));         \
+            const uint32_t dtb = (1u << ((arg >> 20) & 31)) | (1u << ((arg >> 25) & 31));  \
             if ((lane >> B) & 1) {                                                          \
                 cx.tb ^= dtb;                                                               \
                 cx.ts ^= lds_slot(dtb) * (uint32_t)sizeof(T2);                              \
             }                                                                               \
-            if constexpr (OPM == OP_BWD) ival = im_sum<LOG_R, -1, T2, Real>(ps, lm);        \
+            if constexpr (OPM == OP_BWD)                                                    \
+                if (arg & ARG_IVAL) ival = im_sum<LOG_R, -1, T2, Real>(ps, lm);             \
         }                                                                                   \
         break;
 #define QL_LSWAP_M(M) QL_LSWAP(M, 4) QL_LSWAP(M, 5)
@@ -603,15 +609,17 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
                 cz_sel<LOG_R, -1>(lm, loc_bit(arg & 0xffff, cx.tb, cx.gb2) && loc_bit(arg >> 16, cx.tb, cx.gb2));
         } break;
         case H_TRANSPOSE: {
-            const DevPhase& to = phases[arg];
+            const uint32_t ph_to = arg & 0xfffffu;
+            const DevPhase& to = phases[ph_to];
             uint32_t tb_to, ts_to;
             thread_layout<LOG_T>((uint32_t)tid, to, tb_to, ts_to);
             lds_exchange<LOG_R>(ps, lds, phases[cx.ph], to, cx.ts, ts_to);
             if constexpr (OPM != OP_ONE) lds_exchange<LOG_R>(lm, lds, phases[cx.ph], to, cx.ts, ts_to);
-            if constexpr (OPM == OP_BWD) ival = im_sum<LOG_R, -1, T2, Real>(ps, lm);
+            if constexpr (OPM == OP_BWD)
+                if (arg & ARG_IVAL) ival = im_sum<LOG_R, -1, T2, Real>(ps, lm);
             cx.tb = tb_to;
             cx.ts = ts_to;
-            cx.ph = (int)arg;
+            cx.ph = (int)ph_to;
         } break;
         default:
             __builtin_unreachable();
@@ -714,6 +722,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     double* red = (double*)smem;                       // [n][NW]
     constexpr int GW = GRAD_WORDS;
     Real* gacc = (Real*)(red + (size_t)n * NW);        // [n_gslots][NW][GW]
+    Real* gthr = gacc + wave * GW + (lane >> 5);       // this thread's word of accumulator 0
 
     const size_t dim = (size_t)1 << n;
     const T2* psi_s = (const T2*)a.psi + b * dim;
@@ -844,7 +853,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
             for (int o = fwd_begin; o < fwd_end; ++o) {
                 const XOp<Real> nxt = xops[o + 1];
                 run_op<LOG_R, LOG_T, PAIR ? OP_PAIR : OP_ONE>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx,
-                                                              ival, lds, phases, gacc, lane, wave, NW,
+                                                              ival, lds, phases, gthr, lane, wave, NW * GW,
                                                               tid, dz, fz);
                 cur = nxt;
             }
@@ -884,7 +893,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
                     run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, ival, lds,
-                                                 phases, gacc, lane, wave, NW, tid, dz, fz);
+                                                 phases, gthr, lane, wave, NW * GW, tid, dz, fz);
                     cur = nxt;
                 }
             }
