@@ -345,6 +345,12 @@ struct Ctx {
     hipStream_t stream;
     Timer tm;
     bool no_alloc = false;  // make no host or device allocation (no pinned copy, no event)
+    // the angle sources of the current circuits (set by bind(); the
+    // one-wavefront kernel binds the angles itself)
+    const void* inputs = nullptr;
+    const void* weights = nullptr;
+    int64_t v0 = 0;
+    int32_t vper = 0;
 };
 
 int upload_tables(Ctx& x) {
@@ -384,8 +390,13 @@ int upload_tables(Ctx& x) {
 // copies of a parameter-shift chunk: circuit i is virtual circuit v = v0 + i,
 // sample v / vper, and v % vper = 2s+1 (2s+2) shifts rotation slot s by
 // +pi/2 (-pi/2).
-int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0, int32_t vper) {
+int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0, int32_t vper, bool bwd) {
     hipError_t e;
+    x.inputs = inputs;
+    x.weights = weights;
+    x.v0 = v0;
+    x.vper = vper;
+    if (x.pl.whole_state && whole_uses_wave(x.c.n, bwd, B)) return QL_OK;  // bound in the kernel
     if (x.pl.whole_state) {
         BindArgs ba{};
         ba.inputs = inputs;
@@ -472,6 +483,12 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         wa.bwd = bwd ? 1 : 0;
         wa.B = B;
         wa.coef = x.W + x.L.coef;
+        wa.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
+        wa.inputs = x.inputs;
+        wa.weights = x.weights;
+        wa.F = c.n_inputs;
+        wa.v0 = x.v0;
+        wa.vper = x.vper;
         wa.grad_out = grad_out;
         wa.zpart = zpart;
         wa.gpart = gpart;
@@ -620,7 +637,7 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
     x.no_alloc = no_alloc;
     if (no_alloc) x.tm.h = nullptr;  // no timing events either
     if ((rc = upload_tables(x))) return rc;
-    if ((rc = bind(x, B, inputs, weights, 0, 0))) return rc;
+    if ((rc = bind(x, B, inputs, weights, 0, 0, bwd))) return rc;
     if ((rc = embed(x, B, inputs, x.L.psi ? (void*)(x.W + x.L.psi) : nullptr, 0, 0))) return rc;
     if ((rc = state_passes(x, B, bwd, grad_out))) return rc;
     if ((rc = reduce(x, B, bwd, expz, grad_inputs, grad_weights))) return rc;
@@ -699,7 +716,7 @@ int param_shift(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inp
     double* dv = (double*)(x.W + S.dv);
     for (int64_t v0 = 0; v0 < S.total; v0 += S.chunk) {
         const int64_t cb = std::min(S.chunk, S.total - v0);
-        if ((rc = bind(x, cb, inputs, weights, v0, V))) return rc;
+        if ((rc = bind(x, cb, inputs, weights, v0, V, false))) return rc;
         if ((rc = embed(x, cb, inputs, x.L.psi ? (void*)(x.W + x.L.psi) : nullptr, v0, V))) return rc;
         if ((rc = state_passes(x, cb, false, nullptr))) return rc;
         if ((rc = reduce(x, cb, false, ev, nullptr, nullptr))) return rc;
@@ -755,7 +772,7 @@ int state(const ql_circuit* hc, ql_dtype dtype, int64_t B, const void* inputs, c
     if (rc) return rc;
     Ctx x{h, dt, h->c, h->c.plan[dt], h->t[dt], (uint8_t*)ws, L, stream, Timer{h, stream}};
     if ((rc = upload_tables(x))) return rc;
-    if ((rc = bind(x, B, inputs, weights, 0, 0))) return rc;
+    if ((rc = bind(x, B, inputs, weights, 0, 0, false))) return rc;
     if ((rc = embed(x, B, inputs, psi, 0, 0))) return rc;
     if ((rc = state_passes(x, B, false, nullptr, psi))) return rc;
     if (x.pl.whole_state) return QL_OK;  // exact gates: no phase to undo

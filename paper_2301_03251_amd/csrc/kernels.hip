@@ -407,26 +407,114 @@ __device__ __forceinline__ Real wave_grad(const T2* p, const T2* l, const DevGat
     return acc;
 }
 
-// Coefficients of gate g for this sample: (c, s) = (cos t/2, sin t/2), or the
-// Pauli index of a channel in c.
-template <typename T2>
-__device__ __forceinline__ T2 gate_coef(const DevGate& g, const T2* coef) {
-    return g.slot >= 0 ? coef[g.slot] : mk<T2>((decltype(T2::x))1, (decltype(T2::x))0);
+// Handler id of a gate for the one-wavefront kernel: one-qubit kinds (H, RX,
+// RY, RZ, Pauli) 8 * kind + q, CNOT 40 + 8 c + t, CZ 104 + 8 a + b (a < b).
+// Each id is a case of wave_op whose gate is a compile-time constant, so the
+// lane and register choices of wave_gate and wave_grad fold away.
+__device__ __forceinline__ int wave_handler(const DevGate& g) {
+    if (g.kind == K_CNOT) return 40 + 8 * g.q0 + g.q1;
+    if (g.kind == K_CZ) return 104 + 8 * min(g.q0, g.q1) + max(g.q0, g.q1);
+    return 8 * (g.kind == K_PAULI ? 4 : g.kind) + g.q0;
 }
 
-// One wavefront (one sample) per workgroup: the sample index is uniform, so
-// the gate table and the sample's coefficients are scalar loads, issued one
-// gate ahead of their use.
-// The gate table and coefficients come in as restrict parameters: the kernel
-// writes only outputs, so they stay scalar loads even next to those stores.
+// BWD = false: the gate on ps. BWD = true: when `want`, this lane's term of
+// the gradient (before the gate) into *grad, then the inverse on ps and lm.
+template <int R, bool BWD, typename T2, typename Real>
+__device__ __forceinline__ void wave_op(int h, T2* ps, T2* lm, Real c, Real s, int which, int lane, Real* grad,
+                                        bool want) {
+    constexpr int NQ = R == 1 ? 6 : R == 2 ? 7 : 8;  // qubits a sample's registers hold
+#define QL_W(H, KIND, Q0, Q1)                                                             \
+    case H:                                                                               \
+        if constexpr (Q0 < NQ && Q1 < NQ && Q0 != Q1) {                                   \
+            constexpr DevGate g{KIND, Q0, Q1, 0};                                         \
+            if constexpr (BWD) {                                                          \
+                if (want) *grad = wave_grad<R, T2, Real>(ps, lm, g, lane);                \
+                wave_gate<R, T2, Real>(ps, g, c, -s, which, lane);                        \
+                wave_gate<R, T2, Real>(lm, g, c, -s, which, lane);                        \
+            } else {                                                                      \
+                wave_gate<R, T2, Real>(ps, g, c, s, which, lane);                         \
+            }                                                                             \
+        }                                                                                 \
+        break;
+#define QL_W1(Q)                                                                          \
+    QL_W(Q, K_H, Q, -1) QL_W(8 + Q, K_RX, Q, -1) QL_W(16 + Q, K_RY, Q, -1)                 \
+    QL_W(24 + Q, K_RZ, Q, -1) QL_W(32 + Q, K_PAULI, Q, -1)
+#define QL_W2(BASE, KIND, A)                                                              \
+    QL_W(BASE + 8 * A + 0, KIND, A, 0) QL_W(BASE + 8 * A + 1, KIND, A, 1)                 \
+    QL_W(BASE + 8 * A + 2, KIND, A, 2) QL_W(BASE + 8 * A + 3, KIND, A, 3)                 \
+    QL_W(BASE + 8 * A + 4, KIND, A, 4) QL_W(BASE + 8 * A + 5, KIND, A, 5)                 \
+    QL_W(BASE + 8 * A + 6, KIND, A, 6) QL_W(BASE + 8 * A + 7, KIND, A, 7)
+    switch (h) {
+        QL_W1(0) QL_W1(1) QL_W1(2) QL_W1(3) QL_W1(4) QL_W1(5) QL_W1(6) QL_W1(7)
+        QL_W2(40, K_CNOT, 0) QL_W2(40, K_CNOT, 1) QL_W2(40, K_CNOT, 2) QL_W2(40, K_CNOT, 3)
+        QL_W2(40, K_CNOT, 4) QL_W2(40, K_CNOT, 5) QL_W2(40, K_CNOT, 6) QL_W2(40, K_CNOT, 7)
+        QL_W2(104, K_CZ, 0) QL_W2(104, K_CZ, 1) QL_W2(104, K_CZ, 2) QL_W2(104, K_CZ, 3)
+        QL_W2(104, K_CZ, 4) QL_W2(104, K_CZ, 5) QL_W2(104, K_CZ, 6) QL_W2(104, K_CZ, 7)
+        default:
+            break;
+    }
+#undef QL_W
+#undef QL_W1
+#undef QL_W2
+}
+
+// Up to 64 consecutive gates held by the lanes of a wavefront: lane i holds
+// gate base + i (its handler id, slot and kind) and this sample's (cos t/2,
+// sin t/2) of its angle (a Pauli channel: the Pauli's index in c), bound in
+// fp64 as k_bind does. The gate loop then reads them with readlane: no
+// memory access per gate.
+template <typename Real>
+struct WaveChunk {
+    int h, slot, kind;
+    Real c, s;
+};
+
+template <typename Real>
+__device__ __forceinline__ WaveChunk<Real> wave_chunk(const WholeArgs& a, const DevGate* __restrict__ gates,
+                                                      int base, int lane, int64_t b) {
+    WaveChunk<Real> w{0, -1, K_H, (Real)1, (Real)0};
+    const int i = base + lane;
+    if (i >= a.n_gates) return w;
+    const DevGate g = gates[i];
+    w.h = wave_handler(g);
+    w.slot = g.slot;
+    w.kind = g.kind;
+    if (g.slot < 0) return w;
+    const SlotSrc src = a.slots[g.slot];
+    if (src.src == S_PAULI) {
+        w.c = (Real)pauli_of<Real>(a.inputs, a.F, src, b, a.v0, a.vper);
+        return w;
+    }
+    int64_t bs = b;
+    const double th = angle_of<Real>(a.inputs, a.weights, a.F, src, b, a.v0, a.vper, bs) +
+                      shift_of(b, a.v0, a.vper, g.slot);
+    double sn, cs;
+    sincos(0.5 * th, &sn, &cs);
+    w.c = (Real)cs;
+    w.s = (Real)sn;
+    return w;
+}
+
+__device__ __forceinline__ int rl(int v, int i) { return __builtin_amdgcn_readlane(v, i); }
+__device__ __forceinline__ float rl(float v, int i) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), i));
+}
+__device__ __forceinline__ double rl(double v, int i) {
+    const long long u = __builtin_bit_cast(long long, v);
+    const int lo = __builtin_amdgcn_readlane((int)(u & 0xffffffff), i);
+    const int hi = __builtin_amdgcn_readlane((int)(u >> 32), i);
+    return __builtin_bit_cast(double, ((long long)hi << 32) | (unsigned int)lo);
+}
+
+// One wavefront (one sample) per workgroup. The gates stream through the
+// lanes 64 at a time (wave_chunk): the forward walks the chunks in order, the
+// backward in reverse (a circuit of at most 64 gates keeps its one chunk).
 template <typename Real, int R>
-__global__ void __launch_bounds__(64) k_wave(const WholeArgs a, const DevGate* __restrict__ gates,
-                                             const typename Cx<Real>::T* __restrict__ coef_all) {
+__global__ void __launch_bounds__(64) k_wave(const WholeArgs a, const DevGate* __restrict__ gates) {
     using T2 = typename Cx<Real>::T;
     const int lane = threadIdx.x;
     const int64_t b = blockIdx.x;
     const int n = a.n, dim = 1 << n, G = a.n_gates;
-    const T2* coef = coef_all + b * a.n_slots;
     T2 ps[R], lm[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -435,19 +523,15 @@ __global__ void __launch_bounds__(64) k_wave(const WholeArgs a, const DevGate* _
         else if (a.psi_in) ps[r] = ((const T2*)a.psi_in)[b * dim + j];
         else ps[r] = mk<T2>((Real)(j == 0), (Real)0);
     }
-    // gate records two gates ahead, coefficients one ahead: each iteration
-    // waits only for loads issued during the previous gate
-    auto gate_at = [&](int i) { return gates[__builtin_amdgcn_readfirstlane(i < 0 ? 0 : i < G ? i : G - 1)]; };
-    if (G > 0) {
-        DevGate g0 = gate_at(0), g1 = gate_at(1);
-        T2 c0 = gate_coef(g0, coef);
-        for (int gi = 0; gi < G; ++gi) {
-            const T2 c1 = gate_coef(g1, coef);
-            const DevGate g2 = gate_at(gi + 2);
-            wave_gate<R, T2, Real>(ps, g0, c0.x, c0.y, (int)c0.x, lane);
-            g0 = g1;
-            g1 = g2;
-            c0 = c1;
+    WaveChunk<Real> ch{};
+    int loaded = -1;  // base of the chunk in `ch`
+    for (int base = 0; base < G; base += 64) {
+        ch = wave_chunk<Real>(a, gates, base, lane, b);
+        loaded = base;
+        const int cnt = min(64, G - base);
+        for (int i = 0; i < cnt; ++i) {
+            const Real c = rl(ch.c, i);
+            wave_op<R, false, T2, Real>(rl(ch.h, i), ps, lm, c, rl(ch.s, i), (int)c, lane, nullptr, false);
         }
     }
     if (a.psi_out)
@@ -472,21 +556,21 @@ __global__ void __launch_bounds__(64) k_wave(const WholeArgs a, const DevGate* _
         for (int q = 0; q < n; ++q) d += amp_bit(q, lane, r) ? -go[q] : go[q];
         lm[r] = mk<T2>(d * ps[r].x, d * ps[r].y);
     }
-    if (G > 0) {
-        DevGate g0 = gate_at(G - 1), g1 = gate_at(G - 2);
-        T2 c0 = gate_coef(g0, coef);
-        for (int gi = G - 1; gi >= 0; --gi) {
-            const T2 c1 = gate_coef(g1, coef);
-            const DevGate g2 = gate_at(gi - 2);
-            if (g0.slot >= 0 && g0.kind != K_PAULI) {
-                const Real t = wave_to_last(wave_grad<R, T2, Real>(ps, lm, g0, lane));
-                if (lane == 63) a.gpart[(size_t)g0.slot * a.B + b] = (double)t;
+    for (int base = G > 0 ? ((G - 1) / 64) * 64 : -64; base >= 0; base -= 64) {
+        if (base != loaded) {
+            ch = wave_chunk<Real>(a, gates, base, lane, b);
+            loaded = base;
+        }
+        for (int i = min(64, G - base) - 1; i >= 0; --i) {
+            const int slot = rl(ch.slot, i);
+            const bool want = slot >= 0 && rl(ch.kind, i) != K_PAULI;
+            const Real c = rl(ch.c, i);
+            Real part = 0;
+            wave_op<R, true, T2, Real>(rl(ch.h, i), ps, lm, c, rl(ch.s, i), (int)c, lane, &part, want);
+            if (want) {
+                const Real t = wave_to_last(part);
+                if (lane == 63) a.gpart[(size_t)slot * a.B + b] = (double)t;
             }
-            wave_gate<R, T2, Real>(ps, g0, c0.x, -c0.y, (int)c0.x, lane);
-            wave_gate<R, T2, Real>(lm, g0, c0.x, -c0.y, (int)c0.x, lane);
-            g0 = g1;
-            g1 = g2;
-            c0 = c1;
         }
     }
     if (a.lam_out)
@@ -1020,15 +1104,16 @@ hipError_t launch_bind(int dtype, const BindArgs& a, hipStream_t s) {
 // 1.56 against 1.78 ms at 2048, even at 512).
 constexpr int64_t WAVE_MAX_FWD_CIRCUITS = 2048;
 
+bool whole_uses_wave(int n, bool bwd, int64_t B) { return n <= 8 && (bwd || B < WAVE_MAX_FWD_CIRCUITS); }
+
 hipError_t launch_whole(int dtype, const WholeArgs& a, int threads, size_t lds, hipStream_t s) {
-    if (a.n <= 8 && (a.bwd || a.B < WAVE_MAX_FWD_CIRCUITS)) {  // one wavefront per sample
+    if (whole_uses_wave(a.n, a.bwd != 0, a.B)) {  // one wavefront per sample
         const dim3 grid((unsigned)a.B), block(64);
 #define QL_WAVE(REAL)                                                                     \
     {                                                                                     \
-        const auto* cf = (const typename Cx<REAL>::T*)a.coef;                             \
-        if (a.n <= 6) hipLaunchKernelGGL((k_wave<REAL, 1>), grid, block, 0, s, a, a.gates, cf);      \
-        else if (a.n == 7) hipLaunchKernelGGL((k_wave<REAL, 2>), grid, block, 0, s, a, a.gates, cf); \
-        else hipLaunchKernelGGL((k_wave<REAL, 4>), grid, block, 0, s, a, a.gates, cf);               \
+        if (a.n <= 6) hipLaunchKernelGGL((k_wave<REAL, 1>), grid, block, 0, s, a, a.gates);      \
+        else if (a.n == 7) hipLaunchKernelGGL((k_wave<REAL, 2>), grid, block, 0, s, a, a.gates); \
+        else hipLaunchKernelGGL((k_wave<REAL, 4>), grid, block, 0, s, a, a.gates);               \
     }
         if (dtype == 0) {
             QL_WAVE(float)

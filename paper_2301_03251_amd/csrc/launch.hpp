@@ -87,7 +87,14 @@ struct WholeArgs {
     int32_t n_gates, n, n_slots;
     int32_t bwd;          // 1: run the adjoint sweep
     int64_t B;
-    const void* coef;     // [B][n_slots]
+    const void* coef;     // [B][n_slots]: from k_bind (LDS kernel), unused by the wavefront kernel
+    // the angle sources, which the one-wavefront kernel binds itself (as k_bind does)
+    const SlotSrc* slots; // [n_slots]
+    const void* inputs;   // [B][F] Real
+    const void* weights;  // [P] Real
+    int32_t F;
+    int32_t vper;         // parameter-shift chunks: circuits per sample, 0 = plain batch
+    int64_t v0;           // parameter-shift chunks: first virtual circuit
     const void* grad_out; // [B][n] Real
     double* zpart;        // [B][n]           (one workgroup per sample)
     double* gpart;        // [n_slots][B]
@@ -190,6 +197,9 @@ size_t tile_static_lds(int dtype, int log_r, int threads);
 hipError_t launch_bind(int dtype, const BindArgs& a, hipStream_t s);
 hipError_t launch_bind_tile(int dtype, const BindTileArgs& a, hipStream_t s);
 hipError_t launch_whole(int dtype, const WholeArgs& a, int threads, size_t lds, hipStream_t s);
+// Whether launch_whole runs the one-wavefront kernel (which binds the angles
+// itself, so no k_bind launch is needed) for this call.
+bool whole_uses_wave(int n, bool bwd, int64_t B);
 hipError_t launch_tile(int dtype, int log_r, bool bwd, const TileArgs& a, int threads, size_t lds,
                        hipStream_t s);
 hipError_t launch_reduce(int dtype, const ReduceArgs& a, hipStream_t s);
