@@ -184,6 +184,9 @@ def main():
                          "(ql_state) plus this many shots per sample (ql_sample)")
     ap.add_argument("--shift-chunk", type=int, default=0,
                     help="shifted circuits per chunk (0: as many as 8 GiB of states hold)")
+    ap.add_argument("--states", choices=("auto", "kept", "plain"), default="auto",
+                    help="backward workspace: kept forward states when they fit (auto), always "
+                         "(kept), or never (plain: each backward pass stores psi for the next)")
     ap.add_argument("--opt", action="append", default=[],
                     help="planner option key=value (log_regs, log_threads, low_qubits, "
                          "max_gates_per_pass, wg_per_sample)")
@@ -208,7 +211,7 @@ def main():
     opts = {kv.split("=")[0]: int(kv.split("=")[1]) for kv in args.opt}
     circ = Q.Circuit(wl.n, gates, n_in, wl.n_weights, embed=getattr(wl, "embed", None), pauli_p=pauli_p,
                      **opts)
-    runner = Q.Runner(circ, wl.dtype)
+    runner = Q.Runner(circ, wl.dtype, keep_states={"auto": None, "kept": True, "plain": False}[args.states])
     real = torch.float32 if wl.dtype == "c64" else torch.float64
     dev = torch.device("cuda")
     xt = torch.from_numpy(x).to(dev, real)
@@ -313,7 +316,10 @@ def main():
         else:
             state_bytes = circ.state_bytes(wl.dtype, wl.batch, runner.backward_mode(wl.batch))
             flops = algorithmic_flops(gates, wl.batch, wl.n)
-            traffic = profiled_traffic(wl)[0] if args.noise == 0 else None
+            # the committed summaries were taken on the default plan with kept states
+            same_run = (args.noise == 0 and not opts
+                        and runner.backward_mode(wl.batch) == Q.MODE_FWD_BWD_KEEP)
+            traffic = profiled_traffic(wl)[0] if same_run else None
         copy_gbs = profiled_traffic(wl)[1]
         hbm = state_bytes / (tile_ms / 1e3) / 1e9
         alu = flops / (tile_ms / 1e3) / 1e12

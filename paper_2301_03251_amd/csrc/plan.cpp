@@ -757,7 +757,9 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         }
         return cost;
     };
-    const int horizon = G > 4096 ? 4 : 16;
+    // The planning time grows with horizon x gates x passes: full look-aheads
+    // for circuits of the workloads' size, shorter ones for long circuits.
+    const int horizon = G <= 2048 ? 32 : G <= 4096 ? 8 : 4;
     while (remaining > 0 || pl.passes.empty()) {
         // The greedy choice is the candidate that executes the most gates.
         // By default each candidate is instead priced by the cost of its pass

@@ -11,10 +11,11 @@ as ``<workload>.npz`` (plain arrays, no pickle):
   digest        sha256 of the workload's inputs, weights and grad_out
 
 ``16q`` holds the whole batch (all 1024 rows, so ``grad_weights`` is the
-batch sum of the workload itself). ``24q_c128`` is the 24-qubit workload in
-complex128: the same circuit with its inputs drawn and kept in fp64.
+batch sum of the workload itself). ``24q_c128`` and ``30q_c128`` are the 24-
+and 30-qubit workloads in complex128: the same circuits with their inputs
+drawn and kept in fp64.
 
-Usage: python tests/golden/make_golden.py 24q 30q 16q 24q_c128
+Usage: python tests/golden/make_golden.py 24q 30q 16q 24q_c128 30q_c128
 """
 
 from __future__ import annotations
@@ -33,7 +34,7 @@ sys.path.insert(0, ROOT)
 import oracle  # noqa: E402
 import workloads as W  # noqa: E402
 
-ROWS = {"24q": [0, 7, 15], "30q": [0], "16q": list(range(1024)), "24q_c128": [0, 7, 15]}
+ROWS = {"24q": [0, 7, 15], "30q": [0], "16q": list(range(1024)), "24q_c128": [0, 7, 15], "30q_c128": [0]}
 
 
 def workload(name: str):

@@ -299,6 +299,13 @@ def test_pass_search(lib):
         assert np.bincount(greedy.schedule(dt)[0]).min() < 30
     for bad in (1, -2):
         assert _err(lambda: Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights, pass_search=bad)) == -3
+    # on every workload the look-ahead plan has no more passes than greedy
+    for name in W.WORKLOADS:
+        w2 = W.get(name)
+        a = Q.Circuit(w2.n, w2.gates(), w2.n_inputs, w2.n_weights)
+        b = Q.Circuit(w2.n, w2.gates(), w2.n_inputs, w2.n_weights, pass_search=-1)
+        for dt in ("c64", "c128"):
+            assert a.plan_info(dt)["n_passes"] <= b.plan_info(dt)["n_passes"], (name, dt)
 
 
 # ---------------------------------------------------------------------------

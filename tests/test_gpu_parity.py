@@ -209,12 +209,13 @@ def test_workload_16q_sampled():
 
 
 @pytest.mark.parametrize("keep", [True, False], ids=["kept", "plain"])
-@pytest.mark.parametrize("name", ["16q", "24q", "24q_c128", "30q"])
+@pytest.mark.parametrize("name", ["16q", "24q", "24q_c128", "30q", "30q_c128"])
 def test_workload_golden(name, keep):
     """Full workload on the GPU vs oracle values stored by tests/golden/make_golden.py,
     with and without the kept forward states: 16q over its whole batch (so the
     weight gradients are the batch sums of the workload itself), 24q and 30q on
-    sampled rows, and 24q in complex128 (inputs drawn in fp64) at 1e-12."""
+    sampled rows, and 24q and 30q in complex128 (inputs drawn in fp64) at 1e-12
+    (30q complex128 with kept states: a 176 GiB workspace)."""
     path = os.path.join(GOLDEN, f"{name}.npz")
     if not os.path.exists(path):
         pytest.skip(f"{path} not generated")
