@@ -165,11 +165,15 @@ typedef struct {
                                    bits) run as one per-register phase op, and an RZ
                                    that commutes back to an RY on its bit runs in one
                                    op with it; -1: every RZ runs on its own */
-    int32_t pass_search;        /* 0: the tile of each pass is the candidate whose pass
-                                   plus a greedy completion of the rest is cheapest
-                                   under a memory/arithmetic cost model (no nearly
-                                   empty passes at the end of long CNOT chains);
-                                   -1: the candidate that runs the most gates */
+    int32_t pass_search;        /* how the tiles of the passes are chosen. 1: one pass
+                                   at a time, the candidate whose pass plus a greedy
+                                   completion of the rest is cheapest under a
+                                   memory/arithmetic cost model (no nearly empty
+                                   passes at the end of long CNOT chains); -1: one
+                                   pass at a time, the candidate that runs the most
+                                   gates; 0 (default): a beam search over whole pass
+                                   sequences, taken when it needs fewer passes than
+                                   1, else 1 */
 } ql_options;
 
 typedef struct ql_circuit ql_circuit; /* opaque */

@@ -190,7 +190,10 @@ struct Options {
     int force_tiled = 0, wg_per_sample = 0;
     int rz_groups = 0;  // 0: RZs on register bits are grouped into H_DZ ops or joined to their
                         // bit's RY (H_RYZ); -1: every RZ runs on its own
-    int pass_search = 0;  // 0: each pass's tile priced by a look-ahead; -1: the widest pass
+    int pass_search = 0;  // 0: a beam search over pass sequences when it needs fewer passes than
+                          // the look-ahead, else the look-ahead; 1: the look-ahead (each
+                          // pass's tile priced by its pass plus a greedy completion); -1: the
+                          // widest pass each time
 };
 
 // One forward tile pass as planned (host form).

@@ -283,29 +283,35 @@ def test_pass_counts_are_small(lib):
 
 
 def test_pass_search(lib):
-    """The look-ahead tile choice against the widest-pass greedy on the
-    30-qubit CNOT staircase: fewer passes, no nearly empty pass at the end of
-    the chains, and both plans valid. The option takes 0 or -1 only."""
+    """The three tile choices on the 30-qubit CNOT staircase: the look-ahead
+    (pass_search=1) needs fewer passes than the widest-pass greedy (-1) and
+    leaves no nearly empty pass at the end of the chains; the default (0)
+    takes the beam search's plan, fewer passes still (9 in complex64). All
+    plans are valid. The option takes -1, 0 or 1 only."""
     wl = W.get("30q")
     gates = wl.gates()
-    look = Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights)
+    best = Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights)
+    look = Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights, pass_search=1)
     greedy = Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights, pass_search=-1)
     for dt in ("c64", "c128"):
-        _check_schedule(look, gates, dt)
-        _check_schedule(greedy, gates, dt)
-        assert look.plan_info(dt)["n_passes"] < greedy.plan_info(dt)["n_passes"], dt
+        for c in (best, look, greedy):
+            _check_schedule(c, gates, dt)
+        n0, n1, n2 = (c.plan_info(dt)["n_passes"] for c in (best, look, greedy))
+        assert n0 < n1 < n2, (dt, n0, n1, n2)
         sizes = np.bincount(look.schedule(dt)[0])
         assert sizes.min() >= 30, (dt, sizes)
         assert np.bincount(greedy.schedule(dt)[0]).min() < 30
-    for bad in (1, -2):
+    assert best.plan_info("c64")["n_passes"] == 9
+    for bad in (2, -2):
         assert _err(lambda: Q.Circuit(wl.n, gates, wl.n_inputs, wl.n_weights, pass_search=bad)) == -3
-    # on every workload the look-ahead plan has no more passes than greedy
+    # on every workload: default <= look-ahead <= greedy in passes, all valid
     for name in W.WORKLOADS:
         w2 = W.get(name)
-        a = Q.Circuit(w2.n, w2.gates(), w2.n_inputs, w2.n_weights)
-        b = Q.Circuit(w2.n, w2.gates(), w2.n_inputs, w2.n_weights, pass_search=-1)
+        cs = [Q.Circuit(w2.n, w2.gates(), w2.n_inputs, w2.n_weights, pass_search=ps) for ps in (0, 1, -1)]
         for dt in ("c64", "c128"):
-            assert a.plan_info(dt)["n_passes"] <= b.plan_info(dt)["n_passes"], (name, dt)
+            n = [c.plan_info(dt)["n_passes"] for c in cs]
+            assert n[0] <= n[1] <= n[2], (name, dt, n)
+            _check_schedule(cs[0], w2.gates(), dt)
 
 
 # ---------------------------------------------------------------------------
