@@ -174,6 +174,17 @@ typedef struct {
                                    gates; 0 (default): a beam search over whole pass
                                    sequences, taken when it needs fewer passes than
                                    1, else 1 */
+    int32_t product_prefix;     /* the one-qubit gates a qubit meets before any
+                                   two-qubit gate or Pauli channel touches it (the
+                                   product-state prefix of the circuit) need not
+                                   run as tile ops: the first pass can start from
+                                   the product state they make (per-sample
+                                   factors, fp64), and their gradients come from
+                                   each qubit's environment in lambda at the end of
+                                   the backward sweep (tile plans without an
+                                   embedding). 0 (default): so when the other gates
+                                   then plan into fewer passes, or as many with no
+                                   more layout changes; 1: always; -1: never */
 } ql_options;
 
 typedef struct ql_circuit ql_circuit; /* opaque */
@@ -334,13 +345,16 @@ typedef struct {
                               over the forward passes */
     int32_t n_rz_groups;   /* RZ groups (several RZs run as one phase op), all passes */
     int32_t n_ryz_pairs;   /* RZs run together with their bit's RY in one op, all passes */
+    int32_t n_prefix_gates; /* gates of the product-state prefix (the first pass's initial
+                               state; see ql_options.product_prefix) */
 } ql_plan_info;
 
 int ql_plan_info_get(const ql_circuit* c, ql_dtype dtype, ql_plan_info* out);
 
 /* Forward schedule: pass_of_gate[n_gates] receives the pass that applies each
  * gate, order[n_gates] the gate indices in execution order (pass by pass).
- * A controlled rotation or Pauli channel runs as several gates; it is
+ * Gates of the product-state prefix belong to pass 0 and come first, in gate
+ * order. A controlled rotation or Pauli channel runs as several gates; it is
  * reported at the pass and position of the last one (a channel with all
  * probabilities 0 applies nothing: pass -1, listed first). */
 int ql_plan_schedule(const ql_circuit* c, ql_dtype dtype, int32_t* pass_of_gate,

@@ -41,6 +41,7 @@ struct Tables {
     size_t off_pass = 0, off_phase = 0, off_ops = 0, off_gslot = 0, off_slots = 0;
     size_t off_xptr = 0, off_xslot = 0, off_wptr = 0, off_wslot = 0, off_gates = 0, off_diag = 0;
     size_t off_fuse = 0;
+    size_t off_pptr = 0, off_pops = 0;  // product-prefix CSR (per qubit)
     std::vector<DevPass> passes;
     int n_diags = 0, n_fuses = 0;
     int n_ops = 0;
@@ -124,6 +125,8 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
     T.n_diags = (int)pl.diags.size();
     T.off_fuse = put(T.blob, pl.fuses);
     T.n_fuses = (int)pl.fuses.size();
+    T.off_pptr = put(T.blob, pl.pre_ptr);
+    T.off_pops = put(T.blob, pl.pre_ops);
     T.blob.resize(align256(T.blob.size()), 0);
     T.passes = passes;
     T.n_ops = (int)ops.size();
@@ -133,6 +136,7 @@ struct Layout {
     size_t tables = 0, coef = 0, opc = 0, dzc = 0, fzc = 0, zpart = 0, gpart = 0, psi = 0, lam = 0, total = 0;
     size_t enorm = 0, edot = 0;  // embedding: per-circuit |x| or basis index; L_b
     size_t keep = 0;             // kept forward states: n_keep buffers of state_bytes each
+    size_t phi = 0, env = 0;     // product prefix: per-circuit factors; per-tile environment sums
     size_t state_bytes = 0;
     int n_keep = 0;
     int n_wg = 1;
@@ -215,9 +219,22 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
     L.zpart = off;
     if (!mul_ok((size_t)B * (size_t)L.n_wg, (size_t)c.n * 8, sz)) return fail(QL_ENOMEM, "size overflow");
     off = align256(off + sz);
+    if (pl.product) {
+        // per circuit and qubit the prefix factor (phi(0), phi(1)), complex fp64
+        L.phi = off;
+        if (!mul_ok((size_t)B, (size_t)c.n * 32, sz)) return fail(QL_ENOMEM, "size overflow");
+        off = align256(off + sz);
+    }
     if (bwd) {
         L.gpart = off;
         if (!mul_ok((size_t)B * (size_t)L.n_wg, (size_t)std::max(1, (int)c.slots.size()) * 8, sz))
+            return fail(QL_ENOMEM, "size overflow");
+        off = align256(off + sz);
+    }
+    if (bwd && pl.product) {
+        // per sample, environment workgroup and qubit: (re, im) of r_q(0) and r_q(1), fp64
+        L.env = off;
+        if (!mul_ok((size_t)B * (size_t)env_workgroups(c.n, B), (size_t)c.n * 32, sz))
             return fail(QL_ENOMEM, "size overflow");
         off = align256(off + sz);
     }
@@ -230,7 +247,9 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
     const bool multi = !pl.whole_state && pl.passes.size() > 1;
     const bool emb = c.embed != E_NONE, amp_bwd = bwd && c.embed == E_AMPLITUDE;
     const bool keep = multi && mode == QL_MODE_FWD_BWD_KEEP;
-    const bool need_psi = own_psi && (emb || (multi && !keep)), need_lam = (bwd && multi) || amp_bwd;
+    // the product prefix's environment reads lambda at the end of the backward sweep
+    const bool need_psi = own_psi && (emb || (multi && !keep));
+    const bool need_lam = (bwd && multi) || amp_bwd || (bwd && !pl.whole_state && pl.product);
     size_t st = 0;
     if (need_psi || need_lam || keep)
         if (!mul_ok((size_t)B, ((size_t)1 << c.n) * amp, st)) return fail(QL_ENOMEM, "size overflow");
@@ -386,6 +405,26 @@ int upload_tables(Ctx& x) {
     return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("hipEventRecord: ") + hipGetErrorString(e));
 }
 
+// Arguments of the product-prefix kernels for B circuits of this call.
+PrefixArgs prefix_args(const Ctx& x, int64_t B) {
+    PrefixArgs pa{};
+    pa.inputs = x.inputs;
+    pa.weights = x.weights;
+    pa.slots = (const SlotSrc*)(x.W + x.L.tables + x.T.off_slots);
+    pa.pre_ptr = (const int32_t*)(x.W + x.L.tables + x.T.off_pptr);
+    pa.pre_ops = (const DevPrefix*)(x.W + x.L.tables + x.T.off_pops);
+    pa.phi = (double*)(x.W + x.L.phi);
+    pa.lam = x.L.lam ? (const void*)(x.W + x.L.lam) : nullptr;
+    pa.envpart = x.L.env ? (double*)(x.W + x.L.env) : nullptr;
+    pa.gpart = x.L.gpart ? (double*)(x.W + x.L.gpart) : nullptr;
+    pa.B = B;
+    pa.n = x.c.n;
+    pa.F = x.c.n_inputs;
+    pa.n_wg = x.L.n_wg;
+    pa.env_wg = env_workgroups(x.c.n, B);
+    return pa;
+}
+
 // Angle binding for B circuits. With vper > 0 the circuits are the shifted
 // copies of a parameter-shift chunk: circuit i is virtual circuit v = v0 + i,
 // sample v / vper, and v % vper = 2s+1 (2s+2) shifts rotation slot s by
@@ -432,6 +471,12 @@ int bind(Ctx& x, int64_t B, const void* inputs, const void* weights, int64_t v0,
         ba.vper = vper;
         x.tm.start(2);
         e = launch_bind_tile(x.dt, ba, x.stream);
+        if (e == hipSuccess && x.pl.product) {
+            PrefixArgs pa = prefix_args(x, B);
+            pa.v0 = v0;
+            pa.vper = vper;
+            e = launch_bind_prefix(x.dt, pa, x.stream);
+        }
         x.tm.stop();
     }
     return e == hipSuccess ? QL_OK : fail(QL_EHIP, std::string("k_bind: ") + hipGetErrorString(e));
@@ -533,6 +578,7 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         ta.n_wg = x.L.n_wg;
         ta.flags = flags;
         ta.n_gslots = (flags & PF_BWD) ? d.n_gslots : 0;
+        ta.phi = pl.product ? (const double*)(x.W + x.L.phi) : nullptr;
         // dynamic LDS: <Z> scratch and gradient accumulators (the exchange
         // buffer is static)
         const size_t st = tile_static_lds(x.dt, pl.log_r, threads), real = x.dt == 0 ? 4 : 8;
@@ -546,11 +592,12 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         return QL_OK;
     };
     int rc;
-    // the first pass starts from |0...0> in registers unless an embedding
-    // wrote the initial state; the last backward pass stores lambda_0 when the
-    // amplitude-embedding gradient needs it
-    const int init = emb ? 0 : PF_INIT;
-    const int lam0 = amp_bwd ? PF_STORE_LAM : 0;
+    // the first pass starts from |0...0> (or the product state of the prefix
+    // factors) in registers unless an embedding wrote the initial state; the
+    // last backward pass stores lambda_0 when the amplitude-embedding gradient
+    // or the product prefix's environment needs it
+    const int init = emb ? 0 : (pl.product ? PF_PRODUCT : PF_INIT);
+    const int lam0 = (amp_bwd || pl.product) ? PF_STORE_LAM : 0;
     for (int p = 0; p + 1 < m; p++) {
         void* out = keep ? kept(p) : psi_buf;
         void* in = keep && p > 0 ? kept(p - 1) : (p == 0 && !emb ? out : psi_buf);
@@ -640,6 +687,14 @@ int run(const ql_circuit* hc, ql_dtype dtype, int64_t B, int mode, const void* i
     if ((rc = bind(x, B, inputs, weights, 0, 0, bwd))) return rc;
     if ((rc = embed(x, B, inputs, x.L.psi ? (void*)(x.W + x.L.psi) : nullptr, 0, 0))) return rc;
     if ((rc = state_passes(x, B, bwd, grad_out))) return rc;
+    if (bwd && x.pl.product) {  // the prefix rotations' gradient terms, into gpart
+        const PrefixArgs pa = prefix_args(x, B);
+        x.tm.start(3);
+        hipError_t e = launch_env(dt, pa, stream);
+        if (e == hipSuccess) e = launch_env_grad(dt, pa, stream);
+        x.tm.stop();
+        if (e != hipSuccess) return fail(QL_EHIP, std::string("k_env: ") + hipGetErrorString(e));
+    }
     if ((rc = reduce(x, B, bwd, expz, grad_inputs, grad_weights))) return rc;
     if (bwd && grad_inputs && h->c.embed == E_AMPLITUDE) {
         EmbedGradArgs ga{};
@@ -826,6 +881,7 @@ Options to_options(const ql_options* o) {
         r.wg_per_sample = o->wg_per_sample;
         r.rz_groups = o->rz_groups;
         r.pass_search = o->pass_search;
+        r.product_prefix = o->product_prefix;
     }
     return r;
 }
@@ -1049,6 +1105,7 @@ int ql_plan_info_get(const ql_circuit* h, ql_dtype dtype, ql_plan_info* out) {
     r.n_rz_groups = (int)pl.diags.size();
     r.n_ryz_pairs = (int)pl.fuses.size();
     r.n_param_gates = h->c.n_param_slots;
+    r.n_prefix_gates = (int)pl.pre_gates.size();
     *out = r;
     return QL_OK;
 }
@@ -1064,6 +1121,11 @@ int ql_plan_schedule(const ql_circuit* h, ql_dtype dtype, int32_t* pass_of_gate,
     std::vector<int> last(G, -1);
     for (int i = 0; i < G; i++) pass_of_gate[i] = -1;
     int k = 0;
+    for (int gi : pl.pre_gates) {  // the product-state prefix: the first pass's initial state
+        const int u = h->c.gates[gi].user;
+        last[u] = k++;
+        pass_of_gate[u] = 0;
+    }
     for (int p = 0; p < (int)pl.passes.size(); p++)
         for (int gi : pl.passes[p].gates) {
             const int u = h->c.gates[gi].user;
@@ -1086,6 +1148,8 @@ int ql_plan_state_bytes(const ql_circuit* h, ql_dtype dtype, int64_t batch, int 
     double units = 0;
     if (!pl.whole_state && m > 1)
         units = mode == QL_MODE_FWD_BWD ? 6.0 * m - 6.0 : mode == QL_MODE_FWD_BWD_KEEP ? 5.0 * m - 5.0 : 2.0 * m - 2.0;
+    // with a product prefix the last backward pass also stores lambda
+    if (!pl.whole_state && pl.product && (mode == QL_MODE_FWD_BWD || mode == QL_MODE_FWD_BWD_KEEP)) units += 1.0;
     *out = units * S;
     return QL_OK;
 }

@@ -77,6 +77,86 @@ __device__ __forceinline__ double wave_total(double v) {
     return (lane(0) + lane(16)) + (lane(32) + lane(48));
 }
 
+// Complex products of float2 / double2.
+template <typename T2>
+__device__ __forceinline__ T2 cxmul(T2 a, T2 b) {
+    T2 r;
+    r.x = a.x * b.x - a.y * b.y;
+    r.y = a.x * b.y + a.y * b.x;
+    return r;
+}
+// conj(a) * b
+template <typename T2>
+__device__ __forceinline__ T2 cxmulc(T2 a, T2 b) {
+    T2 r;
+    r.x = a.x * b.x + a.y * b.y;
+    r.y = a.x * b.y - a.y * b.x;
+    return r;
+}
+template <typename T2, typename Real>
+__device__ __forceinline__ T2 to_real(double2 v) {
+    return mk<T2>((Real)v.x, (Real)v.y);
+}
+
+// Leave-one-out contractions of a thread's registers with per-bit factors:
+// for every register bit m, S[m][u] = sum over registers i with bit m = u of
+// conj(prod_{m' != m} f_{m'}(bit m' of i)) v[i]. The bits [LO, HI) of v's
+// index are split in halves: contracting the upper half away gives a tensor
+// over the lower half (and the other way round), and each half recurses, so
+// every partial contraction is shared by the bits that need it.
+template <int LO, int HI, typename T2>
+__device__ __forceinline__ void loo_contract(const T2* v, const T2* f0, const T2* f1, T2 (*S)[2]) {
+    if constexpr (HI - LO == 1) {
+        S[LO][0] = v[0];
+        S[LO][1] = v[1];
+    } else {
+        constexpr int MID = (LO + HI) / 2;
+        constexpr int H0 = 1 << (HI - LO - 1);
+        {
+            // contract bits HI-1 .. MID (highest first): a tensor over LO..MID-1
+            T2 w[H0];
+#pragma unroll
+            for (int i = 0; i < H0; ++i) {
+                const T2 x = cxmulc(f0[HI - 1], v[i]), y = cxmulc(f1[HI - 1], v[i + H0]);
+                w[i].x = x.x + y.x;
+                w[i].y = x.y + y.y;
+            }
+#pragma unroll
+            for (int m = HI - 2; m >= MID; --m) {
+#pragma unroll
+                for (int i = 0; i < H0; ++i)
+                    if (i < (1 << (m - LO))) {
+                        const T2 x = cxmulc(f0[m], w[i]), y = cxmulc(f1[m], w[i + (1 << (m - LO))]);
+                        w[i].x = x.x + y.x;
+                        w[i].y = x.y + y.y;
+                    }
+            }
+            loo_contract<LO, MID, T2>(w, f0, f1, S);
+        }
+        {
+            // contract bits LO .. MID-1 (lowest first): a tensor over MID..HI-1
+            T2 w[H0];
+#pragma unroll
+            for (int i = 0; i < H0; ++i) {
+                const T2 x = cxmulc(f0[LO], v[2 * i]), y = cxmulc(f1[LO], v[2 * i + 1]);
+                w[i].x = x.x + y.x;
+                w[i].y = x.y + y.y;
+            }
+#pragma unroll
+            for (int m = LO + 1; m < MID; ++m) {
+#pragma unroll
+                for (int i = 0; i < H0; ++i)
+                    if (i < (1 << (HI - m - 1))) {
+                        const T2 x = cxmulc(f0[m], w[2 * i]), y = cxmulc(f1[m], w[2 * i + 1]);
+                        w[i].x = x.x + y.x;
+                        w[i].y = x.y + y.y;
+                    }
+            }
+            loo_contract<MID, HI, T2>(w, f0, f1, S);
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // angle sources (shared by the binding kernels)
 

@@ -24,6 +24,10 @@
 //   k_embed_* -- basis / amplitude embedding of the initial state, and the
 //               amplitude embedding's VJP from lambda_0
 //   k_shift_dot, k_shift_grad -- parameter-shift VJP from batched shifted circuits
+//   k_bind_prefix, k_env, k_env_grad -- the product-state prefix: per-sample
+//               factors of the first pass's initial state, the environment sums
+//               of lambda at the end of the backward sweep, and the prefix
+//               gates' gradient terms
 //   k_state_phase, k_phase_fix -- the global phase of the tile path's final states
 //   k_block_sums, k_block_scan, k_shots, k_shot_z -- shot sampling by inverse CDF
 #include "kcommon.hpp"
@@ -775,6 +779,259 @@ __global__ void __launch_bounds__(256) k_shift_grad(const ShiftGradArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// product-state prefix
+//
+// The one-qubit gates a qubit meets before anything entangles it (its prefix)
+// act on |0> independently per qubit, so the circuit's first pass starts from
+// the product of the per-qubit states phi_q = G_m ... G_1 |0> (k_bind_prefix,
+// fp64). Their gradients need no pass either: with lambda_P the adjoint state
+// at the end of the prefix and rest the product of the other qubits' factors,
+// the term of gate j of qubit q is Im <lambda_j| P_j |psi_j> = Im <r_q|
+// A_j P_j B_j |0>, where B_j = G_j ... G_1, A_j = G_m ... G_{j+1} and r_q(v) =
+// sum over amplitudes i with bit q = v of lambda_P(i) conj(rest(i)). The last
+// backward pass stores lambda_P; k_env forms every workgroup's share of all
+// r_q in one read of it, and k_env_grad sums the shares and evaluates the
+// terms.
+
+__device__ __forceinline__ double2 zmul(double2 a, double2 b) {
+    return make_double2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+
+// v <- G v for prefix gate kind k with angle t (G = exp(-i t P / 2) for RX,
+// RY, RZ; the Hadamard for H); inv applies G^dagger.
+__device__ __forceinline__ void apply_gate1(int kind, double t, bool inv, double2& v0, double2& v1) {
+    if (kind == K_H) {
+        const double r = 0.70710678118654752440;
+        const double2 a = v0, b = v1;
+        v0 = make_double2(r * (a.x + b.x), r * (a.y + b.y));
+        v1 = make_double2(r * (a.x - b.x), r * (a.y - b.y));
+        return;
+    }
+    if (inv) t = -t;
+    double s, c;
+    sincos(0.5 * t, &s, &c);
+    const double2 a = v0, b = v1;
+    if (kind == K_RX) {  // [[c, -i s], [-i s, c]]
+        v0 = make_double2(c * a.x + s * b.y, c * a.y - s * b.x);
+        v1 = make_double2(s * a.y + c * b.x, -s * a.x + c * b.y);
+    } else if (kind == K_RY) {  // [[c, -s], [s, c]]
+        v0 = make_double2(c * a.x - s * b.x, c * a.y - s * b.y);
+        v1 = make_double2(s * a.x + c * b.x, s * a.y + c * b.y);
+    } else {  // RZ: diag(exp(-i t/2), exp(i t/2))
+        v0 = zmul(a, make_double2(c, -s));
+        v1 = zmul(b, make_double2(c, s));
+    }
+}
+
+// One thread per (circuit, qubit): the qubit's prefix factor.
+template <typename Real>
+__global__ void __launch_bounds__(256) k_bind_prefix(const PrefixArgs a) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= a.B * a.n) return;
+    const int64_t b = t / a.n;
+    const int q = (int)(t - b * a.n);
+    double2 v0 = make_double2(1.0, 0.0), v1 = make_double2(0.0, 0.0);
+    for (int i = a.pre_ptr[q]; i < a.pre_ptr[q + 1]; ++i) {
+        const DevPrefix g = a.pre_ops[i];
+        double th = 0.0;
+        if (g.slot >= 0) {
+            int64_t bs;
+            th = angle_of<Real>(a.inputs, a.weights, a.F, a.slots[g.slot], b, a.v0, a.vper, bs) +
+                 shift_of(b, a.v0, a.vper, g.slot);
+        }
+        apply_gate1(g.kind, th, false, v0, v1);
+    }
+    double2* out = (double2*)a.phi + 2 * t;
+    out[0] = v0;
+    out[1] = v1;
+}
+
+// Environment sums of the prefix: 256 threads (4 wavefronts) per workgroup;
+// a wavefront takes blocks of 64 * 2^LR consecutive amplitudes of lambda_P,
+// so register bit m is qubit m, lane bit t qubit LR + t, and the block index
+// holds the other (fixed) qubits. Per thread the register bits are contracted
+// (Real) with the leave-one-out scheme, and the shares of the register and
+// lane qubits are summed over the wavefront's blocks in registers (Real);
+// only the fixed qubits, whose factors change from block to block, need a
+// wavefront sum per block (lane i then keeps fixed qubit i's share, fp64).
+// The wavefront sums (fp64 across rows) go to LDS at the end and the four
+// wavefronts are combined in a fixed order.
+template <typename Real, int LR>
+__global__ void __launch_bounds__(256) k_env(const PrefixArgs a) {
+    using T2 = typename Cx<Real>::T;
+    constexpr int R = 1 << LR;
+    __shared__ double acc[4][32][4];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int n = a.n;
+    const int64_t b = blockIdx.x / a.env_wg;
+    const int w = (int)(blockIdx.x - b * a.env_wg);
+    for (int i = tid; i < 4 * 32 * 4; i += 256) (&acc[0][0][0])[i] = 0.0;
+    __syncthreads();
+    const double2* fac = (const double2*)a.phi + b * 2 * n;
+    const T2* lam = (const T2*)a.lam + (b << n);
+    const int nfix = n - LR - 6;
+    const int64_t nblk = (int64_t)1 << nfix;
+    T2 f0[LR], f1[LR];
+#pragma unroll
+    for (int m = 0; m < LR; ++m) {
+        f0[m] = to_real<T2, Real>(fac[2 * m]);
+        f1[m] = to_real<T2, Real>(fac[2 * m + 1]);
+    }
+    // the lane's factors: all six (cl) and all but lane bit t (lf[t])
+    double2 cl = make_double2(1.0, 0.0);
+    T2 lf[6];
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+        double2 p = make_double2(1.0, 0.0);
+#pragma unroll
+        for (int t2 = 0; t2 < 6; ++t2)
+            if (t2 != t) p = cxmul(p, fac[2 * (LR + t2) + ((lane >> t2) & 1)]);
+        lf[t] = to_real<T2, Real>(p);
+        cl = t == 0 ? fac[2 * LR + (lane & 1)] : cxmul(cl, fac[2 * (LR + t) + ((lane >> t) & 1)]);
+    }
+    const T2 clr = to_real<T2, Real>(cl);
+    Real sr[LR][4], sl[6][4];  // this lane's shares: register qubits; lane qubits
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+#pragma unroll
+        for (int m = 0; m < LR; ++m) sr[m][c] = 0;
+#pragma unroll
+        for (int t = 0; t < 6; ++t) sl[t][c] = 0;
+    }
+    double fx[4] = {0.0, 0.0, 0.0, 0.0};  // lane i < nfix: fixed qubit LR + 6 + i
+    for (int64_t blk = (int64_t)w * 4 + wave; blk < nblk; blk += (int64_t)a.env_wg * 4) {
+        T2 v[R];
+        const T2* src = lam + (blk << (LR + 6)) + ((int64_t)lane << LR);
+#pragma unroll
+        for (int i = 0; i < R; ++i) v[i] = src[i];
+        T2 S[LR][2];
+        loo_contract<0, LR, T2>(v, f0, f1, S);
+        const T2 T = [&] {
+            const T2 x = cxmulc(f0[0], S[0][0]), y = cxmulc(f1[0], S[0][1]);
+            return mk<T2>(x.x + y.x, x.y + y.y);
+        }();
+        double2 cfix = make_double2(1.0, 0.0);
+        for (int i = 0; i < nfix; ++i) cfix = cxmul(cfix, fac[2 * (LR + 6 + i) + ((blk >> i) & 1)]);
+        const T2 cf = to_real<T2, Real>(cfix);
+        // register qubits: conj(every other factor) S[m][u]
+        const T2 call = cxmul(clr, cf);
+#pragma unroll
+        for (int m = 0; m < LR; ++m) {
+            const T2 s0 = cxmulc(call, S[m][0]), s1 = cxmulc(call, S[m][1]);
+            sr[m][0] += s0.x;
+            sr[m][1] += s0.y;
+            sr[m][2] += s1.x;
+            sr[m][3] += s1.y;
+        }
+        // lane qubits: conj(every non-register factor but t's) T, in the bin
+        // of the lane's bit t
+#pragma unroll
+        for (int t = 0; t < 6; ++t) {
+            const T2 x = cxmulc(cxmul(lf[t], cf), T);
+            const int u = 2 * ((lane >> t) & 1);
+            sl[t][u] += x.x;
+            sl[t][u + 1] += x.y;
+        }
+        // fixed qubits (bits uniform over the block): conj(product of the
+        // other fixed factors) U, U = the wavefront's sum of conj(cl) T
+        const T2 uu = cxmulc(clr, T);
+        const double ux = wave_total(uu.x), uy = wave_total(uu.y);
+        if (lane < nfix) {
+            double2 g = make_double2(1.0, 0.0);
+            for (int i = 0; i < nfix; ++i)
+                if (i != lane) g = cxmul(g, fac[2 * (LR + 6 + i) + ((blk >> i) & 1)]);
+            const double2 r = cxmulc(g, make_double2(ux, uy));
+            const int u = 2 * (int)((blk >> lane) & 1);
+            fx[u] += r.x;
+            fx[u + 1] += r.y;
+        }
+    }
+    // the wavefront's sums into LDS (lane 0; lane i for fixed qubit i)
+#pragma unroll
+    for (int m = 0; m < LR; ++m)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const double t = wave_total(sr[m][c]);
+            if (lane == 0) acc[wave][m][c] = t;
+        }
+#pragma unroll
+    for (int t = 0; t < 6; ++t)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const double x = wave_total(sl[t][c]);
+            if (lane == 0) acc[wave][LR + t][c] = x;
+        }
+    if (lane < nfix)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[wave][LR + 6 + lane][c] = fx[c];
+    __syncthreads();
+    double* dst = a.envpart + ((size_t)b * a.env_wg + w) * n * 4;
+    for (int i = tid; i < n * 4; i += 256) {
+        const double* p = &acc[0][0][0] + i;
+        dst[i] = ((p[0] + p[32 * 4]) + p[2 * 32 * 4]) + p[3 * 32 * 4];
+    }
+}
+
+// One wavefront per (sample, qubit): r_q from the workgroups' environment
+// sums in a fixed order, then the gradient term of every prefix rotation of q.
+template <typename Real>
+__global__ void __launch_bounds__(256) k_env_grad(const PrefixArgs a) {
+    const int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    if (e >= a.B * a.n) return;
+    const int64_t b = e / a.n;
+    const int q = (int)(e - b * a.n);
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int64_t t = lane; t < a.env_wg; t += 64) {
+        const double* src = a.envpart + ((b * a.env_wg + t) * a.n + q) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] += src[c];
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] = wave_sum(acc[c]);
+    const int beg = a.pre_ptr[q], end = a.pre_ptr[q + 1];
+    // zero columns w >= 1 of every prefix rotation's gradient row
+    for (int i = beg; i < end; ++i) {
+        const int s = a.pre_ops[i].slot;
+        if (s < 0) continue;
+        double* row = a.gpart + ((size_t)s * a.B + b) * a.n_wg;
+        for (int w = 1 + lane; w < a.n_wg; w += 64) row[w] = 0.0;
+    }
+    if (lane != 0) return;
+    auto angle = [&](const DevPrefix& gt) {
+        int64_t bs;
+        return gt.slot >= 0 ? angle_of<Real>(a.inputs, a.weights, a.F, a.slots[gt.slot], b, 0, 0, bs) : 0.0;
+    };
+    // f: the factor after all prefix gates; g: r_q
+    double2 f0 = make_double2(1.0, 0.0), f1 = make_double2(0.0, 0.0);
+    for (int i = beg; i < end; ++i) apply_gate1(a.pre_ops[i].kind, angle(a.pre_ops[i]), false, f0, f1);
+    double2 g0 = make_double2(acc[0], acc[1]), g1 = make_double2(acc[2], acc[3]);
+    // walk back: at gate j, f = B_j |0> and g = A_j^dagger r_q
+    for (int i = end - 1; i >= beg; --i) {
+        const DevPrefix gt = a.pre_ops[i];
+        const double t = angle(gt);
+        if (gt.slot >= 0) {
+            // P f for P = X, Y, Z, then Im <g| P f>
+            double2 p0, p1;
+            if (gt.kind == K_RX) {
+                p0 = f1;
+                p1 = f0;
+            } else if (gt.kind == K_RY) {  // Y = [[0, -i], [i, 0]]
+                p0 = make_double2(f1.y, -f1.x);
+                p1 = make_double2(-f0.y, f0.x);
+            } else {
+                p0 = f0;
+                p1 = make_double2(-f1.x, -f1.y);
+            }
+            const double im = (g0.x * p0.y - g0.y * p0.x) + (g1.x * p1.y - g1.y * p1.x);
+            a.gpart[((size_t)gt.slot * a.B + b) * a.n_wg] = im;
+        }
+        apply_gate1(gt.kind, t, true, f0, f1);
+        apply_gate1(gt.kind, t, true, g0, g1);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // exact final states of the tile path
 //
 // The tile kernel applies each rotation with its angle reduced to [-pi, pi]
@@ -1192,6 +1449,50 @@ hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s) {
     const unsigned grid = (unsigned)((waves + 3) / 4);
     if (dtype == 0) hipLaunchKernelGGL(k_shift_grad<float>, dim3(grid), dim3(256), 0, s, a);
     else hipLaunchKernelGGL(k_shift_grad<double>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_bind_prefix(int dtype, const PrefixArgs& a, hipStream_t s) {
+    const int64_t items = a.B * a.n;
+    if (items == 0) return hipSuccess;
+    const unsigned grid = (unsigned)((items + 255) / 256);
+    if (dtype == 0) hipLaunchKernelGGL(k_bind_prefix<float>, dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_bind_prefix<double>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+int env_workgroups(int n, int64_t B) {
+    const int lr = n >= 10 ? 4 : n - 6;
+    const int64_t nblk = (int64_t)1 << (n - lr - 6);
+    const int64_t want = std::max<int64_t>(1, 2048 / std::max<int64_t>(B, 1));
+    return (int)std::max<int64_t>(1, std::min<int64_t>(want, (nblk + 3) / 4));
+}
+
+hipError_t launch_env(int dtype, const PrefixArgs& a, hipStream_t s) {
+    if (a.n < 8 || a.n > 32) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(a.B * a.env_wg));
+    const int lr = a.n >= 10 ? 4 : a.n - 6;
+#define QL_ENV(REAL)                                                                        \
+    switch (lr) {                                                                           \
+        case 2: hipLaunchKernelGGL((k_env<REAL, 2>), grid, dim3(256), 0, s, a); break;      \
+        case 3: hipLaunchKernelGGL((k_env<REAL, 3>), grid, dim3(256), 0, s, a); break;      \
+        default: hipLaunchKernelGGL((k_env<REAL, 4>), grid, dim3(256), 0, s, a); break;     \
+    }
+    if (dtype == 0) {
+        QL_ENV(float)
+    } else {
+        QL_ENV(double)
+    }
+#undef QL_ENV
+    return hipGetLastError();
+}
+
+hipError_t launch_env_grad(int dtype, const PrefixArgs& a, hipStream_t s) {
+    const int64_t waves = a.B * a.n;
+    if (waves == 0) return hipSuccess;
+    const unsigned grid = (unsigned)((waves + 3) / 4);
+    if (dtype == 0) hipLaunchKernelGGL(k_env_grad<float>, dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_env_grad<double>, dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

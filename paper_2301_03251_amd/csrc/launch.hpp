@@ -165,7 +165,36 @@ struct TileArgs {
     int64_t tiles;             // tiles per sample = 2^(n-k)
     int32_t n, n_ops, n_wg, flags;
     int32_t n_gslots;          // gradient accumulators of this pass
+    const double* phi;         // [B][n][2] complex (double2): product-prefix factors (PF_PRODUCT)
 };
+
+// Product-state prefix. Binding: phi[c][q] = the state the prefix gates of
+// qubit q make from |0> (fp64), for every circuit c of the call (parameter-
+// shift chunks as in BindArgs). Environment: from lambda at the end of the
+// backward sweep, each workgroup's share of r_q(v) = sum over amplitudes i
+// with bit q = v of lambda(i) conj(prod_{q' != q} phi_q'(bit q' of i)), as
+// (re, im of v = 0, re, im of v = 1) per qubit. Gradients: r_q summed over the
+// workgroups and, for prefix gate j of qubit q, d = Im <g_j| P_j |f_j> with
+// f_j the factor after gate j and g_j r_q un-applied through the gates after
+// j; written to gpart[slot][b][0] (zeros in the other workgroup columns).
+struct PrefixArgs {
+    const void* inputs;        // [B][F] Real
+    const void* weights;       // [P] Real
+    const SlotSrc* slots;
+    const int32_t* pre_ptr;    // [n + 1]
+    const DevPrefix* pre_ops;
+    double* phi;               // [count][n][2] complex
+    const void* lam;           // [B][2^n] complex: lambda at the end of the backward sweep
+    double* envpart;           // [B][env_wg][n][4]
+    double* gpart;             // [n_slots][B][n_wg]
+    int64_t B;                 // circuits
+    int64_t v0;
+    int32_t vper;
+    int32_t n, F, n_wg;
+    int32_t env_wg;            // workgroups per sample of the environment kernel
+};
+// Workgroups per sample of the environment kernel for n qubits and batch B.
+int env_workgroups(int n, int64_t B);
 // LDS words per (gradient accumulator, wavefront) of the tile kernel
 constexpr int TILE_GRAD_WORDS = 2;
 
@@ -212,6 +241,9 @@ hipError_t launch_state_phase(int dtype, const BindTileArgs& a, double* phase, v
 hipError_t launch_embed(int dtype, const EmbedArgs& a, hipStream_t s);
 hipError_t launch_embed_grad(int dtype, const EmbedGradArgs& a, hipStream_t s);
 hipError_t launch_shift_grad(int dtype, const ShiftGradArgs& a, hipStream_t s);
+hipError_t launch_bind_prefix(int dtype, const PrefixArgs& a, hipStream_t s);
+hipError_t launch_env(int dtype, const PrefixArgs& a, hipStream_t s);
+hipError_t launch_env_grad(int dtype, const PrefixArgs& a, hipStream_t s);
 
 // Raise the dynamic-LDS limit of every kernel on the current device.
 hipError_t configure_kernels(size_t max_lds);

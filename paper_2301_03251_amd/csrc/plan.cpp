@@ -643,6 +643,7 @@ std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, i
     if (o.max_gates_per_pass < 0) return "option: max_gates_per_pass < 0";
     if (o.wg_per_sample < 0) return "option: wg_per_sample < 0";
     if (o.rz_groups != 0 && o.rz_groups != -1) return "option: rz_groups must be 0 or -1";
+    if (o.product_prefix < -1 || o.product_prefix > 1) return "option: product_prefix must be -1, 0 or 1";
     if (o.pass_search < -1 || o.pass_search > 1) return "option: pass_search must be -1, 0 or 1";
     for (int dt = 0; dt < 2; dt++) {
         std::string e = build_plan(out, dt, out.plan[dt]);
@@ -692,6 +693,26 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
     const int G = (int)c.gates.size();
     std::vector<char> done(G, 0);
     int remaining = G;
+    // Product prefix: a one-qubit gate on a qubit that no two-qubit gate or
+    // Pauli channel has touched yet commutes with every earlier gate on other
+    // qubits, so all such gates can run first, on |0...0>, where they make a
+    // product state. They leave the passes (marked done for the planner).
+    std::vector<int> pre_gates;
+    std::vector<std::vector<DevPrefix>> per(c.n);
+    if (c.embed == E_NONE && o.product_prefix >= 0) {
+        uint64_t touched = 0;
+        for (int i = 0; i < G; i++) {
+            const Gate& g = c.gates[i];
+            if (n_qubits_of(g) == 2) {
+                touched |= (1ull << g.q0) | (1ull << g.q1);
+            } else if (g.kind == K_PAULI) {
+                touched |= 1ull << g.q0;
+            } else if (!(touched >> g.q0 & 1)) {
+                per[g.q0].push_back({g.kind, g.slot});
+                pre_gates.push_back(i);
+            }
+        }
+    }
     const uint64_t low_tile = (low >= 64) ? ~0ull : ((1ull << low) - 1);
     // Candidate tiles of the next pass: first-need greedy growth, and
     // contiguous windows of the high qubits.
@@ -758,13 +779,17 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         }
         return cost;
     };
-    // The planning time grows with horizon x gates x passes: full look-aheads
-    // for circuits of the workloads' size, shorter ones for long circuits.
-    const int horizon = G <= 2048 ? 32 : G <= 4096 ? 8 : 4;
+    // The look-ahead's rollouts cost about horizon x candidates^2 x gates per
+    // pass, the beam search width x candidates x gates per depth; both are
+    // sized from the greedy plan's pass count so that planning stays within
+    // a fraction of a second (full look-aheads and a beam of 64 for the
+    // workloads' circuits, shorter and narrower ones for plans of many passes).
+    int horizon = 32, width = 64;
     // Beam search over whole pass sequences: each depth extends every kept
     // partial plan by every candidate tile, keeps the `width` distinct ones
-    // that leave the fewest gates, and stops at the first depth where a plan
-    // is complete, taking the complete plan of least modeled cost.
+    // that leave the fewest gates (ties: least modeled cost), and stops at the
+    // first depth where a plan is complete, returning up to 8 complete plans,
+    // cheapest first.
     auto beam_search = [&](int width) {
         struct St {
             std::vector<char> dn;
@@ -783,11 +808,16 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
                     ns.seq.push_back(std::move(cd));
                     next.push_back(std::move(ns));
                 }
-            if (next.empty()) return std::vector<Cand>();
+            if (next.empty()) return std::vector<std::vector<Cand>>();
             std::stable_sort(next.begin(), next.end(), [](const St& a, const St& b) {
                 return a.rem != b.rem ? a.rem < b.rem : a.cost < b.cost;
             });
-            if (next[0].rem == 0) return std::move(next[0].seq);
+            if (next[0].rem == 0) {  // the complete plans of this depth, cheapest first
+                std::vector<std::vector<Cand>> done_plans;
+                for (St& s : next)
+                    if (s.rem == 0 && done_plans.size() < 8) done_plans.push_back(std::move(s.seq));
+                return done_plans;
+            }
             std::vector<St> kept;
             std::set<std::vector<char>> seen;
             for (St& s : next) {
@@ -831,30 +861,89 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         }
         return seq;
     };
-    // By default the beam search's plan is taken when it needs fewer passes
-    // than the look-ahead's (30q: 9 against 11, 24q: 14 against 15), else
-    // the look-ahead's.
-    std::vector<Cand> seq;
-    if (remaining > 0) {
-        seq = one_at_a_time(o.pass_search != -1);
-        if (seq.empty()) return "planner made no progress";
-        if (o.pass_search == 0) {
-            std::vector<Cand> bs = beam_search(G <= 2048 ? 64 : G <= 4096 ? 16 : 4);
-            if (!bs.empty() && bs.size() < seq.size()) seq = std::move(bs);
+    // Lay out a pass sequence: each pass's register phases, exchanges and ops.
+    auto lay_out = [&](std::vector<Cand> seq, Plan& to) {
+        for (Cand& cd : seq) {
+            uint64_t tile = cd.tile;
+            // fill the tile up to k qubits with the lowest unused qubits
+            for (int q = 0; q < c.n && __builtin_popcountll(tile) < k; q++) tile |= 1ull << q;
+            PassPlan pp;
+            for (int q = 0; q < c.n; q++) if (tile >> q & 1) pp.qubits.push_back(q);
+            pp.gates = std::move(cd.gates);
+            schedule_pass(c.gates, pp, k, log_r, low, dtype == 0 ? 8u : 16u, to.phases,
+                          o.rz_groups == 0 ? &to.diags : nullptr, o.rz_groups == 0 ? &to.fuses : nullptr);
+            to.passes.push_back(std::move(pp));
         }
-    } else {
-        seq.push_back({{}, low_tile});  // no gates: one empty pass
-    }
-    for (Cand& cd : seq) {
-        uint64_t tile = cd.tile;
-        // fill the tile up to k qubits with the lowest unused qubits
-        for (int q = 0; q < c.n && __builtin_popcountll(tile) < k; q++) tile |= 1ull << q;
-        PassPlan pp;
-        for (int q = 0; q < c.n; q++) if (tile >> q & 1) pp.qubits.push_back(q);
-        pp.gates = std::move(cd.gates);
-        schedule_pass(c.gates, pp, k, log_r, low, dtype == 0 ? 8u : 16u, pl.phases,
-                      o.rz_groups == 0 ? &pl.diags : nullptr, o.rz_groups == 0 ? &pl.fuses : nullptr);
-        pl.passes.push_back(std::move(pp));
+    };
+    // By default the plans of fewest passes among the look-ahead's and the
+    // beam search's complete plans are laid out, and the one with the fewest
+    // layout changes is taken (an LDS exchange weighed as three lane swaps):
+    // 30q: 9 passes against the look-ahead's 11, 24q: 14 against 15. Plans
+    // the remaining gates (those not marked done) into `to`; returns its
+    // layout score, or -1 when the planner makes no progress.
+    auto choose = [&](Plan& to) -> int {
+        std::vector<std::vector<Cand>> plans;
+        if (remaining > 0) {
+            plans.push_back(one_at_a_time(false));
+            if (plans[0].empty()) return -1;
+            const double nc = (double)candidates(done).size();
+            const double unit = (double)plans[0].size() * nc * std::max(G, 1);
+            horizon = (int)std::max(2.0, std::min(32.0, 2e8 / (unit * nc)));
+            width = (int)std::max(4.0, std::min(64.0, 1e8 / unit));
+            if (o.pass_search != -1) plans[0] = one_at_a_time(true);
+            if (plans[0].empty()) return -1;
+            if (o.pass_search == 0) {
+                std::vector<std::vector<Cand>> bs = beam_search(width);
+                if (!bs.empty() && bs[0].size() < plans[0].size()) plans.clear();
+                for (auto& p : bs)
+                    if (p.size() == (plans.empty() ? bs[0].size() : plans[0].size())) plans.push_back(std::move(p));
+            }
+        } else {
+            plans.push_back({{{}, low_tile}});  // no gates: one empty pass
+        }
+        int best = -1;
+        for (auto& p : plans) {
+            Plan t;
+            lay_out(std::move(p), t);
+            int score = 0;
+            for (const PassPlan& pp : t.passes) score += 3 * pp.n_transposes + pp.n_lane_swaps;
+            if (best < 0 || score < best) {
+                best = score;
+                to.passes = std::move(t.passes);
+                to.phases = std::move(t.phases);
+                to.diags = std::move(t.diags);
+                to.fuses = std::move(t.fuses);
+            }
+        }
+        return best;
+    };
+    // The product prefix takes its gates out of the passes. By default it is
+    // kept when the rest of the circuit then needs fewer passes, or as many
+    // passes and no more layout changes (30q: 9 passes either way, 24
+    // exchanges and 72 lane swaps against 26 and 76; 16q: 5 passes against
+    // 6); otherwise (24q: 41 exchanges against 35) every gate runs as a tile
+    // op. product_prefix = 1 keeps it always, -1 never.
+    const int score_ops = choose(pl);
+    if (score_ops < 0) return "planner made no progress";
+    if (!pre_gates.empty()) {
+        for (int i : pre_gates) done[i] = 1;
+        remaining -= (int)pre_gates.size();
+        Plan t;
+        const int score_pre = choose(t);
+        if (score_pre >= 0 && (o.product_prefix == 1 || t.passes.size() < pl.passes.size() ||
+                               (t.passes.size() == pl.passes.size() && score_pre <= score_ops))) {
+            pl.passes = std::move(t.passes);
+            pl.phases = std::move(t.phases);
+            pl.diags = std::move(t.diags);
+            pl.fuses = std::move(t.fuses);
+            pl.product = true;
+            pl.pre_gates = pre_gates;
+            pl.pre_ptr.assign(1, 0);
+            for (int q = 0; q < c.n; q++) {
+                pl.pre_ops.insert(pl.pre_ops.end(), per[q].begin(), per[q].end());
+                pl.pre_ptr.push_back((int32_t)pl.pre_ops.size());
+            }
+        }
     }
     if (pl.phases.size() > 65535) return "plan too large (phases)";
     return "";

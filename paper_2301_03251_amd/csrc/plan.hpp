@@ -166,6 +166,13 @@ enum PassFlags : int32_t {
     PF_BWD = 32,        // run the backward ops (needs lambda)
     PF_STORE_PSI = 64,
     PF_STORE_LAM = 128,
+    PF_PRODUCT = 256,   // start from the product state of the per-sample prefix factors
+};
+
+// A gate of a qubit's prefix (its one-qubit gates before any two-qubit gate or
+// Pauli channel touches it): kind K_H/K_RX/K_RY/K_RZ and rotation slot (-1 for H).
+struct DevPrefix {
+    int32_t kind, slot;
 };
 
 struct DevPass {
@@ -190,6 +197,9 @@ struct Options {
     int force_tiled = 0, wg_per_sample = 0;
     int rz_groups = 0;  // 0: RZs on register bits are grouped into H_DZ ops or joined to their
                         // bit's RY (H_RYZ); -1: every RZ runs on its own
+    int product_prefix = 0;  // each qubit's leading one-qubit gates form the initial product state
+                             // (tile plans without an embedding): 0 when the rest plans no worse,
+                             // 1 always, -1 never (they run as ops)
     int pass_search = 0;  // 0: a beam search over pass sequences when it needs fewer passes than
                           // the look-ahead, else the look-ahead; 1: the look-ahead (each
                           // pass's tile priced by its pass plus a greedy completion); -1: the
@@ -217,6 +227,14 @@ struct Plan {
     std::vector<DevDiag> diags;  // RZ groups (H_DZ ops), all passes
     std::vector<DevFuse> fuses;  // RZs of RY-RZ pair ops (H_RYZ), all passes
     int n_slots = 0;           // rotation slots
+    // Product prefix (tile plans): the gates of pre_ops[pre_ptr[q] .. pre_ptr[q+1])
+    // act on qubit q of |0...0> before anything else touches it, so the first
+    // pass starts from the product of the per-qubit states they make, and the
+    // passes hold only the other gates. Empty when product is false.
+    bool product = false;
+    std::vector<int32_t> pre_ptr;   // [n + 1]
+    std::vector<DevPrefix> pre_ops;
+    std::vector<int> pre_gates;     // the prefix gates, in gate order
 };
 
 // Intake extras: the initial-state embedding and the Pauli-channel

@@ -272,6 +272,39 @@ __device__ __forceinline__ void thread_layout(uint32_t tid, const DevPhase& F, u
     }
 }
 
+// ---- product-state prefix (see k_bind_prefix)
+
+// The product state on one tile in layout F: register i of the thread gets
+// C * prod_m phi_{q_m}(bit m of i), with C (fp64) the product of the factors
+// of the thread's tile bits tb and of the tile's fixed amplitude-index bits gb.
+// fac[2q + v] = phi_q(v) of this sample.
+template <int LOG_R, int LOG_T, typename T2, typename Real>
+__device__ __forceinline__ void product_tile(T2* dst, const double2* __restrict__ fac, const DevPass& P,
+                                             const DevPhase& F, uint32_t tb, uint32_t gb) {
+    double2 c = make_double2(1.0, 0.0);
+#pragma unroll
+    for (int t = 0; t < LOG_T; ++t)
+        if (t < P.log_t) {
+            const uint32_t j = F.thr_bit[t];
+            c = cxmul(c, fac[2 * P.tile_qubit[j] + ((tb >> j) & 1u)]);
+        }
+    for (int i = 0; i < P.n_fixed; ++i) {
+        const int q = P.fixed_qubit[i];
+        c = cxmul(c, fac[2 * q + ((gb >> q) & 1u)]);
+    }
+    dst[0] = to_real<T2, Real>(c);
+#pragma unroll
+    for (int m = 0; m < LOG_R; ++m) {
+        const int q = P.tile_qubit[F.reg_bit[m]];
+        const T2 f0 = to_real<T2, Real>(fac[2 * q]), f1 = to_real<T2, Real>(fac[2 * q + 1]);
+#pragma unroll
+        for (int i = 0; i < (1 << m); ++i) {
+            dst[i | (1 << m)] = cxmul(dst[i], f1);
+            dst[i] = cxmul(dst[i], f0);
+        }
+    }
+}
+
 // Exchange the tile through LDS from layout `from` to layout `to`. The slot map
 // is linear over GF(2) and thread and register bits are disjoint, so the byte
 // offset of (thread, register i) is the thread's offset XOR the register's, and
@@ -729,6 +762,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
     T2* psi_o = (T2*)a.psi_out + b * dim;
     T2* lam_s = (T2*)a.lam + b * dim;
     const XOp<Real>* xops = xops_all + b * (a.n_ops + 1);
+    // this sample's product-prefix factors, fac[2q + v] = phi_q(v)
+    const double2* fac = (const double2*)a.phi + (a.phi ? b * 2 * n : 0);
     const T2* dz = dz_all + b * a.n_diags * DZ_REGS;
     const T2* fz = fz_all + b * a.n_fuses;
     const Real* gout = gout_all + b * n;
@@ -795,7 +830,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
         }
     }
 
-    const bool load = !(flags & PF_INIT);
+    const bool load = !(flags & (PF_INIT | PF_PRODUCT));
     const bool load_lam = BWD && (flags & PF_LOAD_LAM);
     auto load_tile = [&](T2* dst, const T2* state, uint32_t gb) {
         const DevPhase& F = phases[ph0];
@@ -826,7 +861,12 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
         cx.tb = tb0;
         cx.ts = ts0;
 
-        if (!load) {
+        if (!load && (flags & PF_PRODUCT)) {
+            const double2* ft = fac;  // opaque: the factor loads stay in the loop
+            asm volatile("" : "+s"(ft));
+            product_tile<LOG_R, LOG_T, T2, Real>(ps, ft, P, phases[ph0], tb0, cx.gb);
+            if constexpr (PAIR) product_tile<LOG_R, LOG_T, T2, Real>(lm, ft, P, phases[ph0], tb0, cx.gb2);
+        } else if (!load) {
 #pragma unroll
             for (int i = 0; i < R; ++i) ps[i] = mk<T2>((Real)0, (Real)0);
             if (cx.gb == 0 && cx.tb == 0) ps[0] = mk<T2>((Real)1, (Real)0);

@@ -31,11 +31,13 @@ int main(int argc, char** argv) {
         ext.embed = hdr[4];
         ext.embed_first = hdr[5];
         ext.pauli_p = nch ? pp.data() : nullptr;
+        // the beam search (the default) on the plain options; the plans of many
+        // passes take the look-ahead alone, which keeps the sanitized run short
         const Options variants[] = {
             Options{},
-            [] { Options o; o.pass_search = -1; return o; }(),
-            [] { Options o; o.rz_groups = -1; o.max_gates_per_pass = 7; return o; }(),
-            [] { Options o; o.log_regs = 3; o.log_threads = 7; o.low_qubits = 2; return o; }(),
+            [] { Options o; o.pass_search = -1; o.product_prefix = -1; return o; }(),
+            [] { Options o; o.rz_groups = -1; o.max_gates_per_pass = 7; o.pass_search = 1; o.product_prefix = 1; return o; }(),
+            [] { Options o; o.log_regs = 3; o.log_threads = 7; o.low_qubits = 2; o.pass_search = 1; return o; }(),
             [] { Options o; o.force_tiled = -1; return o; }(),
         };
         for (const Options& o : variants) {

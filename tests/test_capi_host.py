@@ -167,8 +167,15 @@ def test_workspace_arithmetic(lib):
     assert S <= fw < S + (64 << 20)              # psi only
     assert c.workspace_bytes("c128", 1) >= 4 * S
     m = c.plan_info("c64")["n_passes"]
-    assert c.state_bytes("c64", 1) == (6 * m - 6) * S
+    # with a product prefix the last backward pass also stores lambda (the
+    # environment of the prefix gates is read from it)
+    assert c.plan_info("c64")["n_prefix_gates"] == 90
+    assert c.state_bytes("c64", 1) == (6 * m - 5) * S
     assert c.state_bytes("c64", 1, Q.MODE_FWD) == (2 * m - 2) * S
+    off = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, product_prefix=-1)
+    m2 = off.plan_info("c64")["n_passes"]
+    assert off.plan_info("c64")["n_prefix_gates"] == 0
+    assert off.state_bytes("c64", 1) == (6 * m2 - 6) * S
     small = Q.Circuit(4, W.get("4q").gates(), 4, 16)
     assert small.state_bytes("c128", 8) == 0.0   # whole state in LDS: no HBM state traffic
     # kept forward states: lambda plus one state per pass but the last (no
@@ -176,7 +183,7 @@ def test_workspace_arithmetic(lib):
     keep = c.workspace_bytes("c64", 1, Q.MODE_FWD_BWD_KEEP)
     assert m * S <= keep < m * S + (64 << 20)
     assert keep - fb == (m - 2) * S
-    assert c.state_bytes("c64", 1, Q.MODE_FWD_BWD_KEEP) == (5 * m - 5) * S
+    assert c.state_bytes("c64", 1, Q.MODE_FWD_BWD_KEEP) == (5 * m - 4) * S
     assert small.workspace_bytes("c64", 8, Q.MODE_FWD_BWD_KEEP) == small.workspace_bytes("c64", 8)
     assert _err(lambda: c.workspace_bytes("c64", 1, 3)) == -1
 
@@ -269,8 +276,40 @@ def test_random_plans(lib, seed, opts):
     for dt in ("c64", "c128"):
         _check_schedule(c, gates, dt)
         info = c.plan_info(dt)
-        if opts.get("max_gates_per_pass") == 1:
-            assert info["n_passes"] == gates.shape[0]
+        if opts.get("max_gates_per_pass") == 1:  # one pass per gate outside the product prefix
+            assert info["n_passes"] == gates.shape[0] - info["n_prefix_gates"]
+
+
+def test_product_prefix_plan(lib):
+    """The product-state prefix: every qubit's one-qubit gates before any
+    two-qubit gate or Pauli channel touches it; none with an embedding or when
+    turned off; a circuit of one-qubit gates only is one pass of no ops. The
+    prefix gates are reported in pass 0, first, and every schedule stays
+    valid."""
+    wl = W.get("30q")
+    c = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    for dt in ("c64", "c128"):
+        assert c.plan_info(dt)["n_prefix_gates"] == 90  # RY encoding, RY and RZ of layer 1
+        pog, order = c.schedule(dt)
+        assert np.all(pog[order[:90]] == 0)
+        assert sorted(order[:90].tolist()) == [i for i, g in enumerate(wl.gates())
+                                               if i < 30 or (30 <= i and g[0] in (W.RY, W.RZ) and i < 90)]
+    g = np.array([[W.RY, 0, -1, W.SRC_WEIGHT, 0], [W.RX, 1, -1, W.SRC_WEIGHT, 1], [W.H, 2, -1, 0, 0],
+                  [W.CNOT, 0, 1, 0, 0], [W.RY, 0, -1, W.SRC_WEIGHT, 2],
+                  [W.PAULI, 2, -1, W.SRC_INPUT, 0], [W.RZ, 2, -1, W.SRC_WEIGHT, 3],
+                  [W.RY, 9, -1, W.SRC_WEIGHT, 4]], np.int32)
+    c = Q.Circuit(10, g, 1, 5, pauli_p=[[0.1, 0.1, 0.1]], product_prefix=1)
+    assert c.plan_info("c64")["n_prefix_gates"] == 4   # RY q0, RX q1, H q2, RY q9
+    _check_schedule(c, g, "c64")
+    assert Q.Circuit(10, g, 1, 5, pauli_p=[[0.1, 0.1, 0.1]], product_prefix=-1).plan_info("c64")["n_prefix_gates"] == 0
+    only = np.array([[W.RY, q, -1, W.SRC_WEIGHT, q % 3] for q in range(12)] + [[W.H, 3, -1, 0, 0]], np.int32)
+    c = Q.Circuit(12, only, 0, 3, product_prefix=1)
+    assert c.plan_info("c64")["n_prefix_gates"] == 13 and c.plan_info("c64")["n_passes"] == 1
+    _check_schedule(c, only, "c64")
+    emb = W.get("qae")
+    assert Q.Circuit(emb.n, emb.gates(), emb.n_inputs, emb.n_weights, embed=emb.embed,
+                     force_tiled=1).plan_info("c64")["n_prefix_gates"] == 0
+    assert _err(lambda: Q.Circuit(10, g, 1, 5, pauli_p=[[0.1, 0.1, 0.1]], product_prefix=2)) == -3
 
 
 def test_pass_counts_are_small(lib):

@@ -387,6 +387,62 @@ def test_plans_agree():
             check(got, ref, 1e-12, f"plan {opts}")
 
 
+def prefix_circuit(n, F, P, seed, body=60):
+    """One to three one-qubit gates (H, RX, RY, RZ) on every qubit, then a
+    random circuit of `body` gates: every qubit starts with a product-state
+    prefix of mixed kinds."""
+    rng = np.random.default_rng(seed)
+    g = []
+    for q in range(n):
+        for _ in range(int(rng.integers(1, 4))):
+            k = int(rng.choice([W.H, W.RX, W.RY, W.RZ]))
+            if k == W.H:
+                g.append((W.H, q, -1, 0, 0))
+            elif rng.random() < 0.4:
+                g.append((k, q, -1, W.SRC_INPUT, int(rng.integers(F))))
+            else:
+                g.append((k, q, -1, W.SRC_WEIGHT, int(rng.integers(P))))
+    pre = np.array(g, np.int32).reshape(-1, 5)
+    if body == 0:
+        return pre
+    return np.concatenate([pre, W.random_circuit(n, body, F, P, seed=seed + 1)])
+
+
+PREFIX_CASES = [
+    # n, body gates, planner options
+    (8, 60, {}),                                      # one tile per sample; environment: 4 amplitudes per lane
+    (9, 60, {}),                                      # environment: 8 amplitudes per lane
+    (11, 80, dict(log_regs=2, log_threads=6)),        # small tiles, several per sample
+    (14, 120, {}),
+    (16, 120, dict(max_gates_per_pass=7)),            # many passes
+    (12, 0, {}),                                      # prefix gates only: one pass with no ops
+]
+
+
+@pytest.mark.parametrize("n,body,opts", PREFIX_CASES,
+                         ids=[f"n{c[0]}-g{c[1]}-{'-'.join(f'{k}{v}' for k, v in c[2].items()) or 'default'}"
+                              for c in PREFIX_CASES])
+def test_product_prefix(n, body, opts):
+    """The product-state prefix (first pass from the per-qubit factors, prefix
+    gradients from lambda's environment) against the oracle and against the
+    same plan with the prefix run as tile ops (product_prefix=-1): c128 at
+    1e-12, c64 at 1e-5. Weight 0 is exactly zero, so some factors have a zero
+    component (an RY(0) or RX(0) leaves |0>), which the environment sums must
+    handle without dividing by a factor."""
+    F, P, B = 4, 6, 3
+    gates = prefix_circuit(n, F, P, seed=400 + n + body, body=body)
+    on = Q.Circuit(n, gates, F, P, product_prefix=1, **opts)
+    off = Q.Circuit(n, gates, F, P, product_prefix=-1, **opts)
+    assert on.plan_info("c64")["n_prefix_gates"] > 0 and off.plan_info("c64")["n_prefix_gates"] == 0
+    for dtype in ("c128", "c64"):
+        x, w, g = W.random_inputs(B, F, P, n, seed=401 + n, dtype=dtype)
+        w[0] = 0.0
+        want = oracle.run(n, gates, x, w, grad_out=g)
+        got = gpu_fb(on, dtype, x, w, g)
+        check(got, want, TOL[dtype], f"prefix n={n} {opts} {dtype} vs oracle")
+        check(got, gpu_fb(off, dtype, x, w, g), 2 * TOL[dtype], f"prefix n={n} {opts} {dtype} on vs off")
+
+
 @pytest.mark.parametrize("name", ["24q", "30q"])
 def test_product_state_full_size(name):
     """Workload circuit with its entanglers removed, at full size: every qubit
@@ -406,13 +462,15 @@ def test_product_state_full_size(name):
     close(got["grad_weights"], gw, 1e-5, f"{name} product state", "grad_weights")
 
 
+@pytest.mark.parametrize("prefix", [1, -1], ids=["prefix", "ops"])
 @pytest.mark.parametrize("n,dtype,keep", [(32, "c64", False), (31, "c128", True)],
                          ids=["n32-c64-plain", "n31-c128-kept"])
-def test_maximum_qubits(n, dtype, keep):
+def test_maximum_qubits(n, dtype, keep, prefix):
     """The largest state each dtype allows (32 GiB), one sample: rotation layers
     around CNOT and CZ pairs that cancel (on qubits 0, 3, n-2 and n-1, so the
     top amplitude-index bits take part), against the SO(3) closed form of the
-    product state."""
+    product state; with the first rotation layer as the product-state prefix
+    (one tile pass left), and with every gate as a tile op (several passes)."""
     torch.cuda.empty_cache()
     P = 2 * n
     ry = [(W.RY, q, -1, W.SRC_WEIGHT, q) for q in range(n)]
@@ -421,8 +479,11 @@ def test_maximum_qubits(n, dtype, keep):
     pairs = [(W.CNOT, n - 1, 0, 0, 0), (W.CZ, 3, n - 2, 0, 0)]
     gates = np.array(ry + pairs + pairs + rest, np.int32)
     x, w, g = W.random_inputs(1, 1, P, n, seed=n, dtype=dtype)
-    circ = Q.Circuit(n, gates, 1, P)
-    assert circ.plan_info(dtype)["n_passes"] > 1
+    circ = Q.Circuit(n, gates, 1, P, product_prefix=prefix)
+    if prefix == 1:
+        assert circ.plan_info(dtype)["n_prefix_gates"] >= n
+    else:
+        assert circ.plan_info(dtype)["n_passes"] > 1
     r = Q.Runner(circ, dtype, keep_states=keep)
     got = gpu_fb(circ, dtype, x, w, g, r)
     del r
@@ -643,8 +704,10 @@ def test_rz_groups(n, dtype, opts, shape):
     x, w, g = W.random_inputs(B, F, P, n, seed=71 + n, dtype=dtype)
     x[0, 0] = 9.0      # angles well outside [-pi, pi]
     w[1] = -7.5
-    grouped = Q.Circuit(n, gates, F, P, **opts)
-    single = Q.Circuit(n, gates, F, P, rz_groups=-1, **opts)
+    # the first layer runs as tile ops too (not as the product-state prefix),
+    # so that its RZs form groups and pairs
+    grouped = Q.Circuit(n, gates, F, P, product_prefix=-1, **opts)
+    single = Q.Circuit(n, gates, F, P, rz_groups=-1, product_prefix=-1, **opts)
     assert grouped.plan_info(dtype)["n_rz_groups"] > 0
     if shape == "staircase":
         assert grouped.plan_info(dtype)["n_ryz_pairs"] > 0
@@ -665,7 +728,7 @@ def test_rz_groups_param_shift():
     n, dtype, F, P, B = 13, "c128", 3, 5, 2
     gates = np.concatenate([rz_layer_circuit(n, 1, F, P, seed=90), staircase_circuit(n, 1, F, P, seed=92)])
     x, w, g = W.random_inputs(B, F, P, n, seed=91, dtype=dtype)
-    circ = Q.Circuit(n, gates, F, P)
+    circ = Q.Circuit(n, gates, F, P, product_prefix=-1)  # the first layer as tile ops
     assert circ.plan_info(dtype)["n_rz_groups"] > 0 and circ.plan_info(dtype)["n_ryz_pairs"] > 0
     e, gx, gw = Q.Runner(circ, dtype).param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), max_chunk=37)
     torch.cuda.synchronize()
