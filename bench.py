@@ -68,9 +68,10 @@ def shift_circuits(gates, batch) -> int:
     return batch * (2 * rot + 1)
 
 
-def shift_flops(gates, batch, n) -> float:
-    """Algorithmic flops of one parameter-shift VJP: forward passes only."""
-    per_amp = sum(FLOPS_FWD[int(g[0])] for g in gates)
+def shift_flops(gates, batch, n, ops=None) -> float:
+    """Algorithmic flops of one parameter-shift VJP: forward passes only, over
+    the gates that run as ops (all of them unless `ops` says otherwise)."""
+    per_amp = sum(FLOPS_FWD[int(g[0])] for g in (gates if ops is None else ops))
     return float(per_amp) * shift_circuits(gates, batch) * (1 << n)
 
 
@@ -305,17 +306,24 @@ def main():
         line["vjp_per_s"] = 1e3 / ms_step
     if timing and kcnt[0] > 0:
         tile_ms = kms[0] / args.steps
+        # the tile kernel's own work: the gates of the product-state prefix are
+        # not tile ops (the first pass writes their state from per-qubit
+        # factors; their gradients come from the environment kernels)
+        n_pre = circ.plan_info(wl.dtype)["n_prefix_gates"]
+        tile_gates = gates
+        if n_pre:
+            tile_gates = np.delete(gates, circ.schedule(wl.dtype)[1][:n_pre], axis=0)
         if args.shots > 0:
             state_bytes = circ.state_bytes(wl.dtype, wl.batch, Q.MODE_FWD) + (1 << wl.n) * wl.batch * amp
-            flops = sum(FLOPS_FWD[int(g_[0])] for g_ in gates) * wl.batch * float(1 << wl.n)
+            flops = sum(FLOPS_FWD[int(g_[0])] for g_ in tile_gates) * wl.batch * float(1 << wl.n)
             traffic = None
         elif shift:
             state_bytes = circ.state_bytes(wl.dtype, n_shift, Q.MODE_FWD)
-            flops = shift_flops(gates, wl.batch, wl.n)
+            flops = shift_flops(gates, wl.batch, wl.n, tile_gates)
             traffic = None
         else:
             state_bytes = circ.state_bytes(wl.dtype, wl.batch, runner.backward_mode(wl.batch))
-            flops = algorithmic_flops(gates, wl.batch, wl.n)
+            flops = algorithmic_flops(tile_gates, wl.batch, wl.n)
             # the committed summaries were taken on the default plan with kept states
             same_run = (args.noise == 0 and not opts
                         and runner.backward_mode(wl.batch) == Q.MODE_FWD_BWD_KEEP)
@@ -332,6 +340,7 @@ def main():
                             "launches_per_step": launches,
                             "kernel_ms_per_step": tile_ms,
                             "algorithmic_flops_per_step": flops,
+                            "prefix_gates": n_pre,
                             "algorithmic_bytes_per_step": state_bytes,
                             "issue_peak": ISSUE_PEAK_TFLOPS,
                             "frac_of_issue_peak": alu / ISSUE_PEAK_TFLOPS,

@@ -234,7 +234,7 @@ int compute_layout(const ql_circuit* h, int dt, int64_t B, int mode, Layout& L, 
     if (bwd && pl.product) {
         // per sample, environment workgroup and qubit: (re, im) of r_q(0) and r_q(1), fp64
         L.env = off;
-        if (!mul_ok((size_t)B * (size_t)env_workgroups(c.n, B), (size_t)c.n * 32, sz))
+        if (!mul_ok((size_t)B * (size_t)env_workgroups(dt, c.n, B), (size_t)c.n * 32, sz))
             return fail(QL_ENOMEM, "size overflow");
         off = align256(off + sz);
     }
@@ -421,7 +421,7 @@ PrefixArgs prefix_args(const Ctx& x, int64_t B) {
     pa.n = x.c.n;
     pa.F = x.c.n_inputs;
     pa.n_wg = x.L.n_wg;
-    pa.env_wg = env_workgroups(x.c.n, B);
+    pa.env_wg = env_workgroups(x.dt, x.c.n, B);
     return pa;
 }
 

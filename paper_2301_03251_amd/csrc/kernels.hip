@@ -899,7 +899,17 @@ __global__ void __launch_bounds__(256) k_env(const PrefixArgs a) {
         for (int t = 0; t < 6; ++t) sl[t][c] = 0;
     }
     double fx[4] = {0.0, 0.0, 0.0, 0.0};  // lane i < nfix: fixed qubit LR + 6 + i
-    for (int64_t blk = (int64_t)w * 4 + wave; blk < nblk; blk += (int64_t)a.env_wg * 4) {
+    // this wavefront's blocks are blk0 + k * stride with stride = 4 env_wg, a
+    // power of two: the block bits below lo = log2(stride) are blk0's
+    const int64_t blk0 = (int64_t)w * 4 + wave, stride = (int64_t)a.env_wg * 4;
+    const int lo = std::min(nfix, (int)__builtin_ctzll((unsigned long long)stride));
+    double2 clo = make_double2(1.0, 0.0), glo = make_double2(1.0, 0.0);
+    for (int i = 0; i < lo; ++i) {
+        const double2 f = fac[2 * (LR + 6 + i) + ((blk0 >> i) & 1)];
+        clo = cxmul(clo, f);
+        if (i != lane) glo = cxmul(glo, f);  // lane i < lo: without its own factor
+    }
+    for (int64_t blk = blk0; blk < nblk; blk += stride) {
         T2 v[R];
         const T2* src = lam + (blk << (LR + 6)) + ((int64_t)lane << LR);
 #pragma unroll
@@ -910,9 +920,11 @@ __global__ void __launch_bounds__(256) k_env(const PrefixArgs a) {
             const T2 x = cxmulc(f0[0], S[0][0]), y = cxmulc(f1[0], S[0][1]);
             return mk<T2>(x.x + y.x, x.y + y.y);
         }();
-        double2 cfix = make_double2(1.0, 0.0);
-        for (int i = 0; i < nfix; ++i) cfix = cxmul(cfix, fac[2 * (LR + 6 + i) + ((blk >> i) & 1)]);
-        const T2 cf = to_real<T2, Real>(cfix);
+        // the fixed factors: those of the bits below `lo` are the same for all
+        // of this wavefront's blocks (its stride is a power of two)
+        double2 chi = make_double2(1.0, 0.0);
+        for (int i = lo; i < nfix; ++i) chi = cxmul(chi, fac[2 * (LR + 6 + i) + ((blk >> i) & 1)]);
+        const T2 cf = to_real<T2, Real>(cxmul(clo, chi));
         // register qubits: conj(every other factor) S[m][u]
         const T2 call = cxmul(clr, cf);
 #pragma unroll
@@ -928,22 +940,29 @@ __global__ void __launch_bounds__(256) k_env(const PrefixArgs a) {
 #pragma unroll
         for (int t = 0; t < 6; ++t) {
             const T2 x = cxmulc(cxmul(lf[t], cf), T);
-            const int u = 2 * ((lane >> t) & 1);
-            sl[t][u] += x.x;
-            sl[t][u + 1] += x.y;
+            const bool one = (lane >> t) & 1;
+            sl[t][0] += one ? (Real)0 : x.x;
+            sl[t][1] += one ? (Real)0 : x.y;
+            sl[t][2] += one ? x.x : (Real)0;
+            sl[t][3] += one ? x.y : (Real)0;
         }
         // fixed qubits (bits uniform over the block): conj(product of the
         // other fixed factors) U, U = the wavefront's sum of conj(cl) T
         const T2 uu = cxmulc(clr, T);
         const double ux = wave_total(uu.x), uy = wave_total(uu.y);
         if (lane < nfix) {
-            double2 g = make_double2(1.0, 0.0);
-            for (int i = 0; i < nfix; ++i)
+            // the other fixed factors: the constant low ones (glo leaves out
+            // this lane's if it is low), times the changing high ones but
+            // this lane's
+            double2 g = glo;
+            for (int i = lo; i < nfix; ++i)
                 if (i != lane) g = cxmul(g, fac[2 * (LR + 6 + i) + ((blk >> i) & 1)]);
             const double2 r = cxmulc(g, make_double2(ux, uy));
-            const int u = 2 * (int)((blk >> lane) & 1);
-            fx[u] += r.x;
-            fx[u + 1] += r.y;
+            const bool one = (blk >> lane) & 1;
+            fx[0] += one ? 0.0 : r.x;
+            fx[1] += one ? 0.0 : r.y;
+            fx[2] += one ? r.x : 0.0;
+            fx[3] += one ? r.y : 0.0;
         }
     }
     // the wavefront's sums into LDS (lane 0; lane i for fixed qubit i)
@@ -1461,29 +1480,31 @@ hipError_t launch_bind_prefix(int dtype, const PrefixArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-int env_workgroups(int n, int64_t B) {
-    const int lr = n >= 10 ? 4 : n - 6;
+// Register bits per lane of the environment kernel: 8 (complex64) or 4
+// (complex128) amplitudes per lane keep it at 128 VGPRs or fewer.
+int env_log_regs(int dtype, int n) { return std::min(dtype == 0 ? 3 : 2, n - 6); }
+
+int env_workgroups(int dtype, int n, int64_t B) {
+    const int lr = env_log_regs(dtype, n);
     const int64_t nblk = (int64_t)1 << (n - lr - 6);
-    const int64_t want = std::max<int64_t>(1, 2048 / std::max<int64_t>(B, 1));
-    return (int)std::max<int64_t>(1, std::min<int64_t>(want, (nblk + 3) / 4));
+    // a power of two, so that a wavefront's blocks share their low index bits
+    int64_t want = 1;
+    while (want * 2 * std::max<int64_t>(B, 1) <= 2048) want *= 2;
+    int64_t cap = 1;
+    while (cap * 4 < nblk) cap *= 2;
+    return (int)std::min(want, cap);
 }
 
 hipError_t launch_env(int dtype, const PrefixArgs& a, hipStream_t s) {
     if (a.n < 8 || a.n > 32) return hipErrorInvalidValue;
     const dim3 grid((unsigned)(a.B * a.env_wg));
-    const int lr = a.n >= 10 ? 4 : a.n - 6;
-#define QL_ENV(REAL)                                                                        \
-    switch (lr) {                                                                           \
-        case 2: hipLaunchKernelGGL((k_env<REAL, 2>), grid, dim3(256), 0, s, a); break;      \
-        case 3: hipLaunchKernelGGL((k_env<REAL, 3>), grid, dim3(256), 0, s, a); break;      \
-        default: hipLaunchKernelGGL((k_env<REAL, 4>), grid, dim3(256), 0, s, a); break;     \
-    }
+    const int lr = env_log_regs(dtype, a.n);
     if (dtype == 0) {
-        QL_ENV(float)
+        if (lr == 2) hipLaunchKernelGGL((k_env<float, 2>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((k_env<float, 3>), grid, dim3(256), 0, s, a);
     } else {
-        QL_ENV(double)
+        hipLaunchKernelGGL((k_env<double, 2>), grid, dim3(256), 0, s, a);
     }
-#undef QL_ENV
     return hipGetLastError();
 }
 

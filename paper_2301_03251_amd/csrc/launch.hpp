@@ -194,7 +194,7 @@ struct PrefixArgs {
     int32_t env_wg;            // workgroups per sample of the environment kernel
 };
 // Workgroups per sample of the environment kernel for n qubits and batch B.
-int env_workgroups(int n, int64_t B);
+int env_workgroups(int dtype, int n, int64_t B);
 // LDS words per (gradient accumulator, wavefront) of the tile kernel
 constexpr int TILE_GRAD_WORDS = 2;
 
