@@ -921,10 +921,29 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
     // kept when the rest of the circuit then needs fewer passes, or as many
     // passes and no more layout changes (30q: 9 passes either way, 24
     // exchanges and 72 lane swaps against 26 and 76; 16q: 5 passes against
-    // 6); otherwise (24q: 41 exchanges against 35) every gate runs as a tile
-    // op. product_prefix = 1 keeps it always, -1 never.
+    // 6); otherwise (24q: 41 exchanges against 35) the op plan is kept and
+    // only the prefix gates of its first pass form the product state.
+    // product_prefix = 1 keeps the whole prefix always, -1 never.
     const int score_ops = choose(pl);
     if (score_ops < 0) return "planner made no progress";
+    // take plan t with the prefix gates `absorbed` (each qubit's a leading run
+    // of its prefix) as the initial product state
+    auto take = [&](Plan& t, const std::vector<int>& absorbed) {
+        pl.passes = std::move(t.passes);
+        pl.phases = std::move(t.phases);
+        pl.diags = std::move(t.diags);
+        pl.fuses = std::move(t.fuses);
+        pl.product = true;
+        pl.pre_gates = absorbed;
+        std::vector<std::vector<DevPrefix>> mine(c.n);
+        for (int i : absorbed) mine[c.gates[i].q0].push_back({c.gates[i].kind, c.gates[i].slot});
+        pl.pre_ptr.assign(1, 0);
+        pl.pre_ops.clear();
+        for (int q = 0; q < c.n; q++) {
+            pl.pre_ops.insert(pl.pre_ops.end(), mine[q].begin(), mine[q].end());
+            pl.pre_ptr.push_back((int32_t)pl.pre_ops.size());
+        }
+    };
     if (!pre_gates.empty()) {
         for (int i : pre_gates) done[i] = 1;
         remaining -= (int)pre_gates.size();
@@ -932,16 +951,41 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         const int score_pre = choose(t);
         if (score_pre >= 0 && (o.product_prefix == 1 || t.passes.size() < pl.passes.size() ||
                                (t.passes.size() == pl.passes.size() && score_pre <= score_ops))) {
-            pl.passes = std::move(t.passes);
-            pl.phases = std::move(t.phases);
-            pl.diags = std::move(t.diags);
-            pl.fuses = std::move(t.fuses);
-            pl.product = true;
-            pl.pre_gates = pre_gates;
-            pl.pre_ptr.assign(1, 0);
-            for (int q = 0; q < c.n; q++) {
-                pl.pre_ops.insert(pl.pre_ops.end(), per[q].begin(), per[q].end());
-                pl.pre_ptr.push_back((int32_t)pl.pre_ops.size());
+            take(t, pre_gates);
+        } else if (o.product_prefix == 0 && !pl.passes.empty()) {
+            // Otherwise the prefix gates the first pass of the op plan runs
+            // anyway (a leading run of each of its qubits' prefixes) become
+            // its initial product state; the passes stay as they are.
+            std::vector<char> in0(G, 0);
+            for (int i : pl.passes[0].gates) in0[i] = 1;
+            std::vector<char> take0(G, 0);
+            std::vector<int> absorbed;
+            std::vector<int> by_q(c.n, 0);
+            for (int i : pre_gates) {  // gate order: per qubit, stop at the first one pass 0 lacks
+                const int q = c.gates[i].q0;
+                if (by_q[q] < 0) continue;
+                if (in0[i]) {
+                    take0[i] = 1;
+                    absorbed.push_back(i);
+                } else {
+                    by_q[q] = -1;
+                }
+            }
+            if (!absorbed.empty()) {
+                std::vector<Cand> seq;
+                for (const PassPlan& pp : pl.passes) {
+                    Cand cd;
+                    cd.tile = 0;
+                    for (int q : pp.qubits) cd.tile |= 1ull << q;
+                    for (int i : pp.gates)
+                        if (!take0[i]) cd.gates.push_back(i);
+                    seq.push_back(std::move(cd));
+                }
+                Plan t2;
+                lay_out(std::move(seq), t2);
+                int score = 0;
+                for (const PassPlan& pp : t2.passes) score += 3 * pp.n_transposes + pp.n_lane_swaps;
+                if (score <= score_ops) take(t2, absorbed);
             }
         }
     }
