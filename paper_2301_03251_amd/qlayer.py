@@ -254,7 +254,7 @@ class Runner:
     The memory cost of the default can be large: with m tile passes the kept
     workspace holds m - 1 states of batch * 2^n amplitudes instead of 2. For
     the 30-qubit workload (9 passes, 8 GiB per state) that is a 72 GiB
-    workspace against 16 GiB, for a step about 5 % faster (the backward passes then store no
+    workspace against 16 GiB, for a step about 4 % faster (the backward passes then store no
     state). Pass keep_states=False when the device memory is needed for
     anything else (for example several layers of a model in one step)."""
 
