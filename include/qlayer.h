@@ -185,6 +185,10 @@ typedef struct {
                                    embedding). 0 (default): so when the other gates
                                    then plan into fewer passes, or as many with no
                                    more layout changes; 1: always; -1: never */
+    int32_t cz_groups;          /* 0: two or more CZs of one tile layout that commute
+                                   into one place (each with at least one operand
+                                   outside the registers, or on two register bits)
+                                   run as one sign op; -1: every CZ runs on its own */
 } ql_options;
 
 typedef struct ql_circuit ql_circuit; /* opaque */
@@ -347,6 +351,7 @@ typedef struct {
     int32_t n_ryz_pairs;   /* RZs run together with their bit's RY in one op, all passes */
     int32_t n_prefix_gates; /* gates of the product-state prefix (the first pass's initial
                                state; see ql_options.product_prefix) */
+    int32_t n_cz_groups;   /* CZ groups (several CZs run as one sign op), all passes */
 } ql_plan_info;
 
 int ql_plan_info_get(const ql_circuit* c, ql_dtype dtype, ql_plan_info* out);

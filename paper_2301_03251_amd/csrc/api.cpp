@@ -40,7 +40,7 @@ struct Tables {
     std::vector<uint8_t> blob;
     size_t off_pass = 0, off_phase = 0, off_ops = 0, off_gslot = 0, off_slots = 0;
     size_t off_xptr = 0, off_xslot = 0, off_wptr = 0, off_wslot = 0, off_gates = 0, off_diag = 0;
-    size_t off_fuse = 0;
+    size_t off_fuse = 0, off_czg = 0;
     size_t off_pptr = 0, off_pops = 0;  // product-prefix CSR (per qubit)
     std::vector<DevPass> passes;
     int n_diags = 0, n_fuses = 0;
@@ -125,6 +125,7 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
     T.n_diags = (int)pl.diags.size();
     T.off_fuse = put(T.blob, pl.fuses);
     T.n_fuses = (int)pl.fuses.size();
+    T.off_czg = put(T.blob, pl.czgs);
     T.off_pptr = put(T.blob, pl.pre_ptr);
     T.off_pops = put(T.blob, pl.pre_ops);
     T.blob.resize(align256(T.blob.size()), 0);
@@ -575,6 +576,7 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         ta.n_diags = x.T.n_diags;
         ta.fzc = x.W + x.L.fzc;
         ta.n_fuses = x.T.n_fuses;
+        ta.czg = (const DevCzg*)(x.W + x.L.tables + x.T.off_czg);
         ta.grad_out = grad_out;
         ta.zpart = zpart;
         ta.gpart = gpart;
@@ -889,6 +891,7 @@ Options to_options(const ql_options* o) {
         r.rz_groups = o->rz_groups;
         r.pass_search = o->pass_search;
         r.product_prefix = o->product_prefix;
+        r.cz_groups = o->cz_groups;
     }
     return r;
 }
@@ -1113,6 +1116,7 @@ int ql_plan_info_get(const ql_circuit* h, ql_dtype dtype, ql_plan_info* out) {
     r.n_ryz_pairs = (int)pl.fuses.size();
     r.n_param_gates = h->c.n_param_slots;
     r.n_prefix_gates = (int)pl.pre_gates.size();
+    r.n_cz_groups = (int)pl.czgs.size();
     *out = r;
     return QL_OK;
 }

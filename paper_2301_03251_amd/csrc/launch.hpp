@@ -166,6 +166,7 @@ struct TileArgs {
     int32_t n, n_ops, n_wg, flags;
     int32_t n_gslots;          // gradient accumulators of this pass
     const double* phi;         // [B][n][2] complex (double2): product-prefix factors (PF_PRODUCT)
+    const DevCzg* czg;         // CZ groups (H_CZG ops)
 };
 
 // Product-state prefix. Binding: phi[c][q] = the state the prefix gates of

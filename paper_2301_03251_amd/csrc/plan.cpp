@@ -103,16 +103,31 @@ DevPhase make_phase(const std::vector<int>& tq, const std::vector<int>& reg_bits
 bool commutes_with_z(uint32_t h, uint32_t bits) {
     auto off = [&](uint32_t j) { return !(bits >> j & 1u); };
     if (h < H_G1 + 20) return (h - H_G1) / 5 == 3 || off((h - H_G1) % 5);
-    if (h == H_RZU || (h >= H_CZ_RR && h <= H_CZ_XX)) return true;
+    if (h == H_RZU || (h >= H_CZ_RR && h <= H_CZ_XX) || h == H_CZG) return true;
     if (h >= H_CNOT_RR && h < H_CNOT_T) return off((h - H_CNOT_RR) / 5);
     if (h >= H_CNOT_T && h < H_CZ_RR) return off((h - H_CNOT_T) % 5);
     if (h >= H_PX && h < H_PX + 15) return (h - H_PX) / 5 == 2 || off((h - H_PX) % 5);
     return false;
 }
 
+// Register bits that op h (a gate op within one layout) changes other than
+// by a diagonal factor: a CZ moves past op h when h changes none of the CZ's
+// register bits (diagonal ops commute with it, and an op on other bits acts on
+// other factors of the state).
+uint32_t moved_bits(uint32_t h) {
+    if (h < H_G1 + 20) return (h - H_G1) / 5 == 3 ? 0u : 1u << ((h - H_G1) % 5);
+    if (h == H_RZU || (h >= H_CZ_RR && h <= H_CZ_XX) || h == H_DZ || h == H_CZG || (h >= H_RZN && h < H_RZN + 5))
+        return 0u;
+    if (h >= H_CNOT_RR && h < H_CNOT_T) return 1u << ((h - H_CNOT_RR) / 5);
+    if (h >= H_CNOT_T && h < H_CZ_RR) return 1u << ((h - H_CNOT_T) % 5);
+    if (h >= H_PX && h < H_PX + 15) return (h - H_PX) / 5 == 2 ? 0u : 1u << ((h - H_PX) % 5);
+    if (h >= H_RYZ && h < H_RYZN + 5) return 1u << ((h - H_RYZ) % 5);
+    return ~0u;
+}
+
 void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_r, int low,
                    uint32_t amp, std::vector<DevPhase>& phases, std::vector<DevDiag>* diags,
-                   std::vector<DevFuse>* fuses) {
+                   std::vector<DevFuse>* fuses, std::vector<DevCzg>* czgs) {
     const int r = log_r;
     std::vector<int> bit_of(64, -1);  // qubit -> tile bit
     for (int j = 0; j < k; j++) bit_of[pp.qubits[j]] = j;
@@ -437,6 +452,76 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         recs.swap(out);
     };
 
+    // CZ groups: within the ops of one layout, each CZ moves later, past ops
+    // that change none of its register bits (see moved_bits), and is
+    // collected. An op that changes a register bit of a collected CZ puts out
+    // every collected CZ before it (each has moved only past ops it commutes
+    // with), two or more as one H_CZG op; so does the end of the layout. A
+    // ring of CZs between two rotation layers becomes one op.
+    auto cz_reg_bits = [](uint32_t h) -> uint32_t {
+        if (h >= H_CZ_RR && h < H_CZ_RX) return (1u << ((h - H_CZ_RR) / 5)) | (1u << ((h - H_CZ_RR) % 5));
+        if (h >= H_CZ_RX && h < H_CZ_XX) return 1u << (h - H_CZ_RX);
+        return 0u;
+    };
+    auto group_cz = [&](size_t seg0) {
+        if (!czgs || r > CZG_REG_BITS) return;
+        std::vector<Rec> out(recs.begin(), recs.begin() + (long)seg0);
+        std::vector<Rec> grp;
+        auto emit = [&](const std::vector<Rec>& g) {
+            if (g.size() == 1) out.push_back(g[0]);
+            if (g.size() < 2) return;
+            DevCzg d{};
+            uint32_t tt[MAX_CZG_PAIRS], other[MAX_CZG_PAIRS], n_tt = 0, n_other = 0;
+            auto flush = [&]() {
+                for (uint32_t i = 0; i < n_tt; i++) d.pair[i] = tt[i];
+                for (uint32_t i = 0; i < n_other; i++) d.pair[n_tt + i] = other[i];
+                d.n_tt = n_tt;
+                d.n_pairs = n_tt + n_other;
+                const uint32_t idx = (uint32_t)czgs->size();
+                czgs->push_back(d);
+                out.push_back({make_op(H_CZG, idx, -1, K_CZ), idx});
+                d = DevCzg{};
+                n_tt = n_other = 0;
+            };
+            for (const Rec& rc : g) {
+                const uint32_t h = rc.op.h, w = rc.op.arg;
+                if (h >= H_CZ_RR && h < H_CZ_RX) {
+                    const uint32_t a = (h - H_CZ_RR) / 5, b = (h - H_CZ_RR) % 5;
+                    for (uint32_t i = 0; i < (1u << r); i++)
+                        if ((i >> a & 1u) && (i >> b & 1u)) d.reg_mask ^= 1u << i;
+                } else if (h >= H_CZ_RX && h < H_CZ_XX) {
+                    const uint32_t a = h - H_CZ_RX, pos = w & 0xff;
+                    if (((w >> 8) & 3) == LOC_THR) d.thr[a] ^= 1u << pos;
+                    else d.fix[a] ^= 1u << pos;
+                } else {
+                    if (n_tt + n_other == MAX_CZG_PAIRS) flush();
+                    uint32_t wa = w & 0xffff, wb = w >> 16;
+                    if (((wa >> 8) & 3) != LOC_THR) std::swap(wa, wb);  // a thread operand first
+                    if (((wb >> 8) & 3) == LOC_THR) tt[n_tt++] = (wa & 0xff) | (wb & 0xff) << 8;
+                    else other[n_other++] = wa | wb << 16;
+                }
+            }
+            flush();
+        };
+        for (size_t i = seg0; i < recs.size(); i++) {
+            const uint32_t h = recs[i].op.h;
+            if (h >= H_CZ_RR && h <= H_CZ_XX) {
+                grp.push_back(recs[i]);
+                continue;
+            }
+            const uint32_t mv = moved_bits(h);
+            uint32_t clash = 0;
+            for (const Rec& rc : grp) clash |= cz_reg_bits(rc.op.h) & mv;
+            if (clash || mv == ~0u) {
+                emit(grp);
+                grp.clear();
+            }
+            out.push_back(recs[i]);
+        }
+        emit(grp);
+        recs.swap(out);
+    };
+
     while (!pending.empty()) {
         uint64_t blocked = 0;
         std::vector<int> rest;
@@ -490,6 +575,7 @@ void schedule_pass(const std::vector<Gate>& gates, PassPlan& pp, int k, int log_
         }
         group_rz(seg0);
         pair_ryz(seg0);
+        group_cz(seg0);
         pending.swap(rest);
         if (pending.empty()) break;
         change_to(choose_next());
@@ -643,6 +729,7 @@ std::string build_circuit(int n, const int32_t* g5, int n_gates, int n_inputs, i
     if (o.max_gates_per_pass < 0) return "option: max_gates_per_pass < 0";
     if (o.wg_per_sample < 0) return "option: wg_per_sample < 0";
     if (o.rz_groups != 0 && o.rz_groups != -1) return "option: rz_groups must be 0 or -1";
+    if (o.cz_groups != 0 && o.cz_groups != -1) return "option: cz_groups must be 0 or -1";
     if (o.product_prefix < -1 || o.product_prefix > 1) return "option: product_prefix must be -1, 0 or 1";
     if (o.pass_search < -1 || o.pass_search > 1) return "option: pass_search must be -1, 0 or 1";
     for (int dt = 0; dt < 2; dt++) {
@@ -871,7 +958,8 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
             for (int q = 0; q < c.n; q++) if (tile >> q & 1) pp.qubits.push_back(q);
             pp.gates = std::move(cd.gates);
             schedule_pass(c.gates, pp, k, log_r, low, dtype == 0 ? 8u : 16u, to.phases,
-                          o.rz_groups == 0 ? &to.diags : nullptr, o.rz_groups == 0 ? &to.fuses : nullptr);
+                          o.rz_groups == 0 ? &to.diags : nullptr, o.rz_groups == 0 ? &to.fuses : nullptr,
+                          o.cz_groups == 0 ? &to.czgs : nullptr);
             to.passes.push_back(std::move(pp));
         }
     };
@@ -913,6 +1001,7 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
                 to.phases = std::move(t.phases);
                 to.diags = std::move(t.diags);
                 to.fuses = std::move(t.fuses);
+                to.czgs = std::move(t.czgs);
             }
         }
         return best;
@@ -933,6 +1022,7 @@ std::string build_plan(const Circuit& c, int dtype, Plan& pl) {
         pl.phases = std::move(t.phases);
         pl.diags = std::move(t.diags);
         pl.fuses = std::move(t.fuses);
+        pl.czgs = std::move(t.czgs);
         pl.product = true;
         pl.pre_gates = absorbed;
         std::vector<std::vector<DevPrefix>> mine(c.n);

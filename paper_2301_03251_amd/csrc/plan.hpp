@@ -81,6 +81,7 @@ enum HandlerId : uint32_t {
                        //      binding kernel, as H_RZN for a single RZ)
     H_NOP = 149,
     H_END = 150,
+    H_CZG = 151,       // CZ group: the CZs of one layout in one sign op; arg = group index (DevCzg)
 };
 // The RZ of an RY-RZ pair op (H_RYZ): its rotation slot and gradient slot.
 struct DevFuse {
@@ -101,6 +102,23 @@ struct DevDiag {
     uint32_t gslot[MAX_DZ_BITS];
 };
 static_assert(sizeof(DevDiag) == 32, "DevDiag layout");
+// A CZ group: CZs of one tile layout that commute into one place, applied as
+// one sign pattern. An amplitude is negated when an odd number of the pairs
+// have both operand bits set. Register operands are register bits of the
+// layout; the other operands are thread bits (tile bits the lanes hold) or
+// fixed qubits (uniform per tile).
+constexpr int CZG_REG_BITS = 5;    // register bits of the largest register tile
+constexpr int MAX_CZG_PAIRS = 16;  // pairs with no register operand per group
+struct DevCzg {
+    uint32_t reg_mask;             // registers negated by the pairs of two register bits
+    uint32_t n_tt;                 // pairs of two thread bits: pair[0 .. n_tt)
+    uint32_t n_pairs;              // then thread-fixed and fixed-fixed pairs up to n_pairs
+    uint32_t thr[CZG_REG_BITS];    // per register bit: tile-bit mask of its thread-bit partners
+    uint32_t fix[CZG_REG_BITS];    // per register bit: qubit mask of its fixed-qubit partners
+    uint32_t pair[MAX_CZG_PAIRS];  // thread-thread: tile bits a | b << 8; others: loc words a | b << 16
+    uint32_t pad[3];
+};
+static_assert(sizeof(DevCzg) == 128, "DevCzg layout");
 // Argument of a lane swap: the new phase (< 2^20) and the tile bits x (leaving
 // the lane bit for the registers) and y (taking its place).
 constexpr uint32_t lswap_arg(uint32_t phase, uint32_t x, uint32_t y) {
@@ -200,6 +218,8 @@ struct Options {
     int product_prefix = 0;  // each qubit's leading one-qubit gates form the initial product state
                              // (tile plans without an embedding): 0 when the rest plans no worse,
                              // 1 always, -1 never (they run as ops)
+    int cz_groups = 0;  // 0: CZs of one layout that commute into one place run as one H_CZG
+                        // op (two or more); -1: every CZ runs on its own
     int pass_search = 0;  // 0: a beam search over pass sequences when it needs fewer passes than
                           // the look-ahead, else the look-ahead; 1: the look-ahead (each
                           // pass's tile priced by its pass plus a greedy completion); -1: the
@@ -226,6 +246,7 @@ struct Plan {
     std::vector<DevPhase> phases;
     std::vector<DevDiag> diags;  // RZ groups (H_DZ ops), all passes
     std::vector<DevFuse> fuses;  // RZs of RY-RZ pair ops (H_RYZ), all passes
+    std::vector<DevCzg> czgs;    // CZ groups (H_CZG ops), all passes
     int n_slots = 0;           // rotation slots
     // Product prefix (tile plans): the gates of pre_ops[pre_ptr[q] .. pre_ptr[q+1])
     // act on qubit q of |0...0> before anything else touches it, so the first

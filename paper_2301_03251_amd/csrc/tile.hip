@@ -386,6 +386,58 @@ __device__ __forceinline__ bool loc_bit(uint32_t w, uint32_t tb, uint32_t gb) {
     return (((w >> 8) & 3) == LOC_THR ? (tb >> pos) : (gb >> pos)) & 1u;
 }
 
+// Negate x where bit 31 of s is set (the sign bit of a float; of the high word
+// of a double).
+__device__ __forceinline__ float xor_sign(float x, uint32_t s) {
+    return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, x) ^ s);
+}
+__device__ __forceinline__ double xor_sign(double x, uint32_t s) {
+    return __builtin_bit_cast(double, __builtin_bit_cast(uint64_t, x) ^ ((uint64_t)s << 32));
+}
+
+// CZ group g on a register tile (and on lm too when BOTH: the same tile's
+// second state). Register i of a lane is negated when bit i of the lane's mask
+//   M = (s ? all : 0) ^ sum over register bits a with c_a = 1 of (registers with bit a set)
+//       ^ g.reg_mask
+// is set, with s the parity of the pairs without a register operand (thread-
+// thread pairs from the lane's tile bits tb, thread-fixed pairs linear in tb
+// with coefficients from the tile's fixed bits gb, fixed-fixed pairs uniform)
+// and c_a the parity of register bit a's thread and fixed partners.
+template <int LOG_R, bool BOTH, typename T2>
+__device__ __forceinline__ void czg_apply(T2* ps, T2* lm, const DevCzg* __restrict__ g, uint32_t tb,
+                                          uint32_t gb) {
+    constexpr int R = 1 << LOG_R;
+    const uint32_t n_tt = g->n_tt, n_pairs = g->n_pairs;
+    uint32_t s = 0, lin = 0, u = 0;
+    for (uint32_t p = 0; p < n_tt; ++p) {
+        const uint32_t w = g->pair[p];
+        s ^= (tb >> (w & 0xffu)) & (tb >> ((w >> 8) & 0xffu));
+    }
+    for (uint32_t p = n_tt; p < n_pairs; ++p) {  // second operand: a fixed qubit
+        const uint32_t w = g->pair[p], wa = w & 0xffffu;
+        const uint32_t fb = (gb >> ((w >> 16) & 0xffu)) & 1u;
+        if (((wa >> 8) & 3u) == LOC_THR) lin ^= fb << (wa & 0xffu);
+        else u ^= fb & (gb >> (wa & 0xffu));
+    }
+    // the registers with bit a set, as a mask over the R registers
+    constexpr uint32_t half[5] = {0xaaaaaaaau, 0xccccccccu, 0xf0f0f0f0u, 0xff00ff00u, 0xffff0000u};
+    constexpr uint32_t all = R == 32 ? 0xffffffffu : (1u << R) - 1u;
+    uint32_t m = g->reg_mask ^ (((s ^ u ^ (uint32_t)__builtin_popcount(tb & lin)) & 1u) ? all : 0u);
+#pragma unroll
+    for (int a = 0; a < LOG_R; ++a)
+        if ((__builtin_popcount(tb & g->thr[a]) ^ __builtin_popcount(gb & g->fix[a])) & 1) m ^= half[a] & all;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const uint32_t t = (m << (31 - i)) & 0x80000000u;
+        ps[i].x = xor_sign(ps[i].x, t);
+        ps[i].y = xor_sign(ps[i].y, t);
+        if constexpr (BOTH) {
+            lm[i].x = xor_sign(lm[i].x, t);
+            lm[i].y = xor_sign(lm[i].y, t);
+        }
+    }
+}
+
 // Per-thread tile state shared by the handlers.
 struct TileCtx {
     uint32_t tb;   // tile-index bits of this thread (current phase)
@@ -491,7 +543,8 @@ template <int LOG_R, int LOG_T, int OPM, typename T2, typename Real>
 __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real cb, T2* ps, T2* lm,
                                        TileCtx& cx, Real& ival, unsigned char* lds,
                                        const DevPhase* phases, Real* gacc, int lane, int wave, int nw,
-                                       int tid, const T2* __restrict__ dz, const T2* __restrict__ fz) {
+                                       int tid, const T2* __restrict__ dz, const T2* __restrict__ fz,
+                                       const DevCzg* __restrict__ czg) {
 #define QL_G1_CASE(KIND, J)                                                                 \
     case H_G1 + KIND * 5 + J:                                                               \
         if constexpr (J < LOG_R) {                                                          \
@@ -635,6 +688,16 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
             }
             rz_u<LOG_R>(ps, ca, cb, bit);
         } break;
+        case H_CZG:
+            if constexpr (LOG_R <= CZG_REG_BITS) {
+                if constexpr (OPM == OP_PAIR) {
+                    czg_apply<LOG_R, false>(ps, lm, czg + arg, cx.tb, cx.gb);
+                    czg_apply<LOG_R, false>(lm, ps, czg + arg, cx.tb, cx.gb2);
+                } else {
+                    czg_apply<LOG_R, OPM == OP_BWD>(ps, lm, czg + arg, cx.tb, cx.gb);
+                }
+            }
+            break;
         case H_CZ_XX: {
             const bool on = loc_bit(arg & 0xffff, cx.tb, cx.gb) && loc_bit(arg >> 16, cx.tb, cx.gb);
             cz_sel<LOG_R, -1>(ps, on);
@@ -894,7 +957,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 const XOp<Real> nxt = xops[o + 1];
                 run_op<LOG_R, LOG_T, PAIR ? OP_PAIR : OP_ONE>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx,
                                                               ival, lds, phases, gthr, lane, wave, NW * GW,
-                                                              tid, dz, fz);
+                                                              tid, dz, fz, a.czg);
                 cur = nxt;
             }
         }
@@ -933,7 +996,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
                     run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, ival, lds,
-                                                 phases, gthr, lane, wave, NW * GW, tid, dz, fz);
+                                                 phases, gthr, lane, wave, NW * GW, tid, dz, fz, a.czg);
                     cur = nxt;
                 }
             }

@@ -36,7 +36,7 @@ class _Options(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("log_regs", "log_threads", "low_qubits",
                                               "max_gates_per_pass", "force_tiled",
                                               "wg_per_sample", "rz_groups", "pass_search",
-                                              "product_prefix")]
+                                              "product_prefix", "cz_groups")]
 
 
 class _Desc(ctypes.Structure):
@@ -48,7 +48,7 @@ class _PlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "n_passes", "tile_qubits", "log_regs",
                                               "log_threads", "low_qubits", "n_transposes",
                                               "n_param_gates", "n_lane_swaps", "n_rz_groups",
-                                              "n_ryz_pairs", "n_prefix_gates")]
+                                              "n_ryz_pairs", "n_prefix_gates", "n_cz_groups")]
 
 
 _lib = None

@@ -35,7 +35,7 @@ int main(int argc, char** argv) {
         // passes take the look-ahead alone, which keeps the sanitized run short
         const Options variants[] = {
             Options{},
-            [] { Options o; o.pass_search = -1; o.product_prefix = -1; return o; }(),
+            [] { Options o; o.pass_search = -1; o.product_prefix = -1; o.cz_groups = -1; return o; }(),
             [] { Options o; o.rz_groups = -1; o.max_gates_per_pass = 7; o.pass_search = 1; o.product_prefix = 1; return o; }(),
             [] { Options o; o.log_regs = 3; o.log_threads = 7; o.low_qubits = 2; o.pass_search = 1; return o; }(),
             [] { Options o; o.force_tiled = -1; return o; }(),

@@ -78,7 +78,7 @@ def test_create_rejects(lib, gates, n, F, P, code):
 
 @pytest.mark.parametrize("opts", [dict(log_regs=1), dict(log_regs=6), dict(log_threads=5),
                                   dict(log_threads=10), dict(low_qubits=9), dict(wg_per_sample=-1),
-                                  dict(rz_groups=2)])
+                                  dict(rz_groups=2), dict(cz_groups=1), dict(cz_groups=-2)])
 def test_create_rejects_options(lib, opts):
     assert _err(lambda: Q.Circuit(14, np.array(G1, np.int32), 0, 1, **opts)) == -3
 
@@ -278,6 +278,27 @@ def test_random_plans(lib, seed, opts):
         info = c.plan_info(dt)
         if opts.get("max_gates_per_pass") == 1:  # one pass per gate outside the product prefix
             assert info["n_passes"] == gates.shape[0] - info["n_prefix_gates"]
+
+
+def test_cz_groups_plan(lib):
+    """The 16-qubit workload's rings of CZs run as sign ops: with groups on,
+    the CZs of each layout between rotations form one op (128 CZs: 17 groups
+    and one CZ on its own at c64); off, none. Passes and layout changes are
+    the same either way, and the schedule stays valid."""
+    wl = W.get("16q")
+    on = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights)
+    off = Q.Circuit(wl.n, wl.gates(), wl.n_inputs, wl.n_weights, cz_groups=-1)
+    for dt in ("c64", "c128"):
+        a, b = on.plan_info(dt), off.plan_info(dt)
+        assert a["n_cz_groups"] > 0 and b["n_cz_groups"] == 0
+        for key in ("n_passes", "n_transposes", "n_lane_swaps", "n_prefix_gates"):
+            assert a[key] == b[key], key
+        pog, order = on.schedule(dt)
+        assert sorted(order.tolist()) == list(range(len(wl.gates())))
+    assert on.plan_info("c64")["n_cz_groups"] == 17
+    # a circuit without CZs has no groups
+    w30 = W.get("30q")
+    assert Q.Circuit(w30.n, w30.gates(), w30.n_inputs, w30.n_weights).plan_info("c64")["n_cz_groups"] == 0
 
 
 def test_product_prefix_plan(lib):

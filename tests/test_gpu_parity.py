@@ -722,6 +722,78 @@ def test_rz_groups(n, dtype, opts, shape):
     close(psi.cpu().numpy(), ref, TOL[dtype], f"rz groups n={n} {dtype}", "state")
 
 
+def cz_circuit(n, layers, F, P, seed, extra=6):
+    """Per layer: RY on every qubit, RZ on some, a ring of CZs, `extra` CZs on
+    random pairs (long-range ones reach the fixed qubits of a tile pass) and one
+    pair twice (the two cancel); a CNOT now and then closes a CZ group early."""
+    rng = np.random.default_rng(seed)
+    g = []
+    for layer in range(layers):
+        for q in range(n):
+            src = W.SRC_INPUT if rng.random() < 0.3 else W.SRC_WEIGHT
+            g.append((W.RY, q, -1, src, int(rng.integers(F if src == W.SRC_INPUT else P))))
+            if rng.random() < 0.5:
+                g.append((W.RZ, q, -1, W.SRC_WEIGHT, int(rng.integers(P))))
+        for q in range(n):
+            g.append((W.CZ, q, (q + 1) % n, 0, 0))
+            if layer % 2 and q == n // 2:
+                g.append((W.CNOT, q, (q + 3) % n, 0, 0))
+        for _ in range(extra):
+            a, b = rng.choice(n, 2, replace=False)
+            g.append((W.CZ, int(a), int(b), 0, 0))
+        a, b = rng.choice(n, 2, replace=False)
+        g += [(W.CZ, int(a), int(b), 0, 0)] * 2
+    return np.array(g, np.int32)
+
+
+CZ_GROUP_CASES = [(16, "c64", dict()), (15, "c128", dict()), (12, "c64", dict(log_regs=3, log_threads=6)),
+                  (14, "c64", dict(log_regs=5, log_threads=7)),
+                  (11, "c128", dict(force_tiled=1, log_regs=4, log_threads=6, max_gates_per_pass=30))]
+
+
+@pytest.mark.parametrize("n,dtype,opts", CZ_GROUP_CASES,
+                         ids=[f"n{c[0]}-{c[1]}-{'-'.join(f'{k}{v}' for k, v in c[2].items()) or 'default'}"
+                              for c in CZ_GROUP_CASES])
+def test_cz_groups(n, dtype, opts):
+    """CZ groups (one sign op for the CZs of a layout) against the oracle and
+    against the plan without them: forward + adjoint VJP (the two-tile forward
+    and the backward kernel), and exact final states."""
+    F, P, B = 4, 6, 3
+    gates = cz_circuit(n, 3, F, P, seed=170 + n)
+    x, w, g = W.random_inputs(B, F, P, n, seed=171 + n, dtype=dtype)
+    grouped = Q.Circuit(n, gates, F, P, **opts)
+    single = Q.Circuit(n, gates, F, P, cz_groups=-1, **opts)
+    assert grouped.plan_info(dtype)["n_cz_groups"] > 0
+    assert single.plan_info(dtype)["n_cz_groups"] == 0
+    want = oracle.run(n, gates, x, w, grad_out=g)
+    got = gpu_fb(grouped, dtype, x, w, g)
+    check(got, want, TOL[dtype], f"cz groups n={n} {dtype}")
+    check(got, gpu_fb(single, dtype, x, w, g), TOL[dtype], "grouped vs single")
+    psi = Q.Runner(grouped, dtype).state(_dev(x, dtype), _dev(w, dtype))
+    torch.cuda.synchronize()
+    ref = oracle.run(n, gates, x, w, want_state=True)["state"]
+    close(psi.cpu().numpy(), ref, TOL[dtype], f"cz groups n={n} {dtype}", "state")
+
+
+def test_cz_groups_split():
+    """100 CZs on random pairs after a product-state prefix, all in one pass
+    and one layout: more pairs without a register operand than one group
+    record holds, so the planner splits the collection into several groups."""
+    n, dtype, F, P, B = 16, "c64", 2, 3, 4
+    rng = np.random.default_rng(33)
+    g = [(W.H, q, -1, 0, 0) for q in range(n)] + [(W.RY, q, -1, W.SRC_WEIGHT, q % P) for q in range(n)]
+    for _ in range(100):
+        a, b = rng.choice(n, 2, replace=False)
+        g.append((W.CZ, int(a), int(b), 0, 0))
+    gates = np.array(g, np.int32)
+    x, w, gout = W.random_inputs(B, F, P, n, seed=34, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P)
+    info = circ.plan_info(dtype)
+    assert info["n_passes"] == 1 and info["n_transposes"] + info["n_lane_swaps"] == 0
+    assert info["n_cz_groups"] >= 3
+    check(gpu_fb(circ, dtype, x, w, gout), oracle.run(n, gates, x, w, grad_out=gout), TOL[dtype], "cz split")
+
+
 def test_rz_groups_param_shift():
     """The shifted circuits of a parameter-shift chunk shift one member of an
     RZ group's phase table at a time."""
