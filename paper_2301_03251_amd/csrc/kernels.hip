@@ -849,28 +849,47 @@ __global__ void __launch_bounds__(256) k_bind_prefix(const PrefixArgs a) {
 // Environment sums of the prefix: 256 threads (4 wavefronts) per workgroup;
 // a wavefront takes blocks of 64 * 2^LR consecutive amplitudes of lambda_P,
 // so register bit m is qubit m, lane bit t qubit LR + t, and the block index
-// holds the other (fixed) qubits. Per thread the register bits are contracted
-// (Real) with the leave-one-out scheme, and the shares of the register and
-// lane qubits are summed over the wavefront's blocks in registers (Real);
-// only the fixed qubits, whose factors change from block to block, need a
-// wavefront sum per block (lane i then keeps fixed qubit i's share, fp64).
-// The wavefront sums (fp64 across rows) go to LDS at the end and the four
-// wavefronts are combined in a fixed order.
+// holds the other (fixed) qubits. A wavefront's blocks are blk0 + k * stride
+// (stride a power of two): their fixed bits below lo = log2(stride) are
+// blk0's, the h = nfix - lo bits above are k's (at most ENV_HIGH_BITS, by the
+// launch). Per block and thread the register bits are contracted (Real, leave-
+// one-out); the shares of the register and lane qubits are sums over the
+// blocks of conj(the block's fixed factors) times the contractions (Real, in
+// registers), with each lane's constant factors applied once at the end. The
+// fixed qubits need the block's wavefront sum U(k) of the lane-weighted
+// contraction (fp64), kept in an LDS table, whose leave-one-out contractions
+// over k's bits give them at the end. The wavefront sums (fp64) go to LDS and
+// the four wavefronts are combined in a fixed order.
+constexpr int ENV_HIGH_BITS = 8;
 template <typename Real, int LR>
 __global__ void __launch_bounds__(256) k_env(const PrefixArgs a) {
     using T2 = typename Cx<Real>::T;
-    constexpr int R = 1 << LR;
+    constexpr int R = 1 << LR, KMAX = 1 << ENV_HIGH_BITS;
     __shared__ double acc[4][32][4];
+    __shared__ double2 ut[4][KMAX];  // per wavefront: U(k) of its blocks
+    __shared__ double2 tab[4][32];   // per wavefront: products of the high fixed factors of
+                                     // k's low four bits [0, 16) and of its other bits [16, 32)
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int n = a.n;
     const int64_t b = blockIdx.x / a.env_wg;
     const int w = (int)(blockIdx.x - b * a.env_wg);
     for (int i = tid; i < 4 * 32 * 4; i += 256) (&acc[0][0][0])[i] = 0.0;
-    __syncthreads();
+    for (int i = tid; i < 4 * KMAX; i += 256) (&ut[0][0])[i] = make_double2(0.0, 0.0);
     const double2* fac = (const double2*)a.phi + b * 2 * n;
     const T2* lam = (const T2*)a.lam + (b << n);
     const int nfix = n - LR - 6;
     const int64_t nblk = (int64_t)1 << nfix;
+    const int64_t blk0 = (int64_t)w * 4 + wave, stride = (int64_t)a.env_wg * 4;
+    const int lo = std::min(nfix, (int)__builtin_ctzll((unsigned long long)stride));
+    const int h = nfix - lo, ha = std::min(h, 4), hb = h - ha;
+    auto ffac = [&](int i, int64_t bit) { return fac[2 * (LR + 6 + i) + (int)bit]; };  // fixed qubit i
+    if (lane < 32) {
+        const int e = lane & 15, base = lane < 16 ? 0 : ha, cnt = lane < 16 ? ha : hb;
+        double2 p = make_double2(1.0, 0.0);
+        for (int j = 0; j < cnt; ++j) p = cxmul(p, ffac(lo + base + j, (e >> j) & 1));
+        tab[wave][lane] = p;
+    }
+    __syncthreads();
     T2 f0[LR], f1[LR];
 #pragma unroll
     for (int m = 0; m < LR; ++m) {
@@ -890,25 +909,18 @@ __global__ void __launch_bounds__(256) k_env(const PrefixArgs a) {
         cl = t == 0 ? fac[2 * LR + (lane & 1)] : cxmul(cl, fac[2 * (LR + t) + ((lane >> t) & 1)]);
     }
     const T2 clr = to_real<T2, Real>(cl);
-    Real sr[LR][4], sl[6][4];  // this lane's shares: register qubits; lane qubits
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-#pragma unroll
-        for (int m = 0; m < LR; ++m) sr[m][c] = 0;
-#pragma unroll
-        for (int t = 0; t < 6; ++t) sl[t][c] = 0;
-    }
-    double fx[4] = {0.0, 0.0, 0.0, 0.0};  // lane i < nfix: fixed qubit LR + 6 + i
-    // this wavefront's blocks are blk0 + k * stride with stride = 4 env_wg, a
-    // power of two: the block bits below lo = log2(stride) are blk0's
-    const int64_t blk0 = (int64_t)w * 4 + wave, stride = (int64_t)a.env_wg * 4;
-    const int lo = std::min(nfix, (int)__builtin_ctzll((unsigned long long)stride));
+    // the low fixed factors: all (clo) and all but this lane's (glo, lane < lo)
     double2 clo = make_double2(1.0, 0.0), glo = make_double2(1.0, 0.0);
     for (int i = 0; i < lo; ++i) {
-        const double2 f = fac[2 * (LR + 6 + i) + ((blk0 >> i) & 1)];
+        const double2 f = ffac(i, (blk0 >> i) & 1);
         clo = cxmul(clo, f);
-        if (i != lane) glo = cxmul(glo, f);  // lane i < lo: without its own factor
+        if (i != lane) glo = cxmul(glo, f);
     }
+    Real sr[LR][4], wx = 0, wy = 0;  // sums over the blocks: conj(cf) S[m][u]; conj(cf) T
+#pragma unroll
+    for (int m = 0; m < LR; ++m)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sr[m][c] = 0;
     for (int64_t blk = blk0; blk < nblk; blk += stride) {
         T2 v[R];
         const T2* src = lam + (blk << (LR + 6)) + ((int64_t)lane << LR);
@@ -920,69 +932,91 @@ __global__ void __launch_bounds__(256) k_env(const PrefixArgs a) {
             const T2 x = cxmulc(f0[0], S[0][0]), y = cxmulc(f1[0], S[0][1]);
             return mk<T2>(x.x + y.x, x.y + y.y);
         }();
-        // the fixed factors: those of the bits below `lo` are the same for all
-        // of this wavefront's blocks (its stride is a power of two)
-        double2 chi = make_double2(1.0, 0.0);
-        for (int i = lo; i < nfix; ++i) chi = cxmul(chi, fac[2 * (LR + 6 + i) + ((blk >> i) & 1)]);
-        const T2 cf = to_real<T2, Real>(cxmul(clo, chi));
-        // register qubits: conj(every other factor) S[m][u]
-        const T2 call = cxmul(clr, cf);
+        const int k = (int)(blk >> lo);
+        const T2 cf = to_real<T2, Real>(cxmul(clo, cxmul(tab[wave][k & 15], tab[wave][16 + (k >> 4)])));
 #pragma unroll
         for (int m = 0; m < LR; ++m) {
-            const T2 s0 = cxmulc(call, S[m][0]), s1 = cxmulc(call, S[m][1]);
+            const T2 s0 = cxmulc(cf, S[m][0]), s1 = cxmulc(cf, S[m][1]);
             sr[m][0] += s0.x;
             sr[m][1] += s0.y;
             sr[m][2] += s1.x;
             sr[m][3] += s1.y;
         }
-        // lane qubits: conj(every non-register factor but t's) T, in the bin
-        // of the lane's bit t
-#pragma unroll
-        for (int t = 0; t < 6; ++t) {
-            const T2 x = cxmulc(cxmul(lf[t], cf), T);
-            const bool one = (lane >> t) & 1;
-            sl[t][0] += one ? (Real)0 : x.x;
-            sl[t][1] += one ? (Real)0 : x.y;
-            sl[t][2] += one ? x.x : (Real)0;
-            sl[t][3] += one ? x.y : (Real)0;
-        }
-        // fixed qubits (bits uniform over the block): conj(product of the
-        // other fixed factors) U, U = the wavefront's sum of conj(cl) T
+        const T2 x = cxmulc(cf, T);
+        wx += x.x;
+        wy += x.y;
         const T2 uu = cxmulc(clr, T);
         const double ux = wave_total(uu.x), uy = wave_total(uu.y);
-        if (lane < nfix) {
-            // the other fixed factors: the constant low ones (glo leaves out
-            // this lane's if it is low), times the changing high ones but
-            // this lane's
-            double2 g = glo;
-            for (int i = lo; i < nfix; ++i)
-                if (i != lane) g = cxmul(g, fac[2 * (LR + 6 + i) + ((blk >> i) & 1)]);
-            const double2 r = cxmulc(g, make_double2(ux, uy));
-            const bool one = (blk >> lane) & 1;
-            fx[0] += one ? 0.0 : r.x;
-            fx[1] += one ? 0.0 : r.y;
-            fx[2] += one ? r.x : 0.0;
-            fx[3] += one ? r.y : 0.0;
-        }
+        if (lane == 0) ut[wave][k] = make_double2(ux, uy);
     }
-    // the wavefront's sums into LDS (lane 0; lane i for fixed qubit i)
+    // register qubits: conj(cl) times the sums
 #pragma unroll
-    for (int m = 0; m < LR; ++m)
+    for (int m = 0; m < LR; ++m) {
+        const T2 s0 = cxmulc(clr, mk<T2>(sr[m][0], sr[m][1])), s1 = cxmulc(clr, mk<T2>(sr[m][2], sr[m][3]));
+        const Real q[4] = {s0.x, s0.y, s1.x, s1.y};
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const double t = wave_total(sr[m][c]);
+            const double t = wave_total(q[c]);
             if (lane == 0) acc[wave][m][c] = t;
         }
+    }
+    // lane qubits: conj(every lane factor but t's) times the sum, in the bin of
+    // the lane's bit t
 #pragma unroll
-    for (int t = 0; t < 6; ++t)
+    for (int t = 0; t < 6; ++t) {
+        const T2 x = cxmulc(lf[t], mk<T2>(wx, wy));
+        const bool one = (lane >> t) & 1;
+        const Real q[4] = {one ? (Real)0 : x.x, one ? (Real)0 : x.y, one ? x.x : (Real)0, one ? x.y : (Real)0};
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const double x = wave_total(sl[t][c]);
-            if (lane == 0) acc[wave][LR + t][c] = x;
+            const double s = wave_total(q[c]);
+            if (lane == 0) acc[wave][LR + t][c] = s;
         }
-    if (lane < nfix)
+    }
+    __syncthreads();  // the U table of each wavefront is complete
+    // fixed qubits above lo (bit j of k): U contracted with conj(the low and
+    // the other high factors), in the bin of bit j
+    const int K = 1 << h;
+    for (int j = 0; j < h; ++j) {
+        double r[4] = {0.0, 0.0, 0.0, 0.0};
+        for (int k = lane; k < K; k += 64) {
+            double2 p = clo;
+            for (int j2 = 0; j2 < h; ++j2)
+                if (j2 != j) p = cxmul(p, ffac(lo + j2, (k >> j2) & 1));
+            const double2 x = cxmulc(p, ut[wave][k]);
+            const bool one = (k >> j) & 1;
+            r[0] += one ? 0.0 : x.x;
+            r[1] += one ? 0.0 : x.y;
+            r[2] += one ? x.x : 0.0;
+            r[3] += one ? x.y : 0.0;
+        }
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[wave][LR + 6 + lane][c] = fx[c];
+        for (int c = 0; c < 4; ++c) {
+            const double t = wave_total(r[c]);
+            if (lane == 0) acc[wave][LR + 6 + lo + j][c] = t;
+        }
+    }
+    // fixed qubits below lo (bit i of blk0 in every block): the whole table
+    // contracted with conj(the high factors), times conj(the other low factors)
+    if (lo > 0) {
+        double fx = 0.0, fy = 0.0;
+        for (int k = lane; k < K; k += 64) {
+            double2 p = make_double2(1.0, 0.0);
+            for (int j2 = 0; j2 < h; ++j2) p = cxmul(p, ffac(lo + j2, (k >> j2) & 1));
+            const double2 x = cxmulc(p, ut[wave][k]);
+            fx += x.x;
+            fy += x.y;
+        }
+        const double2 F = make_double2(wave_total(fx), wave_total(fy));
+        if (lane < lo) {
+            const double2 r = cxmulc(glo, F);
+            const bool one = (blk0 >> lane) & 1;
+            acc[wave][LR + 6 + lane][0] = one ? 0.0 : r.x;
+            acc[wave][LR + 6 + lane][1] = one ? 0.0 : r.y;
+            acc[wave][LR + 6 + lane][2] = one ? r.x : 0.0;
+            acc[wave][LR + 6 + lane][3] = one ? r.y : 0.0;
+        }
+    }
     __syncthreads();
     double* dst = a.envpart + ((size_t)b * a.env_wg + w) * n * 4;
     for (int i = tid; i < n * 4; i += 256) {
@@ -1492,13 +1526,20 @@ int env_workgroups(int dtype, int n, int64_t B) {
     while (want * 2 * std::max<int64_t>(B, 1) <= 2048) want *= 2;
     int64_t cap = 1;
     while (cap * 4 < nblk) cap *= 2;
-    return (int)std::min(want, cap);
+    // at most 2^ENV_HIGH_BITS blocks per wavefront (its LDS table of U)
+    int64_t floor = 1;
+    while (floor * 4 * ((int64_t)1 << ENV_HIGH_BITS) < nblk) floor *= 2;
+    return (int)std::max(std::min(want, cap), floor);
 }
 
 hipError_t launch_env(int dtype, const PrefixArgs& a, hipStream_t s) {
     if (a.n < 8 || a.n > 32) return hipErrorInvalidValue;
     const dim3 grid((unsigned)(a.B * a.env_wg));
     const int lr = env_log_regs(dtype, a.n);
+    // a wavefront's blocks fit its LDS table: nblk / (4 env_wg) <= 2^ENV_HIGH_BITS
+    if (a.env_wg < 1 || (a.env_wg & (a.env_wg - 1)) != 0 ||
+        ((int64_t)1 << (a.n - lr - 6)) > (int64_t)a.env_wg * 4 * ((int64_t)1 << ENV_HIGH_BITS))
+        return hipErrorInvalidValue;
     if (dtype == 0) {
         if (lr == 2) hipLaunchKernelGGL((k_env<float, 2>), grid, dim3(256), 0, s, a);
         else hipLaunchKernelGGL((k_env<float, 3>), grid, dim3(256), 0, s, a);
