@@ -794,6 +794,22 @@ def test_cz_groups_split():
     check(gpu_fb(circ, dtype, x, w, gout), oracle.run(n, gates, x, w, grad_out=gout), TOL[dtype], "cz split")
 
 
+def test_cz_groups_param_shift():
+    """The shifted circuits of a parameter-shift chunk run the same CZ groups
+    (two-tile forward launches): shift gradients against the oracle's rule."""
+    n, dtype, F, P, B = 14, "c128", 4, 6, 2
+    gates = cz_circuit(n, 2, F, P, seed=190)
+    x, w, g = W.random_inputs(B, F, P, n, seed=191, dtype=dtype)
+    circ = Q.Circuit(n, gates, F, P)
+    assert circ.plan_info(dtype)["n_cz_groups"] > 0
+    e, gx, gw = Q.Runner(circ, dtype).param_shift(_dev(x, dtype), _dev(w, dtype), _dev(g, dtype), max_chunk=41)
+    torch.cuda.synchronize()
+    got = {"expz": e.cpu().numpy(), "grad_inputs": gx.cpu().numpy(), "grad_weights": gw.cpu().numpy()}
+    ox, ow = oracle.param_shift(n, gates, x, w, g)
+    want = {"expz": oracle.run(n, gates, x, w)["expz"], "grad_inputs": ox, "grad_weights": ow}
+    check(got, want, 1e-12, "cz groups shift")
+
+
 def test_rz_groups_param_shift():
     """The shifted circuits of a parameter-shift chunk shift one member of an
     RZ group's phase table at a time."""
