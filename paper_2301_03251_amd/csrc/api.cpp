@@ -40,7 +40,7 @@ struct Tables {
     std::vector<uint8_t> blob;
     size_t off_pass = 0, off_phase = 0, off_ops = 0, off_gslot = 0, off_slots = 0;
     size_t off_xptr = 0, off_xslot = 0, off_wptr = 0, off_wslot = 0, off_gates = 0, off_diag = 0;
-    size_t off_fuse = 0, off_czg = 0;
+    size_t off_fuse = 0, off_czg = 0, off_pthr = 0;
     size_t off_pptr = 0, off_pops = 0;  // product-prefix CSR (per qubit)
     std::vector<DevPass> passes;
     int n_diags = 0, n_fuses = 0;
@@ -126,6 +126,27 @@ void build_tables(const Circuit& c, int dt, Tables& T) {
     T.off_fuse = put(T.blob, pl.fuses);
     T.n_fuses = (int)pl.fuses.size();
     T.off_czg = put(T.blob, pl.czgs);
+    // per phase, the thread-index part of every thread's layout: tile bits
+    // (low PTHR_TB_BITS bits) and LDS byte offset (above), one word per lane
+    // for the lane bits, one per wavefront index for the higher thread bits;
+    // a thread's layout is its two words XORed
+    std::vector<uint32_t> pthr;
+    if (!pl.whole_state) {
+        pthr.reserve(pl.phases.size() * PTHR_WORDS);
+        for (const DevPhase& F : pl.phases)
+            for (int e = 0; e < PTHR_WORDS; e++) {
+                const int b0 = e < 64 ? 0 : 6, nb = e < 64 ? std::min(6, pl.log_t) : std::max(0, pl.log_t - 6);
+                const uint32_t v = e < 64 ? (uint32_t)e : (uint32_t)(e - 64);
+                uint32_t tb = 0, ts = 0;
+                for (int i = 0; i < nb; i++)
+                    if (v >> i & 1u) {
+                        tb |= 1u << F.thr_bit[b0 + i];
+                        ts ^= F.thr_slot[b0 + i];
+                    }
+                pthr.push_back(tb | ts << PTHR_TB_BITS);
+            }
+    }
+    T.off_pthr = put(T.blob, pthr);
     T.off_pptr = put(T.blob, pl.pre_ptr);
     T.off_pops = put(T.blob, pl.pre_ops);
     T.blob.resize(align256(T.blob.size()), 0);
@@ -577,6 +598,7 @@ int state_passes(Ctx& x, int64_t B, bool bwd, const void* grad_out, void* psi_ex
         ta.fzc = x.W + x.L.fzc;
         ta.n_fuses = x.T.n_fuses;
         ta.czg = (const DevCzg*)(x.W + x.L.tables + x.T.off_czg);
+        ta.pthr = (const uint32_t*)(x.W + x.L.tables + x.T.off_pthr);
         ta.grad_out = grad_out;
         ta.zpart = zpart;
         ta.gpart = gpart;

@@ -167,6 +167,7 @@ struct TileArgs {
     int32_t n_gslots;          // gradient accumulators of this pass
     const double* phi;         // [B][n][2] complex (double2): product-prefix factors (PF_PRODUCT)
     const DevCzg* czg;         // CZ groups (H_CZG ops)
+    const uint32_t* pthr;      // [n_phases][PTHR_WORDS] thread layouts of every phase
 };
 
 // Product-state prefix. Binding: phi[c][q] = the state the prefix gates of

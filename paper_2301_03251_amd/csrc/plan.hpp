@@ -170,6 +170,12 @@ struct DevPhase {
     uint32_t reg_qoff[MAX_R];            // amplitude-index offset of register i's tile bits
 };
 
+// Thread layouts of a phase as tables: PTHR_WORDS words per phase, 64 for
+// the lane bits (indexed by lane) and 8 for the wavefront bits (indexed by
+// wavefront); each word holds the tile bits (low PTHR_TB_BITS bits: k <= 14)
+// and the LDS byte offset (above) that those thread-index bits contribute.
+constexpr int PTHR_WORDS = 72;
+constexpr int PTHR_TB_BITS = 14;
 // Bank-spreading permutation of LDS slots: folds the upper nibbles of the tile
 // index into the lowest one. Linear over GF(2), an involution on each aligned
 // block of 2^16 slots.

@@ -544,7 +544,7 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
                                        TileCtx& cx, Real& ival, unsigned char* lds,
                                        const DevPhase* phases, Real* gacc, int lane, int wave, int nw,
                                        int tid, const T2* __restrict__ dz, const T2* __restrict__ fz,
-                                       const DevCzg* __restrict__ czg) {
+                                       const DevCzg* __restrict__ czg, const uint32_t* __restrict__ pthr) {
 #define QL_G1_CASE(KIND, J)                                                                 \
     case H_G1 + KIND * 5 + J:                                                               \
         if constexpr (J < LOG_R) {                                                          \
@@ -707,8 +707,11 @@ __device__ __forceinline__ void run_op(uint32_t h, uint32_t arg, Real ca, Real c
         case H_TRANSPOSE: {
             const uint32_t ph_to = arg & 0xfffffu;
             const DevPhase& to = phases[ph_to];
-            uint32_t tb_to, ts_to;
-            thread_layout<LOG_T>((uint32_t)tid, to, tb_to, ts_to);
+            // the thread's layout in the new phase, from its lane's and its
+            // wavefront's table words
+            const uint32_t* pt = pthr + (size_t)ph_to * PTHR_WORDS;
+            const uint32_t tw = pt[lane] ^ pt[64 + wave];
+            const uint32_t tb_to = tw & ((1u << PTHR_TB_BITS) - 1u), ts_to = tw >> PTHR_TB_BITS;
             lds_exchange<LOG_R>(ps, lds, phases[cx.ph], to, cx.ts, ts_to);
             if constexpr (OPM != OP_ONE) lds_exchange<LOG_R>(lm, lds, phases[cx.ph], to, cx.ts, ts_to);
             if constexpr (OPM == OP_BWD)
@@ -957,7 +960,7 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 const XOp<Real> nxt = xops[o + 1];
                 run_op<LOG_R, LOG_T, PAIR ? OP_PAIR : OP_ONE>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx,
                                                               ival, lds, phases, gthr, lane, wave, NW * GW,
-                                                              tid, dz, fz, a.czg);
+                                                              tid, dz, fz, a.czg, a.pthr);
                 cur = nxt;
             }
         }
@@ -996,7 +999,8 @@ k_tile(const TileArgs a, const DevPass* __restrict__ pass, const DevPhase* __res
                 for (int o = bwd_begin; o < bwd_end; ++o) {
                     const XOp<Real> nxt = xops[o + 1];
                     run_op<LOG_R, LOG_T, OP_BWD>(cur.h, cur.arg, cur.a, cur.b, ps, lm, cx, ival, lds,
-                                                 phases, gthr, lane, wave, NW * GW, tid, dz, fz, a.czg);
+                                                 phases, gthr, lane, wave, NW * GW, tid, dz, fz, a.czg,
+                                                 a.pthr);
                     cur = nxt;
                 }
             }
